@@ -510,33 +510,35 @@ static double tick(tick_ctx* t, sys_t* S, int action) {
   return r;
 }
 
-/* Observation (Sec. 4.1, R15): every feature computed in fp64, rounded once to fp32. */
+/* Observation (Sec. 4.1, R15): every feature is a raw quantity times the reciprocal of
+ * its normaliser (1/N, 1/T_w, 1/32, 1/C, 1/(lambda_ref*dt), each computed once in fp64),
+ * evaluated in fp64 and rounded once to fp32. */
 static void observe(const orc_cfg* c, const sys_t* S, double t, float* obs) {
   int F = c->obs_dim, K = c->n_servers, C = c->n_classes, N = c->queue_cap;
-  double tw = c->obs_tw;
+  double inv_n = 1.0 / (double)N, inv_tw = 1.0 / c->obs_tw, inv_c = 1.0 / (double)C;
+  double inv_rs = 1.0 / (c->lambda_ref * c->tick_s);
   int i = 0;
   int nq = sumq(S, C);
   int h = hol(S, C);
-  obs[i++] = (float)((double)nq / (double)N);
-  obs[i++] = (float)((h >= 0 ? t - S->ring[h][S->head[h]] : 0.0) / tw);
+  obs[i++] = (float)((double)nq * inv_n);
+  obs[i++] = (float)((h >= 0 ? t - S->ring[h][S->head[h]] : 0.0) * inv_tw);
   for (int j = 0; j < K; j++) {
     obs[i++] = S->busy[j] > t ? 1.0f : 0.0f;
-    obs[i++] = (float)((double)S->last_b[j] / 32.0);
+    obs[i++] = (float)((double)S->last_b[j] * 0.03125);
     if (K > 1) {
       double rem = S->busy[j] > t ? S->busy[j] - t : 0.0;
-      obs[i++] = (float)(rem / tw);
-      obs[i++] = (float)((double)(S->last_cls[j] + 1) / (double)C);
+      obs[i++] = (float)(rem * inv_tw);
+      obs[i++] = (float)((double)(S->last_cls[j] + 1) * inv_c);
     }
   }
   if (C > 1) {
     for (int cc = 0; cc < C; cc++) {
-      obs[i++] = (float)((double)S->q[cc] / (double)N);
+      obs[i++] = (float)((double)S->q[cc] * inv_n);
       double age = S->q[cc] > 0 ? t - S->ring[cc][S->head[cc]] : 0.0;
-      obs[i++] = (float)(age / tw);
+      obs[i++] = (float)(age * inv_tw);
     }
   }
-  double rs = c->lambda_ref * c->tick_s;
-  for (int r = 0; r < 4; r++) obs[i++] = (float)(S->ewma[r] / rs);
+  for (int r = 0; r < 4; r++) obs[i++] = (float)(S->ewma[r] * inv_rs);
   while (i < F) obs[i++] = 0.0f;
 }
 
