@@ -1,0 +1,238 @@
+#!/usr/bin/env python3
+"""Throughput of the batched serving-simulator rollout on one MI355X.
+
+One step = one pass of the whole hot path over one synthetic batch: reset every
+environment, then T ticks of (policy MLP + action sampling on MFMA, simulator tick of the
+learned system and, where configured, of the static shadow system), then returns/GAE
+over the trajectory and the device-side reduction of the per-environment counters.
+value = environments x ticks per second of wall time (inputs resident in HBM).
+
+Prints one JSON line. Kernel durations come from HIP events recorded by the library on
+its own stream around every launch during the timed region.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import threading
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3       # dense fp32 matrix
+
+DESCR = {
+    "C1": "C1: 256 envs x 1000 ticks, 1 server, Poisson 500/s, DET 5ms+0.5ms*b, obs 8, MLP 8-64-64-6 fp32, REINFORCE returns",
+    "C2": "C2: 4096 envs x 2000 ticks, 1 server, MMPP 200/2000 req/s, 2 classes 80/20, obs 12, MLP 12-128-128-6 bf16, REINFORCE returns",
+    "C3": "C3: 16384 envs x 2048 ticks, 4 servers, Poisson 3000/s, 2 classes 70/30, obs 32, MLP 32-256-256-24 bf16, GAE",
+    "C4": "C4: 65536 envs x 1024 ticks, 8 servers, 3-state MMPP, 4 classes lognormal, obs 64, MLP 64-256-256-48 bf16, GAE",
+    "C5": "C5: 262144 envs x 4096 ticks, 16 servers, Pareto ON/OFF bursts 20000/s, 4 classes 50/30/15/5 lognormal, static shadow, obs 96, MLP 96-512-512-96 bf16, GAE",
+}
+
+
+def mlp_flops(w):
+    A1 = 6 * w["n_servers"] + (1 if w["value_head"] else 0)
+    return 2 * (w["obs_dim"] * w["mlp_h1"] + w["mlp_h1"] * w["mlp_h2"] + w["mlp_h2"] * A1)
+
+
+def step_bytes(w, tot, E, T):
+    """Algorithmic HBM bytes per env-tick of the learned-system kernel: the structure-of-
+    arrays state it must read and write, the action, reward and observation, the ring
+    entries touched by accepted arrivals and dispatched requests, and the server entries
+    rewritten by dispatches (busy + meta) and completions (meta)."""
+    K, C, F = w["n_servers"], w["n_classes"], w["obs_dim"]
+    state_rw = 4 + 4 + 8 * C + 4 * 6 + 16 + 8 + 4 + 8 + 8 + 32   # queues, counters, arrivals, ewma
+    fixed = 1 + 2 * state_rw + 12 * K + 4 * F + 8                 # + action, servers read, obs, reward
+    n = E * T
+    c = tot["cnt"][0]
+    var = 8.0 * (c[1] + c[3]) / n + 12.0 * c[4] / n + 4.0 * c[4] / n
+    return fixed + var
+
+
+def static_bytes(w, tot, E, T):
+    """Same for the static shadow kernel (no action, observation or rates)."""
+    K, C = w["n_servers"], w["n_classes"]
+    state_rw = 4 + 4 + 8 * C + 4 * 6 + 16 + 8 + 4 + 8 + 8
+    fixed = 2 * state_rw + 12 * K + 8
+    n = E * T
+    c = tot["cnt"][1]
+    return fixed + 8.0 * (c[1] + c[3]) / n + 16.0 * c[4] / n
+
+
+def kernel_hash():
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2607_05272_amd", "csrc"))):
+        h.update(open(os.path.join(ROOT, "paper_2607_05272_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(kernel, cfg_name):
+    """HBM bytes per launch measured by rocprofv3 PMC counters (profiles/traffic.json),
+    or None if absent or taken on different kernel sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        d = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    ent = d.get(f"{cfg_name}:{kernel}")
+    if not ent or ent.get("kernel_hash") != kernel_hash():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(w, name, budget_s, seed):
+    """The oracle (sequential fp64 simulator + fp64 policy MLP + sampler) on the host
+    cores, over a bounded sample of the same workload, env-steps per second."""
+    import numpy as np
+    import oracle
+    wts = oracle.init_weights(w, seed)
+    threads = max(1, min(16, os.cpu_count() or 1))
+    T = min(w["T"], 256)
+    # calibrate on one env
+    t0 = time.perf_counter()
+    oracle.rollout(w, seed, 32, [0], weights=wts, want_obs=False, want_rec=False)
+    per_step = (time.perf_counter() - t0) / 32
+    n_env = max(threads, int(budget_s * threads / (per_step * T)))
+    n_env = min(n_env, w["n_envs"])
+    ids = np.linspace(0, w["n_envs"] - 1, n_env).astype(np.uint32)
+    chunks = np.array_split(ids, threads)
+
+    def work(c):
+        if len(c):
+            oracle.rollout(w, seed, T, c, weights=wts, want_obs=False, want_rec=False)
+
+    t0 = time.perf_counter()
+    th = [threading.Thread(target=work, args=(c,)) for c in chunks]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    dt = time.perf_counter() - t0
+    return {"value": n_env * T / dt, "unit": "env-steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_env} envs (evenly spaced ids) x {T} ticks of {name}, fp64 policy MLP + "
+                      f"sampler + simulator, {dt:.1f} s wall on {threads} threads"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="C5", choices=sorted(DESCR))
+    ap.add_argument("--ticks", type=int, default=0, help="override T (diagnostics only)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only (environments are independent; the "
+              "multi-GPU design is described in DESIGN.md but not built). Use --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2607_05272_amd as bs
+    from workloads import preset
+
+    w = preset(args.config)
+    if args.ticks:
+        w["T"] = args.ticks
+    E, T, F = w["n_envs"], w["T"], w["obs_dim"]
+    dev = torch.device("cuda")
+    seed = 0x5EED0000 + int(args.config[1])
+    sim = bs.Sim(w)
+    weights = sim.init_weights(seed)
+    traj = bs.Trajectory(T, E, F, dev, value=bool(w["value_head"]), shadow=bool(w["shadow"]))
+    adv = torch.empty((T, E), dtype=torch.float64, device=dev)
+    ret = torch.empty((T, E), dtype=torch.float64, device=dev)
+    gae = bool(w["value_head"])
+    lam = w["lam"] if gae else 1.0
+
+    def one_step(i):
+        sim.reset(seed + i)
+        sim.rollout(weights, T, traj=traj)
+        sim.returns_gae(traj.reward, traj.value if gae else None, w["gamma"], lam, adv, ret)
+        return sim.stats()
+
+    for i in range(args.warmup):
+        one_step(i)
+    sim.sync()
+    torch.cuda.synchronize()
+    sim.get_timing(clear=True)
+    sim.set_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    tot = None
+    for i in range(args.steps):
+        tot = one_step(1000 + i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    sim.sync()
+    timing = sim.get_timing(clear=True)
+    sim.set_timing(False)
+    ms_per_step = (t1 - t0) * 1000.0 / args.steps
+    value = E * T / (ms_per_step / 1000.0)
+
+    kern = {}
+    for k, (ms, n) in timing.items():
+        if n:
+            kern[k] = {"total_ms_per_step": ms / args.steps, "launches_per_step": n // args.steps,
+                       "avg_us": 1000.0 * ms / n}
+    # roofline of each hot kernel class
+    rl = {}
+    if "policy" in kern:
+        fl = mlp_flops(w) * E
+        ach = fl / (kern["policy"]["avg_us"] * 1e-6) / 1e12
+        peak = PEAK_BF16_TFLOPS if w["mlp_bf16"] else PEAK_FP32_TFLOPS
+        rl["policy"] = {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+                        "frac": ach / peak, "traffic": traffic_for("policy", args.config),
+                        "work_per_launch": fl}
+    if "step" in kern:
+        by = step_bytes(w, tot, E, T) * E
+        ach = by / (kern["step"]["avg_us"] * 1e-6) / 1e9
+        rl["step"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                      "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("step", args.config),
+                      "work_per_launch": by}
+    if "static" in kern:
+        by = static_bytes(w, tot, E, T) * E
+        ach = by / (kern["static"]["avg_us"] * 1e-6) / 1e9
+        rl["static"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("static", args.config),
+                        "work_per_launch": by}
+    if "gae" in kern:
+        by = 28.0 * E * T
+        ach = by / (kern["gae"]["avg_us"] * 1e-6) / 1e9
+        rl["gae"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("gae", args.config),
+                     "work_per_launch": by}
+    dom = max(kern, key=lambda k: kern[k]["total_ms_per_step"])
+    roof = dict(rl.get(dom, {}))
+    roof["kernel"] = dom
+    work = roof.pop("work_per_launch", None)
+
+    line = {
+        "metric": "simulated env-steps/sec on 1 MI355X + % of HBM roofline (MLP: % MFMA peak)",
+        "value": value, "unit": "env-steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64 simulator + bf16 MLP (fp32 accumulate)" if w["mlp_bf16"] else "f64 simulator + f32 MLP",
+        "data": "synthetic (seeded workload generator; untrained Xavier policy)",
+        "config": {"workload": DESCR[args.config] if not args.ticks else DESCR[args.config] + f" [T={T}]",
+                   "envs": E, "ticks": T, "env_steps_per_step": E * T},
+        "roofline": roof,
+        "kernels": {k: dict(v, **{kk: vv for kk, vv in rl.get(k, {}).items()
+                                  if kk in ("achieved", "unit", "frac")}) for k, v in kern.items()},
+        "work_per_launch": work,
+        "totals": {"arrivals": int(tot["cnt"][0][0]), "dropped": int(tot["cnt"][0][2]),
+                   "dispatched": int(tot["cnt"][0][3]), "batches": int(tot["cnt"][0][4])},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, args.config, args.cpu_seconds, seed)
+    sim.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,239 @@
+/* batchsim.h -- C ABI of the MI355X (gfx950) batched serving-simulator rollout library.
+ *
+ * Paper: "Adaptive Inference Batching using Policy Gradients". The library steps many
+ * independent environments in lockstep. Each environment is the paper's discrete-event
+ * inference-serving simulator (Sec. 3.1): requests arrive (Sec. 3.2 workloads), wait in
+ * per-class FIFO queues capped at N with load shedding, and are dispatched in batches to
+ * K simulated servers whose batch latency is alpha + beta*b. The agent's MDP (Sec. 4.1)
+ * observes a state vector, chooses a (server, batch size) action and receives a reward of
+ * throughput minus weighted latency. The policy is an MLP (Sec. 4.2) and the rollout feeds
+ * discounted returns / GAE (Sec. 4.3).
+ *
+ * Conventions
+ *   - Every call returns an int status: SIM_OK (0) or a negative SIM_E* code. The message
+ *     of the last failure on the calling thread is returned by sim_last_error(); the
+ *     string is owned by the library. No call aborts or throws across the ABI.
+ *   - "d_" pointers are device pointers (HBM of the context's device), allocated and
+ *     owned by the caller; "h_" pointers are host pointers. The library owns the context
+ *     and the per-environment state it allocates in sim_create and frees in sim_destroy.
+ *   - All device work is enqueued on the stream given to sim_create and is asynchronous;
+ *     errors detected on the device (an action out of range, an event loop exceeding its
+ *     bound) are latched in a device flag and reported by sim_sync().
+ *   - Layouts are time-major, environment-minor: element (t, e) of a [T][E] array is at
+ *     t*E + e; feature f of environment e in an [F][E] observation is at f*E + e.
+ *   - Times are fp64 seconds; rates are requests per second.
+ *   - Randomness is a counter-based Philox4x32-10 stream keyed by the seed, with counter
+ *     (env, step, purpose<<24 | j, system); the same seed gives the same rollout.
+ */
+#ifndef BATCHSIM_H
+#define BATCHSIM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BATCHSIM_ABI_VERSION 1u
+
+enum sim_status {
+  SIM_OK = 0,
+  SIM_EINVAL = -1,       /* invalid argument or configuration */
+  SIM_ENOMEM = -2,       /* device allocation failed */
+  SIM_EDEVICE = -3,      /* a HIP runtime call failed */
+  SIM_ESTATE = -4,       /* call out of order, or a latched device-side error */
+  SIM_EUNSUPPORTED = -5  /* configuration outside the compiled shapes */
+};
+
+enum { SIM_ARR_MODULATED = 0, SIM_ARR_TRACE = 1 };
+enum { SIM_DWELL_INF = 0, SIM_DWELL_EXP = 1, SIM_DWELL_PARETO = 2 };
+enum { SIM_SVC_DET = 0, SIM_SVC_LOGN = 1, SIM_SVC_EXP = 2 };
+
+#define SIM_MAX_SERVERS 16
+#define SIM_MAX_CLASSES 4
+#define SIM_MAX_STATES 4
+#define SIM_MAX_QUEUE 255
+
+/* Simulator and policy configuration (plain data, copied by sim_create).
+ *  n_envs          environments stepped in lockstep (E >= 1)
+ *  n_servers       K simulated servers per environment (1..16); actions are 6K (Sec. 4.1)
+ *  n_classes       request classes / model types (1..4) (Sec. 3.1 request model)
+ *  queue_cap       N, waiting requests per environment over all classes (Sec. 3.1, N=100)
+ *  obs_dim         F, observation width, at least the state layout's width
+ *  tick_s          decision interval (the agent acts once per tick)
+ *  arrival_kind    SIM_ARR_MODULATED (Poisson / MMPP / ON-OFF) or SIM_ARR_TRACE
+ *  n_states        states of the modulating process (1 = plain Poisson)
+ *  rate[i]         arrival rate in state i (0 = no arrivals)
+ *  dwell_kind[i]   law of the time spent in state i: INF, EXP(mean dwell_mean[i]) or
+ *                  PARETO(pareto_alpha[i], pareto_xm[i])
+ *  class_mix[c]    probability that an arrival is of class c
+ *  service_kind[c] DET: alpha + beta*n; LOGN: median*exp(sigma*Z) + beta*n;
+ *                  EXP: Exp with mean alpha + beta*n (Sec. 3.1 execution model)
+ *  w_thr, w_class  reward weights: w_thr * throughput - latency weighted by class
+ *                  (Sec. 4.1); reward_sum = 1 sums the weighted latencies, 0 averages them
+ *  obs_tw          time normaliser of ages in the observation (T_window of Sec. 4.1)
+ *  lambda_ref      rate normaliser of the arrival-rate features
+ *  shadow          1 runs a second system per environment on the same arrivals under the
+ *                  static rule "dispatch when static_bmax requests wait or the oldest has
+ *                  waited static_timeout" (Sec. 1), with its own reward and counters
+ *  mlp_h1, mlp_h2  hidden widths of the policy MLP; mlp_bf16 = 1 for bf16 weights and
+ *                  activations with fp32 accumulation, 0 for fp32 throughout
+ *  value_head      1 adds a value output column (Sec. 4.2 value head)
+ *  trace_max_len   per-environment capacity of the arrays given to sim_set_trace        */
+typedef struct sim_cfg {
+  uint32_t abi_version; /* BATCHSIM_ABI_VERSION */
+  uint32_t struct_size; /* sizeof(sim_cfg) */
+  int32_t n_envs, n_servers, n_classes, queue_cap, obs_dim;
+  double tick_s;
+  int32_t arrival_kind, n_states;
+  double rate[SIM_MAX_STATES];
+  int32_t dwell_kind[SIM_MAX_STATES];
+  double dwell_mean[SIM_MAX_STATES], pareto_alpha[SIM_MAX_STATES], pareto_xm[SIM_MAX_STATES];
+  double class_mix[SIM_MAX_CLASSES];
+  int32_t service_kind[SIM_MAX_CLASSES];
+  double svc_alpha[SIM_MAX_CLASSES], svc_beta[SIM_MAX_CLASSES], svc_median[SIM_MAX_CLASSES];
+  double svc_sigma;
+  double w_thr, w_class[SIM_MAX_CLASSES];
+  int32_t reward_sum;
+  double obs_tw, lambda_ref;
+  int32_t shadow;
+  double static_timeout;
+  int32_t static_bmax;
+  int32_t mlp_h1, mlp_h2, mlp_bf16, value_head;
+  int32_t trace_max_len;
+} sim_cfg;
+
+/* Byte offsets of the policy weights inside one caller-owned device buffer. Weights are
+ * [in][out] row-major; W1 is [F][H1], W2 [H1][H2], W3 [H2][A'] with A' = 6K + value_head.
+ * Matrices are fp32, or bf16 (raw 16-bit patterns) when mlp_bf16 = 1; biases are fp32.  */
+typedef struct sim_wlayout {
+  size_t w1, b1, w2, b2, w3, b3; /* offsets in bytes, 256-byte aligned */
+  size_t bytes;                  /* total size of the buffer */
+  int32_t n_out;                 /* A' */
+  int32_t elem_bytes;            /* 4 (fp32) or 2 (bf16) */
+} sim_wlayout;
+
+/* Caller-owned device buffers filled by sim_rollout. Only `actions` is required; any
+ * other pointer may be NULL to skip that output.                                       */
+typedef struct sim_traj {
+  uint8_t* actions;       /* [T][E] sampled actions */
+  float* logp;            /* [T][E] log-probability of the sampled action */
+  double* reward;         /* [T][E] learned system's reward r_k */
+  double* reward_shadow;  /* [T][E] static shadow system's reward (cfg.shadow = 1) */
+  float* value;           /* [T+1][E] value head (cfg.value_head = 1); row T is V(obs_T) */
+  float* obs;             /* [T+1][F][E] observations obs_k, k = 0..T */
+  uint64_t* rchk;         /* [T][E] learned system's running checksum after each tick */
+} sim_traj;
+
+/* Per-environment integer counters and sums, system s in {0 learned, 1 shadow}. */
+#define SIM_NCNT 7 /* arrivals, accepted, dropped, dispatched, batches, completed, inflight */
+#define SIM_NSUM 2 /* latency sum, weighted latency sum (seconds) */
+
+typedef struct sim_totals {
+  int64_t cnt[2][SIM_NCNT]; /* summed over environments */
+  double sum[2][SIM_NSUM];
+} sim_totals;
+
+typedef struct sim_ctx sim_ctx;
+
+/* Message of the last failed call on this thread (library-owned, never NULL). */
+const char* sim_last_error(void);
+
+/* Library ABI version (BATCHSIM_ABI_VERSION). */
+uint32_t sim_abi_version(void);
+
+/* Creates a context on the current HIP device: validates cfg (SIM_EINVAL with a message
+ * naming the field), allocates the structure-of-arrays environment state and queues in
+ * HBM (SIM_ENOMEM). `hip_stream` is a hipStream_t (NULL = default stream). The context is
+ * not usable until sim_reset. On failure *out is NULL and nothing stays allocated.     */
+int sim_create(const sim_cfg* cfg, void* hip_stream, sim_ctx** out);
+
+/* Waits for the context's stream and frees everything it owns. NULL is allowed.        */
+int sim_destroy(sim_ctx* ctx);
+
+/* Explicit arrivals for SIM_ARR_TRACE (Sec. 3.2 trace replay): device arrays times
+ * [E][trace_max_len] (nondecreasing seconds), classes [E][trace_max_len], counts [E].
+ * The arrays must stay valid until the context is destroyed or given new ones.        */
+int sim_set_trace(sim_ctx* ctx, const double* d_times, const uint8_t* d_classes,
+                  const int32_t* d_counts);
+
+/* Resets every environment at t = 0 (empty queues, idle servers, zero counters, the
+ * modulating state drawn from its stationary law) and sets the tick counter to 0.      */
+int sim_reset(sim_ctx* ctx, uint64_t seed);
+
+/* Copies the current observation [F][E] fp32 (the state of Sec. 4.1) to d_obs.         */
+int sim_obs(sim_ctx* ctx, float* d_obs);
+
+/* Advances every environment by one tick under the given actions (d_actions [E], values
+ * in [0, 6K): server a/6, batch size 2^(a%6)). Optional outputs: the next observation
+ * [F][E], the learned and shadow rewards [E]. An action out of range latches SIM_ESTATE.*/
+int sim_step(sim_ctx* ctx, const uint8_t* d_actions, float* d_obs_next, double* d_reward,
+             double* d_reward_shadow);
+
+/* Current tick index (number of ticks since the last reset). */
+int sim_tick(sim_ctx* ctx, int32_t* h_tick);
+
+/* Layout of the weights buffer for this configuration (no device work).                */
+int sim_weights_layout(const sim_cfg* cfg, sim_wlayout* out);
+
+/* Writes Xavier-uniform weights drawn from `seed` and zero biases into d_weights
+ * (layout of sim_weights_layout).                                                      */
+int sim_init_weights(sim_ctx* ctx, uint64_t seed, void* d_weights);
+
+/* Policy on one batch of observations d_obs [F][E]: MLP forward, then an action sampled
+ * from the softmax of the logits with the ACTION uniform of (env, step). Outputs (any may
+ * be NULL): d_act [E], d_logp [E], d_value [E] (value head), d_logits [A'][E] fp32.     */
+int sim_policy(sim_ctx* ctx, const void* d_weights, const float* d_obs, uint32_t step,
+               uint8_t* d_act, float* d_logp, float* d_value, float* d_logits);
+
+/* T ticks of policy + simulator from the current state (obs_k -> a_k -> obs_{k+1}),
+ * writing the trajectory; with a value head, row T of traj->value holds V(obs_T).       */
+int sim_rollout(sim_ctx* ctx, const void* d_weights, int32_t T, const sim_traj* traj);
+
+/* Discounted returns and GAE (Sec. 4.3), per environment backwards in t:
+ *   delta_t = (r_t + gamma V_{t+1}) - V_t,  A_t = delta_t + (gamma*lambda) A_{t+1},
+ *   A_T = 0,  R_t = A_t + V_t.
+ * d_r [T][E] fp64; d_v [T+1][E] fp32 or NULL for V = 0 (with lambda = 1 this is the
+ * REINFORCE return). Writes d_adv and d_ret [T][E] fp64.                                */
+int returns_gae(sim_ctx* ctx, int32_t T, const double* d_r, const float* d_v, double gamma,
+                double lambda, double* d_adv, double* d_ret);
+
+/* Per-environment counters [2][SIM_NCNT][E] int64 and sums [2][SIM_NSUM][E] fp64 into
+ * device buffers (either may be NULL).                                                  */
+int sim_counters(sim_ctx* ctx, int64_t* d_cnt, double* d_sum);
+
+/* Per-environment integer-state checksums [2][E] (learned, shadow) into d_chk.          */
+int sim_checksums(sim_ctx* ctx, uint64_t* d_chk);
+
+/* Totals of the counters over all environments, reduced on the device, into h_out.
+ * Synchronises the stream.                                                              */
+int sim_stats(sim_ctx* ctx, sim_totals* h_out);
+
+/* Waits for the stream; returns SIM_ESTATE if a device-side error was latched (and
+ * clears it), with the reason in sim_last_error().                                     */
+int sim_sync(sim_ctx* ctx);
+
+/* Kernel classes for tracing. */
+enum sim_kernel_class {
+  SIM_KC_POLICY = 0,  /* policy MLP + sampler */
+  SIM_KC_STEP = 1,    /* learned system, one tick */
+  SIM_KC_STATIC = 2,  /* static shadow system, one tick */
+  SIM_KC_GAE = 3,     /* returns / GAE */
+  SIM_KC_RESET = 4,   /* reset */
+  SIM_KC_OTHER = 5,   /* weight repack / init, counters, totals */
+  SIM_KC_COUNT = 6
+};
+
+/* Tracing: with `on` != 0 every kernel launch of the context is bracketed by a pair of
+ * HIP events recorded on the context's stream. sim_get_timing synchronises the stream
+ * and adds the elapsed time of every completed pair to per-class totals, then writes the
+ * totals (milliseconds) and launch counts to h_ms[SIM_KC_COUNT] and
+ * h_launches[SIM_KC_COUNT]; `clear` != 0 zeroes the totals afterwards.               */
+int sim_set_timing(sim_ctx* ctx, int32_t on);
+int sim_get_timing(sim_ctx* ctx, double* h_ms, int64_t* h_launches, int32_t clear);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BATCHSIM_H */

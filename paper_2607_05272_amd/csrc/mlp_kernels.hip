@@ -1,0 +1,312 @@
+// mlp_kernels.hip -- policy MLP (paper Sec. 4.2) on MFMA, fused with action sampling.
+//
+// obs [F][E] -> h1 = GELU(x W1 + b1) -> h2 = GELU(h1 W2 + b2) -> out = h2 W3 + b3, where
+// out[0..A) are the logits of the categorical action distribution and out[A] (when the
+// value head is on) is V(s). In bf16 mode each layer's input is rounded to bf16 (RNE) and
+// multiplied by bf16 weights with fp32 accumulation (v_mfma_f32_16x16x32_bf16); bias and
+// GELU are fp32. In fp32 mode the products use v_mfma_f32_16x16x4_f32.
+//
+// One workgroup (4 waves) owns 64 environments. Activations of its 64 rows live in LDS
+// (x, then h1, then h2); each wave produces a quarter of the output columns of every layer
+// for all 64 rows, reading weight fragments (16 bytes per lane in bf16 mode) straight from
+// the repacked out-major weights, which stay resident in L2. The epilogue of the last
+// layer samples the action by inverse CDF of the fp32 softmax with the ACTION uniform of
+// (env, step) and writes action, log-probability and value.
+#include "devmath.hpp"
+#include "params.hpp"
+
+namespace bsim {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+constexpr int kRows = 64;      // environments per workgroup
+constexpr int kThreads = 256;  // 4 waves
+
+struct Bf16Mode {
+  typedef uint16_t elem;
+  typedef bf16x8 frag;
+  static constexpr int KS = 32;   // K per MFMA
+  static constexpr int KL = 8;    // K elements per lane
+  static constexpr int PAD = 8;   // LDS row padding (elements)
+  __device__ static frag load(const elem* p) { return *reinterpret_cast<const frag*>(p); }
+  __device__ static f32x4 mfma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static elem from_f32(float f) { return bf16_bits(f); }
+};
+
+struct F32Mode {
+  typedef float elem;
+  typedef float frag;
+  static constexpr int KS = 4;
+  static constexpr int KL = 1;
+  static constexpr int PAD = 4;
+  __device__ static frag load(const elem* p) { return *p; }
+  __device__ static f32x4 mfma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static elem from_f32(float f) { return f; }
+};
+
+__device__ __forceinline__ float gelu(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
+
+// out[64][N] = act_in[64][K] * W^T  (W packed out-major [N][K]); epilogue: +bias, then
+// GELU + rounding into act_out (hidden layers) or fp32 into lg (last layer).
+template <class M, int K, int N, bool LAST>
+__device__ __forceinline__ void layer(const typename M::elem* __restrict__ in,
+                                      const typename M::elem* __restrict__ W,
+                                      const float* __restrict__ bias,
+                                      typename M::elem* __restrict__ out, float* __restrict__ lg,
+                                      int lg_stride) {
+  constexpr int NT = N / 16;             // column tiles
+  constexpr int NTW = (NT + 3) / 4;      // column tiles per wave
+  constexpr int SIN = K + M::PAD;        // LDS row stride of the input
+  constexpr int SOUT = N + M::PAD;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kq = lane >> 4;
+  f32x4 acc[4][NTW];
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+    for (int c = 0; c < NTW; ++c) acc[rt][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+  for (int kb = 0; kb < K; kb += M::KS) {
+    typename M::frag bfr[NTW];
+#pragma unroll
+    for (int c = 0; c < NTW; ++c) {
+      const int ct = wave + 4 * c;
+      if (ct < NT) bfr[c] = M::load(W + (size_t)(ct * 16 + r16) * K + kb + kq * M::KL);
+    }
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      const typename M::frag a = M::load(in + (rt * 16 + r16) * SIN + kb + kq * M::KL);
+#pragma unroll
+      for (int c = 0; c < NTW; ++c)
+        if (wave + 4 * c < NT) acc[rt][c] = M::mfma(a, bfr[c], acc[rt][c]);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < NTW; ++c) {
+    const int ct = wave + 4 * c;
+    if (ct >= NT) continue;
+    const int col = ct * 16 + r16;
+    const float bv = bias[col];
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = rt * 16 + kq * 4 + i;
+        const float v = acc[rt][c][i] + bv;
+        if (LAST) lg[row * lg_stride + col] = v;
+        else out[row * SOUT + col] = M::from_f32(gelu(v));
+      }
+    }
+  }
+}
+
+template <class M, int FP, int H1, int H2, int AP>
+struct Shape {
+  typedef typename M::elem E;
+  static constexpr int SX = FP + M::PAD, S1 = H1 + M::PAD, S2 = H2 + M::PAD, SL = AP + 1;
+  static constexpr size_t X_BYTES = (size_t)kRows * SX * sizeof(E);
+  static constexpr size_t H1_BYTES = (size_t)kRows * S1 * sizeof(E);
+  static constexpr size_t H2_BYTES = (size_t)kRows * S2 * sizeof(E);
+  static constexpr size_t L_BYTES = (size_t)kRows * SL * sizeof(float);
+  // x shares the h2 region (dead before h2 is written), logits share the h1 region
+  static constexpr size_t REGION_A = H2_BYTES > X_BYTES ? H2_BYTES : X_BYTES;
+  static constexpr size_t REGION_B = H1_BYTES > L_BYTES ? H1_BYTES : L_BYTES;
+  static constexpr size_t LDS = REGION_A + REGION_B;
+};
+
+template <class M, int FP, int H1, int H2, int AP>
+__global__ __launch_bounds__(kThreads) void policy_k(MlpParams m, const float* __restrict__ obs,
+                                                     uint64_t seed, uint32_t step,
+                                                     uint8_t* __restrict__ act,
+                                                     float* __restrict__ logp,
+                                                     float* __restrict__ value,
+                                                     float* __restrict__ logits) {
+  typedef Shape<M, FP, H1, H2, AP> Sh;
+  typedef typename M::elem E;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  E* xs = reinterpret_cast<E*>(smem);
+  E* h2s = reinterpret_cast<E*>(smem);
+  E* h1s = reinterpret_cast<E*>(smem + Sh::REGION_A);
+  float* lg = reinterpret_cast<float*>(smem + Sh::REGION_A);
+  const int e0 = blockIdx.x * kRows;
+  const int tid = threadIdx.x;
+  // stage x: obs [F][E] fp32 -> rows of the tile, rounded to the layer's input type
+  for (int idx = tid; idx < kRows * FP; idx += kThreads) {
+    const int r = idx % kRows, f = idx / kRows;
+    const int e = e0 + r;
+    float v = 0.f;
+    if (f < m.F && e < m.E) v = obs[(size_t)f * m.E + e];
+    xs[r * Sh::SX + f] = M::from_f32(v);
+  }
+  __syncthreads();
+  layer<M, FP, H1, false>(xs, static_cast<const E*>(m.w1), m.b1, h1s, nullptr, 0);
+  __syncthreads();
+  layer<M, H1, H2, false>(h1s, static_cast<const E*>(m.w2), m.b2, h2s, nullptr, 0);
+  __syncthreads();
+  layer<M, H2, AP, true>(h2s, static_cast<const E*>(m.w3), m.b3, nullptr, lg, Sh::SL);
+  __syncthreads();
+  // sampling epilogue: one lane per environment row
+  if (tid < kRows) {
+    const int e = e0 + tid;
+    if (e < m.E) {
+      const float* l = lg + tid * Sh::SL;
+      const int A = m.A;
+      if (act || logp) {
+        float mx = l[0];
+        for (int i = 1; i < A; ++i) mx = l[i] > mx ? l[i] : mx;
+        float S = 0.f;
+        for (int i = 0; i < A; ++i) S += expf(l[i] - mx);
+        const u32x4 w = draw(seed, (uint32_t)e, step, P_ACTION, 0, 0);
+        const float u = ((float)(w.x >> 9) + 0.5f) * 0x1p-23f;
+        const float target = u * S;
+        float cum = 0.f;
+        int a = A - 1;
+        for (int i = 0; i < A; ++i) {
+          cum += expf(l[i] - mx);
+          if (target < cum) { a = i; break; }
+        }
+        if (act) act[e] = (uint8_t)a;
+        if (logp) logp[e] = (l[a] - mx) - logf(S);
+      }
+      if (value && m.value_head) value[e] = l[A];
+      if (logits)
+        for (int i = 0; i < m.Ap; ++i) logits[(size_t)i * m.E + e] = l[i];
+    }
+  }
+}
+
+// packed weights: W^T [Npad][Kpad] in the compute type, zero padded; bias fp32 [Npad]
+template <typename T>
+__global__ void repack_k(const unsigned char* __restrict__ src, size_t woff, size_t boff, int K,
+                         int N, int Kp, int Np, T* __restrict__ w, float* __restrict__ b) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t total = (size_t)Np * Kp;
+  if (idx < total) {
+    const int n = (int)(idx / Kp), k = (int)(idx % Kp);
+    T v = T(0);
+    if (n < N && k < K) v = reinterpret_cast<const T*>(src + woff)[(size_t)k * N + n];
+    w[idx] = v;
+  }
+  if (idx < (size_t)Np) {
+    const int n = (int)idx;
+    b[n] = n < N ? reinterpret_cast<const float*>(src + boff)[n] : 0.f;
+  }
+}
+
+// Xavier-uniform: element i of layer l takes u from the WEIGHTS block at counter
+// (i, 0xFFFFFFFE, WEIGHTS<<24 | l, 0); w = (2u - 1) * lim in fp64, then fp32 (then bf16).
+__global__ void init_w_k(uint64_t seed, int layer, size_t n, double lim, int bf16,
+                         unsigned char* __restrict__ dst) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const u32x4 w = draw(seed, (uint32_t)i, 0xFFFFFFFEu, P_WEIGHTS, (uint32_t)layer, 0);
+  const double u = unit(w.x, w.y);
+  const float f = (float)((2.0 * u - 1.0) * lim);
+  if (bf16) reinterpret_cast<uint16_t*>(dst)[i] = bf16_bits(f);
+  else reinterpret_cast<float*>(dst)[i] = f;
+}
+
+__global__ void zero_f32_k(float* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0.f;
+}
+
+template <class M, int FP, int H1, int H2, int AP>
+hipError_t run_policy(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
+                      uint8_t* act, float* logp, float* value, float* logits, hipStream_t st) {
+  typedef Shape<M, FP, H1, H2, AP> Sh;
+  auto kern = policy_k<M, FP, H1, H2, AP>;
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)Sh::LDS);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const dim3 grid((m.E + kRows - 1) / kRows), block(kThreads);
+  hipLaunchKernelGGL(kern, grid, block, Sh::LDS, st, m, obs, seed, step, act, logp, value, logits);
+  return hipGetLastError();
+}
+
+struct ShapeKey { int bf16, FP, H1, H2, AP; };
+constexpr ShapeKey kShapes[] = {
+    {0, 8, 64, 64, 16},      // 8-64-64-6 fp32
+    {1, 32, 128, 128, 16},   // 12-128-128-6 bf16
+    {1, 32, 256, 256, 32},   // 32-256-256-24(+1) bf16
+    {1, 64, 256, 256, 64},   // 64-256-256-48(+1) bf16
+    {1, 96, 512, 512, 112},  // 96-512-512-96(+1) bf16
+};
+
+}  // namespace
+
+static int pad_up(int x, int m) { return (x + m - 1) / m * m; }
+
+bool policy_shape_supported(const MlpParams& m) {
+  for (const ShapeKey& s : kShapes)
+    if (s.bf16 == m.bf16 && s.FP == m.FP && s.H1 == m.H1 && s.H2 == m.H2 && s.AP == m.AP)
+      return true;
+  return false;
+}
+
+hipError_t launch_policy(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
+                         uint8_t* act, float* logp, float* value, float* logits, hipStream_t st) {
+  if (!m.bf16 && m.FP == 8 && m.H1 == 64 && m.H2 == 64 && m.AP == 16)
+    return run_policy<F32Mode, 8, 64, 64, 16>(m, obs, seed, step, act, logp, value, logits, st);
+  if (m.bf16 && m.FP == 32 && m.H1 == 128 && m.H2 == 128 && m.AP == 16)
+    return run_policy<Bf16Mode, 32, 128, 128, 16>(m, obs, seed, step, act, logp, value, logits, st);
+  if (m.bf16 && m.FP == 32 && m.H1 == 256 && m.H2 == 256 && m.AP == 32)
+    return run_policy<Bf16Mode, 32, 256, 256, 32>(m, obs, seed, step, act, logp, value, logits, st);
+  if (m.bf16 && m.FP == 64 && m.H1 == 256 && m.H2 == 256 && m.AP == 64)
+    return run_policy<Bf16Mode, 64, 256, 256, 64>(m, obs, seed, step, act, logp, value, logits, st);
+  if (m.bf16 && m.FP == 96 && m.H1 == 512 && m.H2 == 512 && m.AP == 112)
+    return run_policy<Bf16Mode, 96, 512, 512, 112>(m, obs, seed, step, act, logp, value, logits, st);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_repack(const MlpParams& m, const void* d_weights, const size_t off[6],
+                         void* w1, float* b1, void* w2, float* b2, void* w3, float* b3,
+                         hipStream_t st) {
+  const unsigned char* src = static_cast<const unsigned char*>(d_weights);
+  const int Ks[3] = {m.F, m.H1, m.H2}, Ns[3] = {m.H1, m.H2, m.Ap};
+  const int Kp[3] = {m.FP, m.H1, m.H2}, Np[3] = {m.H1, m.H2, m.AP};
+  void* ws[3] = {w1, w2, w3};
+  float* bs[3] = {b1, b2, b3};
+  for (int l = 0; l < 3; ++l) {
+    const size_t total = (size_t)Np[l] * Kp[l];
+    const dim3 grid((unsigned)((total + 255) / 256));
+    if (m.bf16)
+      hipLaunchKernelGGL(repack_k<uint16_t>, grid, dim3(256), 0, st, src, off[2 * l], off[2 * l + 1],
+                         Ks[l], Ns[l], Kp[l], Np[l], static_cast<uint16_t*>(ws[l]), bs[l]);
+    else
+      hipLaunchKernelGGL(repack_k<float>, grid, dim3(256), 0, st, src, off[2 * l], off[2 * l + 1],
+                         Ks[l], Ns[l], Kp[l], Np[l], static_cast<float*>(ws[l]), bs[l]);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_init_weights(int F, int H1, int H2, int Ap, int bf16, uint64_t seed,
+                               void* d_weights, const size_t off[6], hipStream_t st) {
+  unsigned char* dst = static_cast<unsigned char*>(d_weights);
+  const int dims[4] = {F, H1, H2, Ap};
+  for (int l = 0; l < 3; ++l) {
+    const size_t n = (size_t)dims[l] * dims[l + 1];
+    const double lim = sqrt(6.0 / (double)(dims[l] + dims[l + 1]));
+    hipLaunchKernelGGL(init_w_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, seed, l, n,
+                       lim, bf16, dst + off[2 * l]);
+    hipLaunchKernelGGL(zero_f32_k, dim3((dims[l + 1] + 255) / 256), dim3(256), 0, st,
+                       reinterpret_cast<float*>(dst + off[2 * l + 1]), dims[l + 1]);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace bsim

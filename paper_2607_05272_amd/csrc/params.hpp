@@ -1,0 +1,93 @@
+// params.hpp -- kernel parameter blocks and launch entry points shared by the runtime
+// (runtime.hip) and the kernel translation units of this library.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace bsim {
+
+constexpr int kMaxK = 16, kMaxC = 4, kMaxS = 4;
+constexpr int kNcnt = 6;                 // arrivals, accepted, dropped, dispatched, batches, completed
+constexpr uint32_t kMaxEventsPerTick = 1u << 16;
+enum : uint32_t { ERR_ACTION = 1u, ERR_EVENTS = 2u, ERR_TRACE = 4u };
+
+// Simulator constants, all derived on the host once per context.
+struct SimParams {
+  int E, K, C, N, F, S;
+  int arrival_kind, shadow, bmax, reward_sum;
+  double dt;
+  double rate[kMaxS], mean_gap[kMaxS], dwell_mean[kMaxS], inv_alpha[kMaxS], xm[kMaxS];
+  int dwell_kind[kMaxS];
+  double stat_cum[kMaxS], class_cum[kMaxC];
+  int svc_kind[kMaxC];
+  double svc_alpha[kMaxC], svc_beta[kMaxC], svc_median[kMaxC], svc_sigma;
+  double w_thr, w_class[kMaxC];
+  double inv_n, inv_tw, inv_c, inv_rs;   // observation normalisers (reciprocals)
+  double static_timeout;
+  const double* tr_times;
+  const uint8_t* tr_cls;
+  const int32_t* tr_cnt;
+  int tr_len;
+};
+
+// Structure-of-arrays state of one queueing system; each array is [field][E]. Each system
+// carries its own copy of the arrival process: its draws do not depend on the system, so
+// both copies follow the same arrivals.
+struct SysState {
+  uint32_t* qpack;   // [E]     Q_c in byte c
+  uint32_t* hpack;   // [E]     ring head of class c in byte c
+  double* hts;       // [C][E]  arrival time of the head request of class c
+  double* busy;      // [K][E]  busy-until time of server j
+  uint32_t* meta;    // [K][E]  inflight | last_b << 8 | last_class << 16 (0xFF = none)
+  uint32_t* cnt;     // [6][E]  arrivals, accepted, dropped, dispatched, batches, completed
+  double* sums;      // [2][E]  latency sum, weighted latency sum
+  uint64_t* chk;     // [E]     checksum of the integer-state sequence
+  double* ring;      // [E][C][N] arrival timestamps (per-class FIFO rings)
+  uint32_t* proc;    // [E]     modulating state of the arrival process
+  double* next_sw;   // [E]     next modulating-state switch
+  double* next_arr;  // [E]     next arrival
+  uint32_t* tr_idx;  // [E]     next trace arrival index
+};
+
+struct EnvState {
+  SysState sys[2];   // 0 learned, 1 static shadow
+  double* ewma;      // [4][E] exponentially weighted arrival counts (learned system)
+  float* obs;        // [F][E] current observation
+  uint32_t* err;     // [1] latched error flags
+};
+
+// Kernel launchers (asynchronous on `st`); each returns the launch's hipError_t.
+hipError_t launch_reset(const SimParams& p, const EnvState& s, uint64_t seed, hipStream_t st);
+hipError_t launch_step(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
+                       const uint8_t* act, float* obs_out, double* rew, uint64_t* rchk,
+                       hipStream_t st);
+hipError_t launch_static(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
+                         double* rew_sh, hipStream_t st);
+hipError_t launch_counters(const SimParams& p, const EnvState& s, int64_t* cnt, double* sums,
+                           hipStream_t st);
+hipError_t launch_totals(const SimParams& p, const EnvState& s, int64_t* d_tot_cnt,
+                         double* d_tot_sum, hipStream_t st);
+hipError_t launch_gae(int T, int E, const double* r, const float* v, double gamma, double lam,
+                      double* adv, double* ret, hipStream_t st);
+
+// Policy network shapes and packed weights (MFMA-friendly, out-major, zero padded).
+struct MlpParams {
+  int E, F, H1, H2, A, Ap;      // A = 6K actions, Ap = A + value_head
+  int bf16, value_head;
+  int FP, AP;                   // padded input width and padded output width
+  const void* w1; const float* b1;   // packed [H1][FP]
+  const void* w2; const float* b2;   // packed [H2][H1]
+  const void* w3; const float* b3;   // packed [AP][H2]
+};
+hipError_t launch_repack(const MlpParams& m, const void* d_weights, const size_t off[6],
+                         void* w1, float* b1, void* w2, float* b2, void* w3, float* b3,
+                         hipStream_t st);
+hipError_t launch_policy(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
+                         uint8_t* act, float* logp, float* value, float* logits,
+                         hipStream_t st);
+hipError_t launch_init_weights(int F, int H1, int H2, int Ap, int bf16, uint64_t seed,
+                               void* d_weights, const size_t off[6], hipStream_t st);
+bool policy_shape_supported(const MlpParams& m);
+
+}  // namespace bsim

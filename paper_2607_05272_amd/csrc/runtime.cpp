@@ -1,0 +1,580 @@
+// runtime.cpp -- host runtime behind the C ABI of include/batchsim.h: configuration
+// validation, derived constants, structure-of-arrays allocation in HBM, and the ordering
+// of kernel launches on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/batchsim.h"
+#include "params.hpp"
+
+using namespace bsim;
+
+namespace {
+
+thread_local std::string g_err = "no error";
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(SIM_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIPCHK(call, what)                        \
+  do {                                            \
+    hipError_t e_ = (call);                       \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int obs_width(const sim_cfg& c) {
+  return 2 + c.n_servers * (c.n_servers > 1 ? 4 : 2) + (c.n_classes > 1 ? 2 * c.n_classes : 0) + 4;
+}
+
+int pad_to(int x, int m) { return (x + m - 1) / m * m; }
+
+}  // namespace
+
+struct sim_ctx {
+  sim_cfg cfg;
+  hipStream_t stream = nullptr;
+  int device = 0;
+  SimParams p{};
+  EnvState s{};
+  MlpParams m{};
+  void* arena = nullptr;   // all environment state
+  size_t arena_bytes = 0;
+  void* wpack = nullptr;   // repacked policy weights
+  int64_t* d_tot_cnt = nullptr;
+  double* d_tot_sum = nullptr;
+  uint32_t tick = 0;
+  uint64_t seed = 0;
+  bool reset_done = false;
+  bool trace_set = false;
+  // tracing: event pairs around kernel launches, per kernel class
+  struct Pending { int cls; hipEvent_t a, b; };
+  bool timing = false;
+  std::vector<hipEvent_t> pool;
+  std::vector<Pending> pending;
+  double ms[SIM_KC_COUNT] = {};
+  int64_t launches[SIM_KC_COUNT] = {};
+
+  hipError_t event(hipEvent_t* ev) {
+    if (!pool.empty()) {
+      *ev = pool.back();
+      pool.pop_back();
+      return hipSuccess;
+    }
+    return hipEventCreate(ev);
+  }
+  // runs `launch` (which enqueues one kernel on `stream`), bracketed by events if tracing
+  template <class F>
+  hipError_t timed(int cls, F launch) {
+    if (!timing) return launch();
+    hipEvent_t a, b;
+    hipError_t e = event(&a);
+    if (e != hipSuccess) return e;
+    e = event(&b);
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(a, stream);
+    if (e != hipSuccess) return e;
+    e = launch();
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(b, stream);
+    if (e != hipSuccess) return e;
+    pending.push_back({cls, a, b});
+    return hipSuccess;
+  }
+};
+
+extern "C" {
+
+const char* sim_last_error(void) { return g_err.c_str(); }
+
+uint32_t sim_abi_version(void) { return BATCHSIM_ABI_VERSION; }
+
+static int validate(const sim_cfg* c) {
+  if (!c) return fail(SIM_EINVAL, "cfg is NULL");
+  if (c->abi_version != BATCHSIM_ABI_VERSION)
+    return fail(SIM_EINVAL, "abi_version %u, library is %u", c->abi_version, BATCHSIM_ABI_VERSION);
+  if (c->struct_size != sizeof(sim_cfg))
+    return fail(SIM_EINVAL, "struct_size %u, expected %zu", c->struct_size, sizeof(sim_cfg));
+  if (c->n_envs < 1) return fail(SIM_EINVAL, "n_envs must be >= 1");
+  if (c->n_servers < 1 || c->n_servers > SIM_MAX_SERVERS)
+    return fail(SIM_EINVAL, "n_servers must be in 1..%d", SIM_MAX_SERVERS);
+  if (6 * c->n_servers > 255) return fail(SIM_EINVAL, "6*n_servers must fit a uint8 action");
+  if (c->n_classes < 1 || c->n_classes > SIM_MAX_CLASSES)
+    return fail(SIM_EINVAL, "n_classes must be in 1..%d", SIM_MAX_CLASSES);
+  if (c->queue_cap < 1 || c->queue_cap > SIM_MAX_QUEUE)
+    return fail(SIM_EINVAL, "queue_cap must be in 1..%d", SIM_MAX_QUEUE);
+  if (c->obs_dim < obs_width(*c))
+    return fail(SIM_EINVAL, "obs_dim %d is below the state width %d", c->obs_dim, obs_width(*c));
+  if (!(c->tick_s > 0.0)) return fail(SIM_EINVAL, "tick_s must be > 0");
+  if (c->arrival_kind != SIM_ARR_MODULATED && c->arrival_kind != SIM_ARR_TRACE)
+    return fail(SIM_EINVAL, "arrival_kind");
+  if (c->n_states < 1 || c->n_states > SIM_MAX_STATES)
+    return fail(SIM_EINVAL, "n_states must be in 1..%d", SIM_MAX_STATES);
+  if (c->arrival_kind == SIM_ARR_MODULATED) {
+    for (int i = 0; i < c->n_states; ++i) {
+      if (!(c->rate[i] >= 0.0)) return fail(SIM_EINVAL, "rate[%d] must be >= 0", i);
+      const int k = c->dwell_kind[i];
+      if (k < 0 || k > 2) return fail(SIM_EINVAL, "dwell_kind[%d]", i);
+      if (c->n_states > 1 && k == SIM_DWELL_INF)
+        return fail(SIM_EINVAL, "dwell_kind[%d] must be finite with several states", i);
+      if (k == SIM_DWELL_EXP && !(c->dwell_mean[i] > 0.0))
+        return fail(SIM_EINVAL, "dwell_mean[%d] must be > 0", i);
+      if (k == SIM_DWELL_PARETO && (!(c->pareto_alpha[i] > 1.0) || !(c->pareto_xm[i] > 0.0)))
+        return fail(SIM_EINVAL, "pareto_alpha[%d] must be > 1 and pareto_xm > 0", i);
+    }
+  } else if (c->trace_max_len < 1) {
+    return fail(SIM_EINVAL, "trace_max_len must be >= 1 for trace arrivals");
+  }
+  double mix = 0.0;
+  for (int i = 0; i < c->n_classes; ++i) {
+    if (!(c->class_mix[i] >= 0.0)) return fail(SIM_EINVAL, "class_mix[%d] must be >= 0", i);
+    mix += c->class_mix[i];
+    const int k = c->service_kind[i];
+    if (k < 0 || k > 2) return fail(SIM_EINVAL, "service_kind[%d]", i);
+    if (!(c->svc_beta[i] >= 0.0) || !(c->svc_alpha[i] >= 0.0))
+      return fail(SIM_EINVAL, "svc_alpha/svc_beta[%d] must be >= 0", i);
+    if (k == SIM_SVC_LOGN && !(c->svc_median[i] > 0.0))
+      return fail(SIM_EINVAL, "svc_median[%d] must be > 0", i);
+    if (k == SIM_SVC_DET && !(c->svc_alpha[i] + c->svc_beta[i] > 0.0))
+      return fail(SIM_EINVAL, "deterministic service of class %d must be > 0", i);
+  }
+  if (std::fabs(mix - 1.0) > 1e-9) return fail(SIM_EINVAL, "class_mix must sum to 1");
+  if (!(c->obs_tw > 0.0) || !(c->lambda_ref > 0.0))
+    return fail(SIM_EINVAL, "obs_tw and lambda_ref must be > 0");
+  if (c->shadow && (c->static_bmax < 1 || c->static_bmax > 255 || !(c->static_timeout >= 0.0)))
+    return fail(SIM_EINVAL, "static rule needs 1 <= static_bmax <= 255, static_timeout >= 0");
+  return SIM_OK;
+}
+
+static void derive(sim_ctx* x) {
+  const sim_cfg& c = x->cfg;
+  SimParams& p = x->p;
+  p.E = c.n_envs; p.K = c.n_servers; p.C = c.n_classes; p.N = c.queue_cap;
+  p.F = c.obs_dim; p.S = c.arrival_kind == SIM_ARR_TRACE ? 1 : c.n_states;
+  p.arrival_kind = c.arrival_kind; p.shadow = c.shadow; p.bmax = c.static_bmax;
+  p.reward_sum = c.reward_sum; p.dt = c.tick_s;
+  double mdw[kMaxS], tot = 0.0;
+  for (int i = 0; i < kMaxS; ++i) {
+    const bool on = i < p.S;
+    p.rate[i] = on ? c.rate[i] : 0.0;
+    p.mean_gap[i] = on && c.rate[i] > 0.0 ? 1.0 / c.rate[i] : 0.0;
+    p.dwell_kind[i] = on ? c.dwell_kind[i] : 0;
+    p.dwell_mean[i] = on ? c.dwell_mean[i] : 0.0;
+    p.inv_alpha[i] = on && c.dwell_kind[i] == SIM_DWELL_PARETO ? 1.0 / c.pareto_alpha[i] : 0.0;
+    p.xm[i] = on ? c.pareto_xm[i] : 0.0;
+    if (on) {
+      // stationary time share of a state is proportional to its mean dwell
+      if (c.dwell_kind[i] == SIM_DWELL_EXP) mdw[i] = c.dwell_mean[i];
+      else if (c.dwell_kind[i] == SIM_DWELL_PARETO)
+        mdw[i] = c.pareto_alpha[i] * c.pareto_xm[i] / (c.pareto_alpha[i] - 1.0);
+      else mdw[i] = 1.0;
+      tot = tot + mdw[i];
+    }
+  }
+  double acc = 0.0;
+  for (int i = 0; i < kMaxS; ++i) {
+    if (i < p.S) { acc = acc + mdw[i]; p.stat_cum[i] = acc / tot; }
+    else p.stat_cum[i] = 1.0;
+  }
+  p.stat_cum[p.S - 1] = 1.0;
+  acc = 0.0;
+  for (int i = 0; i < kMaxC; ++i) {
+    const bool on = i < p.C;
+    if (on) { acc = acc + c.class_mix[i]; p.class_cum[i] = acc; }
+    else p.class_cum[i] = 1.0;
+    p.svc_kind[i] = on ? c.service_kind[i] : 0;
+    p.svc_alpha[i] = on ? c.svc_alpha[i] : 0.0;
+    p.svc_beta[i] = on ? c.svc_beta[i] : 0.0;
+    p.svc_median[i] = on ? c.svc_median[i] : 0.0;
+    p.w_class[i] = on ? c.w_class[i] : 0.0;
+  }
+  p.class_cum[p.C - 1] = 1.0;
+  p.svc_sigma = c.svc_sigma;
+  p.w_thr = c.w_thr;
+  p.inv_n = 1.0 / (double)c.queue_cap;
+  p.inv_tw = 1.0 / c.obs_tw;
+  p.inv_c = 1.0 / (double)c.n_classes;
+  p.inv_rs = 1.0 / (c.lambda_ref * c.tick_s);
+  p.static_timeout = c.static_timeout;
+  p.tr_times = nullptr; p.tr_cls = nullptr; p.tr_cnt = nullptr; p.tr_len = c.trace_max_len;
+
+  MlpParams& m = x->m;
+  m.E = c.n_envs; m.F = c.obs_dim; m.H1 = c.mlp_h1; m.H2 = c.mlp_h2;
+  m.A = 6 * c.n_servers; m.Ap = m.A + (c.value_head ? 1 : 0);
+  m.bf16 = c.mlp_bf16; m.value_head = c.value_head;
+  m.FP = pad_to(c.obs_dim, c.mlp_bf16 ? 32 : 4);
+  m.AP = pad_to(m.Ap, 16);
+}
+
+int sim_create(const sim_cfg* cfg, void* hip_stream, sim_ctx** out) {
+  if (!out) return fail(SIM_EINVAL, "out is NULL");
+  *out = nullptr;
+  int rc = validate(cfg);
+  if (rc) return rc;
+  sim_ctx* x = new (std::nothrow) sim_ctx();
+  if (!x) return fail(SIM_ENOMEM, "host allocation of the context failed");
+  x->cfg = *cfg;
+  x->stream = static_cast<hipStream_t>(hip_stream);
+  (void)hipGetDevice(&x->device);
+  derive(x);
+  const size_t E = (size_t)cfg->n_envs, K = cfg->n_servers, C = cfg->n_classes, N = cfg->queue_cap;
+  const int nsys = cfg->shadow ? 2 : 1;
+  // layout of the arena: per system, then shared fields
+  std::vector<std::pair<void**, size_t>> parts;
+  for (int s = 0; s < nsys; ++s) {
+    SysState& g = x->s.sys[s];
+    parts.push_back({(void**)&g.qpack, 4 * E});
+    parts.push_back({(void**)&g.hpack, 4 * E});
+    parts.push_back({(void**)&g.hts, 8 * C * E});
+    parts.push_back({(void**)&g.busy, 8 * K * E});
+    parts.push_back({(void**)&g.meta, 4 * K * E});
+    parts.push_back({(void**)&g.cnt, 4 * kNcnt * E});
+    parts.push_back({(void**)&g.sums, 8 * 2 * E});
+    parts.push_back({(void**)&g.chk, 8 * E});
+    parts.push_back({(void**)&g.ring, 8 * C * N * E});
+    parts.push_back({(void**)&g.proc, 4 * E});
+    parts.push_back({(void**)&g.next_sw, 8 * E});
+    parts.push_back({(void**)&g.next_arr, 8 * E});
+    parts.push_back({(void**)&g.tr_idx, 4 * E});
+  }
+  parts.push_back({(void**)&x->s.ewma, 8 * 4 * E});
+  parts.push_back({(void**)&x->s.obs, 4 * (size_t)cfg->obs_dim * E});
+  parts.push_back({(void**)&x->s.err, 256});
+  parts.push_back({(void**)&x->d_tot_cnt, 8 * 2 * 7});
+  parts.push_back({(void**)&x->d_tot_sum, 8 * 2 * 2});
+  size_t total = 0;
+  for (auto& pr : parts) total += align256(pr.second);
+  hipError_t he = hipMalloc(&x->arena, total);
+  if (he != hipSuccess) {
+    delete x;
+    return fail(SIM_ENOMEM, "hipMalloc of %zu bytes of environment state failed: %s", total,
+                hipGetErrorString(he));
+  }
+  x->arena_bytes = total;
+  size_t off = 0;
+  for (auto& pr : parts) {
+    *pr.first = static_cast<unsigned char*>(x->arena) + off;
+    off += align256(pr.second);
+  }
+  he = hipMemsetAsync(x->s.err, 0, 256, x->stream);
+  if (he != hipSuccess) {
+    (void)hipFree(x->arena);
+    delete x;
+    return hip_fail(he, "hipMemsetAsync");
+  }
+  // packed policy weights (only for supported shapes; checked at use)
+  const MlpParams& m = x->m;
+  const size_t eb = m.bf16 ? 2 : 4;
+  const size_t wbytes = align256(eb * m.H1 * m.FP) + align256(4 * m.H1) + align256(eb * m.H2 * m.H1) +
+                        align256(4 * m.H2) + align256(eb * m.AP * m.H2) + align256(4 * m.AP);
+  he = hipMalloc(&x->wpack, wbytes);
+  if (he != hipSuccess) {
+    (void)hipFree(x->arena);
+    delete x;
+    return fail(SIM_ENOMEM, "hipMalloc of packed weights failed: %s", hipGetErrorString(he));
+  }
+  unsigned char* wp = static_cast<unsigned char*>(x->wpack);
+  x->m.w1 = wp; wp += align256(eb * m.H1 * m.FP);
+  x->m.b1 = reinterpret_cast<float*>(wp); wp += align256(4 * m.H1);
+  x->m.w2 = wp; wp += align256(eb * m.H2 * m.H1);
+  x->m.b2 = reinterpret_cast<float*>(wp); wp += align256(4 * m.H2);
+  x->m.w3 = wp; wp += align256(eb * m.AP * m.H2);
+  x->m.b3 = reinterpret_cast<float*>(wp);
+  *out = x;
+  return SIM_OK;
+}
+
+int sim_destroy(sim_ctx* x) {
+  if (!x) return SIM_OK;
+  (void)hipStreamSynchronize(x->stream);
+  for (auto& pd : x->pending) {
+    (void)hipEventDestroy(pd.a);
+    (void)hipEventDestroy(pd.b);
+  }
+  for (hipEvent_t ev : x->pool) (void)hipEventDestroy(ev);
+  (void)hipFree(x->arena);
+  (void)hipFree(x->wpack);
+  delete x;
+  return SIM_OK;
+}
+
+int sim_set_trace(sim_ctx* x, const double* d_times, const uint8_t* d_classes,
+                  const int32_t* d_counts) {
+  if (!x) return fail(SIM_EINVAL, "ctx is NULL");
+  if (x->cfg.arrival_kind != SIM_ARR_TRACE)
+    return fail(SIM_ESTATE, "sim_set_trace needs arrival_kind = SIM_ARR_TRACE");
+  if (!d_times || !d_classes || !d_counts) return fail(SIM_EINVAL, "trace arrays must be non-NULL");
+  x->p.tr_times = d_times;
+  x->p.tr_cls = d_classes;
+  x->p.tr_cnt = d_counts;
+  x->trace_set = true;
+  return SIM_OK;
+}
+
+int sim_reset(sim_ctx* x, uint64_t seed) {
+  if (!x) return fail(SIM_EINVAL, "ctx is NULL");
+  if (x->cfg.arrival_kind == SIM_ARR_TRACE && !x->trace_set)
+    return fail(SIM_ESTATE, "trace arrivals need sim_set_trace before sim_reset");
+  HIPCHK(x->timed(SIM_KC_RESET, [&] { return launch_reset(x->p, x->s, seed, x->stream); }),
+         "reset kernel launch");
+  x->seed = seed;
+  x->tick = 0;
+  x->reset_done = true;
+  return SIM_OK;
+}
+
+int sim_obs(sim_ctx* x, float* d_obs) {
+  if (!x || !d_obs) return fail(SIM_EINVAL, "NULL argument");
+  if (!x->reset_done) return fail(SIM_ESTATE, "sim_obs before sim_reset");
+  HIPCHK(hipMemcpyAsync(d_obs, x->s.obs, 4 * (size_t)x->cfg.obs_dim * x->cfg.n_envs,
+                        hipMemcpyDeviceToDevice, x->stream), "hipMemcpyAsync obs");
+  return SIM_OK;
+}
+
+static int enqueue_tick(sim_ctx* x, const uint8_t* act, float* obs_out, double* rew,
+                        double* rew_sh, uint64_t* rchk) {
+  HIPCHK(x->timed(SIM_KC_STEP, [&] {
+           return launch_step(x->p, x->s, x->seed, x->tick, act, obs_out, rew, rchk, x->stream);
+         }), "step kernel launch");
+  if (x->cfg.shadow)
+    HIPCHK(x->timed(SIM_KC_STATIC, [&] {
+             return launch_static(x->p, x->s, x->seed, x->tick, rew_sh, x->stream);
+           }), "static kernel launch");
+  return SIM_OK;
+}
+
+int sim_step(sim_ctx* x, const uint8_t* d_actions, float* d_obs_next, double* d_reward,
+             double* d_reward_shadow) {
+  if (!x || !d_actions) return fail(SIM_EINVAL, "NULL argument");
+  if (!x->reset_done) return fail(SIM_ESTATE, "sim_step before sim_reset");
+  if (x->tick == 0xFFFFFFFEu) return fail(SIM_ESTATE, "tick counter exhausted");
+  int rc = enqueue_tick(x, d_actions, d_obs_next, d_reward, d_reward_shadow, nullptr);
+  if (rc) return rc;
+  x->tick++;
+  return SIM_OK;
+}
+
+int sim_tick(sim_ctx* x, int32_t* h_tick) {
+  if (!x || !h_tick) return fail(SIM_EINVAL, "NULL argument");
+  *h_tick = (int32_t)x->tick;
+  return SIM_OK;
+}
+
+int sim_weights_layout(const sim_cfg* c, sim_wlayout* o) {
+  if (!c || !o) return fail(SIM_EINVAL, "NULL argument");
+  if (c->mlp_h1 < 1 || c->mlp_h2 < 1 || c->obs_dim < 1 || c->n_servers < 1)
+    return fail(SIM_EINVAL, "MLP dimensions must be positive");
+  const size_t eb = c->mlp_bf16 ? 2 : 4;
+  const size_t F = c->obs_dim, H1 = c->mlp_h1, H2 = c->mlp_h2;
+  const size_t Ap = 6 * (size_t)c->n_servers + (c->value_head ? 1 : 0);
+  size_t off = 0;
+  o->w1 = off; off += align256(eb * F * H1);
+  o->b1 = off; off += align256(4 * H1);
+  o->w2 = off; off += align256(eb * H1 * H2);
+  o->b2 = off; off += align256(4 * H2);
+  o->w3 = off; off += align256(eb * H2 * Ap);
+  o->b3 = off; off += align256(4 * Ap);
+  o->bytes = off;
+  o->n_out = (int32_t)Ap;
+  o->elem_bytes = (int32_t)eb;
+  return SIM_OK;
+}
+
+static void offsets(const sim_cfg& c, size_t off[6]) {
+  sim_wlayout L;
+  sim_weights_layout(&c, &L);
+  off[0] = L.w1; off[1] = L.b1; off[2] = L.w2; off[3] = L.b2; off[4] = L.w3; off[5] = L.b3;
+}
+
+int sim_init_weights(sim_ctx* x, uint64_t seed, void* d_weights) {
+  if (!x || !d_weights) return fail(SIM_EINVAL, "NULL argument");
+  size_t off[6];
+  offsets(x->cfg, off);
+  HIPCHK(x->timed(SIM_KC_OTHER, [&] {
+           return launch_init_weights(x->cfg.obs_dim, x->cfg.mlp_h1, x->cfg.mlp_h2, x->m.Ap,
+                                      x->cfg.mlp_bf16, seed, d_weights, off, x->stream);
+         }), "weight init launch");
+  return SIM_OK;
+}
+
+static int prepare_policy(sim_ctx* x, const void* d_weights) {
+  if (!policy_shape_supported(x->m))
+    return fail(SIM_EUNSUPPORTED,
+                "policy shape (bf16=%d, F_pad=%d, H1=%d, H2=%d, A_pad=%d) is not compiled",
+                x->m.bf16, x->m.FP, x->m.H1, x->m.H2, x->m.AP);
+  size_t off[6];
+  offsets(x->cfg, off);
+  HIPCHK(x->timed(SIM_KC_OTHER, [&] {
+           return launch_repack(x->m, d_weights, off, const_cast<void*>(x->m.w1),
+                                const_cast<float*>(x->m.b1), const_cast<void*>(x->m.w2),
+                                const_cast<float*>(x->m.b2), const_cast<void*>(x->m.w3),
+                                const_cast<float*>(x->m.b3), x->stream);
+         }), "weight repack launch");
+  return SIM_OK;
+}
+
+int sim_policy(sim_ctx* x, const void* d_weights, const float* d_obs, uint32_t step,
+               uint8_t* d_act, float* d_logp, float* d_value, float* d_logits) {
+  if (!x || !d_weights || !d_obs) return fail(SIM_EINVAL, "NULL argument");
+  if (d_value && !x->cfg.value_head) return fail(SIM_EINVAL, "d_value needs value_head = 1");
+  int rc = prepare_policy(x, d_weights);
+  if (rc) return rc;
+  HIPCHK(x->timed(SIM_KC_POLICY, [&] {
+           return launch_policy(x->m, d_obs, x->seed, step, d_act, d_logp, d_value, d_logits,
+                                x->stream);
+         }), "policy kernel launch");
+  return SIM_OK;
+}
+
+int sim_rollout(sim_ctx* x, const void* d_weights, int32_t T, const sim_traj* tr) {
+  if (!x || !d_weights || !tr || !tr->actions) return fail(SIM_EINVAL, "NULL argument");
+  if (T < 1) return fail(SIM_EINVAL, "T must be >= 1");
+  if (!x->reset_done) return fail(SIM_ESTATE, "sim_rollout before sim_reset");
+  if (tr->value && !x->cfg.value_head) return fail(SIM_EINVAL, "traj.value needs value_head = 1");
+  if (tr->reward_shadow && !x->cfg.shadow)
+    return fail(SIM_EINVAL, "traj.reward_shadow needs shadow = 1");
+  if ((uint64_t)x->tick + (uint64_t)T >= 0xFFFFFFFFull) return fail(SIM_ESTATE, "tick counter exhausted");
+  int rc = prepare_policy(x, d_weights);
+  if (rc) return rc;
+  const size_t E = (size_t)x->cfg.n_envs, F = (size_t)x->cfg.obs_dim;
+  if (tr->obs)
+    HIPCHK(hipMemcpyAsync(tr->obs, x->s.obs, 4 * F * E, hipMemcpyDeviceToDevice, x->stream),
+           "hipMemcpyAsync obs_0");
+  for (int32_t k = 0; k < T; ++k) {
+    const size_t row = (size_t)k * E;
+    HIPCHK(x->timed(SIM_KC_POLICY, [&] {
+             return launch_policy(x->m, x->s.obs, x->seed, x->tick, tr->actions + row,
+                                  tr->logp ? tr->logp + row : nullptr,
+                                  tr->value ? tr->value + row : nullptr, nullptr, x->stream);
+           }), "policy kernel launch");
+    rc = enqueue_tick(x, tr->actions + row, tr->obs ? tr->obs + (size_t)(k + 1) * F * E : nullptr,
+                      tr->reward ? tr->reward + row : nullptr,
+                      tr->reward_shadow ? tr->reward_shadow + row : nullptr,
+                      tr->rchk ? tr->rchk + row : nullptr);
+    if (rc) return rc;
+    x->tick++;
+  }
+  if (tr->value)
+    HIPCHK(x->timed(SIM_KC_POLICY, [&] {
+             return launch_policy(x->m, x->s.obs, x->seed, x->tick, nullptr, nullptr,
+                                  tr->value + (size_t)T * E, nullptr, x->stream);
+           }), "policy kernel launch (final value)");
+  return SIM_OK;
+}
+
+int returns_gae(sim_ctx* x, int32_t T, const double* d_r, const float* d_v, double gamma,
+                double lambda, double* d_adv, double* d_ret) {
+  if (!x || !d_r || !d_adv || !d_ret) return fail(SIM_EINVAL, "NULL argument");
+  if (T < 1) return fail(SIM_EINVAL, "T must be >= 1");
+  HIPCHK(x->timed(SIM_KC_GAE, [&] {
+           return launch_gae(T, x->cfg.n_envs, d_r, d_v, gamma, lambda, d_adv, d_ret, x->stream);
+         }), "gae kernel launch");
+  return SIM_OK;
+}
+
+int sim_counters(sim_ctx* x, int64_t* d_cnt, double* d_sum) {
+  if (!x) return fail(SIM_EINVAL, "ctx is NULL");
+  if (!x->reset_done) return fail(SIM_ESTATE, "sim_counters before sim_reset");
+  HIPCHK(x->timed(SIM_KC_OTHER, [&] { return launch_counters(x->p, x->s, d_cnt, d_sum, x->stream); }),
+         "counters kernel launch");
+  return SIM_OK;
+}
+
+int sim_checksums(sim_ctx* x, uint64_t* d_chk) {
+  if (!x || !d_chk) return fail(SIM_EINVAL, "NULL argument");
+  if (!x->reset_done) return fail(SIM_ESTATE, "sim_checksums before sim_reset");
+  const size_t E = (size_t)x->cfg.n_envs;
+  HIPCHK(hipMemcpyAsync(d_chk, x->s.sys[0].chk, 8 * E, hipMemcpyDeviceToDevice, x->stream),
+         "hipMemcpyAsync checksums");
+  if (x->cfg.shadow)
+    HIPCHK(hipMemcpyAsync(d_chk + E, x->s.sys[1].chk, 8 * E, hipMemcpyDeviceToDevice, x->stream),
+           "hipMemcpyAsync checksums");
+  else
+    HIPCHK(hipMemsetAsync(d_chk + E, 0, 8 * E, x->stream), "hipMemsetAsync checksums");
+  return SIM_OK;
+}
+
+int sim_stats(sim_ctx* x, sim_totals* h) {
+  if (!x || !h) return fail(SIM_EINVAL, "NULL argument");
+  if (!x->reset_done) return fail(SIM_ESTATE, "sim_stats before sim_reset");
+  HIPCHK(hipMemsetAsync(x->d_tot_cnt, 0, 8 * 2 * 7, x->stream), "hipMemsetAsync");
+  HIPCHK(hipMemsetAsync(x->d_tot_sum, 0, 8 * 2 * 2, x->stream), "hipMemsetAsync");
+  HIPCHK(x->timed(SIM_KC_OTHER, [&] {
+           return launch_totals(x->p, x->s, x->d_tot_cnt, x->d_tot_sum, x->stream);
+         }), "totals kernel launch");
+  int64_t c[14];
+  double s[4];
+  HIPCHK(hipMemcpyAsync(c, x->d_tot_cnt, sizeof c, hipMemcpyDeviceToHost, x->stream), "copy totals");
+  HIPCHK(hipMemcpyAsync(s, x->d_tot_sum, sizeof s, hipMemcpyDeviceToHost, x->stream), "copy totals");
+  HIPCHK(hipStreamSynchronize(x->stream), "hipStreamSynchronize");
+  for (int sy = 0; sy < 2; ++sy) {
+    for (int i = 0; i < SIM_NCNT; ++i) h->cnt[sy][i] = c[sy * 7 + i];
+    for (int i = 0; i < SIM_NSUM; ++i) h->sum[sy][i] = s[sy * 2 + i];
+  }
+  return SIM_OK;
+}
+
+int sim_sync(sim_ctx* x) {
+  if (!x) return fail(SIM_EINVAL, "ctx is NULL");
+  HIPCHK(hipStreamSynchronize(x->stream), "hipStreamSynchronize");
+  uint32_t err = 0;
+  HIPCHK(hipMemcpy(&err, x->s.err, 4, hipMemcpyDeviceToHost), "copy error flags");
+  if (err) {
+    HIPCHK(hipMemset(x->s.err, 0, 4), "clear error flags");
+    return fail(SIM_ESTATE, "device error flags 0x%x:%s%s%s", err,
+                (err & ERR_ACTION) ? " action out of range;" : "",
+                (err & ERR_EVENTS) ? " event bound exceeded in a tick;" : "",
+                (err & ERR_TRACE) ? " trace overrun;" : "");
+  }
+  return SIM_OK;
+}
+
+int sim_set_timing(sim_ctx* x, int32_t on) {
+  if (!x) return fail(SIM_EINVAL, "ctx is NULL");
+  x->timing = on != 0;
+  return SIM_OK;
+}
+
+int sim_get_timing(sim_ctx* x, double* h_ms, int64_t* h_launches, int32_t clear) {
+  if (!x) return fail(SIM_EINVAL, "ctx is NULL");
+  HIPCHK(hipStreamSynchronize(x->stream), "hipStreamSynchronize");
+  for (auto& pd : x->pending) {
+    float f = 0.f;
+    HIPCHK(hipEventElapsedTime(&f, pd.a, pd.b), "hipEventElapsedTime");
+    x->ms[pd.cls] += (double)f;
+    x->launches[pd.cls] += 1;
+    x->pool.push_back(pd.a);
+    x->pool.push_back(pd.b);
+  }
+  x->pending.clear();
+  for (int i = 0; i < SIM_KC_COUNT; ++i) {
+    if (h_ms) h_ms[i] = x->ms[i];
+    if (h_launches) h_launches[i] = x->launches[i];
+    if (clear) {
+      x->ms[i] = 0.0;
+      x->launches[i] = 0;
+    }
+  }
+  return SIM_OK;
+}
+
+}  // extern "C"

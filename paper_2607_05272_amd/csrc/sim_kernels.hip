@@ -1,0 +1,725 @@
+// sim_kernels.hip -- reset and one-tick step of the batched discrete-event simulator.
+//
+// One lane owns one environment for the whole tick: its structure-of-arrays state is read
+// with coalesced loads into registers, the tick's events are processed in time order, and
+// the state is written back. Model (paper Sec. 3.1, Sec. 4.1):
+//   - arrivals from a modulated Poisson process (Poisson, MMPP or heavy-tailed ON/OFF,
+//     Sec. 3.2) or an explicit trace; each arrival carries a class (model type);
+//   - per-class FIFO queues holding at most N waiting requests in total, arrivals beyond
+//     that are dropped (load shedding);
+//   - K servers; a batch of n requests of one class occupies a server for alpha + beta*n
+//     (or a lognormal / exponential time);
+//   - the learned system dispatches exactly b = 2^(a%6) requests of the head-of-line class
+//     to server a/6 whenever that server is idle and the class holds >= b requests;
+//   - the optional shadow system applies the static rule (B requests or timeout T) to the
+//     same arrivals;
+//   - reward = w_thr * dispatched/dt - mean (or sum) of the class-weighted latencies of the
+//     requests dispatched in the tick, attributed at dispatch.
+// A batch is dispatched at the earliest event instant of the tick at which its condition
+// holds; the loop visits every arrival, switch, completion of a relevant server and
+// timeout instant in time order. Ties at one instant: switch, arrival, then dispatch.
+//
+// The learned system only touches server a/6 inside the tick, so its kernel keeps that one
+// server in registers and streams over all servers once at the end of the tick
+// (completions and observation). The static system needs every server inside the tick
+// (lowest idle server, next completion) and runs as its own kernel with all of them in
+// registers. Each system advances its own copy of the arrival process with the same
+// draws, so both see the same arrivals.
+#include "devmath.hpp"
+#include "params.hpp"
+
+namespace bsim {
+namespace {
+
+enum { C_ARR = 0, C_ACC = 1, C_DROP = 2, C_DISP = 3, C_BATCH = 4, C_DONE = 5 };
+constexpr double kInf = __builtin_huge_val();
+
+// Per-lane select from a small array with compile-time bound M (register arrays stay in
+// registers instead of going to scratch for a runtime index).
+template <int M, typename T, int L>
+__device__ __forceinline__ T pick(const T (&a)[L], int i) {
+  T v = a[0];
+#pragma unroll
+  for (int c = 1; c < M; ++c)
+    if (i == c) v = a[c];
+  return v;
+}
+template <int M, typename T, int L>
+__device__ __forceinline__ void put(T (&a)[L], int i, T v) {
+#pragma unroll
+  for (int c = 0; c < M; ++c)
+    if (i == c) a[c] = v;
+}
+
+// ---- per-class FIFO queues of one system ---------------------------------------------------
+template <int CM>
+struct Queue {
+  uint32_t qp, hp;  // per-class length / ring head, one byte per class
+  double hts[CM];   // arrival time of each class's head request
+  int qsum;
+  double* ring;     // this environment's rings [C][N]
+  __device__ __forceinline__ int q(int c) const { return (int)((qp >> (8 * c)) & 0xffu); }
+  __device__ __forceinline__ int hd(int c) const { return (int)((hp >> (8 * c)) & 0xffu); }
+};
+
+template <int CM>
+__device__ __forceinline__ void load_queue(Queue<CM>& Q, const SysState& g, const SimParams& p,
+                                           int e) {
+  const size_t E = (size_t)p.E;
+  Q.qp = g.qpack[e];
+  Q.hp = g.hpack[e];
+  Q.qsum = 0;
+#pragma unroll
+  for (int c = 0; c < CM; ++c) {
+    Q.hts[c] = c < p.C ? g.hts[(size_t)c * E + e] : 0.0;
+    Q.qsum += Q.q(c);
+  }
+  Q.ring = g.ring + (size_t)e * p.C * p.N;
+}
+
+template <int CM>
+__device__ __forceinline__ void store_queue(const Queue<CM>& Q, const SysState& g,
+                                            const SimParams& p, int e) {
+  const size_t E = (size_t)p.E;
+  g.qpack[e] = Q.qp;
+  g.hpack[e] = Q.hp;
+#pragma unroll
+  for (int c = 0; c < CM; ++c)
+    if (c < p.C) g.hts[(size_t)c * E + e] = Q.hts[c];
+}
+
+// head-of-line class: oldest head request, ties to the lower class index; -1 if empty
+template <int CM>
+__device__ __forceinline__ int hol(const Queue<CM>& Q, const SimParams& p, double& ts) {
+  int h = -1;
+  ts = 0.0;
+#pragma unroll
+  for (int c = 0; c < CM; ++c) {
+    if (c < p.C && Q.q(c) > 0 && (h < 0 || Q.hts[c] < ts)) {
+      h = c;
+      ts = Q.hts[c];
+    }
+  }
+  return h;
+}
+
+// ---- counters of one system -----------------------------------------------------------------
+struct Count {
+  uint32_t c[kNcnt];
+  double lat, wlat;
+  uint64_t chk;
+  int n_k;        // requests dispatched this tick
+  double Lw;      // weighted latency of this tick's dispatches (FIFO order)
+  uint32_t jsvc;  // service draws this tick
+};
+
+__device__ __forceinline__ void load_count(Count& C, const SysState& g, const SimParams& p, int e) {
+  const size_t E = (size_t)p.E;
+#pragma unroll
+  for (int i = 0; i < kNcnt; ++i) C.c[i] = g.cnt[(size_t)i * E + e];
+  C.lat = g.sums[e];
+  C.wlat = g.sums[E + e];
+  C.chk = g.chk[e];
+  C.n_k = 0;
+  C.Lw = 0.0;
+  C.jsvc = 0;
+}
+
+__device__ __forceinline__ void store_count(const Count& C, const SysState& g, const SimParams& p,
+                                            int e) {
+  const size_t E = (size_t)p.E;
+#pragma unroll
+  for (int i = 0; i < kNcnt; ++i) g.cnt[(size_t)i * E + e] = C.c[i];
+  g.sums[e] = C.lat;
+  g.sums[E + e] = C.wlat;
+  g.chk[e] = C.chk;
+}
+
+// ---- arrival process (one copy per system; identical draws) ---------------------------------
+struct Arrivals {
+  uint32_t proc;
+  double next_sw, next_arr;
+  uint32_t tr_idx;
+  int tr_cnt;
+  uint32_t jarr, jproc;
+};
+
+__device__ __forceinline__ void load_arrivals(Arrivals& A, const SysState& g, const SimParams& p,
+                                              int e) {
+  A.proc = g.proc[e];
+  A.next_sw = g.next_sw[e];
+  A.next_arr = g.next_arr[e];
+  A.tr_idx = 0;
+  A.tr_cnt = 0;
+  if (p.arrival_kind == 1) {
+    A.tr_idx = g.tr_idx[e];
+    const int c = p.tr_cnt[e];
+    A.tr_cnt = c < 0 ? 0 : (c < p.tr_len ? c : p.tr_len);  // reset flags invalid counts
+  }
+  A.jarr = 0;
+  A.jproc = 0;
+}
+
+__device__ __forceinline__ void store_arrivals(const Arrivals& A, const SysState& g,
+                                               const SimParams& p, int e) {
+  g.proc[e] = A.proc;
+  g.next_sw[e] = A.next_sw;
+  g.next_arr[e] = A.next_arr;
+  if (p.arrival_kind == 1) g.tr_idx[e] = A.tr_idx;
+}
+
+__device__ __forceinline__ double dwell(const SimParams& p, int st, double u) {
+  const int kind = pick<kMaxS>(p.dwell_kind, st);
+  if (kind == 1) return -dlog(u) * pick<kMaxS>(p.dwell_mean, st);
+  if (kind == 2) return pick<kMaxS>(p.xm, st) * dexp(-dlog(u) * pick<kMaxS>(p.inv_alpha, st));
+  return kInf;
+}
+
+// Processes the switch and/or arrival due at `now` (switch first: it redraws the pending
+// arrival from the switch instant). Returns the class of an arrival at `now`, or -1.
+template <int CM>
+__device__ __forceinline__ int advance(Arrivals& A, const SimParams& p, uint64_t seed, int e,
+                                       uint32_t k, double now) {
+  if (A.next_sw == now) {
+    const u32x4 w = draw(seed, (uint32_t)e, k, P_PROCESS, A.jproc++, 0);
+    int nxt;
+    if (p.S == 2) {
+      nxt = 1 - (int)A.proc;
+    } else {
+      const int idx = (int)(unit(w.z, w.w) * (double)(p.S - 1));
+      nxt = idx < (int)A.proc ? idx : idx + 1;
+    }
+    A.proc = (uint32_t)nxt;
+    A.next_sw = now + dwell(p, nxt, unit(w.x, w.y));
+    if (pick<kMaxS>(p.rate, nxt) > 0.0) {
+      const u32x4 w2 = draw(seed, (uint32_t)e, k, P_ARRIVAL, A.jarr++, 0);
+      A.next_arr = now + -dlog(unit(w2.x, w2.y)) * pick<kMaxS>(p.mean_gap, nxt);
+    } else {
+      A.next_arr = kInf;
+    }
+  }
+  if (!(A.next_arr == now)) return -1;
+  int cls;
+  if (p.arrival_kind == 1) {
+    const size_t base = (size_t)e * p.tr_len;
+    cls = p.tr_cls[base + A.tr_idx];
+    if (cls >= p.C) cls = p.C - 1;  // reset validated every class id; never index past C
+    ++A.tr_idx;
+    A.next_arr = (int)A.tr_idx < A.tr_cnt ? p.tr_times[base + A.tr_idx] : kInf;
+  } else {
+    const u32x4 w = draw(seed, (uint32_t)e, k, P_ARRIVAL, A.jarr++, 0);
+    const double uc = unit(w.z, w.w);
+    cls = CM - 1;
+#pragma unroll
+    for (int c = CM - 2; c >= 0; --c)
+      if (uc < p.class_cum[c]) cls = c;
+    A.next_arr = now + -dlog(unit(w.x, w.y)) * pick<kMaxS>(p.mean_gap, (int)A.proc);
+  }
+  return cls;
+}
+
+// arrival at `now`: FIFO push, or drop when N requests wait (load shedding)
+template <int CM>
+__device__ __forceinline__ void enqueue(Queue<CM>& Q, Count& C, const SimParams& p, int cls,
+                                        double now) {
+  C.c[C_ARR] += 1u;
+  if (Q.qsum == p.N) {
+    C.c[C_DROP] += 1u;
+    return;
+  }
+  const int qc = Q.q(cls);
+  int pos = Q.hd(cls) + qc;
+  if (pos >= p.N) pos -= p.N;
+  Q.ring[(size_t)cls * p.N + pos] = now;
+  if (qc == 0) put<CM>(Q.hts, cls, now);
+  Q.qp += 1u << (8 * cls);
+  Q.qsum += 1;
+  C.c[C_ACC] += 1u;
+}
+
+// Stochastic service time of a batch of n (once per dispatch; kept out of line).
+// kind 1: median * exp(sigma Z) + beta n with Z = sqrt(-2 log u1) cos(2 pi u2) (Box-Muller);
+// kind 2: -log(u1) (alpha + beta n).
+__device__ __noinline__ double service_draw(int kind, double al, double be, double med,
+                                            double sigma, int n, uint64_t seed, uint32_t env,
+                                            uint32_t k, uint32_t j, uint32_t sys) {
+  const u32x4 w = draw(seed, env, k, P_SERVICE, j, sys);
+  const double u1 = unit(w.x, w.y);
+  if (kind == 2) return -dlog(u1) * (al + be * (double)n);
+  const double u2 = unit(w.z, w.w);
+  const double z = sqrt(-2.0 * dlog(u1)) * dcos(kTwoPi * u2);
+  return med * dexp(sigma * z) + be * (double)n;
+}
+
+// Pops n requests of class h dispatched at `now` to server j, on which they complete at
+// cdone = now + service; accumulates their latencies in FIFO order. Returns cdone.
+template <int CM>
+__device__ __forceinline__ double pop_batch(Queue<CM>& Q, Count& C, const SimParams& p,
+                                            uint64_t seed, int e, uint32_t k, int sys, int j,
+                                            int h, int n, double now) {
+  const int kind = pick<CM>(p.svc_kind, h);
+  const double al = pick<CM>(p.svc_alpha, h), be = pick<CM>(p.svc_beta, h);
+  double sv;
+  if (kind == 0) sv = al + be * (double)n;
+  else sv = service_draw(kind, al, be, pick<CM>(p.svc_median, h), p.svc_sigma, n, seed,
+                         (uint32_t)e, k, C.jsvc++, (uint32_t)sys);
+  const double cdone = now + sv;
+  const double wh = pick<CM>(p.w_class, h);
+  const int N = p.N;
+  const double* rb = Q.ring + (size_t)h * N;
+  int pos = Q.hd(h);
+  double Lw = C.Lw, lat = C.lat, wlat = C.wlat;
+  for (int i = 0; i < n; ++i) {
+    const double a = rb[pos];
+    pos = pos + 1 == N ? 0 : pos + 1;
+    const double l = cdone - a;
+    const double wl = wh * l;
+    Lw = Lw + wl;
+    lat = lat + l;
+    wlat = wlat + wl;
+  }
+  C.Lw = Lw; C.lat = lat; C.wlat = wlat;
+  const int sh = 8 * h;
+  const int qh = Q.q(h) - n;
+  Q.qp = (Q.qp & ~(0xffu << sh)) | ((uint32_t)qh << sh);
+  Q.hp = (Q.hp & ~(0xffu << sh)) | ((uint32_t)pos << sh);
+  Q.qsum -= n;
+  if (qh > 0) put<CM>(Q.hts, h, rb[pos]);
+  C.c[C_DISP] += (uint32_t)n;
+  C.c[C_BATCH] += 1u;
+  C.chk = fnv(C.chk, ((uint64_t)(k + 1) << 32) | ((uint64_t)j << 16) | ((uint64_t)h << 8) |
+                         (uint64_t)n);
+  C.n_k += n;
+  return cdone;
+}
+
+// end-of-tick checksum word pair and reward
+template <int CM>
+__device__ __forceinline__ double close_tick(const Queue<CM>& Q, Count& C, const SimParams& p,
+                                             uint32_t proc, int A_k) {
+  uint64_t qp = (uint64_t)Q.qp;
+  if (CM < 4) qp &= (1ull << (8 * CM)) - 1;
+  qp |= ((uint64_t)proc) << 32;
+  qp |= ((uint64_t)(A_k & 0xffff)) << 40;
+  C.chk = fnv(C.chk, qp);
+  C.chk = fnv(C.chk, ((uint64_t)C.c[C_DONE] << 32) | (uint64_t)C.c[C_DROP]);
+  const double thr = (double)C.n_k / p.dt;
+  if (p.reward_sum) return p.w_thr * thr - C.Lw;
+  return p.w_thr * thr - (C.n_k > 0 ? C.Lw / (double)C.n_k : 0.0);
+}
+
+__device__ __forceinline__ void put_obs(float* obs, size_t E, int i, int e, double v) {
+  obs[(size_t)i * E + e] = (float)v;
+}
+
+// ---- learned system: one tick ---------------------------------------------------------------
+template <int CM>
+__global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64_t seed,
+                                                 uint32_t k, const uint8_t* __restrict__ act,
+                                                 float* __restrict__ obs_out,
+                                                 double* __restrict__ rew,
+                                                 uint64_t* __restrict__ rchk) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= p.E) return;
+  const size_t E = (size_t)p.E;
+  const SysState& G = g.sys[0];
+  int a = act[e];
+  if (a >= 6 * p.K) {
+    atomicOr(g.err, ERR_ACTION);
+    a = 0;
+  }
+  const int s = a / 6, b = 1 << (a % 6);
+  Queue<CM> Q;
+  load_queue(Q, G, p, e);
+  Count C;
+  load_count(C, G, p, e);
+  Arrivals A;
+  load_arrivals(A, G, p, e);
+  double busy_s = G.busy[(size_t)s * E + e];
+  uint32_t meta_s = G.meta[(size_t)s * E + e];
+  bool dirty_s = false;
+
+  const double t0 = (double)k * p.dt, t1 = (double)(k + 1) * p.dt;
+  int A_k = 0;
+  double now = t0;
+  for (uint32_t it = 0;; ++it) {
+    if (it > 0) {
+      double te = A.next_sw < A.next_arr ? A.next_sw : A.next_arr;
+      if (busy_s > now && busy_s < te) te = busy_s;
+      if (!(te < t1)) break;
+      if (it > kMaxEventsPerTick) {
+        atomicOr(g.err, ERR_EVENTS);
+        break;
+      }
+      now = te;
+      const int cls = advance<CM>(A, p, seed, e, k, now);
+      if (cls >= 0) {
+        ++A_k;
+        enqueue(Q, C, p, cls, now);
+      }
+    }
+    // exactly b requests of the head-of-line class whenever server s is idle
+    while (busy_s <= now && Q.qsum > 0) {
+      double ts;
+      const int h = hol(Q, p, ts);
+      if (Q.q(h) < b) break;
+      C.c[C_DONE] += meta_s & 0xffu;  // the previous batch on s finished at busy_s <= now
+      busy_s = pop_batch(Q, C, p, seed, e, k, 0, s, h, b, now);
+      meta_s = (uint32_t)b | ((uint32_t)b << 8) | ((uint32_t)h << 16);
+      dirty_s = true;
+    }
+  }
+
+  // end of tick: completions before t1 and the per-server part of obs_{k+1}
+  float* obs = g.obs;
+  const int per = p.K > 1 ? 4 : 2;
+  for (int j = 0; j < p.K; ++j) {
+    const bool mine = j == s;
+    const double bu = mine ? busy_s : G.busy[(size_t)j * E + e];
+    uint32_t m = mine ? meta_s : G.meta[(size_t)j * E + e];
+    bool dirty = mine && dirty_s;
+    const uint32_t infl = m & 0xffu;
+    if (infl > 0 && bu < t1) {
+      C.c[C_DONE] += infl;
+      m &= ~0xffu;
+      dirty = true;
+    }
+    if (dirty) {
+      if (mine) G.busy[(size_t)j * E + e] = bu;
+      G.meta[(size_t)j * E + e] = m;
+    }
+    const int base = 2 + per * j;
+    const double bflag = bu > t1 ? 1.0 : 0.0;
+    const double lb = (double)((m >> 8) & 0xffu) * 0.03125;
+    put_obs(obs, E, base, e, bflag);
+    put_obs(obs, E, base + 1, e, lb);
+    if (obs_out) {
+      put_obs(obs_out, E, base, e, bflag);
+      put_obs(obs_out, E, base + 1, e, lb);
+    }
+    if (p.K > 1) {
+      const double rem = (bu > t1 ? bu - t1 : 0.0) * p.inv_tw;
+      const uint32_t lc = (m >> 16) & 0xffu;
+      const double lcv = (double)((lc == 0xffu ? -1 : (int)lc) + 1) * p.inv_c;
+      put_obs(obs, E, base + 2, e, rem);
+      put_obs(obs, E, base + 3, e, lcv);
+      if (obs_out) {
+        put_obs(obs_out, E, base + 2, e, rem);
+        put_obs(obs_out, E, base + 3, e, lcv);
+      }
+    }
+  }
+  const double r = close_tick(Q, C, p, A.proc, A_k);
+  if (rew) rew[e] = r;
+  if (rchk) rchk[e] = C.chk;
+
+  // rates: exponentially weighted arrival counts with weights 1, 1/4, 1/16, 1/64
+  double ew[4];
+  const double ewc[4] = {1.0, 0.25, 0.0625, 0.015625};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const double v = g.ewma[(size_t)i * E + e];
+    ew[i] = v + ewc[i] * ((double)A_k - v);
+    g.ewma[(size_t)i * E + e] = ew[i];
+  }
+  // queue part of obs_{k+1}
+  double ts;
+  const int h = hol(Q, p, ts);
+  const double f0 = (double)Q.qsum * p.inv_n, f1 = (h >= 0 ? t1 - ts : 0.0) * p.inv_tw;
+  put_obs(obs, E, 0, e, f0);
+  put_obs(obs, E, 1, e, f1);
+  if (obs_out) {
+    put_obs(obs_out, E, 0, e, f0);
+    put_obs(obs_out, E, 1, e, f1);
+  }
+  int i = 2 + per * p.K;
+  if (p.C > 1) {
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+      if (c < p.C) {
+        const int qc = Q.q(c);
+        const double fq = (double)qc * p.inv_n;
+        const double fa = (qc > 0 ? t1 - Q.hts[c] : 0.0) * p.inv_tw;
+        put_obs(obs, E, i, e, fq);
+        put_obs(obs, E, i + 1, e, fa);
+        if (obs_out) {
+          put_obs(obs_out, E, i, e, fq);
+          put_obs(obs_out, E, i + 1, e, fa);
+        }
+        i += 2;
+      }
+    }
+  }
+#pragma unroll
+  for (int r4 = 0; r4 < 4; ++r4) {
+    const double fr = ew[r4] * p.inv_rs;
+    put_obs(obs, E, i, e, fr);
+    if (obs_out) put_obs(obs_out, E, i, e, fr);
+    ++i;
+  }
+  for (; i < p.F; ++i) {
+    obs[(size_t)i * E + e] = 0.0f;
+    if (obs_out) obs_out[(size_t)i * E + e] = 0.0f;
+  }
+
+  store_queue(Q, G, p, e);
+  store_count(C, G, p, e);
+  store_arrivals(A, G, p, e);
+}
+
+// ---- static shadow system: one tick ---------------------------------------------------------
+template <int KM, int CM>
+__global__ __launch_bounds__(256) void static_k(SimParams p, EnvState g, uint64_t seed, uint32_t k,
+                                                double* __restrict__ rew) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= p.E) return;
+  const size_t E = (size_t)p.E;
+  const SysState& G = g.sys[1];
+  Queue<CM> Q;
+  load_queue(Q, G, p, e);
+  Count C;
+  load_count(C, G, p, e);
+  Arrivals A;
+  load_arrivals(A, G, p, e);
+  double busy[KM];
+  uint32_t meta[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    busy[j] = j < p.K ? G.busy[(size_t)j * E + e] : kInf;
+    meta[j] = j < p.K ? G.meta[(size_t)j * E + e] : 0u;
+  }
+  uint32_t dirty = 0;
+
+  const double t0 = (double)k * p.dt, t1 = (double)(k + 1) * p.dt;
+  int A_k = 0;
+  double now = t0;
+  for (uint32_t it = 0;; ++it) {
+    if (it > 0) {
+      double te = A.next_sw < A.next_arr ? A.next_sw : A.next_arr;
+      bool idle = false;
+#pragma unroll
+      for (int j = 0; j < KM; ++j) {
+        if (busy[j] > now && busy[j] < te) te = busy[j];
+        idle = idle || busy[j] <= now;
+      }
+      if (Q.qsum > 0 && idle) {
+        double ts;
+        hol(Q, p, ts);
+        const double tout = ts + p.static_timeout;
+        if (tout > now && tout < te) te = tout;
+      }
+      if (!(te < t1)) break;
+      if (it > kMaxEventsPerTick) {
+        atomicOr(g.err, ERR_EVENTS);
+        break;
+      }
+      now = te;
+      const int cls = advance<CM>(A, p, seed, e, k, now);
+      if (cls >= 0) {
+        ++A_k;
+        enqueue(Q, C, p, cls, now);
+      }
+    }
+    // lowest idle server; min(B, Q_h) of the HoL class if Q_h >= B or its head waited T
+    for (;;) {
+      int j = -1;
+#pragma unroll
+      for (int jj = KM - 1; jj >= 0; --jj)
+        if (busy[jj] <= now) j = jj;
+      if (j < 0 || Q.qsum == 0) break;
+      double ts;
+      const int h = hol(Q, p, ts);
+      const int qh = Q.q(h);
+      if (!(qh >= p.bmax || now >= ts + p.static_timeout)) break;
+      const int n = qh < p.bmax ? qh : p.bmax;
+      C.c[C_DONE] += pick<KM>(meta, j) & 0xffu;
+      put<KM>(busy, j, pop_batch(Q, C, p, seed, e, k, 1, j, h, n, now));
+      put<KM>(meta, j, (uint32_t)n | ((uint32_t)n << 8) | ((uint32_t)h << 16));
+      dirty |= 1u << j;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    const uint32_t infl = meta[j] & 0xffu;
+    if (infl > 0 && busy[j] < t1) {
+      C.c[C_DONE] += infl;
+      meta[j] &= ~0xffu;
+      dirty |= 1u << j;
+    }
+  }
+  const double r = close_tick(Q, C, p, A.proc, A_k);
+  if (rew) rew[e] = r;
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    if (dirty & (1u << j)) {
+      G.busy[(size_t)j * E + e] = busy[j];
+      G.meta[(size_t)j * E + e] = meta[j];
+    }
+  }
+  store_queue(Q, G, p, e);
+  store_count(C, G, p, e);
+  store_arrivals(A, G, p, e);
+}
+
+// ---- reset ------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void reset_k(SimParams p, EnvState g, uint64_t seed) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= p.E) return;
+  const size_t E = (size_t)p.E;
+  // modulating state from its stationary law, its dwell, then the first arrival
+  uint32_t proc = 0;
+  double next_sw = kInf, next_arr = kInf;
+  if (p.arrival_kind == 1) {
+    // validate the caller's trace: count within capacity, classes within range
+    const int cnt = p.tr_cnt[e];
+    bool bad = cnt < 0 || cnt > p.tr_len;
+    const int n = cnt < 0 ? 0 : (cnt > p.tr_len ? p.tr_len : cnt);
+    for (int i = 0; i < n; ++i) bad = bad || p.tr_cls[(size_t)e * p.tr_len + i] >= p.C;
+    if (bad) atomicOr(g.err, ERR_TRACE);
+    next_arr = n > 0 ? p.tr_times[(size_t)e * p.tr_len] : kInf;
+  } else {
+    if (p.S > 1) {
+      const u32x4 w = draw(seed, (uint32_t)e, STEP_RESET, P_PROCESS, 0, 0);
+      const double us = unit(w.z, w.w);
+      int st = p.S - 1;
+#pragma unroll
+      for (int i = kMaxS - 2; i >= 0; --i)
+        if (i < p.S - 1 && us < p.stat_cum[i]) st = i;
+      proc = (uint32_t)st;
+      next_sw = dwell(p, st, unit(w.x, w.y));
+    }
+    if (pick<kMaxS>(p.rate, (int)proc) > 0.0) {
+      const u32x4 w = draw(seed, (uint32_t)e, STEP_RESET, P_ARRIVAL, 0, 0);
+      next_arr = -dlog(unit(w.x, w.y)) * pick<kMaxS>(p.mean_gap, (int)proc);
+    }
+  }
+  const int nsys = p.shadow ? 2 : 1;
+  for (int sy = 0; sy < nsys; ++sy) {
+    const SysState& s = g.sys[sy];
+    s.qpack[e] = 0u;
+    s.hpack[e] = 0u;
+    for (int c = 0; c < p.C; ++c) s.hts[(size_t)c * E + e] = 0.0;
+    for (int j = 0; j < p.K; ++j) {
+      s.busy[(size_t)j * E + e] = 0.0;
+      s.meta[(size_t)j * E + e] = 0xffu << 16;
+    }
+    for (int i = 0; i < kNcnt; ++i) s.cnt[(size_t)i * E + e] = 0u;
+    s.sums[e] = 0.0;
+    s.sums[E + e] = 0.0;
+    s.chk[e] = kFnvInit;
+    s.proc[e] = proc;
+    s.next_sw[e] = next_sw;
+    s.next_arr[e] = next_arr;
+    s.tr_idx[e] = 0u;
+  }
+  for (int r = 0; r < 4; ++r) g.ewma[(size_t)r * E + e] = 0.0;
+  // obs_0 is all zeros: empty queues, idle servers, no last batch (class feature
+  // (none + 1)/C = 0), zero rates
+  for (int i = 0; i < p.F; ++i) g.obs[(size_t)i * E + e] = 0.0f;
+}
+
+// per-env counters out: [2][7][E] int64 (7th = inflight), sums [2][2][E]
+__global__ void counters_k(SimParams p, EnvState g, int64_t* cnt, double* sums) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= p.E) return;
+  const size_t E = (size_t)p.E;
+  for (int sy = 0; sy < 2; ++sy) {
+    const bool on = sy == 0 || p.shadow;
+    const SysState& s = g.sys[sy];
+    if (cnt) {
+      int64_t* o = cnt + (size_t)sy * 7 * E;
+      int64_t infl = 0;
+      for (int i = 0; i < kNcnt; ++i)
+        o[(size_t)i * E + e] = on ? (int64_t)s.cnt[(size_t)i * E + e] : 0;
+      if (on)
+        for (int j = 0; j < p.K; ++j) infl += s.meta[(size_t)j * E + e] & 0xffu;
+      o[(size_t)6 * E + e] = infl;
+    }
+    if (sums) {
+      double* o = sums + (size_t)sy * 2 * E;
+      o[e] = on ? s.sums[e] : 0.0;
+      o[E + e] = on ? s.sums[E + e] : 0.0;
+    }
+  }
+}
+
+// totals over environments: wave shuffle reduction, then one atomic per wave
+__global__ __launch_bounds__(256) void totals_k(SimParams p, EnvState g, int64_t* tc, double* ts) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t E = (size_t)p.E;
+  const int lane = threadIdx.x & 63;
+  for (int sy = 0; sy < 2; ++sy) {
+    const bool on = (sy == 0 || p.shadow) && e < p.E;
+    const SysState& s = g.sys[sy];
+    for (int i = 0; i < 7; ++i) {
+      long long v = 0;
+      if (on) {
+        if (i < kNcnt) {
+          v = s.cnt[(size_t)i * E + e];
+        } else {
+          for (int j = 0; j < p.K; ++j) v += s.meta[(size_t)j * E + e] & 0xffu;
+        }
+      }
+      for (int off = 32; off > 0; off >>= 1) v += __shfl_down(v, off, 64);
+      if (lane == 0 && v) atomicAdd((unsigned long long*)&tc[sy * 7 + i], (unsigned long long)v);
+    }
+    for (int i = 0; i < 2; ++i) {
+      double v = on ? s.sums[(size_t)i * E + e] : 0.0;
+      for (int off = 32; off > 0; off >>= 1) v += __shfl_down(v, off, 64);
+      if (lane == 0) atomicAdd(&ts[sy * 2 + i], v);
+    }
+  }
+}
+
+template <int CM>
+void launch_static_c(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
+                     double* rew_sh, hipStream_t st) {
+  const dim3 grid((p.E + 255) / 256), block(256);
+  if (p.K <= 1) hipLaunchKernelGGL((static_k<1, CM>), grid, block, 0, st, p, s, seed, k, rew_sh);
+  else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM>), grid, block, 0, st, p, s, seed, k, rew_sh);
+  else if (p.K <= 8) hipLaunchKernelGGL((static_k<8, CM>), grid, block, 0, st, p, s, seed, k, rew_sh);
+  else hipLaunchKernelGGL((static_k<16, CM>), grid, block, 0, st, p, s, seed, k, rew_sh);
+}
+
+}  // namespace
+
+hipError_t launch_reset(const SimParams& p, const EnvState& s, uint64_t seed, hipStream_t st) {
+  hipLaunchKernelGGL(reset_k, dim3((p.E + 255) / 256), dim3(256), 0, st, p, s, seed);
+  return hipGetLastError();
+}
+
+hipError_t launch_step(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
+                       const uint8_t* act, float* obs_out, double* rew, uint64_t* rchk,
+                       hipStream_t st) {
+  const dim3 grid((p.E + 255) / 256), block(256);
+  if (p.C <= 1)
+    hipLaunchKernelGGL(learned_k<1>, grid, block, 0, st, p, s, seed, k, act, obs_out, rew, rchk);
+  else if (p.C <= 2)
+    hipLaunchKernelGGL(learned_k<2>, grid, block, 0, st, p, s, seed, k, act, obs_out, rew, rchk);
+  else
+    hipLaunchKernelGGL(learned_k<4>, grid, block, 0, st, p, s, seed, k, act, obs_out, rew, rchk);
+  return hipGetLastError();
+}
+
+hipError_t launch_static(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
+                         double* rew_sh, hipStream_t st) {
+  if (p.C <= 1) launch_static_c<1>(p, s, seed, k, rew_sh, st);
+  else if (p.C <= 2) launch_static_c<2>(p, s, seed, k, rew_sh, st);
+  else launch_static_c<4>(p, s, seed, k, rew_sh, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_counters(const SimParams& p, const EnvState& s, int64_t* cnt, double* sums,
+                           hipStream_t st) {
+  hipLaunchKernelGGL(counters_k, dim3((p.E + 255) / 256), dim3(256), 0, st, p, s, cnt, sums);
+  return hipGetLastError();
+}
+
+hipError_t launch_totals(const SimParams& p, const EnvState& s, int64_t* d_tot_cnt,
+                         double* d_tot_sum, hipStream_t st) {
+  hipLaunchKernelGGL(totals_k, dim3((p.E + 255) / 256), dim3(256), 0, st, p, s, d_tot_cnt,
+                     d_tot_sum);
+  return hipGetLastError();
+}
+
+}  // namespace bsim

@@ -1,0 +1,371 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, on the same seeded
+inputs. Integer state bit-exact; fp64 floats within 1e-9 relative; fp32/bf16 policy
+outputs within a tolerance derived from the rounding points (see the MLP tests)."""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from workloads import preset, trace_preset
+from workloads.gen import seeded_actions, seeded_obs, seeded_rewards_values
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "hand_traces.json")))
+NAMES = ["C1", "C2", "C3", "C4", "C5"]
+RTOL = 1e-9
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def bs():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2607_05272_amd as m
+    m.load()
+    return m
+
+
+def gpu_run_actions(bs, w, E, T, seed, acts, store_obs=True):
+    """reset + T sim_step calls with the given actions [T][E] (host uint8)."""
+    sim = bs.Sim(w, n_envs=E)
+    sim.reset(seed)
+    dev = torch.device("cuda")
+    obs = [sim.obs()] if store_obs else None
+    rew, rsh = [], []
+    a_dev = torch.from_numpy(np.ascontiguousarray(acts)).to(dev)
+    for k in range(T):
+        o, r, rs = sim.step(a_dev[k], want_obs=store_obs)
+        if store_obs:
+            obs.append(o)
+        rew.append(r)
+        if rs is not None:
+            rsh.append(rs)
+    sim.sync()
+    cnt, sums = sim.counters()
+    chk = sim.checksums()
+    tot = sim.stats()
+    out = dict(reward=torch.stack(rew).cpu().numpy(),
+               cnt=cnt.cpu().numpy(), sums=sums.cpu().numpy(),
+               chk=chk.cpu().numpy().view(np.uint64), tot=tot)
+    if rsh:
+        out["reward_shadow"] = torch.stack(rsh).cpu().numpy()
+    if store_obs:
+        out["obs"] = torch.stack(obs).cpu().numpy()  # [T+1][F][E]
+    sim.close()
+    return out
+
+
+def assert_close_rel(a, b, what):
+    a = np.asarray(a); b = np.asarray(b)
+    err = np.abs(a - b) / np.maximum(np.abs(b), 1e-300)
+    bad = ~((err <= RTOL) | (a == b))
+    assert not bad.any(), f"{what}: {bad.sum()} mismatches, first at {np.argwhere(bad)[0]}"
+
+
+def compare_sim(orc_res, g, w, env_cols, nsys):
+    """Oracle result for envs env_cols (in that order) vs GPU arrays indexed by env."""
+    for s in range(nsys):
+        assert np.array_equal(g["chk"][s, env_cols], orc_res["chk"][:, s]), f"checksum sys {s}"
+        assert np.array_equal(g["cnt"][s, :, env_cols], orc_res["counters"][:, s]), f"counters sys {s}"
+        assert_close_rel(g["sums"][s, :, env_cols], orc_res["sums"][:, s, :2], f"sums sys {s}")
+    assert_close_rel(g["reward"][:, env_cols], orc_res["reward"], "reward")
+    if nsys == 2:
+        assert_close_rel(g["reward_shadow"][:, env_cols], orc_res["reward_shadow"], "reward_shadow")
+    if "obs" in g:
+        go = np.transpose(g["obs"][:, :, env_cols], (0, 2, 1))
+        assert np.array_equal(go, orc_res["obs"]), "observations differ"
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_sim_step_parity_small(bs, orc, name):
+    """All envs of a 300-env batch (one full block of 256 + a ragged tail), 200 ticks,
+    seeded actions: checksums, counters, rewards and observations against the oracle."""
+    w = preset(name)
+    E, T, seed = 300, 200, 0xC0FFEE + NAMES.index(name)
+    acts = seeded_actions(seed, T, E, 6 * w["n_servers"], small_bias=0.5)
+    say(f"[parity-small] {name} E={E} T={T}")
+    g = gpu_run_actions(bs, w, E, T, seed, acts)
+    r = orc.rollout(w, seed, T, np.arange(E), actions=acts)
+    nsys = 2 if w["shadow"] else 1
+    compare_sim(r, g, w, np.arange(E), nsys)
+    assert g["cnt"][0, 3].sum() > 0 and g["cnt"][0, 0].sum() > 0
+    # device totals equal the per-env counters summed
+    assert np.array_equal(g["tot"]["cnt"][0], g["cnt"][0].sum(axis=1))
+    if nsys == 2:
+        assert np.array_equal(g["tot"]["cnt"][1], g["cnt"][1].sum(axis=1))
+
+
+def _step_actions(seed, k, E, A):
+    return np.random.default_rng([seed, k]).integers(0, A, size=E, dtype=np.int64).astype(np.uint8)
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_sim_step_parity_full_size_sampled(bs, orc, name):
+    """Full E and T of each configuration in the simulator kernels' launch shape; the
+    oracle replays sampled envs (first, last, a spread and a random set) under the same
+    seeded per-step actions."""
+    w = preset(name)
+    E, T = w["n_envs"], w["T"]
+    seed = 0xC0FFEE + NAMES.index(name)
+    A = 6 * w["n_servers"]
+    rng = np.random.default_rng(seed)
+    cols = np.unique(np.concatenate([[0, 1, 255, 256, E - 1], rng.choice(E, 27, replace=False)]))
+    cols = cols[cols < E]
+    say(f"[parity-full] {name} E={E} T={T} sampled={len(cols)}")
+    sim = bs.Sim(w)
+    sim.reset(seed)
+    dev = torch.device("cuda")
+    rew = np.zeros((T, len(cols)))
+    rsh = np.zeros((T, len(cols)))
+    acts_cols = np.zeros((T, len(cols)), np.uint8)
+    cols_dev = torch.from_numpy(cols).to(dev)
+    for k in range(T):
+        a = _step_actions(seed, k, E, A)
+        acts_cols[k] = a[cols]
+        _, r, rs = sim.step(torch.from_numpy(a).to(dev), want_obs=False)
+        rew[k] = r[cols_dev].cpu().numpy()
+        if rs is not None:
+            rsh[k] = rs[cols_dev].cpu().numpy()
+        if k % 512 == 0:
+            say(f"  tick {k}")
+    sim.sync()
+    cnt, sums = sim.counters()
+    chk = sim.checksums().cpu().numpy().view(np.uint64)
+    cnt = cnt.cpu().numpy(); sums = sums.cpu().numpy()
+    sim.close()
+    res = orc.rollout(w, seed, T, cols, actions=acts_cols, want_obs=False, want_rec=False)
+    nsys = 2 if w["shadow"] else 1
+    for s in range(nsys):
+        assert np.array_equal(chk[s, cols], res["chk"][:, s]), f"checksum sys {s}"
+        assert np.array_equal(cnt[s][:, cols].T, res["counters"][:, s])
+        assert_close_rel(sums[s][:, cols].T, res["sums"][:, s, :2], "sums")
+    assert_close_rel(rew, res["reward"], "reward")
+    if nsys == 2:
+        assert_close_rel(rsh, res["reward_shadow"], "reward_shadow")
+
+
+def _trace_tensors(g, dev):
+    arr = g["arrivals"]
+    L = len(arr)
+    times = torch.tensor([[a[0] for a in arr]], dtype=torch.float64, device=dev)
+    cls = torch.tensor([[a[1] for a in arr]], dtype=torch.uint8, device=dev)
+    cnt = torch.tensor([L], dtype=torch.int32, device=dev)
+    return times, cls, cnt, L
+
+
+@pytest.mark.parametrize("tr", ["T1", "T2", "T3"])
+def test_hand_traces_on_gpu(bs, orc, tr):
+    g = GOLD[tr]
+    w = trace_preset(**g["cfg"])
+    dev = torch.device("cuda")
+    times, cls, cnt, L = _trace_tensors(g, dev)
+    w["trace_max_len"] = L
+    T = g["T"]
+    if tr == "T1":
+        acts = np.full((T, 1), g["action"], np.uint8)
+    elif tr == "T2":
+        acts = np.array(g["actions"], np.uint8)[:, None]
+    else:
+        acts = np.zeros((T, 1), np.uint8)
+    say(f"[trace] {tr}")
+    sim = bs.Sim(w, n_envs=1)
+    sim.set_trace(times, cls, cnt)
+    sim.reset(0)
+    rews, rshs, obs = [], [], [sim.obs()]
+    a_dev = torch.from_numpy(acts).to(dev)
+    for k in range(T):
+        o, r, rs = sim.step(a_dev[k])
+        rews.append(r); obs.append(o)
+        if rs is not None:
+            rshs.append(rs)
+    sim.sync()
+    rew = torch.stack(rews).cpu().numpy()[:, 0]
+    cnt_, sums = sim.counters()
+    cnt_ = cnt_.cpu().numpy(); sums = sums.cpu().numpy()
+    if tr in ("T1", "T2"):
+        for k, v in g["rewards"].items():
+            assert abs(rew[int(k)] - v) <= 1e-9 * max(1.0, abs(v))
+        nz = [k for k in range(T) if str(k) not in g["rewards"]]
+        assert np.all(rew[nz] == 0.0)
+    if tr == "T1":
+        o1 = obs[1].cpu().numpy()[:, 0]
+        np.testing.assert_allclose(o1, np.array(g["obs1"], np.float32), rtol=1e-6)
+        assert cnt_[0, 2, 0] == g["dropped_cum"][-1] and cnt_[0, 5, 0] == g["completed_cum"][-1]
+    if tr == "T3":
+        assert abs(sums[1, 0, 0] - g["shadow_latency_sum"]) < 1e-12
+        assert cnt_[1, 4, 0] == len(g["shadow_dispatches"])
+    # and the oracle agrees on everything
+    trace = dict(times=times.cpu().numpy(), classes=cls.cpu().numpy(), counts=cnt.cpu().numpy())
+    res = orc.rollout(w, 0, T, [0], actions=acts, trace=trace)
+    assert np.array_equal(sim.checksums().cpu().numpy().view(np.uint64)[:, 0][: 2 if w["shadow"] else 1],
+                          res["chk"][0, : 2 if w["shadow"] else 1])
+    sim.close()
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_init_weights_bit_identical(bs, orc, name):
+    w = preset(name)
+    sim = bs.Sim(w, n_envs=64)
+    buf = sim.init_weights(1234)
+    torch.cuda.synchronize()
+    got = bs.unpack_weights(w, buf.cpu().numpy())
+    ref = orc.init_weights(w, 1234)
+    for k in ("w1", "b1", "w2", "b2", "w3", "b3"):
+        assert np.array_equal(got[k], ref[k]), k
+    sim.close()
+
+
+def mlp_tol(w, wts, obs):
+    """Per-output tolerance |gpu - oracle| <= tol_a = c * sum_i |W3_ia| |h2_i| + |b3_a| eps.
+
+    fp32 mode: only accumulation order differs (fp32 sums of <= 64 terms): c = 2^-18.
+    bf16 mode: each layer input is rounded to bf16; a value whose fp32 (GPU) and fp64
+    (oracle) pre-rounding images straddle a rounding boundary can round one bf16 ulp
+    (2^-8 relative) apart, and the two hidden layers propagate such flips, so c = 2^-6
+    (one ulp at each of the two hidden rounding points, with a factor-of-two margin)."""
+    import torch.nn.functional as Fn
+    bf = bool(w["mlp_bf16"])
+
+    def rnd(t):
+        return t.to(torch.float32).to(torch.bfloat16).to(torch.float64) if bf else t
+    x = rnd(torch.tensor(obs, dtype=torch.float64))
+    W = {k: torch.tensor(v, dtype=torch.float64) for k, v in wts.items()}
+    h1 = rnd(Fn.gelu(x @ W["w1"] + W["b1"]))
+    h2 = rnd(Fn.gelu(h1 @ W["w2"] + W["b2"]))
+    scale = (h2.abs() @ W["w3"].abs()).numpy() + np.abs(wts["b3"])[None, :]
+    return scale * (2.0 ** -6 if bf else 2.0 ** -18)
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_policy_parity(bs, orc, name):
+    """MLP logits/value within the derived tolerance; sampled actions identical wherever
+    the oracle's uniform is farther than 2*max|dlogit| from a CDF boundary; logp close."""
+    w = preset(name)
+    E = 1000
+    step = 17
+    seed = 0x5EED
+    wts = orc.init_weights(w, 99)
+    obs = seeded_obs(21, E, w["obs_dim"])
+    say(f"[policy] {name}")
+    sim = bs.Sim(w, n_envs=E)
+    sim.reset(seed)
+    wb = sim.upload_weights(wts)
+    out = sim.policy(wb, torch.from_numpy(np.ascontiguousarray(obs.T)).cuda(), step, want_logits=True)
+    torch.cuda.synchronize()
+    lg = out["logits"].cpu().numpy().T.astype(np.float64)
+    act = out["actions"].cpu().numpy()
+    logp = out["logp"].cpu().numpy().astype(np.float64)
+    ref = orc.policy(w, wts, seed, step, obs, np.arange(E))
+    tol = mlp_tol(w, wts, obs)
+    err = np.abs(lg - ref["logits"])
+    assert np.all(err <= tol), f"max err/tol {np.max(err / tol):.3g}"
+    A = 6 * w["n_servers"]
+    eps = 2 * err[:, :A].max(axis=1) + 1e-5
+    sure = ref["margin"] > eps
+    assert np.array_equal(act[sure], ref["actions"][sure]), "actions differ away from ties"
+    say(f"  near-ties {np.sum(~sure)} of {E}; max logit err {err.max():.3g}")
+    assert np.all(np.abs(logp[sure] - ref["logp"][sure]) <= eps[sure] + 1e-5)
+    if w["value_head"]:
+        v = out["value"].cpu().numpy()
+        assert np.array_equal(v, lg[:, A].astype(np.float32))
+    sim.close()
+
+
+@pytest.mark.parametrize("name", ["C1", "C3", "C5"])
+def test_gae_bit_exact(bs, orc, name):
+    w = preset(name)
+    T, E = 300, 777
+    r, v = seeded_rewards_values(5, T, E, value=bool(w["value_head"]))
+    sim = bs.Sim(w, n_envs=E)
+    lam = w["lam"]
+    rd = torch.from_numpy(r).cuda()
+    vd = torch.from_numpy(v).cuda() if v is not None else None
+    adv, ret = sim.returns_gae(rd, vd, w["gamma"], lam)
+    torch.cuda.synchronize()
+    ra, rr = orc.gae(r, v, w["gamma"], lam)
+    assert np.array_equal(adv.cpu().numpy(), ra)
+    assert np.array_equal(ret.cpu().numpy(), rr)
+    sim.close()
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_rollout_parity_and_validity(bs, orc, name):
+    """sim_rollout (policy + sampler + simulator, T ticks) checked three ways:
+    (1) the oracle's own policy rollout with the same weights agrees exactly, per env, on
+        every tick before the first decision whose uniform lies within the tie band of a
+        CDF boundary (the band is 2*max|dlogit| + 1e-5, measured below);
+    (2) validity of the simulator part: replaying the rollout's actions in the oracle gives
+        the same running checksums, rewards and observations at every tick;
+    (3) validity of every decision: on the rollout's observations the oracle policy picks
+        the same action wherever its uniform is outside the tie band."""
+    w = preset(name)
+    E, T, seed = 300, 100, 0xC0FFEE + 10 + NAMES.index(name)
+    A = 6 * w["n_servers"]
+    wts = orc.init_weights(w, 7)
+    say(f"[rollout] {name}")
+    sim = bs.Sim(w, n_envs=E)
+    sim.reset(seed)
+    wb = sim.upload_weights(wts)
+    tr = sim.rollout(wb, T, store_obs=True, rchk=True)
+    sim.sync()
+    ga = tr.actions.cpu().numpy()
+    gr = tr.reward.cpu().numpy()
+    gobs = tr.obs.cpu().numpy()                      # [T+1][F][E]
+    go = np.transpose(gobs, (0, 2, 1))               # [T+1][E][F]
+    grchk = tr.rchk.cpu().numpy().view(np.uint64)
+    # (2) replay of the rollout's actions
+    rep = orc.rollout(w, seed, T, np.arange(E), actions=ga, want_rchk=True)
+    assert np.array_equal(rep["rchk"], grchk), "running checksums differ"
+    assert_close_rel(gr, rep["reward"], "reward")
+    assert np.array_equal(rep["obs"], go), "observations differ"
+    # (3) every decision against the oracle policy on the same observation
+    lg_err = 0.0
+    ties = 0
+    band_te = np.zeros((T, E))
+    for t in range(T):
+        out = sim.policy(wb, tr.obs[t].contiguous(), t, want_logits=True)
+        glg = out["logits"].cpu().numpy().T.astype(np.float64)
+        ref = orc.policy(w, wts, seed, t, go[t], np.arange(E))
+        err = np.abs(glg - ref["logits"])[:, :A].max(axis=1)
+        lg_err = max(lg_err, float(err.max()))
+        band_te[t] = 2 * err + 1e-5
+        sure = ref["margin"] > band_te[t]
+        ties += int(np.sum(~sure))
+        assert np.array_equal(ga[t][sure], ref["actions"][sure]), f"tick {t}: decision differs"
+    # (1) independent rollout of the oracle, compared before the first near-tie; on that
+    # common prefix both sides saw the same observations, so the band measured in (3)
+    # for (t, env) applies
+    res = orc.rollout(w, seed, T, np.arange(E), weights=wts)
+    tie = res["margin"] <= band_te
+    first = np.where(tie.any(axis=0), tie.argmax(axis=0), T)
+    checked = 0
+    for e in range(E):
+        f = first[e]
+        assert np.array_equal(ga[:f, e], res["actions"][:f, e]), f"env {e} actions before tick {f}"
+        assert_close_rel(gr[:f, e], res["reward"][:f, e], f"env {e} reward")
+        assert np.array_equal(go[: f + 1, e], res["obs"][: f + 1, e]), f"env {e} obs"
+        checked += f
+    say(f"  max|dlogit| {lg_err:.3g}, decisions in tie band {ties}/{E * T}, "
+        f"independent prefix covers {checked}/{E * T} env-ticks")
+    assert checked > 0
+    sim.close()
+
+
+def test_action_out_of_range_is_latched(bs):
+    w = preset("C1")
+    sim = bs.Sim(w, n_envs=70)
+    sim.reset(1)
+    a = torch.zeros(70, dtype=torch.uint8, device="cuda")
+    a[69] = 6
+    sim.step(a)
+    with pytest.raises(bs.SimError, match="action out of range"):
+        sim.sync()
+    sim.sync()  # the flag was cleared
+    sim.close()
