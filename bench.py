@@ -126,7 +126,19 @@ def main():
     ap.add_argument("--ticks", type=int, default=0, help="override T (diagnostics only)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="only copy this many MiB device-to-device (HBM counter calibration)")
     args = ap.parse_args()
+    if args.calib_copy_mib:
+        import torch
+        n = args.calib_copy_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calib_copy_bytes": n, "copies": 3}))
+        return
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU only (environments are independent; the "
               "multi-GPU design is described in DESIGN.md but not built). Use --gpus 1.",

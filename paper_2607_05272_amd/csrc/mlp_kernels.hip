@@ -217,6 +217,241 @@ __global__ void zero_f32_k(float* p, int n) {
   if (i < n) p[i] = 0.f;
 }
 
+// ---- bf16 policy kernel: 16*RT environments per workgroup, NW waves ------------------------
+// Every layer is computed transposed, out^T = W^T act^T: the weight tile is the MFMA A
+// operand (16 output units x 32 inputs, 16 contiguous bytes per lane from the out-major
+// repacked weights) and the activation tile the B operand (32 inputs x 16 environments, 16
+// contiguous bytes per lane from the row-major [env][unit] LDS buffer). A lane's four
+// accumulator values are then four consecutive output units of one environment, so the
+// epilogue writes them to the next layer's buffer as one 8-byte store after two packed
+// fp32->bf16 conversions. Each wave owns a disjoint set of output-unit tiles, so a workgroup
+// reads every weight once (from L2); the next k-step's weight fragments are loaded while
+// the current step's MFMAs run.
+typedef __attribute__((ext_vector_type(2))) float f32x2;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
+}
+
+template <int K, int N, int RT, int NW>
+__device__ __forceinline__ void mma_t(const uint16_t* __restrict__ act, int sa,
+                                      const uint16_t* __restrict__ W,
+                                      f32x4 (&acc)[(N / 16 + NW - 1) / NW][RT]) {
+  constexpr int NT = N / 16, CTW = (NT + NW - 1) / NW, KS = K / 32;
+  constexpr bool kEven = NT % NW == 0;  // every wave owns CTW output tiles
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kq = lane >> 4;
+#pragma unroll
+  for (int c = 0; c < CTW; ++c)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) acc[c][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 w[2][CTW];
+  const uint16_t* wbase = W + (size_t)(wave * 16 + r16) * K + kq * 8;
+  constexpr size_t WSTEP = (size_t)NW * 16 * K;  // elements between a wave's output tiles
+  const uint16_t* brow = act + r16 * sa + kq * 8;
+  auto loadw = [&](int buf, int ks) {
+#pragma unroll
+    for (int c = 0; c < CTW; ++c)
+      if (kEven || wave + NW * c < NT)
+        w[buf][c] = *reinterpret_cast<const bf16x8*>(wbase + c * WSTEP + ks * 32);
+  };
+  auto mma = [&](int buf, int ks) {
+    bf16x8 b[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+      b[rt] = *reinterpret_cast<const bf16x8*>(brow + rt * 16 * sa + ks * 32);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int c = 0; c < CTW; ++c)
+        if (kEven || wave + NW * c < NT)
+          acc[c][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[buf][c], b[rt], acc[c][rt], 0, 0, 0);
+  };
+  loadw(0, 0);
+#pragma unroll 1
+  for (int ks = 0; ks < KS; ks += 2) {
+    if (ks + 1 < KS) loadw(1, ks + 1);
+    mma(0, ks);
+    if (ks + 2 < KS) loadw(0, ks + 2);
+    if (ks + 1 < KS) mma(1, ks + 1);
+  }
+}
+
+// GELU(x) = x Phi(x) = relu(x) - 0.5 |x| erfc(|x| / sqrt 2) (x erf(x/sqrt2) is even in x),
+// with erfc from Abramowitz & Stegun, Handbook of Mathematical Functions, formula 7.1.26:
+// erfc(z) = (a1 t + a2 t^2 + ... + a5 t^5) exp(-z^2), t = 1 / (1 + p z), |error| <= 1.5e-7,
+// far below the bf16 rounding that follows. Constants: p / sqrt 2 and a_i / 2 are folded in;
+// exp(-x^2 / 2) = 2^(-x^2 log2(e) / 2).
+__device__ __forceinline__ float gelu_fast(float x) {
+  const float a = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.23164189f, a, 1.0f));   // p / sqrt 2
+  float poly = fmaf(0.5307027145f, t, -0.7265760135f);                // a5/2, a4/2
+  poly = fmaf(poly, t, 0.7107068705f);                                // a3/2
+  poly = fmaf(poly, t, -0.142248368f);                                // a2/2
+  poly = fmaf(poly, t, 0.127414796f);                                 // a1/2
+  const float e = __builtin_amdgcn_exp2f((x * -0.72134752044f) * x);   // exp(-x^2/2)
+  return fmaxf(x, 0.0f) - (a * (poly * t)) * e;
+}
+
+// bias + GELU + bf16 rounding; four consecutive units of one environment per 8-byte store
+template <int N, int RT, int NW>
+__device__ __forceinline__ void store_hidden_t(const f32x4 (&acc)[(N / 16 + NW - 1) / NW][RT],
+                                               const float* __restrict__ bias, uint16_t* out,
+                                               int so) {
+  constexpr int NT = N / 16, CTW = (NT + NW - 1) / NW;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kq = lane >> 4;
+#pragma unroll
+  for (int c = 0; c < CTW; ++c) {
+    const int ot = wave + NW * c;
+    if (ot >= NT) continue;
+    const int u0 = ot * 16 + kq * 4;
+    const f32x4 bv = *reinterpret_cast<const f32x4*>(bias + u0);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const f32x4 v = acc[c][rt];
+      u32x2 pk;
+      pk.x = pack_bf16(gelu_fast(v[0] + bv[0]), gelu_fast(v[1] + bv[1]));
+      pk.y = pack_bf16(gelu_fast(v[2] + bv[2]), gelu_fast(v[3] + bv[3]));
+      *reinterpret_cast<u32x2*>(out + (rt * 16 + r16) * so + u0) = pk;
+    }
+  }
+}
+
+template <int FP, int H1, int H2, int AP, int RT, int NW>
+struct BigShape {
+  static constexpr int ROWS = 16 * RT;
+  static constexpr int SX = FP + 8, SH = (H1 > H2 ? H1 : H2) + 8, SL = AP + 4;
+  static constexpr size_t X_BYTES = (size_t)ROWS * SX * 2;
+  static constexpr size_t H_BYTES = (size_t)ROWS * SH * 2;
+  static constexpr size_t L_BYTES = (size_t)ROWS * SL * 4;
+  static constexpr size_t HREG = H_BYTES > L_BYTES ? H_BYTES : L_BYTES;
+  static constexpr size_t LDS = X_BYTES + HREG;
+};
+
+template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB>
+__global__ __launch_bounds__(NW * 64, MINB) void policy_bf16_k(MlpParams m, const float* __restrict__ obs,
+                                                               uint64_t seed, uint32_t step,
+                                                               uint8_t* __restrict__ act,
+                                                               float* __restrict__ logp,
+                                                               float* __restrict__ value,
+                                                               float* __restrict__ logits) {
+  typedef BigShape<FP, H1, H2, AP, RT, NW> Sh;
+  constexpr int ROWS = Sh::ROWS, NTHR = NW * 64;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  uint16_t* xs = reinterpret_cast<uint16_t*>(smem);
+  uint16_t* hs = reinterpret_cast<uint16_t*>(smem + Sh::X_BYTES);
+  float* lg = reinterpret_cast<float*>(smem + Sh::X_BYTES);
+  const int e0 = blockIdx.x * ROWS;
+  const int tid = threadIdx.x;
+  // stage x: obs [F][E] fp32 -> [env][feature] bf16, two features per 4-byte store
+  for (int idx = tid; idx < ROWS * (FP / 2); idx += NTHR) {
+    const int r = idx % ROWS, f = 2 * (idx / ROWS);
+    const int e = e0 + r;
+    float v0 = 0.f, v1 = 0.f;
+    if (e < m.E) {
+      if (f < m.F) v0 = obs[(size_t)f * m.E + e];
+      if (f + 1 < m.F) v1 = obs[(size_t)(f + 1) * m.E + e];
+    }
+    *reinterpret_cast<uint32_t*>(xs + r * Sh::SX + f) = pack_bf16(v0, v1);
+  }
+  __syncthreads();
+  {
+    f32x4 acc[(H1 / 16 + NW - 1) / NW][RT];
+    mma_t<FP, H1, RT, NW>(xs, Sh::SX, static_cast<const uint16_t*>(m.w1), acc);
+    store_hidden_t<H1, RT, NW>(acc, m.b1, hs, Sh::SH);
+  }
+  __syncthreads();
+  {
+    f32x4 acc[(H2 / 16 + NW - 1) / NW][RT];
+    mma_t<H1, H2, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w2), acc);
+    __syncthreads();  // every wave has finished reading h1
+    store_hidden_t<H2, RT, NW>(acc, m.b2, hs, Sh::SH);
+  }
+  __syncthreads();
+  {
+    constexpr int NT = AP / 16, CTW = (NT + NW - 1) / NW;
+    f32x4 acc[CTW][RT];
+    mma_t<H2, AP, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w3), acc);
+    __syncthreads();  // every wave has finished reading h2
+    const int lane = tid & 63, wave = tid >> 6, r16 = lane & 15, kq = lane >> 4;
+#pragma unroll
+    for (int c = 0; c < CTW; ++c) {
+      const int ot = wave + NW * c;
+      if (ot >= NT) continue;
+      const int u0 = ot * 16 + kq * 4;
+      const f32x4 bv = *reinterpret_cast<const f32x4*>(m.b3 + u0);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+        *reinterpret_cast<f32x4*>(lg + (rt * 16 + r16) * Sh::SL + u0) = acc[c][rt] + bv;
+    }
+  }
+  __syncthreads();
+  // sampling: four lanes per environment row (lanes 4r..4r+3 of the workgroup), each over a
+  // contiguous quarter of the actions; max and sum by xor shuffles, then the quarter whose
+  // cumulative range holds u*S walks its actions in order
+  for (int row0 = 0; row0 < ROWS; row0 += NTHR / 4) {
+    const int row = row0 + tid / 4, part = tid & 3;
+    const int e = e0 + row;
+    const bool live = row < ROWS && e < m.E;
+    const float* l = lg + (row < ROWS ? row : 0) * Sh::SL;
+    const int A = m.A;
+    const int chunk = (A + 3) / 4;
+    const int lo = part * chunk, hi = lo + chunk < A ? lo + chunk : A;
+    float mx = -3.0e38f;
+    for (int i = lo; i < hi; ++i) mx = l[i] > mx ? l[i] : mx;
+    mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
+    float part_sum = 0.f;
+    for (int i = lo; i < hi; ++i) part_sum += __expf(l[i] - mx);
+    const float s0 = __shfl(part_sum, (tid & ~3) & 63, 64), s1 = __shfl(part_sum, ((tid & ~3) + 1) & 63, 64);
+    const float s2 = __shfl(part_sum, ((tid & ~3) + 2) & 63, 64), s3 = __shfl(part_sum, ((tid & ~3) + 3) & 63, 64);
+    const float S = (s0 + s1) + (s2 + s3);
+    const float before = part == 0 ? 0.f : part == 1 ? s0 : part == 2 ? s0 + s1 : (s0 + s1) + s2;
+    const u32x4 w = draw(seed, (uint32_t)(live ? e : 0), step, P_ACTION, 0, 0);
+    const float u = ((float)(w.x >> 9) + 0.5f) * 0x1p-23f;
+    const float target = u * S;
+    int found = -1;
+    if (live && (act || logp)) {
+      float cum = before;
+      for (int i = lo; i < hi; ++i) {
+        cum += __expf(l[i] - mx);
+        if (target < cum) { found = i; break; }
+      }
+    }
+    const int f0 = __shfl(found, (tid & ~3) & 63, 64), f1 = __shfl(found, ((tid & ~3) + 1) & 63, 64);
+    const int f2 = __shfl(found, ((tid & ~3) + 2) & 63, 64), f3 = __shfl(found, ((tid & ~3) + 3) & 63, 64);
+    if (live && part == 0) {
+      const int a = f0 >= 0 ? f0 : f1 >= 0 ? f1 : f2 >= 0 ? f2 : f3 >= 0 ? f3 : A - 1;
+      if (act) act[e] = (uint8_t)a;
+      if (logp) logp[e] = (l[a] - mx) - __logf(S);
+      if (value && m.value_head) value[e] = l[A];
+    }
+    if (live && logits)
+      for (int i = part; i < m.Ap; i += 4) logits[(size_t)i * m.E + e] = l[i];
+  }
+}
+
+template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB>
+hipError_t run_policy_bf16(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
+                           uint8_t* act, float* logp, float* value, float* logits, hipStream_t st) {
+  typedef BigShape<FP, H1, H2, AP, RT, NW> Sh;
+  static_assert(Sh::LDS <= 160 * 1024, "LDS budget");
+  auto kern = policy_bf16_k<FP, H1, H2, AP, RT, NW, MINB>;
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)Sh::LDS);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const dim3 grid((m.E + Sh::ROWS - 1) / Sh::ROWS), block(NW * 64);
+  hipLaunchKernelGGL(kern, grid, block, Sh::LDS, st, m, obs, seed, step, act, logp, value, logits);
+  return hipGetLastError();
+}
+
 template <class M, int FP, int H1, int H2, int AP>
 hipError_t run_policy(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
                       uint8_t* act, float* logp, float* value, float* logits, hipStream_t st) {
@@ -258,14 +493,21 @@ hipError_t launch_policy(const MlpParams& m, const float* obs, uint64_t seed, ui
                          uint8_t* act, float* logp, float* value, float* logits, hipStream_t st) {
   if (!m.bf16 && m.FP == 8 && m.H1 == 64 && m.H2 == 64 && m.AP == 16)
     return run_policy<F32Mode, 8, 64, 64, 16>(m, obs, seed, step, act, logp, value, logits, st);
+  // bf16 shapes: 64-row tiles with 4 waves, two workgroups per CU, when there are enough
+  // rows to fill the chip; 32-row tiles otherwise
+  const bool big = m.E >= 64 * 512;
   if (m.bf16 && m.FP == 32 && m.H1 == 128 && m.H2 == 128 && m.AP == 16)
-    return run_policy<Bf16Mode, 32, 128, 128, 16>(m, obs, seed, step, act, logp, value, logits, st);
+    return big ? run_policy_bf16<32, 128, 128, 16, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, st)
+               : run_policy_bf16<32, 128, 128, 16, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, st);
   if (m.bf16 && m.FP == 32 && m.H1 == 256 && m.H2 == 256 && m.AP == 32)
-    return run_policy<Bf16Mode, 32, 256, 256, 32>(m, obs, seed, step, act, logp, value, logits, st);
+    return big ? run_policy_bf16<32, 256, 256, 32, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, st)
+               : run_policy_bf16<32, 256, 256, 32, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, st);
   if (m.bf16 && m.FP == 64 && m.H1 == 256 && m.H2 == 256 && m.AP == 64)
-    return run_policy<Bf16Mode, 64, 256, 256, 64>(m, obs, seed, step, act, logp, value, logits, st);
+    return big ? run_policy_bf16<64, 256, 256, 64, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, st)
+               : run_policy_bf16<64, 256, 256, 64, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, st);
   if (m.bf16 && m.FP == 96 && m.H1 == 512 && m.H2 == 512 && m.AP == 112)
-    return run_policy<Bf16Mode, 96, 512, 512, 112>(m, obs, seed, step, act, logp, value, logits, st);
+    return big ? run_policy_bf16<96, 512, 512, 112, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, st)
+               : run_policy_bf16<96, 512, 512, 112, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, st);
   return hipErrorInvalidValue;
 }
 

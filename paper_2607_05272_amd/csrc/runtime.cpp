@@ -11,7 +11,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/batchsim.h"
+#include "batchsim.h"
 #include "params.hpp"
 
 using namespace bsim;
