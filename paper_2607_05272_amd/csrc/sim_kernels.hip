@@ -218,6 +218,94 @@ __device__ __forceinline__ int advance(Arrivals& A, const SimParams& p, uint64_t
   return cls;
 }
 
+// ---- wave-cooperative staging of ARRIVAL draws -------------------------------------------
+// Block j of purpose ARRIVAL for (env, tick) gives the exponential variate E_j = -log u(w0,w1)
+// and the class uniform uc_j = u(w2,w3); neither depends on the environment's state, only on
+// j. Each lane walks its events in order and reads E_j, uc_j from a per-wave LDS stage of
+// kStage slots per lane. When lanes run short, the whole wave refills: lane l of the wave
+// computes work items l, l+64, ... of the list (needing lane, block), so the Philox draws and
+// logarithms of a few bursting environments are spread over all 64 lanes.
+constexpr int kStage = 8;
+struct ArrStage {
+  double E[kStage][64];
+  double uc[kStage][64];
+  uint32_t owner[64];
+  uint32_t j0[64];
+};
+
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Called by all 64 lanes of the wave. Lanes with `need` get blocks [jneed, jneed+kStage).
+__device__ __forceinline__ void refill(ArrStage& st, bool need, uint32_t jneed, uint32_t& staged_hi,
+                                       uint64_t seed, int e_lane0, uint32_t k, int lane) {
+  const uint64_t mask = __ballot(need);
+  const int nneed = __popcll(mask);
+  if (need) {
+    const int rank = __popcll(mask & ((1ull << lane) - 1ull));
+    st.owner[rank] = (uint32_t)lane;
+    st.j0[rank] = jneed;
+  }
+  wave_sync_lds();
+  for (int w = lane; w < kStage * nneed; w += 64) {
+    const int r = w / kStage;
+    const uint32_t own = st.owner[r];
+    const uint32_t j = st.j0[r] + (uint32_t)(w % kStage);
+    const u32x4 d = draw(seed, (uint32_t)(e_lane0 + (int)own), k, P_ARRIVAL, j, 0);
+    st.E[j % kStage][own] = -dlog(unit(d.x, d.y));
+    st.uc[j % kStage][own] = unit(d.z, d.w);
+  }
+  wave_sync_lds();
+  if (need) staged_hi = jneed + kStage;
+}
+
+// As `advance`, with ARRIVAL blocks read from the stage (the caller guarantees that the two
+// blocks an instant can consume, a switch redraw and an arrival, are staged).
+template <int CM>
+__device__ __forceinline__ int advance_staged(Arrivals& A, const SimParams& p, const ArrStage& st,
+                                              int lane, uint64_t seed, int e, uint32_t k,
+                                              double now) {
+  if (A.next_sw == now) {
+    const u32x4 w = draw(seed, (uint32_t)e, k, P_PROCESS, A.jproc++, 0);
+    int nxt;
+    if (p.S == 2) {
+      nxt = 1 - (int)A.proc;
+    } else {
+      const int idx = (int)(unit(w.z, w.w) * (double)(p.S - 1));
+      nxt = idx < (int)A.proc ? idx : idx + 1;
+    }
+    A.proc = (uint32_t)nxt;
+    A.next_sw = now + dwell(p, nxt, unit(w.x, w.y));
+    if (pick<kMaxS>(p.rate, nxt) > 0.0) {
+      const uint32_t j = A.jarr++;
+      A.next_arr = now + st.E[j % kStage][lane] * pick<kMaxS>(p.mean_gap, nxt);
+    } else {
+      A.next_arr = kInf;
+    }
+  }
+  if (!(A.next_arr == now)) return -1;
+  int cls;
+  if (p.arrival_kind == 1) {
+    const size_t base = (size_t)e * p.tr_len;
+    cls = p.tr_cls[base + A.tr_idx];
+    if (cls >= p.C) cls = p.C - 1;  // reset validated every class id; never index past C
+    ++A.tr_idx;
+    A.next_arr = (int)A.tr_idx < A.tr_cnt ? p.tr_times[base + A.tr_idx] : kInf;
+  } else {
+    const uint32_t j = A.jarr++;
+    const double uc = st.uc[j % kStage][lane];
+    cls = CM - 1;
+#pragma unroll
+    for (int c = CM - 2; c >= 0; --c)
+      if (uc < p.class_cum[c]) cls = c;
+    A.next_arr = now + st.E[j % kStage][lane] * pick<kMaxS>(p.mean_gap, (int)A.proc);
+  }
+  return cls;
+}
+
 // arrival at `now`: FIFO push, or drop when N requests wait (load shedding)
 template <int CM>
 __device__ __forceinline__ void enqueue(Queue<CM>& Q, Count& C, const SimParams& p, int cls,
@@ -267,17 +355,31 @@ __device__ __forceinline__ double pop_batch(Queue<CM>& Q, Count& C, const SimPar
   const double wh = pick<CM>(p.w_class, h);
   const int N = p.N;
   const double* rb = Q.ring + (size_t)h * N;
-  int pos = Q.hd(h);
+  const int head = Q.hd(h);
   double Lw = C.Lw, lat = C.lat, wlat = C.wlat;
-  for (int i = 0; i < n; ++i) {
-    const double a = rb[pos];
-    pos = pos + 1 == N ? 0 : pos + 1;
-    const double l = cdone - a;
-    const double wl = wh * l;
-    Lw = Lw + wl;
-    lat = lat + l;
-    wlat = wlat + wl;
+  // the timestamps are loaded eight at a time (independent loads in flight together),
+  // then accumulated in FIFO order
+  for (int i0 = 0; i0 < n; i0 += 8) {
+    double a[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      int q = head + i0 + j;
+      q = q >= N ? q - N : q;
+      a[j] = i0 + j < n ? rb[q] : 0.0;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (i0 + j < n) {
+        const double l = cdone - a[j];
+        const double wl = wh * l;
+        Lw = Lw + wl;
+        lat = lat + l;
+        wlat = wlat + wl;
+      }
+    }
   }
+  int pos = head + n;
+  pos = pos >= N ? pos - N : pos;
   C.Lw = Lw; C.lat = lat; C.wlat = wlat;
   const int sh = 8 * h;
   const int qh = Q.q(h) - n;
@@ -319,56 +421,84 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
                                                  float* __restrict__ obs_out,
                                                  double* __restrict__ rew,
                                                  uint64_t* __restrict__ rchk) {
-  const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= p.E) return;
+  __shared__ ArrStage stage[4];
+  const int lane = threadIdx.x & 63;
+  ArrStage& st = stage[threadIdx.x >> 6];
+  const int e_lane0 = blockIdx.x * blockDim.x + (threadIdx.x & ~63);
+  const int e = e_lane0 + lane;
+  // lanes past the last environment stay in the loop (the wave refills together) but idle
+  const bool live = e < p.E;
+  if (__ballot(live) == 0ull) return;
+  const int ee = live ? e : 0;
   const size_t E = (size_t)p.E;
   const SysState& G = g.sys[0];
-  int a = act[e];
+  int a = live ? act[ee] : 0;
   if (a >= 6 * p.K) {
     atomicOr(g.err, ERR_ACTION);
     a = 0;
   }
   const int s = a / 6, b = 1 << (a % 6);
   Queue<CM> Q;
-  load_queue(Q, G, p, e);
+  load_queue(Q, G, p, ee);
   Count C;
-  load_count(C, G, p, e);
+  load_count(C, G, p, ee);
   Arrivals A;
-  load_arrivals(A, G, p, e);
-  double busy_s = G.busy[(size_t)s * E + e];
-  uint32_t meta_s = G.meta[(size_t)s * E + e];
+  load_arrivals(A, G, p, ee);
+  double busy_s = G.busy[(size_t)s * E + ee];
+  uint32_t meta_s = G.meta[(size_t)s * E + ee];
   bool dirty_s = false;
 
   const double t0 = (double)k * p.dt, t1 = (double)(k + 1) * p.dt;
   int A_k = 0;
   double now = t0;
-  for (uint32_t it = 0;; ++it) {
-    if (it > 0) {
-      double te = A.next_sw < A.next_arr ? A.next_sw : A.next_arr;
+  uint32_t staged_hi = 0;
+  bool done = !live;
+  uint32_t it = 0;
+  bool first = true;
+  for (;;) {
+    bool go = false;
+    bool need = false;
+    double te = now;
+    if (!done && !first) {
+      te = A.next_sw < A.next_arr ? A.next_sw : A.next_arr;
       if (busy_s > now && busy_s < te) te = busy_s;
-      if (!(te < t1)) break;
-      if (it > kMaxEventsPerTick) {
+      if (!(te < t1)) {
+        done = true;
+      } else if (it > kMaxEventsPerTick) {
         atomicOr(g.err, ERR_EVENTS);
-        break;
+        done = true;
+      } else {
+        need = p.arrival_kind != 1 && (A.next_sw == te || A.next_arr == te) &&
+               A.jarr + 2u > staged_hi;
+        go = !need;
       }
+    }
+    if (__ballot(need) != 0ull) refill(st, need, A.jarr, staged_hi, seed, e_lane0, k, lane);
+    if (go) {
+      ++it;
       now = te;
-      const int cls = advance<CM>(A, p, seed, e, k, now);
+      const int cls = advance_staged<CM>(A, p, st, lane, seed, ee, k, now);
       if (cls >= 0) {
         ++A_k;
         enqueue(Q, C, p, cls, now);
       }
     }
-    // exactly b requests of the head-of-line class whenever server s is idle
-    while (busy_s <= now && Q.qsum > 0) {
-      double ts;
-      const int h = hol(Q, p, ts);
-      if (Q.q(h) < b) break;
-      C.c[C_DONE] += meta_s & 0xffu;  // the previous batch on s finished at busy_s <= now
-      busy_s = pop_batch(Q, C, p, seed, e, k, 0, s, h, b, now);
-      meta_s = (uint32_t)b | ((uint32_t)b << 8) | ((uint32_t)h << 16);
-      dirty_s = true;
+    if (go || (first && !done)) {
+      // exactly b requests of the head-of-line class whenever server s is idle
+      while (busy_s <= now && Q.qsum > 0) {
+        double ts;
+        const int h = hol(Q, p, ts);
+        if (Q.q(h) < b) break;
+        C.c[C_DONE] += meta_s & 0xffu;  // the previous batch on s finished at busy_s <= now
+        busy_s = pop_batch(Q, C, p, seed, ee, k, 0, s, h, b, now);
+        meta_s = (uint32_t)b | ((uint32_t)b << 8) | ((uint32_t)h << 16);
+        dirty_s = true;
+      }
     }
+    first = false;
+    if (__ballot(!done) == 0ull) break;
   }
+  if (!live) return;
 
   // end of tick: completions before t1 and the per-server part of obs_{k+1}
   float* obs = g.obs;
@@ -468,76 +598,120 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
 }
 
 // ---- static shadow system: one tick ---------------------------------------------------------
+// The set of idle servers {j : busy_j <= now} and the next completion min{busy_j > now} only
+// change at a completion instant or a dispatch, so they are kept as a bit mask and a time and
+// recomputed by one scan of the servers at those points (not at every arrival).
+template <int KM>
+__device__ __forceinline__ void server_scan(const double (&busy)[KM], int K, double now,
+                                            uint32_t& idle, double& next_done) {
+  idle = 0u;
+  next_done = kInf;
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    if (j < K) {
+      if (busy[j] <= now) idle |= 1u << j;
+      else if (busy[j] < next_done) next_done = busy[j];
+    }
+  }
+}
+
 template <int KM, int CM>
 __global__ __launch_bounds__(256) void static_k(SimParams p, EnvState g, uint64_t seed, uint32_t k,
                                                 double* __restrict__ rew) {
-  const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= p.E) return;
+  __shared__ ArrStage stage[4];
+  const int lane = threadIdx.x & 63;
+  ArrStage& st = stage[threadIdx.x >> 6];
+  const int e_lane0 = blockIdx.x * blockDim.x + (threadIdx.x & ~63);
+  const int e = e_lane0 + lane;
+  const bool live = e < p.E;
+  if (__ballot(live) == 0ull) return;
+  const int ee = live ? e : 0;
   const size_t E = (size_t)p.E;
   const SysState& G = g.sys[1];
   Queue<CM> Q;
-  load_queue(Q, G, p, e);
+  load_queue(Q, G, p, ee);
   Count C;
-  load_count(C, G, p, e);
+  load_count(C, G, p, ee);
   Arrivals A;
-  load_arrivals(A, G, p, e);
+  load_arrivals(A, G, p, ee);
   double busy[KM];
   uint32_t meta[KM];
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
-    busy[j] = j < p.K ? G.busy[(size_t)j * E + e] : kInf;
-    meta[j] = j < p.K ? G.meta[(size_t)j * E + e] : 0u;
+    busy[j] = j < p.K ? G.busy[(size_t)j * E + ee] : kInf;
+    meta[j] = j < p.K ? G.meta[(size_t)j * E + ee] : 0u;
   }
   uint32_t dirty = 0;
 
   const double t0 = (double)k * p.dt, t1 = (double)(k + 1) * p.dt;
   int A_k = 0;
   double now = t0;
-  for (uint32_t it = 0;; ++it) {
-    if (it > 0) {
-      double te = A.next_sw < A.next_arr ? A.next_sw : A.next_arr;
-      bool idle = false;
-#pragma unroll
-      for (int j = 0; j < KM; ++j) {
-        if (busy[j] > now && busy[j] < te) te = busy[j];
-        idle = idle || busy[j] <= now;
-      }
-      if (Q.qsum > 0 && idle) {
+  uint32_t idle;
+  double next_done;
+  server_scan(busy, p.K, now, idle, next_done);
+  uint32_t staged_hi = 0;
+  bool done = !live;
+  uint32_t it = 0;
+  bool first = true;
+  for (;;) {
+    bool go = false;
+    bool need = false;
+    double te = now;
+    if (!done && !first) {
+      te = A.next_sw < A.next_arr ? A.next_sw : A.next_arr;
+      if (next_done < te) te = next_done;
+      if (Q.qsum > 0 && idle != 0u) {
         double ts;
         hol(Q, p, ts);
         const double tout = ts + p.static_timeout;
         if (tout > now && tout < te) te = tout;
       }
-      if (!(te < t1)) break;
-      if (it > kMaxEventsPerTick) {
+      if (!(te < t1)) {
+        done = true;
+      } else if (it > kMaxEventsPerTick) {
         atomicOr(g.err, ERR_EVENTS);
-        break;
+        done = true;
+      } else {
+        need = p.arrival_kind != 1 && (A.next_sw == te || A.next_arr == te) &&
+               A.jarr + 2u > staged_hi;
+        go = !need;
       }
+    }
+    if (__ballot(need) != 0ull) refill(st, need, A.jarr, staged_hi, seed, e_lane0, k, lane);
+    if (go) {
+      ++it;
       now = te;
-      const int cls = advance<CM>(A, p, seed, e, k, now);
+      if (next_done == now) server_scan(busy, p.K, now, idle, next_done);
+      const int cls = advance_staged<CM>(A, p, st, lane, seed, ee, k, now);
       if (cls >= 0) {
         ++A_k;
         enqueue(Q, C, p, cls, now);
       }
     }
-    // lowest idle server; min(B, Q_h) of the HoL class if Q_h >= B or its head waited T
-    for (;;) {
-      int j = -1;
-#pragma unroll
-      for (int jj = KM - 1; jj >= 0; --jj)
-        if (busy[jj] <= now) j = jj;
-      if (j < 0 || Q.qsum == 0) break;
-      double ts;
-      const int h = hol(Q, p, ts);
-      const int qh = Q.q(h);
-      if (!(qh >= p.bmax || now >= ts + p.static_timeout)) break;
-      const int n = qh < p.bmax ? qh : p.bmax;
-      C.c[C_DONE] += pick<KM>(meta, j) & 0xffu;
-      put<KM>(busy, j, pop_batch(Q, C, p, seed, e, k, 1, j, h, n, now));
-      put<KM>(meta, j, (uint32_t)n | ((uint32_t)n << 8) | ((uint32_t)h << 16));
-      dirty |= 1u << j;
+    if (go || (first && !done)) {
+      // lowest idle server; min(B, Q_h) of the HoL class if Q_h >= B or its head waited T
+      while (idle != 0u && Q.qsum > 0) {
+        const int j = __builtin_ctz(idle);
+        double ts;
+        const int h = hol(Q, p, ts);
+        const int qh = Q.q(h);
+        if (!(qh >= p.bmax || now >= ts + p.static_timeout)) break;
+        const int n = qh < p.bmax ? qh : p.bmax;
+        C.c[C_DONE] += pick<KM>(meta, j) & 0xffu;
+        const double cdone = pop_batch(Q, C, p, seed, ee, k, 1, j, h, n, now);
+        put<KM>(busy, j, cdone);
+        put<KM>(meta, j, (uint32_t)n | ((uint32_t)n << 8) | ((uint32_t)h << 16));
+        dirty |= 1u << j;
+        if (cdone > now) {
+          idle &= ~(1u << j);
+          if (cdone < next_done) next_done = cdone;
+        }
+      }
     }
+    first = false;
+    if (__ballot(!done) == 0ull) break;
   }
+  if (!live) return;
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
     const uint32_t infl = meta[j] & 0xffu;
