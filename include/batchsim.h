@@ -199,6 +199,31 @@ int sim_rollout(sim_ctx* ctx, const void* d_weights, int32_t T, const sim_traj* 
 int returns_gae(sim_ctx* ctx, int32_t T, const double* d_r, const float* d_v, double gamma,
                 double lambda, double* d_adv, double* d_ret);
 
+/* One PPO minibatch (Sec. 4.3, clipped surrogate): M samples (t, env) drawn with
+ * replacement, sample m taking u from the MINIBATCH block at counter
+ * (m, 0xFFFFFFFD, MINIBATCH<<24, 0) under `seed` and index i = floor(u T E), t = i / E,
+ * env = i % E. Forward through the policy (layer inputs rounded as in sim_policy, exact
+ * GELU) and the loss
+ *   L = -mean(min(rho A, clip(rho, 1-clip, 1+clip) A)) + c_value mean((V - R)^2)
+ *       - c_entropy mean(H),   rho = exp(logp(a) - logp_old),
+ * then dL/dW for every weight, the roundings passed through as the identity.
+ * Inputs (device, read only): d_weights (layout of sim_weights_layout), d_obs [T][F][E]
+ * fp32 (rows 0..T-1 of a rollout's observations), d_actions [T][E] u8, d_logp_old [T][E]
+ * fp32, d_adv and d_ret [T][E] fp64. Outputs (device, caller-owned): d_grads fp32,
+ * W1 [F][H1], b1 [H1], W2 [H1][H2], b2 [H2], W3 [H2][A'], b3 [A'] packed back to back
+ * (A' = 6K + 1; sim_ppo_grad_count gives the total); d_loss [4] fp64 = total, policy,
+ * value and entropy terms; d_index [M] int64 (t E + env) or NULL. Requires value_head = 1,
+ * M > 0 and a multiple of 16. Scratch of about 4 M (F + 3 H1 + 3 H2 + A') bytes is held by
+ * the context after the first call. A stored action out of range latches SIM_ESTATE
+ * (reported by sim_sync); that sample then contributes nothing.                         */
+int ppo_minibatch_grad(sim_ctx* ctx, const void* d_weights, int32_t T, const float* d_obs,
+                       const uint8_t* d_actions, const float* d_logp_old, const double* d_adv,
+                       const double* d_ret, int32_t M, uint64_t seed, float clip, float c_value,
+                       float c_entropy, float* d_grads, double* d_loss, int64_t* d_index);
+
+/* Number of fp32 gradient values written by ppo_minibatch_grad (no device work).       */
+int sim_ppo_grad_count(const sim_cfg* cfg, int64_t* h_count);
+
 /* Per-environment counters [2][SIM_NCNT][E] int64 and sums [2][SIM_NSUM][E] fp64 into
  * device buffers (either may be NULL).                                                  */
 int sim_counters(sim_ctx* ctx, int64_t* d_cnt, double* d_sum);
@@ -222,7 +247,8 @@ enum sim_kernel_class {
   SIM_KC_GAE = 3,     /* returns / GAE */
   SIM_KC_RESET = 4,   /* reset */
   SIM_KC_OTHER = 5,   /* weight repack / init, counters, totals */
-  SIM_KC_COUNT = 6
+  SIM_KC_PPO = 6,     /* PPO minibatch gradient */
+  SIM_KC_COUNT = 7
 };
 
 /* Tracing: with `on` != 0 every kernel launch of the context is bracketed by a pair of

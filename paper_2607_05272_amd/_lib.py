@@ -20,8 +20,9 @@ STATUS = {0: "SIM_OK", -1: "SIM_EINVAL", -2: "SIM_ENOMEM", -3: "SIM_EDEVICE", -4
 SYMBOLS = ("sim_last_error", "sim_abi_version", "sim_create", "sim_destroy", "sim_set_trace",
            "sim_reset", "sim_obs", "sim_step", "sim_tick", "sim_weights_layout",
            "sim_init_weights", "sim_policy", "sim_rollout", "returns_gae", "sim_counters",
-           "sim_checksums", "sim_stats", "sim_sync", "sim_set_timing", "sim_get_timing")
-KERNEL_CLASSES = ("policy", "step", "static", "gae", "reset", "other")
+           "sim_checksums", "sim_stats", "sim_sync", "sim_set_timing", "sim_get_timing",
+           "ppo_minibatch_grad", "sim_ppo_grad_count")
+KERNEL_CLASSES = ("policy", "step", "static", "gae", "reset", "other", "ppo")
 
 
 class SimCfg(C.Structure):
@@ -89,6 +90,9 @@ def load():
         "returns_gae": [vp, i32, vp, vp, dbl, dbl, vp, vp], "sim_counters": [vp, vp, vp],
         "sim_checksums": [vp, vp], "sim_stats": [vp, vp], "sim_sync": [vp],
         "sim_set_timing": [vp, i32], "sim_get_timing": [vp, vp, vp, i32],
+        "ppo_minibatch_grad": [vp, vp, i32, vp, vp, vp, vp, vp, i32, u64, C.c_float, C.c_float,
+                               C.c_float, vp, vp, vp],
+        "sim_ppo_grad_count": [vp, vp],
     }
     for name, args in sig.items():
         f = getattr(L, name)

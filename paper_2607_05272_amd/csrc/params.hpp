@@ -89,5 +89,13 @@ hipError_t launch_policy(const MlpParams& m, const float* obs, uint64_t seed, ui
 hipError_t launch_init_weights(int F, int H1, int H2, int Ap, int bf16, uint64_t seed,
                                void* d_weights, const size_t off[6], hipStream_t st);
 bool policy_shape_supported(const MlpParams& m);
+// PPO minibatch gradient (ppo_kernels.hip); M a multiple of 16, value head required
+hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t off[6], int T,
+                      const float* obs, const uint8_t* act, const float* logp_old,
+                      const double* adv, const double* ret, int M, uint64_t seed, float clip,
+                      float c_v, float c_h, float* scratch, double* loss_out, float* grads,
+                      int64_t* idx_out, uint32_t* err, hipStream_t st);
+size_t ppo_scratch_floats(const MlpParams& m, int M);
+size_t ppo_lds_bytes(const MlpParams& m);   // at most 64 KiB is supported
 
 }  // namespace bsim

@@ -1,0 +1,322 @@
+// ppo_kernels.hip -- one PPO minibatch (paper Sec. 4.3): gather, forward, clipped-surrogate
+// + value + entropy loss, and its gradient with respect to every policy weight.
+//
+// M samples (t, env) are drawn with replacement: sample m takes u from the MINIBATCH block at
+// counter (m, 0xFFFFFFFD, MINIBATCH<<24, 0) and index floor(u * T * E). The forward repeats
+// the rollout policy's rounding points (every layer input rounded to bf16) with fp32
+// arithmetic and saves pre-activations; gradients pass through the bf16 roundings as the
+// identity. Loss
+//   L = -mean(min(rho A, clip(rho, 1-eps, 1+eps) A)) + c_v mean((V - R)^2) - c_h mean(H),
+//   rho = exp(logp_new(a) - logp_old), H the entropy of the action distribution.
+// Work is split into: forward (16 samples per workgroup, one output unit per thread),
+// backward through the activations (same split, reading the out-major repacked weights so
+// that threads walk consecutive inputs), and weight gradients (one output element per
+// thread, fp64 accumulation over the samples in order, so results are deterministic).
+#include "devmath.hpp"
+#include "params.hpp"
+
+namespace bsim {
+namespace {
+
+constexpr int kSpb = 16;   // samples per workgroup
+constexpr int kThr = 256;
+constexpr size_t kMaxLds = 64 * 1024;  // dynamic LDS per workgroup used by the forward
+
+__device__ __forceinline__ float bf16_round(float f) { return bf16_to_f32(bf16_bits(f)); }
+__device__ __forceinline__ float gelu_exact(float z) {
+  return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
+}
+__device__ __forceinline__ float gelu_grad(float z) {
+  return 0.5f * (1.0f + erff(z * 0.70710678118654752f)) + z * expf(-0.5f * z * z) * 0.39894228040143268f;
+}
+
+__device__ __forceinline__ float wval(const void* w, size_t i, int bf16) {
+  return bf16 ? bf16_to_f32(static_cast<const uint16_t*>(w)[i]) : static_cast<const float*>(w)[i];
+}
+
+// out[s][j] = sum_i in[s][i] W[i][j] + b[j] for the workgroup's samples; W is [K][N] in-major
+__device__ void dense_fwd(const float* in, int K, const void* W, const float* b, int N, int bf16,
+                          float* out) {
+  for (int j = threadIdx.x; j < N; j += kThr) {
+    float acc[kSpb];
+#pragma unroll
+    for (int s = 0; s < kSpb; ++s) acc[s] = b[j];
+    for (int i = 0; i < K; ++i) {
+      const float wv = wval(W, (size_t)i * N + j, bf16);
+#pragma unroll
+      for (int s = 0; s < kSpb; ++s) acc[s] = fmaf(in[s * K + i], wv, acc[s]);
+    }
+#pragma unroll
+    for (int s = 0; s < kSpb; ++s) out[s * N + j] = acc[s];
+  }
+}
+
+struct PpoArgs {
+  int F, H1, H2, A, Ap, E, T, M, bf16;
+  const void* w1; const float* b1;   // ABI weights, in-major
+  const void* w2; const float* b2;
+  const void* w3; const float* b3;
+  const void* w2t; const void* w3t; // repacked out-major: [H2][H1], [AP][H2]
+  int AP;
+  const float* obs;                  // [T(+1)][F][E]
+  const uint8_t* act;
+  const float* logp_old;
+  const double* adv;
+  const double* ret;
+  uint64_t seed;
+  float clip, c_v, c_h;
+  float* x; float* z1; float* h1; float* z2; float* h2; float* dout;
+  float* dz1; float* dz2;
+  double* terms;                     // [M][3] policy, value, entropy per sample
+  int64_t* idx_out;                  // optional [M] sampled t * E + env
+  uint32_t* err;                     // device error flags
+};
+
+__global__ __launch_bounds__(kThr) void ppo_fwd_k(PpoArgs a) {
+  extern __shared__ float sm[];
+  float* xs = sm;                          // [kSpb][F]
+  float* h1s = xs + kSpb * a.F;            // [kSpb][H1]
+  float* h2s = h1s + kSpb * a.H1;          // [kSpb][H2]
+  float* os = h2s + kSpb * a.H2;           // [kSpb][Ap]
+  __shared__ int ts_[kSpb], es_[kSpb];
+  const int m0 = blockIdx.x * kSpb;
+  if (threadIdx.x < kSpb) {
+    const int m = m0 + threadIdx.x;
+    const u32x4 w = draw(a.seed, (uint32_t)m, 0xFFFFFFFDu, P_MINIBATCH, 0, 0);
+    const double n = (double)a.T * (double)a.E;
+    long long i = (long long)(unit(w.x, w.y) * n);
+    if (i > (long long)a.T * a.E - 1) i = (long long)a.T * a.E - 1;
+    ts_[threadIdx.x] = (int)(i / a.E);
+    es_[threadIdx.x] = (int)(i % a.E);
+    if (a.idx_out) a.idx_out[m] = i;
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < kSpb * a.F; idx += kThr) {
+    const int s = idx / a.F, f = idx % a.F;
+    float v = a.obs[((size_t)ts_[s] * a.F + f) * a.E + es_[s]];
+    if (a.bf16) v = bf16_round(v);
+    xs[idx] = v;
+    a.x[(size_t)(m0 + s) * a.F + f] = v;
+  }
+  __syncthreads();
+  dense_fwd(xs, a.F, a.w1, a.b1, a.H1, a.bf16, h1s);
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < kSpb * a.H1; idx += kThr) {
+    const float z = h1s[idx];
+    float h = gelu_exact(z);
+    if (a.bf16) h = bf16_round(h);
+    a.z1[(size_t)m0 * a.H1 + idx] = z;
+    a.h1[(size_t)m0 * a.H1 + idx] = h;
+    h1s[idx] = h;
+  }
+  __syncthreads();
+  dense_fwd(h1s, a.H1, a.w2, a.b2, a.H2, a.bf16, h2s);
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < kSpb * a.H2; idx += kThr) {
+    const float z = h2s[idx];
+    float h = gelu_exact(z);
+    if (a.bf16) h = bf16_round(h);
+    a.z2[(size_t)m0 * a.H2 + idx] = z;
+    a.h2[(size_t)m0 * a.H2 + idx] = h;
+    h2s[idx] = h;
+  }
+  __syncthreads();
+  dense_fwd(h2s, a.H2, a.w3, a.b3, a.Ap, a.bf16, os);
+  __syncthreads();
+  // loss gradient with respect to the outputs, one thread per sample
+  if (threadIdx.x < kSpb) {
+    const int s = threadIdx.x, m = m0 + s;
+    const float* l = os + s * a.Ap;
+    float* d = a.dout + (size_t)m * a.Ap;
+    const size_t ti = (size_t)ts_[s] * a.E + es_[s];
+    const int act = a.act[ti];
+    double* tm = a.terms + (size_t)m * 3;
+    if (act >= a.A) {  // invalid stored action: flag it, the sample contributes nothing
+      atomicOr(a.err, ERR_ACTION);
+      for (int i = 0; i < a.Ap; ++i) d[i] = 0.0f;
+      tm[0] = tm[1] = tm[2] = 0.0;
+      return;
+    }
+    const float adv = (float)a.adv[ti], ret = (float)a.ret[ti], lpo = a.logp_old[ti];
+    float mx = l[0];
+    for (int i = 1; i < a.A; ++i) mx = fmaxf(mx, l[i]);
+    float S = 0.f;
+    for (int i = 0; i < a.A; ++i) S += expf(l[i] - mx);
+    const float lS = logf(S);
+    float H = 0.f;
+    for (int i = 0; i < a.A; ++i) {
+      const float lp = (l[i] - mx) - lS;
+      H -= expf(lp) * lp;
+    }
+    const float logp = (l[act] - mx) - lS;
+    const float rho = expf(logp - lpo);
+    const float lo = 1.0f - a.clip, hi = 1.0f + a.clip;
+    const float rc = fminf(fmaxf(rho, lo), hi);
+    const float s1 = rho * adv, s2 = rc * adv;
+    const float g_rho = s1 <= s2 ? adv : ((rho > lo && rho < hi) ? adv : 0.0f);
+    const float invM = 1.0f / (float)a.M;
+    const float dlogp = -g_rho * rho * invM;
+    for (int i = 0; i < a.A; ++i) {
+      const float lp = (l[i] - mx) - lS;
+      const float p = expf(lp);
+      float g = -dlogp * p + a.c_h * invM * p * (lp + H);
+      if (i == act) g += dlogp;
+      d[i] = g;
+    }
+    const float v = l[a.A];
+    d[a.A] = 2.0f * a.c_v * (v - ret) * invM;
+    tm[0] = -(double)fminf(s1, s2);
+    tm[1] = (double)(v - ret) * (double)(v - ret);
+    tm[2] = (double)H;
+  }
+}
+
+// dz2 = (dout W3^T) * gelu'(z2); dz1 = (dz2 W2^T) * gelu'(z1). Out-major weights make
+// consecutive threads read consecutive inputs.
+__global__ __launch_bounds__(kThr) void ppo_bwd_k(PpoArgs a) {
+  extern __shared__ float sm[];
+  float* ds = sm;                          // [kSpb][Ap]
+  float* d2 = ds + kSpb * a.Ap;            // [kSpb][H2]
+  const int m0 = blockIdx.x * kSpb;
+  for (int idx = threadIdx.x; idx < kSpb * a.Ap; idx += kThr) ds[idx] = a.dout[(size_t)m0 * a.Ap + idx];
+  __syncthreads();
+  for (int j = threadIdx.x; j < a.H2; j += kThr) {
+    float acc[kSpb];
+#pragma unroll
+    for (int s = 0; s < kSpb; ++s) acc[s] = 0.f;
+    for (int o = 0; o < a.Ap; ++o) {
+      const float wv = wval(a.w3t, (size_t)o * a.H2 + j, a.bf16);
+#pragma unroll
+      for (int s = 0; s < kSpb; ++s) acc[s] = fmaf(ds[s * a.Ap + o], wv, acc[s]);
+    }
+#pragma unroll
+    for (int s = 0; s < kSpb; ++s) {
+      const float g = acc[s] * gelu_grad(a.z2[(size_t)(m0 + s) * a.H2 + j]);
+      d2[s * a.H2 + j] = g;
+      a.dz2[(size_t)(m0 + s) * a.H2 + j] = g;
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < a.H1; i += kThr) {
+    float acc[kSpb];
+#pragma unroll
+    for (int s = 0; s < kSpb; ++s) acc[s] = 0.f;
+    for (int j = 0; j < a.H2; ++j) {
+      const float wv = wval(a.w2t, (size_t)j * a.H1 + i, a.bf16);
+#pragma unroll
+      for (int s = 0; s < kSpb; ++s) acc[s] = fmaf(d2[s * a.H2 + j], wv, acc[s]);
+    }
+#pragma unroll
+    for (int s = 0; s < kSpb; ++s)
+      a.dz1[(size_t)(m0 + s) * a.H1 + i] = acc[s] * gelu_grad(a.z1[(size_t)(m0 + s) * a.H1 + i]);
+  }
+}
+
+// dW[i][j] = sum_m A[m][i] B[m][j] (fp64, samples in order); db[j] = sum_m B[m][j]
+__global__ __launch_bounds__(kThr) void ppo_wgrad_k(const float* __restrict__ Am, int K,
+                                                    const float* __restrict__ Bm, int N, int M,
+                                                    float* __restrict__ dW, float* __restrict__ db) {
+  const int idx = blockIdx.x * kThr + threadIdx.x;
+  if (idx < K * N) {
+    const int i = idx / N, j = idx % N;
+    double acc = 0.0;
+    for (int m = 0; m < M; ++m) acc += (double)Am[(size_t)m * K + i] * (double)Bm[(size_t)m * N + j];
+    dW[idx] = (float)acc;
+  } else if (idx < K * N + N) {
+    const int j = idx - K * N;
+    double acc = 0.0;
+    for (int m = 0; m < M; ++m) acc += (double)Bm[(size_t)m * N + j];
+    db[j] = (float)acc;
+  }
+}
+
+// loss terms summed in a fixed order by one workgroup
+__global__ __launch_bounds__(kThr) void ppo_loss_k(const double* terms, int M, float c_v, float c_h,
+                                                   double* out) {
+  __shared__ double part[3][kThr];
+  for (int c = 0; c < 3; ++c) {
+    double s = 0.0;
+    for (int m = threadIdx.x; m < M; m += kThr) s += terms[(size_t)m * 3 + c];
+    part[c][threadIdx.x] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double t[3] = {0.0, 0.0, 0.0};
+    for (int c = 0; c < 3; ++c)
+      for (int i = 0; i < kThr; ++i) t[c] += part[c][i];
+    const double pi = t[0] / M, v = c_v * t[1] / M, h = -c_h * t[2] / M;
+    out[0] = pi + v + h;
+    out[1] = pi;
+    out[2] = v;
+    out[3] = h;
+  }
+}
+
+}  // namespace
+
+size_t ppo_lds_bytes(const MlpParams& m) {
+  return (size_t)kSpb * (m.F + m.H1 + m.H2 + m.Ap) * sizeof(float);
+}
+
+hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t off[6], int T,
+                      const float* obs, const uint8_t* act, const float* logp_old,
+                      const double* adv, const double* ret, int M, uint64_t seed, float clip,
+                      float c_v, float c_h, float* scratch, double* loss_out, float* grads,
+                      int64_t* idx_out, uint32_t* err, hipStream_t st) {
+  const unsigned char* wb = static_cast<const unsigned char*>(d_weights);
+  PpoArgs a;
+  a.F = m.F; a.H1 = m.H1; a.H2 = m.H2; a.A = m.A; a.Ap = m.Ap; a.E = m.E; a.T = T; a.M = M;
+  a.bf16 = m.bf16; a.AP = m.AP;
+  a.w1 = wb + off[0]; a.b1 = reinterpret_cast<const float*>(wb + off[1]);
+  a.w2 = wb + off[2]; a.b2 = reinterpret_cast<const float*>(wb + off[3]);
+  a.w3 = wb + off[4]; a.b3 = reinterpret_cast<const float*>(wb + off[5]);
+  a.w2t = m.w2; a.w3t = m.w3;
+  a.obs = obs; a.act = act; a.logp_old = logp_old; a.adv = adv; a.ret = ret;
+  a.seed = seed; a.clip = clip; a.c_v = c_v; a.c_h = c_h;
+  a.idx_out = idx_out; a.err = err;
+  float* p = scratch;
+  a.x = p; p += (size_t)M * m.F;
+  a.z1 = p; p += (size_t)M * m.H1;
+  a.h1 = p; p += (size_t)M * m.H1;
+  a.z2 = p; p += (size_t)M * m.H2;
+  a.h2 = p; p += (size_t)M * m.H2;
+  a.dout = p; p += (size_t)M * m.Ap;
+  a.dz1 = p; p += (size_t)M * m.H1;
+  a.dz2 = p; p += (size_t)M * m.H2;
+  a.terms = reinterpret_cast<double*>(p);
+  const int blocks = M / kSpb;
+  const size_t lds_f = ppo_lds_bytes(m);
+  if (lds_f > kMaxLds || M % kSpb) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ppo_fwd_k, dim3(blocks), dim3(kThr), lds_f, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t lds_b = (size_t)kSpb * (m.Ap + m.H2) * sizeof(float);
+  hipLaunchKernelGGL(ppo_bwd_k, dim3(blocks), dim3(kThr), lds_b, st, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // gradient layout: W1 [F][H1], b1, W2 [H1][H2], b2, W3 [H2][Ap], b3 (fp32, contiguous)
+  float* gw1 = grads;
+  float* gb1 = gw1 + (size_t)m.F * m.H1;
+  float* gw2 = gb1 + m.H1;
+  float* gb2 = gw2 + (size_t)m.H1 * m.H2;
+  float* gw3 = gb2 + m.H2;
+  float* gb3 = gw3 + (size_t)m.H2 * m.Ap;
+  const struct { const float* A; int K; const float* B; int N; float* dW; float* db; } g[3] = {
+      {a.x, m.F, a.dz1, m.H1, gw1, gb1}, {a.h1, m.H1, a.dz2, m.H2, gw2, gb2},
+      {a.h2, m.H2, a.dout, m.Ap, gw3, gb3}};
+  for (int l = 0; l < 3; ++l) {
+    const int n = g[l].K * g[l].N + g[l].N;
+    hipLaunchKernelGGL(ppo_wgrad_k, dim3((n + kThr - 1) / kThr), dim3(kThr), 0, st, g[l].A, g[l].K,
+                       g[l].B, g[l].N, M, g[l].dW, g[l].db);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(ppo_loss_k, dim3(1), dim3(kThr), 0, st, a.terms, M, c_v, c_h, loss_out);
+  return hipGetLastError();
+}
+
+size_t ppo_scratch_floats(const MlpParams& m, int M) {
+  return (size_t)M * (m.F + 2 * m.H1 + 2 * m.H2 + m.Ap + m.H1 + m.H2) + (size_t)M * 3 * 2 + 64;
+}
+
+}  // namespace bsim

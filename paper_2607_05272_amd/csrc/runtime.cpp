@@ -60,6 +60,8 @@ struct sim_ctx {
   void* arena = nullptr;   // all environment state
   size_t arena_bytes = 0;
   void* wpack = nullptr;   // repacked policy weights
+  void* ppo_scratch = nullptr;  // PPO minibatch activations, grown on demand
+  size_t ppo_bytes = 0;
   int64_t* d_tot_cnt = nullptr;
   double* d_tot_sum = nullptr;
   uint32_t tick = 0;
@@ -313,6 +315,7 @@ int sim_destroy(sim_ctx* x) {
   for (hipEvent_t ev : x->pool) (void)hipEventDestroy(ev);
   (void)hipFree(x->arena);
   (void)hipFree(x->wpack);
+  (void)hipFree(x->ppo_scratch);
   delete x;
   return SIM_OK;
 }
@@ -416,11 +419,7 @@ int sim_init_weights(sim_ctx* x, uint64_t seed, void* d_weights) {
   return SIM_OK;
 }
 
-static int prepare_policy(sim_ctx* x, const void* d_weights) {
-  if (!policy_shape_supported(x->m))
-    return fail(SIM_EUNSUPPORTED,
-                "policy shape (bf16=%d, F_pad=%d, H1=%d, H2=%d, A_pad=%d) is not compiled",
-                x->m.bf16, x->m.FP, x->m.H1, x->m.H2, x->m.AP);
+static int repack_weights(sim_ctx* x, const void* d_weights) {
   size_t off[6];
   offsets(x->cfg, off);
   HIPCHK(x->timed(SIM_KC_OTHER, [&] {
@@ -430,6 +429,14 @@ static int prepare_policy(sim_ctx* x, const void* d_weights) {
                                 const_cast<float*>(x->m.b3), x->stream);
          }), "weight repack launch");
   return SIM_OK;
+}
+
+static int prepare_policy(sim_ctx* x, const void* d_weights) {
+  if (!policy_shape_supported(x->m))
+    return fail(SIM_EUNSUPPORTED,
+                "policy shape (bf16=%d, F_pad=%d, H1=%d, H2=%d, A_pad=%d) is not compiled",
+                x->m.bf16, x->m.FP, x->m.H1, x->m.H2, x->m.AP);
+  return repack_weights(x, d_weights);
 }
 
 int sim_policy(sim_ctx* x, const void* d_weights, const float* d_obs, uint32_t step,
@@ -488,6 +495,55 @@ int returns_gae(sim_ctx* x, int32_t T, const double* d_r, const float* d_v, doub
   HIPCHK(x->timed(SIM_KC_GAE, [&] {
            return launch_gae(T, x->cfg.n_envs, d_r, d_v, gamma, lambda, d_adv, d_ret, x->stream);
          }), "gae kernel launch");
+  return SIM_OK;
+}
+
+int sim_ppo_grad_count(const sim_cfg* c, int64_t* h_count) {
+  if (!c || !h_count) return fail(SIM_EINVAL, "NULL argument");
+  const int64_t F = c->obs_dim, H1 = c->mlp_h1, H2 = c->mlp_h2;
+  const int64_t Ap = 6 * (int64_t)c->n_servers + (c->value_head ? 1 : 0);
+  *h_count = F * H1 + H1 + H1 * H2 + H2 + H2 * Ap + Ap;
+  return SIM_OK;
+}
+
+int ppo_minibatch_grad(sim_ctx* x, const void* d_weights, int32_t T, const float* d_obs,
+                       const uint8_t* d_actions, const float* d_logp_old, const double* d_adv,
+                       const double* d_ret, int32_t M, uint64_t seed, float clip, float c_value,
+                       float c_entropy, float* d_grads, double* d_loss, int64_t* d_index) {
+  if (!x || !d_weights || !d_obs || !d_actions || !d_logp_old || !d_adv || !d_ret || !d_grads ||
+      !d_loss)
+    return fail(SIM_EINVAL, "NULL argument");
+  if (!x->cfg.value_head) return fail(SIM_EUNSUPPORTED, "ppo_minibatch_grad needs value_head = 1");
+  if (T < 1) return fail(SIM_EINVAL, "T must be >= 1");
+  if (M < 16 || M % 16) return fail(SIM_EINVAL, "M = %d must be a positive multiple of 16", M);
+  if ((int64_t)T * x->cfg.n_envs > 0x7FFFFFFFll)
+    return fail(SIM_EINVAL, "T * E must stay below 2^31");
+  if (!(clip > 0.0f && clip < 1.0f)) return fail(SIM_EINVAL, "clip must lie in (0, 1)");
+  if (ppo_lds_bytes(x->m) > 64 * 1024)
+    return fail(SIM_EUNSUPPORTED, "PPO forward needs %zu bytes of LDS (at most 65536)",
+                ppo_lds_bytes(x->m));
+  const size_t need = ppo_scratch_floats(x->m, M) * sizeof(float);
+  if (need > x->ppo_bytes) {
+    (void)hipStreamSynchronize(x->stream);
+    (void)hipFree(x->ppo_scratch);
+    x->ppo_scratch = nullptr;
+    x->ppo_bytes = 0;
+    hipError_t he = hipMalloc(&x->ppo_scratch, need);
+    if (he != hipSuccess)
+      return fail(SIM_ENOMEM, "hipMalloc of %zu bytes of PPO scratch failed: %s", need,
+                  hipGetErrorString(he));
+    x->ppo_bytes = need;
+  }
+  int rc = repack_weights(x, d_weights);
+  if (rc) return rc;
+  size_t off[6];
+  offsets(x->cfg, off);
+  HIPCHK(x->timed(SIM_KC_PPO, [&] {
+           return launch_ppo(x->m, d_weights, off, T, d_obs, d_actions, d_logp_old, d_adv, d_ret,
+                             M, seed, clip, c_value, c_entropy,
+                             static_cast<float*>(x->ppo_scratch), d_loss, d_grads, d_index,
+                             x->s.err, x->stream);
+         }), "PPO kernel launch");
   return SIM_OK;
 }
 

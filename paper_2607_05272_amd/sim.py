@@ -200,6 +200,39 @@ class Sim:
                                      C.c_double(lam), _p(adv), _p(ret)), "returns_gae")
         return adv, ret
 
+    def ppo_grad_count(self):
+        n = C.c_int64()
+        L.check(self.lib.sim_ppo_grad_count(C.byref(self.cfg), C.byref(n)), "sim_ppo_grad_count")
+        return n.value
+
+    def ppo_minibatch_grad(self, weights, obs, actions, logp_old, adv, ret, M, seed, clip=0.2,
+                           c_value=0.5, c_entropy=0.01, want_index=False, grads=None, loss=None):
+        """One PPO minibatch: obs [T(+1)][F][E] (rows 0..T-1 used), actions/logp_old/adv/ret
+        [T][E]. Returns (grads fp32 flat W1,b1,W2,b2,W3,b3; loss [4] fp64; index or None)."""
+        T = actions.shape[0]
+        assert actions.shape[1] == self.E and obs.shape[1] == self.F and obs.shape[0] >= T
+        grads = (torch.empty(self.ppo_grad_count(), dtype=torch.float32, device=self.device)
+                 if grads is None else grads)
+        loss = torch.empty(4, dtype=torch.float64, device=self.device) if loss is None else loss
+        idx = torch.empty(M, dtype=torch.int64, device=self.device) if want_index else None
+        L.check(self.lib.ppo_minibatch_grad(self._ctx, _p(weights), T, _p(obs), _p(actions),
+                                            _p(logp_old), _p(adv), _p(ret), M, C.c_uint64(seed),
+                                            clip, c_value, c_entropy, _p(grads), _p(loss),
+                                            _p(idx)), "ppo_minibatch_grad")
+        return grads, loss, idx
+
+    def unflatten_grads(self, g):
+        """Split a flat gradient vector (host numpy) into W1,b1,W2,b2,W3,b3 arrays."""
+        F, H1, H2, Ap = self.F, self.w["mlp_h1"], self.w["mlp_h2"], self.Ap
+        shapes = [("w1", (F, H1)), ("b1", (H1,)), ("w2", (H1, H2)), ("b2", (H2,)),
+                  ("w3", (H2, Ap)), ("b3", (Ap,))]
+        out, o = {}, 0
+        for k, sh in shapes:
+            n = int(np.prod(sh))
+            out[k] = np.asarray(g[o:o + n]).reshape(sh)
+            o += n
+        return out
+
     # -- statistics -------------------------------------------------------------------
     def counters(self):
         cnt = torch.empty((2, L.NCNT, self.E), dtype=torch.int64, device=self.device)

@@ -13,7 +13,7 @@ HEADER = os.path.join(ROOT, "include", "batchsim.h")
 def declared_functions():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(sim_[a-z_0-9]+|returns_gae)\s*\(",
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(sim_[a-z_0-9]+|returns_gae|ppo_[a-z_0-9]+)\s*\(",
                                  src, flags=re.M)))
 
 

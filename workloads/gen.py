@@ -48,3 +48,33 @@ def seeded_weights_f32(seed, dims, bf16=False):
         out[f"w{l + 1}"] = w
         out[f"b{l + 1}"] = (rng.standard_normal(fo) * 0.1).astype(np.float32)
     return out
+
+
+def hashed_u24(salt, t, f, e):
+    """24-bit integers from a multiplicative hash of (salt, t, f, e); works on numpy int64
+    arrays and on torch int64 tensors alike (only +, *, &, >> on values below 2^63), so a
+    device-side fill and a host-side lookup of single entries give the same numbers."""
+    s = (t * 1000003 + f * 7919 + e * 104729 + salt * 15485863) & 0xFFFFFFFF
+    return ((s * 0x5BD1E995) >> 7) & 0xFFFFFF
+
+
+def ppo_inputs_at(salt, t, e, n_actions):
+    """Stored-rollout stand-ins at positions (t, e): action (uint8), advantage and return
+    (fp64, exact dyadic values). Same formulas on numpy or torch int64 inputs."""
+    def f64(h):
+        return h.double() if hasattr(h, "double") else np.asarray(h, dtype=np.float64)
+    act = hashed_u24(salt, t, 0, e) % n_actions
+    adv = (f64(hashed_u24(salt + 1, t, 0, e)) * 2.0 ** -24 - 0.5) * 8.0
+    ret = (f64(hashed_u24(salt + 2, t, 0, e)) * 2.0 ** -24 - 0.5) * 4.0
+    return act, adv, ret
+
+
+def ratio_offsets(seed, n, lo=-0.5, hi=0.5, avoid=(), gap=0.01):
+    """Log-ratio offsets d in [lo, hi] (fp64) kept at least `gap` away from every value in
+    `avoid` (values that fall inside a gap are moved to its upper edge plus `gap`)."""
+    rng = np.random.default_rng(seed)
+    d = rng.uniform(lo, hi, size=n)
+    for a in avoid:
+        near = np.abs(d - a) < gap
+        d[near] = a + 2.0 * gap
+    return d
