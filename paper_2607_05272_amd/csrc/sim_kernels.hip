@@ -218,17 +218,19 @@ __device__ __forceinline__ int advance(Arrivals& A, const SimParams& p, uint64_t
   return cls;
 }
 
-// ---- wave-cooperative staging of ARRIVAL draws -------------------------------------------
+// ---- wave-cooperative staging of ARRIVAL draws ---------------------------------------------
 // Block j of purpose ARRIVAL for (env, tick) gives the exponential variate E_j = -log u(w0,w1)
-// and the class uniform uc_j = u(w2,w3); neither depends on the environment's state, only on
-// j. Each lane walks its events in order and reads E_j, uc_j from a per-wave LDS stage of
-// kStage slots per lane. When lanes run short, the whole wave refills: lane l of the wave
-// computes work items l, l+64, ... of the list (needing lane, block), so the Philox draws and
-// logarithms of a few bursting environments are spread over all 64 lanes.
+// and, through the class mix, the class of uc_j = u(w2,w3); neither depends on the
+// environment's state, only on j. Each lane reads them from a per-wave LDS stage of kStage
+// slots; when lanes run short, the whole wave refills: lane l of the wave computes work
+// items l, l+64, ... of the list of (needing lane, block), so the Philox draws and
+// logarithms of a few bursting environments are spread over all 64 lanes. (Service draws
+// are not staged: an environment dispatches a few batches per tick at most, and the lanes
+// dispatching at one instant already draw together.)
 constexpr int kStage = 8;
-struct ArrStage {
+struct Stage {
   double E[kStage][64];
-  double uc[kStage][64];
+  uint8_t cls[kStage][64];
   uint32_t owner[64];
   uint32_t j0[64];
 };
@@ -239,9 +241,11 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Called by all 64 lanes of the wave. Lanes with `need` get blocks [jneed, jneed+kStage).
-__device__ __forceinline__ void refill(ArrStage& st, bool need, uint32_t jneed, uint32_t& staged_hi,
-                                       uint64_t seed, int e_lane0, uint32_t k, int lane) {
+// Called by all 64 lanes of the wave. Lanes with `need` get blocks [jneed, jneed + KS):
+// fill(owner lane, j) computes one block into the stage.
+template <int KS, class Fill>
+__device__ __forceinline__ void wave_refill(Stage& st, bool need, uint32_t jneed,
+                                            uint32_t& staged_hi, int lane, Fill&& fill) {
   const uint64_t mask = __ballot(need);
   const int nneed = __popcll(mask);
   if (need) {
@@ -250,22 +254,34 @@ __device__ __forceinline__ void refill(ArrStage& st, bool need, uint32_t jneed, 
     st.j0[rank] = jneed;
   }
   wave_sync_lds();
-  for (int w = lane; w < kStage * nneed; w += 64) {
-    const int r = w / kStage;
-    const uint32_t own = st.owner[r];
-    const uint32_t j = st.j0[r] + (uint32_t)(w % kStage);
-    const u32x4 d = draw(seed, (uint32_t)(e_lane0 + (int)own), k, P_ARRIVAL, j, 0);
-    st.E[j % kStage][own] = -dlog(unit(d.x, d.y));
-    st.uc[j % kStage][own] = unit(d.z, d.w);
+  for (int w = lane; w < KS * nneed; w += 64) {
+    const int r = w / KS;
+    fill(st.owner[r], st.j0[r] + (uint32_t)(w % KS));
   }
   wave_sync_lds();
-  if (need) staged_hi = jneed + kStage;
+  if (need) staged_hi = jneed + KS;
+}
+
+template <int CM>
+__device__ __forceinline__ void refill_arrivals(Stage& st, const SimParams& p, bool need,
+                                                uint32_t jneed, uint32_t& staged_hi,
+                                                uint64_t seed, int e_lane0, uint32_t k, int lane) {
+  wave_refill<kStage>(st, need, jneed, staged_hi, lane, [&](uint32_t own, uint32_t j) {
+    const u32x4 d = draw(seed, (uint32_t)(e_lane0 + (int)own), k, P_ARRIVAL, j, 0);
+    st.E[j % kStage][own] = -dlog(unit(d.x, d.y));
+    const double uc = unit(d.z, d.w);
+    int cls = CM - 1;
+#pragma unroll
+    for (int c = CM - 2; c >= 0; --c)
+      if (uc < p.class_cum[c]) cls = c;
+    st.cls[j % kStage][own] = (uint8_t)cls;
+  });
 }
 
 // As `advance`, with ARRIVAL blocks read from the stage (the caller guarantees that the two
 // blocks an instant can consume, a switch redraw and an arrival, are staged).
 template <int CM>
-__device__ __forceinline__ int advance_staged(Arrivals& A, const SimParams& p, const ArrStage& st,
+__device__ __forceinline__ int advance_staged(Arrivals& A, const SimParams& p, const Stage& st,
                                               int lane, uint64_t seed, int e, uint32_t k,
                                               double now) {
   if (A.next_sw == now) {
@@ -296,11 +312,7 @@ __device__ __forceinline__ int advance_staged(Arrivals& A, const SimParams& p, c
     A.next_arr = (int)A.tr_idx < A.tr_cnt ? p.tr_times[base + A.tr_idx] : kInf;
   } else {
     const uint32_t j = A.jarr++;
-    const double uc = st.uc[j % kStage][lane];
-    cls = CM - 1;
-#pragma unroll
-    for (int c = CM - 2; c >= 0; --c)
-      if (uc < p.class_cum[c]) cls = c;
+    cls = st.cls[j % kStage][lane];
     A.next_arr = now + st.E[j % kStage][lane] * pick<kMaxS>(p.mean_gap, (int)A.proc);
   }
   return cls;
@@ -325,9 +337,10 @@ __device__ __forceinline__ void enqueue(Queue<CM>& Q, Count& C, const SimParams&
   C.c[C_ACC] += 1u;
 }
 
-// Stochastic service time of a batch of n (once per dispatch; kept out of line).
-// kind 1: median * exp(sigma Z) + beta n with Z = sqrt(-2 log u1) cos(2 pi u2) (Box-Muller);
-// kind 2: -log(u1) (alpha + beta n).
+// Service time of a batch of n requests of class h (kept out of line: drawn once per
+// dispatch). kind 0: alpha + beta n; kind 1: median * exp(sigma Z) + beta n with
+// Z = sqrt(-2 log u1) cos(2 pi u2) (Box-Muller); kind 2: -log(u1) (alpha + beta n), with
+// u1, u2 from SERVICE block j of (env, tick, system).
 __device__ __noinline__ double service_draw(int kind, double al, double be, double med,
                                             double sigma, int n, uint64_t seed, uint32_t env,
                                             uint32_t k, uint32_t j, uint32_t sys) {
@@ -339,38 +352,46 @@ __device__ __noinline__ double service_draw(int kind, double al, double be, doub
   return med * dexp(sigma * z) + be * (double)n;
 }
 
-// Pops n requests of class h dispatched at `now` to server j, on which they complete at
-// cdone = now + service; accumulates their latencies in FIFO order. Returns cdone.
 template <int CM>
-__device__ __forceinline__ double pop_batch(Queue<CM>& Q, Count& C, const SimParams& p,
-                                            uint64_t seed, int e, uint32_t k, int sys, int j,
-                                            int h, int n, double now) {
+__device__ __forceinline__ double service(Count& C, const SimParams& p, uint64_t seed, int e,
+                                          uint32_t k, int sys, int h, int n) {
   const int kind = pick<CM>(p.svc_kind, h);
   const double al = pick<CM>(p.svc_alpha, h), be = pick<CM>(p.svc_beta, h);
-  double sv;
-  if (kind == 0) sv = al + be * (double)n;
-  else sv = service_draw(kind, al, be, pick<CM>(p.svc_median, h), p.svc_sigma, n, seed,
-                         (uint32_t)e, k, C.jsvc++, (uint32_t)sys);
+  if (kind == 0) return al + be * (double)n;
+  return service_draw(kind, al, be, pick<CM>(p.svc_median, h), p.svc_sigma, n, seed,
+                      (uint32_t)e, k, C.jsvc++, (uint32_t)sys);
+}
+
+// Pops n requests of class h dispatched at `now` to server j, on which they complete at
+// cdone = now + sv; accumulates their latencies in FIFO order. Returns cdone.
+template <int CM>
+__device__ __forceinline__ double pop_batch(Queue<CM>& Q, Count& C, const SimParams& p,
+                                            uint32_t k, int j, int h, int n, double now,
+                                            double sv) {
   const double cdone = now + sv;
   const double wh = pick<CM>(p.w_class, h);
   const int N = p.N;
   const double* rb = Q.ring + (size_t)h * N;
   const int head = Q.hd(h);
+  int pos = head + n;
+  pos = pos >= N ? pos - N : pos;
+  const int qh = Q.q(h) - n;
+  // the new head's timestamp (read even when the class empties: pos is inside the ring) and
+  // the popped timestamps, eight at a time, are loaded before any of them is used
+  const double next_head = rb[pos];
   double Lw = C.Lw, lat = C.lat, wlat = C.wlat;
-  // the timestamps are loaded eight at a time (independent loads in flight together),
-  // then accumulated in FIFO order
   for (int i0 = 0; i0 < n; i0 += 8) {
     double a[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      int q = head + i0 + j;
+    for (int i = 0; i < 8; ++i) {
+      int q = head + i0 + i;
       q = q >= N ? q - N : q;
-      a[j] = i0 + j < n ? rb[q] : 0.0;
+      a[i] = i0 + i < n ? rb[q] : 0.0;
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      if (i0 + j < n) {
-        const double l = cdone - a[j];
+    for (int i = 0; i < 8; ++i) {
+      if (i0 + i < n) {
+        const double l = cdone - a[i];
         const double wl = wh * l;
         Lw = Lw + wl;
         lat = lat + l;
@@ -378,15 +399,12 @@ __device__ __forceinline__ double pop_batch(Queue<CM>& Q, Count& C, const SimPar
       }
     }
   }
-  int pos = head + n;
-  pos = pos >= N ? pos - N : pos;
   C.Lw = Lw; C.lat = lat; C.wlat = wlat;
   const int sh = 8 * h;
-  const int qh = Q.q(h) - n;
   Q.qp = (Q.qp & ~(0xffu << sh)) | ((uint32_t)qh << sh);
   Q.hp = (Q.hp & ~(0xffu << sh)) | ((uint32_t)pos << sh);
   Q.qsum -= n;
-  if (qh > 0) put<CM>(Q.hts, h, rb[pos]);
+  if (qh > 0) put<CM>(Q.hts, h, next_head);
   C.c[C_DISP] += (uint32_t)n;
   C.c[C_BATCH] += 1u;
   C.chk = fnv(C.chk, ((uint64_t)(k + 1) << 32) | ((uint64_t)j << 16) | ((uint64_t)h << 8) |
@@ -421,9 +439,9 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
                                                  float* __restrict__ obs_out,
                                                  double* __restrict__ rew,
                                                  uint64_t* __restrict__ rchk) {
-  __shared__ ArrStage stage[4];
+  __shared__ Stage stage[4];
   const int lane = threadIdx.x & 63;
-  ArrStage& st = stage[threadIdx.x >> 6];
+  Stage& st = stage[threadIdx.x >> 6];
   const int e_lane0 = blockIdx.x * blockDim.x + (threadIdx.x & ~63);
   const int e = e_lane0 + lane;
   // lanes past the last environment stay in the loop (the wave refills together) but idle
@@ -473,7 +491,8 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
         go = !need;
       }
     }
-    if (__ballot(need) != 0ull) refill(st, need, A.jarr, staged_hi, seed, e_lane0, k, lane);
+    if (__ballot(need) != 0ull)
+      refill_arrivals<CM>(st, p, need, A.jarr, staged_hi, seed, e_lane0, k, lane);
     if (go) {
       ++it;
       now = te;
@@ -490,7 +509,8 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
         const int h = hol(Q, p, ts);
         if (Q.q(h) < b) break;
         C.c[C_DONE] += meta_s & 0xffu;  // the previous batch on s finished at busy_s <= now
-        busy_s = pop_batch(Q, C, p, seed, ee, k, 0, s, h, b, now);
+        const double sv = service<CM>(C, p, seed, ee, k, 0, h, b);
+        busy_s = pop_batch(Q, C, p, k, s, h, b, now, sv);
         meta_s = (uint32_t)b | ((uint32_t)b << 8) | ((uint32_t)h << 16);
         dirty_s = true;
       }
@@ -616,11 +636,11 @@ __device__ __forceinline__ void server_scan(const double (&busy)[KM], int K, dou
 }
 
 template <int KM, int CM>
-__global__ __launch_bounds__(256) void static_k(SimParams p, EnvState g, uint64_t seed, uint32_t k,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void static_k(SimParams p, EnvState g, uint64_t seed, uint32_t k,
                                                 double* __restrict__ rew) {
-  __shared__ ArrStage stage[4];
+  __shared__ Stage stage[4];
   const int lane = threadIdx.x & 63;
-  ArrStage& st = stage[threadIdx.x >> 6];
+  Stage& st = stage[threadIdx.x >> 6];
   const int e_lane0 = blockIdx.x * blockDim.x + (threadIdx.x & ~63);
   const int e = e_lane0 + lane;
   const bool live = e < p.E;
@@ -634,12 +654,17 @@ __global__ __launch_bounds__(256) void static_k(SimParams p, EnvState g, uint64_
   load_count(C, G, p, ee);
   Arrivals A;
   load_arrivals(A, G, p, ee);
+  // busy-until times in registers; of each server's meta word only the in-flight count
+  // (low byte) is kept, four servers to a register (the word is stored at dispatch)
+  constexpr int KW = (KM + 3) / 4;
   double busy[KM];
-  uint32_t meta[KM];
+  uint32_t infl[KW];
+#pragma unroll
+  for (int w = 0; w < KW; ++w) infl[w] = 0u;
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
     busy[j] = j < p.K ? G.busy[(size_t)j * E + ee] : kInf;
-    meta[j] = j < p.K ? G.meta[(size_t)j * E + ee] : 0u;
+    if (j < p.K) infl[j / 4] |= (G.meta[(size_t)j * E + ee] & 0xffu) << (8 * (j % 4));
   }
   uint32_t dirty = 0;
 
@@ -677,7 +702,8 @@ __global__ __launch_bounds__(256) void static_k(SimParams p, EnvState g, uint64_
         go = !need;
       }
     }
-    if (__ballot(need) != 0ull) refill(st, need, A.jarr, staged_hi, seed, e_lane0, k, lane);
+    if (__ballot(need) != 0ull)
+      refill_arrivals<CM>(st, p, need, A.jarr, staged_hi, seed, e_lane0, k, lane);
     if (go) {
       ++it;
       now = te;
@@ -697,10 +723,14 @@ __global__ __launch_bounds__(256) void static_k(SimParams p, EnvState g, uint64_
         const int qh = Q.q(h);
         if (!(qh >= p.bmax || now >= ts + p.static_timeout)) break;
         const int n = qh < p.bmax ? qh : p.bmax;
-        C.c[C_DONE] += pick<KM>(meta, j) & 0xffu;
-        const double cdone = pop_batch(Q, C, p, seed, ee, k, 1, j, h, n, now);
+        const int jw = j >> 2, jb = 8 * (j & 3);
+        const uint32_t iw = pick<KW>(infl, jw);
+        C.c[C_DONE] += (iw >> jb) & 0xffu;  // the previous batch on j finished at busy_j <= now
+        put<KW>(infl, jw, (iw & ~(0xffu << jb)) | ((uint32_t)n << jb));
+        const double sv = service<CM>(C, p, seed, ee, k, 1, h, n);
+        const double cdone = pop_batch(Q, C, p, k, j, h, n, now, sv);
         put<KM>(busy, j, cdone);
-        put<KM>(meta, j, (uint32_t)n | ((uint32_t)n << 8) | ((uint32_t)h << 16));
+        G.meta[(size_t)j * E + ee] = (uint32_t)n | ((uint32_t)n << 8) | ((uint32_t)h << 16);
         dirty |= 1u << j;
         if (cdone > now) {
           idle &= ~(1u << j);
@@ -712,24 +742,27 @@ __global__ __launch_bounds__(256) void static_k(SimParams p, EnvState g, uint64_
     if (__ballot(!done) == 0ull) break;
   }
   if (!live) return;
+  // completions before t1: count them and clear the in-flight byte of the stored word
+  uint32_t clear = 0;
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
-    const uint32_t infl = meta[j] & 0xffu;
-    if (infl > 0 && busy[j] < t1) {
-      C.c[C_DONE] += infl;
-      meta[j] &= ~0xffu;
-      dirty |= 1u << j;
+    const uint32_t n = (infl[j / 4] >> (8 * (j % 4))) & 0xffu;
+    if (j < p.K && n > 0 && busy[j] < t1) {
+      C.c[C_DONE] += n;
+      clear |= 1u << j;
     }
   }
+  uint32_t m[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) m[j] = (clear >> j) & 1u ? G.meta[(size_t)j * E + e] : 0u;
+#pragma unroll
+  for (int j = 0; j < KM; ++j)
+    if ((clear >> j) & 1u) G.meta[(size_t)j * E + e] = m[j] & ~0xffu;
   const double r = close_tick(Q, C, p, A.proc, A_k);
   if (rew) rew[e] = r;
 #pragma unroll
-  for (int j = 0; j < KM; ++j) {
-    if (dirty & (1u << j)) {
-      G.busy[(size_t)j * E + e] = busy[j];
-      G.meta[(size_t)j * E + e] = meta[j];
-    }
-  }
+  for (int j = 0; j < KM; ++j)
+    if (dirty & (1u << j)) G.busy[(size_t)j * E + e] = busy[j];
   store_queue(Q, G, p, e);
   store_count(C, G, p, e);
   store_arrivals(A, G, p, e);
