@@ -34,21 +34,21 @@ namespace {
 enum { C_ARR = 0, C_ACC = 1, C_DROP = 2, C_DISP = 3, C_BATCH = 4, C_DONE = 5 };
 constexpr double kInf = __builtin_huge_val();
 
-// Per-lane select from a small array with compile-time bound M (register arrays stay in
-// registers instead of going to scratch for a runtime index).
+// Per-lane select from / update of a small array with compile-time bound M. Both are
+// written as selects of values on every element (no conditional store), so that the
+// array stays in registers: a store through a selected element address would force it
+// into scratch memory.
 template <int M, typename T, int L>
 __device__ __forceinline__ T pick(const T (&a)[L], int i) {
   T v = a[0];
 #pragma unroll
-  for (int c = 1; c < M; ++c)
-    if (i == c) v = a[c];
+  for (int c = 1; c < M; ++c) v = i == c ? a[c] : v;
   return v;
 }
 template <int M, typename T, int L>
 __device__ __forceinline__ void put(T (&a)[L], int i, T v) {
 #pragma unroll
-  for (int c = 0; c < M; ++c)
-    if (i == c) a[c] = v;
+  for (int c = 0; c < M; ++c) a[c] = i == c ? v : a[c];
 }
 
 // ---- per-class FIFO queues of one system ---------------------------------------------------
@@ -635,6 +635,21 @@ __device__ __forceinline__ void server_scan(const double (&busy)[KM], int K, dou
   }
 }
 
+// one byte per server (at most 16) in two 64-bit registers
+struct ServerBytes {
+  uint64_t lo = 0, hi = 0;
+  __device__ __forceinline__ uint32_t get(int j) const {
+    return (uint32_t)(((j < 8 ? lo : hi) >> (8 * (j & 7))) & 0xffu);
+  }
+  __device__ __forceinline__ void set(int j, uint32_t v) {
+    const int sh = 8 * (j & 7);
+    const uint64_t keep = ~(0xffull << sh), x = (uint64_t)(v & 0xffu) << sh;
+    lo = j < 8 ? (lo & keep) | x : lo;
+    hi = j < 8 ? hi : (hi & keep) | x;
+  }
+};
+static_assert(kMaxK <= 16, "ServerBytes holds 16 servers");
+
 template <int KM, int CM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void static_k(SimParams p, EnvState g, uint64_t seed, uint32_t k,
                                                 double* __restrict__ rew) {
@@ -655,16 +670,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   Arrivals A;
   load_arrivals(A, G, p, ee);
   // busy-until times in registers; of each server's meta word only the in-flight count
-  // (low byte) is kept, four servers to a register (the word is stored at dispatch)
-  constexpr int KW = (KM + 3) / 4;
+  // (low byte) is kept, eight servers to a 64-bit register (the word is stored at dispatch)
   double busy[KM];
-  uint32_t infl[KW];
-#pragma unroll
-  for (int w = 0; w < KW; ++w) infl[w] = 0u;
+  ServerBytes infl;
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
     busy[j] = j < p.K ? G.busy[(size_t)j * E + ee] : kInf;
-    if (j < p.K) infl[j / 4] |= (G.meta[(size_t)j * E + ee] & 0xffu) << (8 * (j % 4));
+    if (j < p.K) infl.set(j, G.meta[(size_t)j * E + ee] & 0xffu);
   }
   uint32_t dirty = 0;
 
@@ -723,10 +735,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         const int qh = Q.q(h);
         if (!(qh >= p.bmax || now >= ts + p.static_timeout)) break;
         const int n = qh < p.bmax ? qh : p.bmax;
-        const int jw = j >> 2, jb = 8 * (j & 3);
-        const uint32_t iw = pick<KW>(infl, jw);
-        C.c[C_DONE] += (iw >> jb) & 0xffu;  // the previous batch on j finished at busy_j <= now
-        put<KW>(infl, jw, (iw & ~(0xffu << jb)) | ((uint32_t)n << jb));
+        C.c[C_DONE] += infl.get(j);  // the previous batch on j finished at busy_j <= now
+        infl.set(j, (uint32_t)n);
         const double sv = service<CM>(C, p, seed, ee, k, 1, h, n);
         const double cdone = pop_batch(Q, C, p, k, j, h, n, now, sv);
         put<KM>(busy, j, cdone);
@@ -746,7 +756,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   uint32_t clear = 0;
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
-    const uint32_t n = (infl[j / 4] >> (8 * (j % 4))) & 0xffu;
+    const uint32_t n = infl.get(j);
     if (j < p.K && n > 0 && busy[j] < t1) {
       C.c[C_DONE] += n;
       clear |= 1u << j;
