@@ -181,7 +181,31 @@ __global__ __launch_bounds__(kThreads) void policy_k(MlpParams m, const float* _
   }
 }
 
-// packed weights: W^T [Npad][Kpad] in the compute type, zero padded; bias fp32 [Npad]
+// packed bf16 weights in MFMA fragment order: for output tile t (16 units) and k-step ks (32
+// inputs), the 64 lanes' 16-byte A fragments lie back to back, lane = kq*16 + r16 holding
+// W[ks*32 + kq*8 + j][t*16 + r16], j = 0..7 (zero padded). A wave's load of one fragment is
+// one contiguous kilobyte, and consecutive k-steps of a tile are consecutive kilobytes.
+__global__ void repack_frag_k(const unsigned char* __restrict__ src, size_t woff, size_t boff,
+                              int K, int N, int KS, int NTp, uint16_t* __restrict__ w,
+                              float* __restrict__ b) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t total = (size_t)NTp * KS * 512;
+  if (idx < total) {
+    const int t = (int)(idx / ((size_t)KS * 512));
+    const int rem = (int)(idx % ((size_t)KS * 512));
+    const int ks = rem / 512, l = (rem % 512) / 8, j = rem % 8;
+    const int n = t * 16 + (l & 15), k = ks * 32 + (l >> 4) * 8 + j;
+    uint16_t v = 0;
+    if (n < N && k < K) v = reinterpret_cast<const uint16_t*>(src + woff)[(size_t)k * N + n];
+    w[idx] = v;
+  }
+  if (idx < (size_t)NTp * 16) {
+    const int n = (int)idx;
+    b[n] = n < N ? reinterpret_cast<const float*>(src + boff)[n] : 0.f;
+  }
+}
+
+// packed fp32 weights: W^T [Npad][Kpad], zero padded; bias fp32 [Npad]
 template <typename T>
 __global__ void repack_k(const unsigned char* __restrict__ src, size_t woff, size_t boff, int K,
                          int N, int Kp, int Np, T* __restrict__ w, float* __restrict__ b) {
@@ -219,8 +243,8 @@ __global__ void zero_f32_k(float* p, int n) {
 
 // ---- bf16 policy kernel: 16*RT environments per workgroup, NW waves ------------------------
 // Every layer is computed transposed, out^T = W^T act^T: the weight tile is the MFMA A
-// operand (16 output units x 32 inputs, 16 contiguous bytes per lane from the out-major
-// repacked weights) and the activation tile the B operand (32 inputs x 16 environments, 16
+// operand (16 output units x 32 inputs, 16 contiguous bytes per lane from the weights
+// repacked in fragment order) and the activation tile the B operand (32 inputs x 16 environments, 16
 // contiguous bytes per lane from the row-major [env][unit] LDS buffer). A lane's four
 // accumulator values are then four consecutive output units of one environment, so the
 // epilogue writes them to the next layer's buffer as one 8-byte store after two packed
@@ -238,24 +262,30 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 template <int K, int N, int RT, int NW>
 __device__ __forceinline__ void mma_t(const uint16_t* __restrict__ act, int sa,
                                       const uint16_t* __restrict__ W,
+                                      const float* __restrict__ bias,
                                       f32x4 (&acc)[(N / 16 + NW - 1) / NW][RT]) {
   constexpr int NT = N / 16, CTW = (NT + NW - 1) / NW, KS = K / 32;
   constexpr bool kEven = NT % NW == 0;  // every wave owns CTW output tiles
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
+  // the accumulators start at the bias: a lane's four values are units u0..u0+3
 #pragma unroll
-  for (int c = 0; c < CTW; ++c)
+  for (int c = 0; c < CTW; ++c) {
+    f32x4 bv = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (kEven || wave + NW * c < NT)
+      bv = *reinterpret_cast<const f32x4*>(bias + (wave + NW * c) * 16 + kq * 4);
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) acc[c][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int rt = 0; rt < RT; ++rt) acc[c][rt] = bv;
+  }
   bf16x8 w[2][CTW];
-  const uint16_t* wbase = W + (size_t)(wave * 16 + r16) * K + kq * 8;
-  constexpr size_t WSTEP = (size_t)NW * 16 * K;  // elements between a wave's output tiles
+  const uint16_t* wbase = W + (size_t)wave * KS * 512 + lane * 8;   // fragment order
+  constexpr size_t WSTEP = (size_t)NW * KS * 512;  // elements between a wave's output tiles
   const uint16_t* brow = act + r16 * sa + kq * 8;
   auto loadw = [&](int buf, int ks) {
 #pragma unroll
     for (int c = 0; c < CTW; ++c)
       if (kEven || wave + NW * c < NT)
-        w[buf][c] = *reinterpret_cast<const bf16x8*>(wbase + c * WSTEP + ks * 32);
+        w[buf][c] = *reinterpret_cast<const bf16x8*>(wbase + c * WSTEP + ks * 512);
   };
   auto mma = [&](int buf, int ks) {
     bf16x8 b[RT];
@@ -292,14 +322,15 @@ __device__ __forceinline__ float gelu_fast(float x) {
   poly = fmaf(poly, t, -0.142248368f);                                // a2/2
   poly = fmaf(poly, t, 0.127414796f);                                 // a1/2
   const float e = __builtin_amdgcn_exp2f((x * -0.72134752044f) * x);   // exp(-x^2/2)
-  return fmaxf(x, 0.0f) - (a * (poly * t)) * e;
+  const float q = (poly * t) * e;                                      // erfc(|x|/sqrt2)/2
+  return fmaf(-a, q, fmaxf(x, 0.0f));
 }
 
-// bias + GELU + bf16 rounding; four consecutive units of one environment per 8-byte store
+// GELU + bf16 rounding (the bias is already in the accumulators); four consecutive units of
+// one environment per 8-byte store
 template <int N, int RT, int NW>
 __device__ __forceinline__ void store_hidden_t(const f32x4 (&acc)[(N / 16 + NW - 1) / NW][RT],
-                                               const float* __restrict__ bias, uint16_t* out,
-                                               int so) {
+                                               uint16_t* out, int so) {
   constexpr int NT = N / 16, CTW = (NT + NW - 1) / NW;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
@@ -308,13 +339,12 @@ __device__ __forceinline__ void store_hidden_t(const f32x4 (&acc)[(N / 16 + NW -
     const int ot = wave + NW * c;
     if (ot >= NT) continue;
     const int u0 = ot * 16 + kq * 4;
-    const f32x4 bv = *reinterpret_cast<const f32x4*>(bias + u0);
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const f32x4 v = acc[c][rt];
       u32x2 pk;
-      pk.x = pack_bf16(gelu_fast(v[0] + bv[0]), gelu_fast(v[1] + bv[1]));
-      pk.y = pack_bf16(gelu_fast(v[2] + bv[2]), gelu_fast(v[3] + bv[3]));
+      pk.x = pack_bf16(gelu_fast(v[0]), gelu_fast(v[1]));
+      pk.y = pack_bf16(gelu_fast(v[2]), gelu_fast(v[3]));
       *reinterpret_cast<u32x2*>(out + (rt * 16 + r16) * so + u0) = pk;
     }
   }
@@ -360,21 +390,21 @@ __global__ __launch_bounds__(NW * 64, MINB) void policy_bf16_k(MlpParams m, cons
   __syncthreads();
   {
     f32x4 acc[(H1 / 16 + NW - 1) / NW][RT];
-    mma_t<FP, H1, RT, NW>(xs, Sh::SX, static_cast<const uint16_t*>(m.w1), acc);
-    store_hidden_t<H1, RT, NW>(acc, m.b1, hs, Sh::SH);
+    mma_t<FP, H1, RT, NW>(xs, Sh::SX, static_cast<const uint16_t*>(m.w1), m.b1, acc);
+    store_hidden_t<H1, RT, NW>(acc, hs, Sh::SH);
   }
   __syncthreads();
   {
     f32x4 acc[(H2 / 16 + NW - 1) / NW][RT];
-    mma_t<H1, H2, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w2), acc);
+    mma_t<H1, H2, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w2), m.b2, acc);
     __syncthreads();  // every wave has finished reading h1
-    store_hidden_t<H2, RT, NW>(acc, m.b2, hs, Sh::SH);
+    store_hidden_t<H2, RT, NW>(acc, hs, Sh::SH);
   }
   __syncthreads();
   {
     constexpr int NT = AP / 16, CTW = (NT + NW - 1) / NW;
     f32x4 acc[CTW][RT];
-    mma_t<H2, AP, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w3), acc);
+    mma_t<H2, AP, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w3), m.b3, acc);
     __syncthreads();  // every wave has finished reading h2
     const int lane = tid & 63, wave = tid >> 6, r16 = lane & 15, kq = lane >> 4;
 #pragma unroll
@@ -382,10 +412,9 @@ __global__ __launch_bounds__(NW * 64, MINB) void policy_bf16_k(MlpParams m, cons
       const int ot = wave + NW * c;
       if (ot >= NT) continue;
       const int u0 = ot * 16 + kq * 4;
-      const f32x4 bv = *reinterpret_cast<const f32x4*>(m.b3 + u0);
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
-        *reinterpret_cast<f32x4*>(lg + (rt * 16 + r16) * Sh::SL + u0) = acc[c][rt] + bv;
+        *reinterpret_cast<f32x4*>(lg + (rt * 16 + r16) * Sh::SL + u0) = acc[c][rt];
     }
   }
   __syncthreads();
@@ -523,8 +552,8 @@ hipError_t launch_repack(const MlpParams& m, const void* d_weights, const size_t
     const size_t total = (size_t)Np[l] * Kp[l];
     const dim3 grid((unsigned)((total + 255) / 256));
     if (m.bf16)
-      hipLaunchKernelGGL(repack_k<uint16_t>, grid, dim3(256), 0, st, src, off[2 * l], off[2 * l + 1],
-                         Ks[l], Ns[l], Kp[l], Np[l], static_cast<uint16_t*>(ws[l]), bs[l]);
+      hipLaunchKernelGGL(repack_frag_k, grid, dim3(256), 0, st, src, off[2 * l], off[2 * l + 1],
+                         Ks[l], Ns[l], Kp[l] / 32, Np[l] / 16, static_cast<uint16_t*>(ws[l]), bs[l]);
     else
       hipLaunchKernelGGL(repack_k<float>, grid, dim3(256), 0, st, src, off[2 * l], off[2 * l + 1],
                          Ks[l], Ns[l], Kp[l], Np[l], static_cast<float*>(ws[l]), bs[l]);

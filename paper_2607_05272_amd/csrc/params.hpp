@@ -76,9 +76,11 @@ struct MlpParams {
   int E, F, H1, H2, A, Ap;      // A = 6K actions, Ap = A + value_head
   int bf16, value_head;
   int FP, AP;                   // padded input width and padded output width
-  const void* w1; const float* b1;   // packed [H1][FP]
-  const void* w2; const float* b2;   // packed [H2][H1]
-  const void* w3; const float* b3;   // packed [AP][H2]
+  // repacked weights: bf16 in MFMA fragment order (see repack_frag_k), fp32 as W^T
+  // [H1][FP], [H2][H1], [AP][H2]; biases zero padded to the padded output widths
+  const void* w1; const float* b1;
+  const void* w2; const float* b2;
+  const void* w3; const float* b3;
 };
 hipError_t launch_repack(const MlpParams& m, const void* d_weights, const size_t off[6],
                          void* w1, float* b1, void* w2, float* b2, void* w3, float* b3,

@@ -56,7 +56,6 @@ struct PpoArgs {
   const void* w1; const float* b1;   // ABI weights, in-major
   const void* w2; const float* b2;
   const void* w3; const float* b3;
-  const void* w2t; const void* w3t; // repacked out-major: [H2][H1], [AP][H2]
   int AP;
   const float* obs;                  // [T(+1)][F][E]
   const uint8_t* act;
@@ -171,8 +170,8 @@ __global__ __launch_bounds__(kThr) void ppo_fwd_k(PpoArgs a) {
   }
 }
 
-// dz2 = (dout W3^T) * gelu'(z2); dz1 = (dz2 W2^T) * gelu'(z1). Out-major weights make
-// consecutive threads read consecutive inputs.
+// dz2 = (dout W3^T) * gelu'(z2); dz1 = (dz2 W2^T) * gelu'(z1); thread j walks row j of the
+// in-major weights.
 __global__ __launch_bounds__(kThr) void ppo_bwd_k(PpoArgs a) {
   extern __shared__ float sm[];
   float* ds = sm;                          // [kSpb][Ap]
@@ -185,7 +184,7 @@ __global__ __launch_bounds__(kThr) void ppo_bwd_k(PpoArgs a) {
 #pragma unroll
     for (int s = 0; s < kSpb; ++s) acc[s] = 0.f;
     for (int o = 0; o < a.Ap; ++o) {
-      const float wv = wval(a.w3t, (size_t)o * a.H2 + j, a.bf16);
+      const float wv = wval(a.w3, (size_t)j * a.Ap + o, a.bf16);
 #pragma unroll
       for (int s = 0; s < kSpb; ++s) acc[s] = fmaf(ds[s * a.Ap + o], wv, acc[s]);
     }
@@ -202,7 +201,7 @@ __global__ __launch_bounds__(kThr) void ppo_bwd_k(PpoArgs a) {
 #pragma unroll
     for (int s = 0; s < kSpb; ++s) acc[s] = 0.f;
     for (int j = 0; j < a.H2; ++j) {
-      const float wv = wval(a.w2t, (size_t)j * a.H1 + i, a.bf16);
+      const float wv = wval(a.w2, (size_t)i * a.H2 + j, a.bf16);
 #pragma unroll
       for (int s = 0; s < kSpb; ++s) acc[s] = fmaf(d2[s * a.H2 + j], wv, acc[s]);
     }
@@ -270,7 +269,6 @@ hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t of
   a.w1 = wb + off[0]; a.b1 = reinterpret_cast<const float*>(wb + off[1]);
   a.w2 = wb + off[2]; a.b2 = reinterpret_cast<const float*>(wb + off[3]);
   a.w3 = wb + off[4]; a.b3 = reinterpret_cast<const float*>(wb + off[5]);
-  a.w2t = m.w2; a.w3t = m.w3;
   a.obs = obs; a.act = act; a.logp_old = logp_old; a.adv = adv; a.ret = ret;
   a.seed = seed; a.clip = clip; a.c_v = c_v; a.c_h = c_h;
   a.idx_out = idx_out; a.err = err;

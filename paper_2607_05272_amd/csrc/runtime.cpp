@@ -534,8 +534,6 @@ int ppo_minibatch_grad(sim_ctx* x, const void* d_weights, int32_t T, const float
                   hipGetErrorString(he));
     x->ppo_bytes = need;
   }
-  int rc = repack_weights(x, d_weights);
-  if (rc) return rc;
   size_t off[6];
   offsets(x->cfg, off);
   HIPCHK(x->timed(SIM_KC_PPO, [&] {
