@@ -249,7 +249,7 @@ __global__ void zero_f32_k(float* p, int n) {
 // accumulator values are then four consecutive output units of one environment, so the
 // epilogue writes them to the next layer's buffer as one 8-byte store after two packed
 // fp32->bf16 conversions. Each wave owns a disjoint set of output-unit tiles, so a workgroup
-// reads every weight once (from L2); the next k-step's weight fragments are loaded while
+// reads every weight once (from L2); weight fragments of the next k-steps are loaded while
 // the current step's MFMAs run.
 typedef __attribute__((ext_vector_type(2))) float f32x2;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
@@ -266,46 +266,45 @@ __device__ __forceinline__ void mma_t(const uint16_t* __restrict__ act, int sa,
                                       f32x4 (&acc)[(N / 16 + NW - 1) / NW][RT]) {
   constexpr int NT = N / 16, CTW = (NT + NW - 1) / NW, KS = K / 32;
   constexpr bool kEven = NT % NW == 0;  // every wave owns CTW output tiles
+  // k-steps of weight fragments in flight ahead of their use: a wave with few output tiles
+  // has registers for a deeper ring
+  constexpr int D = CTW <= 2 ? 3 : 1, S = D + 1;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
-  // the accumulators start at the bias: a lane's four values are units u0..u0+3
+  // bias of the wave's tiles: a lane's four values are units u0..u0+3; it is the C operand
+  // of the first k-step
+  f32x4 bv[CTW];
 #pragma unroll
   for (int c = 0; c < CTW; ++c) {
-    f32x4 bv = f32x4{0.f, 0.f, 0.f, 0.f};
+    bv[c] = f32x4{0.f, 0.f, 0.f, 0.f};
     if (kEven || wave + NW * c < NT)
-      bv = *reinterpret_cast<const f32x4*>(bias + (wave + NW * c) * 16 + kq * 4);
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) acc[c][rt] = bv;
+      bv[c] = *reinterpret_cast<const f32x4*>(bias + (wave + NW * c) * 16 + kq * 4);
   }
-  bf16x8 w[2][CTW];
+  bf16x8 w[S][CTW];
   const uint16_t* wbase = W + (size_t)wave * KS * 512 + lane * 8;   // fragment order
   constexpr size_t WSTEP = (size_t)NW * KS * 512;  // elements between a wave's output tiles
   const uint16_t* brow = act + r16 * sa + kq * 8;
-  auto loadw = [&](int buf, int ks) {
+  auto loadw = [&](int slot, int ks) {
 #pragma unroll
     for (int c = 0; c < CTW; ++c)
       if (kEven || wave + NW * c < NT)
-        w[buf][c] = *reinterpret_cast<const bf16x8*>(wbase + c * WSTEP + ks * 512);
+        w[slot][c] = *reinterpret_cast<const bf16x8*>(wbase + c * WSTEP + ks * 512);
   };
-  auto mma = [&](int buf, int ks) {
-    bf16x8 b[RT];
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-      b[rt] = *reinterpret_cast<const bf16x8*>(brow + rt * 16 * sa + ks * 32);
+  for (int s = 0; s < D; ++s)
+    if (s < KS) loadw(s, s);
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
+  for (int ks = 0; ks < KS; ++ks) {
+    if (ks + D < KS) loadw((ks + D) % S, ks + D);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const bf16x8 b = *reinterpret_cast<const bf16x8*>(brow + rt * 16 * sa + ks * 32);
 #pragma unroll
       for (int c = 0; c < CTW; ++c)
         if (kEven || wave + NW * c < NT)
-          acc[c][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[buf][c], b[rt], acc[c][rt], 0, 0, 0);
-  };
-  loadw(0, 0);
-#pragma unroll 1
-  for (int ks = 0; ks < KS; ks += 2) {
-    if (ks + 1 < KS) loadw(1, ks + 1);
-    mma(0, ks);
-    if (ks + 2 < KS) loadw(0, ks + 2);
-    if (ks + 1 < KS) mma(1, ks + 1);
+          acc[c][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[ks % S][c], b,
+                                                               ks == 0 ? bv[c] : acc[c][rt], 0, 0, 0);
+    }
   }
 }
 
@@ -535,7 +534,7 @@ hipError_t launch_policy(const MlpParams& m, const float* obs, uint64_t seed, ui
     return big ? run_policy_bf16<64, 256, 256, 64, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, st)
                : run_policy_bf16<64, 256, 256, 64, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, st);
   if (m.bf16 && m.FP == 96 && m.H1 == 512 && m.H2 == 512 && m.AP == 112)
-    return big ? run_policy_bf16<96, 512, 512, 112, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, st)
+    return big ? run_policy_bf16<96, 512, 512, 112, 8, 16, 1>(m, obs, seed, step, act, logp, value, logits, st)
                : run_policy_bf16<96, 512, 512, 112, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, st);
   return hipErrorInvalidValue;
 }

@@ -243,39 +243,53 @@ def mlp_tol(w, wts, obs):
     return scale * (2.0 ** -6 if bf else 2.0 ** -18)
 
 
-@pytest.mark.parametrize("name", NAMES)
-def test_policy_parity(bs, orc, name):
-    """MLP logits/value within the derived tolerance; sampled actions identical wherever
-    the oracle's uniform is farther than 2*max|dlogit| from a CDF boundary; logp close."""
-    w = preset(name)
-    E = 1000
-    step = 17
-    seed = 0x5EED
+def check_policy(bs, orc, w, E, ids, step=17, seed=0x5EED):
+    """Policy on E seeded observations through the C ABI; the oracle evaluates rows `ids`.
+    MLP logits/value within the derived tolerance; sampled actions identical wherever the
+    oracle's uniform is farther than 2*max|dlogit| from a CDF boundary; logp close."""
     wts = orc.init_weights(w, 99)
     obs = seeded_obs(21, E, w["obs_dim"])
-    say(f"[policy] {name}")
     sim = bs.Sim(w, n_envs=E)
     sim.reset(seed)
     wb = sim.upload_weights(wts)
     out = sim.policy(wb, torch.from_numpy(np.ascontiguousarray(obs.T)).cuda(), step, want_logits=True)
     torch.cuda.synchronize()
-    lg = out["logits"].cpu().numpy().T.astype(np.float64)
-    act = out["actions"].cpu().numpy()
-    logp = out["logp"].cpu().numpy().astype(np.float64)
-    ref = orc.policy(w, wts, seed, step, obs, np.arange(E))
-    tol = mlp_tol(w, wts, obs)
+    lg = out["logits"].cpu().numpy().T.astype(np.float64)[ids]
+    act = out["actions"].cpu().numpy()[ids]
+    logp = out["logp"].cpu().numpy().astype(np.float64)[ids]
+    ref = orc.policy(w, wts, seed, step, obs[ids], ids)
+    tol = mlp_tol(w, wts, obs[ids])
     err = np.abs(lg - ref["logits"])
     assert np.all(err <= tol), f"max err/tol {np.max(err / tol):.3g}"
     A = 6 * w["n_servers"]
     eps = 2 * err[:, :A].max(axis=1) + 1e-5
     sure = ref["margin"] > eps
     assert np.array_equal(act[sure], ref["actions"][sure]), "actions differ away from ties"
-    say(f"  near-ties {np.sum(~sure)} of {E}; max logit err {err.max():.3g}")
+    say(f"  near-ties {np.sum(~sure)} of {len(ids)}; max logit err {err.max():.3g}")
     assert np.all(np.abs(logp[sure] - ref["logp"][sure]) <= eps[sure] + 1e-5)
     if w["value_head"]:
-        v = out["value"].cpu().numpy()
+        v = out["value"].cpu().numpy()[ids]
         assert np.array_equal(v, lg[:, A].astype(np.float32))
     sim.close()
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_policy_parity(bs, orc, name):
+    """Every environment of a batch below the large-batch tiling threshold."""
+    say(f"[policy] {name}")
+    check_policy(bs, orc, preset(name), 1000, np.arange(1000))
+
+
+@pytest.mark.parametrize("name", ["C2", "C3", "C4", "C5"])
+def test_policy_parity_large_batch(bs, orc, name):
+    """A batch above the large-batch threshold (64 * 512 environments) with a ragged last
+    workgroup: the first and last environments and a seeded sample in between."""
+    E = 64 * 512 + 77
+    rng = np.random.default_rng(7)
+    ids = np.unique(np.concatenate([np.arange(96), np.arange(E - 160, E),
+                                    rng.integers(0, E, 256)])).astype(np.int64)
+    say(f"[policy large] {name} E={E}")
+    check_policy(bs, orc, preset(name), E, ids)
 
 
 @pytest.mark.parametrize("name", ["C1", "C3", "C5"])
