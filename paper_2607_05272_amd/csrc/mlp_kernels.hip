@@ -308,21 +308,16 @@ __device__ __forceinline__ void mma_t(const uint16_t* __restrict__ act, int sa,
   }
 }
 
-// GELU(x) = x Phi(x) = relu(x) - 0.5 |x| erfc(|x| / sqrt 2) (x erf(x/sqrt2) is even in x),
-// with erfc from Abramowitz & Stegun, Handbook of Mathematical Functions, formula 7.1.26:
-// erfc(z) = (a1 t + a2 t^2 + ... + a5 t^5) exp(-z^2), t = 1 / (1 + p z), |error| <= 1.5e-7,
-// far below the bf16 rounding that follows. Constants: p / sqrt 2 and a_i / 2 are folded in;
-// exp(-x^2 / 2) = 2^(-x^2 log2(e) / 2).
+// GELU(x) = x Phi(x) with Phi(x) = logistic(h(x)), h(x) = -log2(e)^-1 x (c1 + c3 x^2 + c5 x^4)
+// written for exp2: GELU(x) = x / (1 + 2^(x (k1 + k3 x^2 + k5 x^4))). The odd polynomial is
+// a least-maximum-error fit of logit(Phi) over |x| <= 10 (largest absolute GELU error
+// 2.6e-5, below the bf16 rounding that follows for every activation above 1e-2 in
+// magnitude); x^2 is clamped at 64, where the argument is still increasing, so that for
+// |x| > 8 it grows linearly and the result saturates to 0 or x.
 __device__ __forceinline__ float gelu_fast(float x) {
-  const float a = fabsf(x);
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.23164189f, a, 1.0f));   // p / sqrt 2
-  float poly = fmaf(0.5307027145f, t, -0.7265760135f);                // a5/2, a4/2
-  poly = fmaf(poly, t, 0.7107068705f);                                // a3/2
-  poly = fmaf(poly, t, -0.142248368f);                                // a2/2
-  poly = fmaf(poly, t, 0.127414796f);                                 // a1/2
-  const float e = __builtin_amdgcn_exp2f((x * -0.72134752044f) * x);   // exp(-x^2/2)
-  const float q = (poly * t) * e;                                      // erfc(|x|/sqrt2)/2
-  return fmaf(-a, q, fmaxf(x, 0.0f));
+  const float x2 = fminf(x * x, 64.0f);
+  const float w = fmaf(fmaf(0.001014263f, x2, -0.10677572f), x2, -2.3011212f);
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * w));
 }
 
 // GELU + bf16 rounding (the bias is already in the accumulators); four consecutive units of
@@ -417,48 +412,59 @@ __global__ __launch_bounds__(NW * 64, MINB) void policy_bf16_k(MlpParams m, cons
     }
   }
   __syncthreads();
-  // sampling: four lanes per environment row (lanes 4r..4r+3 of the workgroup), each over a
-  // contiguous quarter of the actions; max and sum by xor shuffles, then the quarter whose
-  // cumulative range holds u*S walks its actions in order
-  for (int row0 = 0; row0 < ROWS; row0 += NTHR / 4) {
-    const int row = row0 + tid / 4, part = tid & 3;
+  // sampling: G lanes per environment row (an aligned group of G lanes), each over a
+  // contiguous slice of the actions whose exponentials it keeps in registers; max, prefix
+  // sums and the first slice holding the target u*S by shuffles within the group
+  constexpr int G = 8, KMAX = (AP + G - 1) / G;
+  static_assert(NTHR % G == 0, "sampler groups");
+  for (int row0 = 0; row0 < ROWS; row0 += NTHR / G) {
+    const int row = row0 + tid / G, part = tid % G;
     const int e = e0 + row;
     const bool live = row < ROWS && e < m.E;
     const float* l = lg + (row < ROWS ? row : 0) * Sh::SL;
     const int A = m.A;
-    const int chunk = (A + 3) / 4;
-    const int lo = part * chunk, hi = lo + chunk < A ? lo + chunk : A;
+    const int chunk = (A + G - 1) / G;
+    const int lo = part * chunk;
     float mx = -3.0e38f;
-    for (int i = lo; i < hi; ++i) mx = l[i] > mx ? l[i] : mx;
-    mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
-    float part_sum = 0.f;
-    for (int i = lo; i < hi; ++i) part_sum += __expf(l[i] - mx);
-    const float s0 = __shfl(part_sum, (tid & ~3) & 63, 64), s1 = __shfl(part_sum, ((tid & ~3) + 1) & 63, 64);
-    const float s2 = __shfl(part_sum, ((tid & ~3) + 2) & 63, 64), s3 = __shfl(part_sum, ((tid & ~3) + 3) & 63, 64);
-    const float S = (s0 + s1) + (s2 + s3);
-    const float before = part == 0 ? 0.f : part == 1 ? s0 : part == 2 ? s0 + s1 : (s0 + s1) + s2;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i)
+      if (i < chunk && lo + i < A) mx = fmaxf(mx, l[lo + i]);
+#pragma unroll
+    for (int off = 1; off < G; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, G));
+    float pe[KMAX];
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) {
+      pe[i] = (i < chunk && lo + i < A) ? __expf(l[lo + i] - mx) : 0.f;
+      ps += pe[i];
+    }
+    float incl = ps;
+#pragma unroll
+    for (int off = 1; off < G; off <<= 1) {
+      const float t = __shfl_up(incl, off, G);
+      if (part >= off) incl += t;
+    }
+    const float S = __shfl(incl, G - 1, G);
     const u32x4 w = draw(seed, (uint32_t)(live ? e : 0), step, P_ACTION, 0, 0);
     const float u = ((float)(w.x >> 9) + 0.5f) * 0x1p-23f;
     const float target = u * S;
-    int found = -1;
-    if (live && (act || logp)) {
-      float cum = before;
-      for (int i = lo; i < hi; ++i) {
-        cum += __expf(l[i] - mx);
-        if (target < cum) { found = i; break; }
-      }
+    int found = 0x7fffffff;
+    float cum = incl - ps;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) {
+      cum += pe[i];
+      if (found == 0x7fffffff && i < chunk && lo + i < A && target < cum) found = lo + i;
     }
-    const int f0 = __shfl(found, (tid & ~3) & 63, 64), f1 = __shfl(found, ((tid & ~3) + 1) & 63, 64);
-    const int f2 = __shfl(found, ((tid & ~3) + 2) & 63, 64), f3 = __shfl(found, ((tid & ~3) + 3) & 63, 64);
+#pragma unroll
+    for (int off = 1; off < G; off <<= 1) found = min(found, __shfl_xor(found, off, G));
     if (live && part == 0) {
-      const int a = f0 >= 0 ? f0 : f1 >= 0 ? f1 : f2 >= 0 ? f2 : f3 >= 0 ? f3 : A - 1;
+      const int a = found < A ? found : A - 1;
       if (act) act[e] = (uint8_t)a;
       if (logp) logp[e] = (l[a] - mx) - __logf(S);
       if (value && m.value_head) value[e] = l[A];
     }
     if (live && logits)
-      for (int i = part; i < m.Ap; i += 4) logits[(size_t)i * m.E + e] = l[i];
+      for (int i = part; i < m.Ap; i += G) logits[(size_t)i * m.E + e] = l[i];
   }
 }
 

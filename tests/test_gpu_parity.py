@@ -223,13 +223,17 @@ def test_init_weights_bit_identical(bs, orc, name):
 
 
 def mlp_tol(w, wts, obs):
-    """Per-output tolerance |gpu - oracle| <= tol_a = c * sum_i |W3_ia| |h2_i| + |b3_a| eps.
+    """Per-output tolerance |gpu - oracle| <= tol_a = c * sum_i |W3_ia| |h2_i| + |b3_a| eps
+    (+ the GELU term below in bf16 mode).
 
     fp32 mode: only accumulation order differs (fp32 sums of <= 64 terms): c = 2^-18.
     bf16 mode: each layer input is rounded to bf16; a value whose fp32 (GPU) and fp64
     (oracle) pre-rounding images straddle a rounding boundary can round one bf16 ulp
     (2^-8 relative) apart, and the two hidden layers propagate such flips, so c = 2^-6
-    (one ulp at each of the two hidden rounding points, with a factor-of-two margin)."""
+    (one ulp at each of the two hidden rounding points, with a factor-of-two margin).
+    The bf16 kernels evaluate GELU to within eps_G = 2^-15 absolute (a fitted logistic
+    form); that error enters h1 directly and h2 directly and through W2 (GELU' <= 1.13):
+    + eps_G * sum_i |W3_ia| (1 + 1.13 sum_j |W2_ji|)."""
     import torch.nn.functional as Fn
     bf = bool(w["mlp_bf16"])
 
@@ -240,7 +244,10 @@ def mlp_tol(w, wts, obs):
     h1 = rnd(Fn.gelu(x @ W["w1"] + W["b1"]))
     h2 = rnd(Fn.gelu(h1 @ W["w2"] + W["b2"]))
     scale = (h2.abs() @ W["w3"].abs()).numpy() + np.abs(wts["b3"])[None, :]
-    return scale * (2.0 ** -6 if bf else 2.0 ** -18)
+    if not bf:
+        return scale * 2.0 ** -18
+    gelu_term = 2.0 ** -15 * ((1.0 + 1.13 * np.abs(wts["w2"]).sum(axis=0)) @ np.abs(wts["w3"]))
+    return scale * 2.0 ** -6 + gelu_term[None, :]
 
 
 def check_policy(bs, orc, w, E, ids, step=17, seed=0x5EED):
