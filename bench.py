@@ -4,7 +4,8 @@
 One step = one pass of the whole hot path over one synthetic batch: reset every
 environment, then T ticks of (policy MLP + action sampling on MFMA, simulator tick of the
 learned system and, where configured, of the static shadow system), then returns/GAE
-over the trajectory and the device-side reduction of the per-environment counters.
+over the trajectory, for workloads with a PPO minibatch (C4) one minibatch gradient over
+the stored trajectory, and the device-side reduction of the per-environment counters.
 value = environments x ticks per second of wall time (inputs resident in HBM).
 
 Prints one JSON line. Kernel durations come from HIP events recorded by the library on
@@ -24,6 +25,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3       # dense fp32 matrix
+PEAK_FP32_VALU_TFLOPS = 157.3  # fp32 vector FMA: 256 CUs x 4 SIMD x 2 x 64 lanes x 2.4 GHz
 
 DESCR = {
     "C1": "C1: 256 envs x 1000 ticks, 1 server, Poisson 500/s, DET 5ms+0.5ms*b, obs 8, MLP 8-64-64-6 fp32, REINFORCE returns",
@@ -37,6 +39,16 @@ DESCR = {
 def mlp_flops(w):
     A1 = 6 * w["n_servers"] + (1 if w["value_head"] else 0)
     return 2 * (w["obs_dim"] * w["mlp_h1"] + w["mlp_h1"] * w["mlp_h2"] + w["mlp_h2"] * A1)
+
+
+def ppo_flops(w):
+    """One PPO minibatch: forward, backward through the activations (all but the input
+    layer) and the three weight gradients, 2 flops per multiply-add."""
+    M = w["ppo_minibatch"]
+    F, H1, H2 = w["obs_dim"], w["mlp_h1"], w["mlp_h2"]
+    Ap = 6 * w["n_servers"] + 1
+    fwd = F * H1 + H1 * H2 + H2 * Ap
+    return 2 * M * (fwd + (H1 * H2 + H2 * Ap) + fwd)
 
 
 def step_bytes(w, tot, E, T):
@@ -84,6 +96,64 @@ def traffic_for(kernel, cfg_name):
     return ent.get("bytes_per_launch")
 
 
+KERNEL_OF = {"policy": "policy_", "step": "learned_k", "static": "static_k", "gae": "gae_k",
+             "ppo": "ppo_"}
+
+
+def _pmc_rows(d):
+    import csv
+    import glob
+    rows = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        rows += list(csv.DictReader(open(f)))
+    return rows
+
+
+def _per_dispatch(rows, counter, match, launch=None):
+    """Counter total over the kernels that `match`, per launch (a launch counted once per
+    dispatch of the kernels that `launch` matches, default `match`)."""
+    launch = launch or match
+    tot, disp = 0.0, set()
+    for r in rows:
+        if r["Counter_Name"] != counter:
+            continue
+        if match(r["Kernel_Name"]):
+            tot += float(r["Counter_Value"])
+        if launch(r["Kernel_Name"]):
+            disp.add(r.get("Dispatch_Id") or r.get("Correlation_Id"))
+    return (tot / len(disp), len(disp)) if disp else (None, 0)
+
+
+def write_traffic(d, cfg_name):
+    """HBM bytes per launch of each kernel class from FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch), each scaled so that the calibration copy reads and writes its known size."""
+    calib = 1024 << 20
+    cf, _ = _per_dispatch(_pmc_rows(os.path.join(d, "cfetch")), "FETCH_SIZE",
+                          lambda k: "elementwise" in k and "Mul" in k)
+    cw, _ = _per_dispatch(_pmc_rows(os.path.join(d, "cwrite")), "WRITE_SIZE",
+                          lambda k: "elementwise" in k and "Mul" in k)
+    f_fac = calib / (cf * 1024.0)
+    w_fac = calib / (cw * 1024.0)
+    fr, wr = _pmc_rows(os.path.join(d, "fetch")), _pmc_rows(os.path.join(d, "write"))
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        out = json.load(open(path))
+    except (OSError, ValueError):
+        out = {}
+    for cls, pat in KERNEL_OF.items():
+        first = (lambda k: "ppo_fwd_k" in k) if cls == "ppo" else None
+        fk, nf = _per_dispatch(fr, "FETCH_SIZE", lambda k, p=pat: p in k, first)
+        wk, nw = _per_dispatch(wr, "WRITE_SIZE", lambda k, p=pat: p in k, first)
+        if fk is None or wk is None:
+            continue
+        out[f"{cfg_name}:{cls}"] = {
+            "bytes_per_launch": fk * 1024.0 * f_fac + wk * 1024.0 * w_fac,
+            "fetch_kib_raw": fk, "write_kib_raw": wk, "dispatches": [nf, nw],
+            "fetch_factor": f_fac, "write_factor": w_fac, "kernel_hash": kernel_hash()}
+    json.dump(out, open(path, "w"), indent=1, sort_keys=True)
+    print(json.dumps(out, indent=1, sort_keys=True))
+
+
 def cpu_baseline(w, name, budget_s, seed):
     """The oracle (sequential fp64 simulator + fp64 policy MLP + sampler) on the host
     cores, over a bounded sample of the same workload, env-steps per second."""
@@ -128,16 +198,24 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="only copy this many MiB device-to-device (HBM counter calibration)")
+    ap.add_argument("--write-traffic", default="",
+                    help="directory of rocprofv3 --pmc runs (fetch/, write/, cfetch/, cwrite/): "
+                         "write profiles/traffic.json and exit")
     args = ap.parse_args()
     if args.calib_copy_mib:
+        # a plain elementwise copy of known size (reads n bytes, writes n bytes), for
+        # scaling the HBM byte counters of the profiler
         import torch
         n = args.calib_copy_mib << 20
-        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         for _ in range(3):
-            dst.copy_(src)
+            torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
         print(json.dumps({"calib_copy_bytes": n, "copies": 3}))
+        return
+    if args.write_traffic:
+        write_traffic(args.write_traffic, args.config)
         return
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU only (environments are independent; the "
@@ -156,7 +234,11 @@ def main():
     seed = 0x5EED0000 + int(args.config[1])
     sim = bs.Sim(w)
     weights = sim.init_weights(seed)
-    traj = bs.Trajectory(T, E, F, dev, value=bool(w["value_head"]), shadow=bool(w["shadow"]))
+    ppo = w.get("ppo_minibatch", 0) > 0
+    traj = bs.Trajectory(T, E, F, dev, value=bool(w["value_head"]), shadow=bool(w["shadow"]),
+                         obs=ppo)
+    grads = torch.empty(sim.ppo_grad_count(), dtype=torch.float32, device=dev) if ppo else None
+    ploss = torch.empty(4, dtype=torch.float64, device=dev) if ppo else None
     adv = torch.empty((T, E), dtype=torch.float64, device=dev)
     ret = torch.empty((T, E), dtype=torch.float64, device=dev)
     gae = bool(w["value_head"])
@@ -166,6 +248,9 @@ def main():
         sim.reset(seed + i)
         sim.rollout(weights, T, traj=traj)
         sim.returns_gae(traj.reward, traj.value if gae else None, w["gamma"], lam, adv, ret)
+        if ppo:
+            sim.ppo_minibatch_grad(weights, traj.obs, traj.actions, traj.logp, adv, ret,
+                                   w["ppo_minibatch"], seed + i, grads=grads, loss=ploss)
         return sim.stats()
 
     for i in range(args.warmup):
@@ -219,6 +304,12 @@ def main():
         rl["gae"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("gae", args.config),
                      "work_per_launch": by}
+    if "ppo" in kern:
+        fl = ppo_flops(w)
+        ach = fl / (kern["ppo"]["avg_us"] * 1e-6) / 1e12
+        rl["ppo"] = {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS,
+                     "unit": "TFLOP/s", "frac": ach / PEAK_FP32_VALU_TFLOPS,
+                     "traffic": traffic_for("ppo", args.config), "work_per_launch": fl}
     dom = max(kern, key=lambda k: kern[k]["total_ms_per_step"])
     roof = dict(rl.get(dom, {}))
     roof["kernel"] = dom
