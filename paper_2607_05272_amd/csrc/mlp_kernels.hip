@@ -259,55 +259,6 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
-template <int K, int N, int RT, int NW>
-__device__ __forceinline__ void mma_t(const uint16_t* __restrict__ act, int sa,
-                                      const uint16_t* __restrict__ W,
-                                      const float* __restrict__ bias,
-                                      f32x4 (&acc)[(N / 16 + NW - 1) / NW][RT]) {
-  constexpr int NT = N / 16, CTW = (NT + NW - 1) / NW, KS = K / 32;
-  constexpr bool kEven = NT % NW == 0;  // every wave owns CTW output tiles
-  // k-steps of weight fragments in flight ahead of their use: a wave with few output tiles
-  // has registers for a deeper ring
-  constexpr int D = CTW <= 2 ? 3 : 1, S = D + 1;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r16 = lane & 15, kq = lane >> 4;
-  // bias of the wave's tiles: a lane's four values are units u0..u0+3; it is the C operand
-  // of the first k-step
-  f32x4 bv[CTW];
-#pragma unroll
-  for (int c = 0; c < CTW; ++c) {
-    bv[c] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (kEven || wave + NW * c < NT)
-      bv[c] = *reinterpret_cast<const f32x4*>(bias + (wave + NW * c) * 16 + kq * 4);
-  }
-  bf16x8 w[S][CTW];
-  const uint16_t* wbase = W + (size_t)wave * KS * 512 + lane * 8;   // fragment order
-  constexpr size_t WSTEP = (size_t)NW * KS * 512;  // elements between a wave's output tiles
-  const uint16_t* brow = act + r16 * sa + kq * 8;
-  auto loadw = [&](int slot, int ks) {
-#pragma unroll
-    for (int c = 0; c < CTW; ++c)
-      if (kEven || wave + NW * c < NT)
-        w[slot][c] = *reinterpret_cast<const bf16x8*>(wbase + c * WSTEP + ks * 512);
-  };
-#pragma unroll
-  for (int s = 0; s < D; ++s)
-    if (s < KS) loadw(s, s);
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    if (ks + D < KS) loadw((ks + D) % S, ks + D);
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const bf16x8 b = *reinterpret_cast<const bf16x8*>(brow + rt * 16 * sa + ks * 32);
-#pragma unroll
-      for (int c = 0; c < CTW; ++c)
-        if (kEven || wave + NW * c < NT)
-          acc[c][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[ks % S][c], b,
-                                                               ks == 0 ? bv[c] : acc[c][rt], 0, 0, 0);
-    }
-  }
-}
-
 // GELU(x) = x Phi(x) with Phi(x) = logistic(h(x)), h(x) = -log2(e)^-1 x (c1 + c3 x^2 + c5 x^4)
 // written for exp2: GELU(x) = x / (1 + 2^(x (k1 + k3 x^2 + k5 x^4))). The odd polynomial is
 // a least-maximum-error fit of logit(Phi) over |x| <= 10 (largest absolute GELU error
@@ -320,26 +271,118 @@ __device__ __forceinline__ float gelu_fast(float x) {
   return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * w));
 }
 
-// GELU + bf16 rounding (the bias is already in the accumulators); four consecutive units of
-// one environment per 8-byte store
-template <int N, int RT, int NW>
-__device__ __forceinline__ void store_hidden_t(const f32x4 (&acc)[(N / 16 + NW - 1) / NW][RT],
-                                               uint16_t* out, int so) {
-  constexpr int NT = N / 16, CTW = (NT + NW - 1) / NW;
+__device__ __forceinline__ u32x2 gelu_pack4(const f32x4 v) {
+  u32x2 pk;
+  pk.x = pack_bf16(gelu_fast(v[0]), gelu_fast(v[1]));
+  pk.y = pack_bf16(gelu_fast(v[2]), gelu_fast(v[3]));
+  return pk;
+}
+
+// One output tile (16 units) of a layer for RTN consecutive environment tiles starting at rt0:
+// acc[rt] = act[rows] W[:, tile] + bias, with a ring of D k-steps of weight fragments in flight.
+// hook(ks) runs after each k-step's MFMAs: the caller puts independent VALU work there, which
+// the SIMD issues while the matrix core is busy.
+template <int K, int RTN, class Hook>
+__device__ __forceinline__ void mma_tile(const uint16_t* __restrict__ act, int sa,
+                                         const uint16_t* __restrict__ W,
+                                         const float* __restrict__ bias, int tile, int rt0,
+                                         f32x4 (&acc)[RTN], Hook&& hook) {
+  constexpr int KS = K / 32, D = KS < 4 ? KS : 4, S = D + 1;
+  const int lane = threadIdx.x & 63, r16 = lane & 15, kq = lane >> 4;
+  const f32x4 bv = *reinterpret_cast<const f32x4*>(bias + tile * 16 + kq * 4);
+  const uint16_t* wp = W + (size_t)tile * KS * 512 + lane * 8;  // fragment order
+  const uint16_t* brow = act + (rt0 * 16 + r16) * sa + kq * 8;
+  bf16x8 w[S];
+#pragma unroll
+  for (int s = 0; s < D; ++s) w[s] = *reinterpret_cast<const bf16x8*>(wp + s * 512);
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    if (ks + D < KS) w[(ks + D) % S] = *reinterpret_cast<const bf16x8*>(wp + (ks + D) * 512);
+#pragma unroll
+    for (int rt = 0; rt < RTN; ++rt) {
+      const bf16x8 b = *reinterpret_cast<const bf16x8*>(brow + rt * 16 * sa + ks * 32);
+      acc[rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[ks % S], b, ks == 0 ? bv : acc[rt],
+                                                        0, 0, 0);
+    }
+    hook(ks);
+  }
+}
+
+// One hidden layer, out = bf16(GELU(act W + b)), for the wave's output tiles wave, wave + NW,
+// ...: the GELU of each tile is placed inside the next tile's k-loop (the last one after it);
+// the compiler is free to schedule it (pinning it there was measured slower at the 128-VGPR
+// budget). A lane's four accumulator values are four consecutive units of one environment,
+// written as one 8-byte store. In place (out aliases act) the packed results wait in
+// registers until every wave has finished reading act.
+template <int K, int N, int RT, int NW, bool kInPlace>
+__device__ __forceinline__ void hidden_layer(const uint16_t* __restrict__ act, int sa,
+                                             const uint16_t* __restrict__ W,
+                                             const float* __restrict__ bias, uint16_t* out,
+                                             int so) {
+  constexpr int NT = N / 16, CTW = NT / NW, KS = K / 32;
+  static_assert(NT % NW == 0, "hidden tiles divide evenly over the waves");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
+  f32x4 acc[2][RT];
+  u32x2 pk[kInPlace ? CTW : 1][RT];
+  auto finish = [&](int c, int rt) {
+    const u32x2 v = gelu_pack4(acc[c & 1][rt]);
+    if (kInPlace) pk[kInPlace ? c : 0][rt] = v;
+    else *reinterpret_cast<u32x2*>(out + (rt * 16 + r16) * so + (wave + NW * c) * 16 + kq * 4) = v;
+  };
 #pragma unroll
   for (int c = 0; c < CTW; ++c) {
-    const int ot = wave + NW * c;
-    if (ot >= NT) continue;
-    const int u0 = ot * 16 + kq * 4;
+    mma_tile<K, RT>(act, sa, W, bias, wave + NW * c, 0, acc[c & 1], [&](int ks) {
+      if (c > 0) {
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const f32x4 v = acc[c][rt];
-      u32x2 pk;
-      pk.x = pack_bf16(gelu_fast(v[0]), gelu_fast(v[1]));
-      pk.y = pack_bf16(gelu_fast(v[2]), gelu_fast(v[3]));
-      *reinterpret_cast<u32x2*>(out + (rt * 16 + r16) * so + u0) = pk;
+        for (int rt = 0; rt < RT; ++rt)
+          if (rt * KS / RT == ks) finish(c - 1, rt);
+      }
+    });
+  }
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) finish(CTW - 1, rt);
+  if (kInPlace) {
+    __syncthreads();  // every wave has finished reading act
+#pragma unroll
+    for (int c = 0; c < CTW; ++c)
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+        *reinterpret_cast<u32x2*>(out + (rt * 16 + r16) * so + (wave + NW * c) * 16 + kq * 4) =
+            pk[kInPlace ? c : 0][rt];
+  }
+}
+
+__host__ __device__ constexpr int pow2_floor(int v) { return v >= 8 ? 8 : v >= 4 ? 4 : v >= 2 ? 2 : 1; }
+
+// Output layer (logits and value, fp32 into lg, which aliases act): NT tiles x G groups of
+// environment tiles are spread over the waves so that narrow heads still keep most waves busy.
+template <int K, int NO, int RT, int NW>
+__device__ __forceinline__ void output_layer(const uint16_t* __restrict__ act, int sa,
+                                             const uint16_t* __restrict__ W,
+                                             const float* __restrict__ bias, float* lg, int sl) {
+  constexpr int NT = NO / 16;
+  constexpr int G = pow2_floor(RT < NW / NT ? RT : (NW / NT > 0 ? NW / NT : 1));
+  constexpr int RTI = RT / G, ITEMS = NT * G, IPW = (ITEMS + NW - 1) / NW;
+  static_assert(RT % G == 0, "environment-tile groups");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kq = lane >> 4;
+  f32x4 acc[IPW][RTI];
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) {
+    const int item = wave + NW * i;
+    if (item < ITEMS) mma_tile<K, RTI>(act, sa, W, bias, item % NT, (item / NT) * RTI, acc[i],
+                                      [](int) {});
+  }
+  __syncthreads();  // every wave has finished reading act
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) {
+    const int item = wave + NW * i;
+    if (item < ITEMS) {
+      const int t = item % NT, rt0 = (item / NT) * RTI;
+#pragma unroll
+      for (int rt = 0; rt < RTI; ++rt)
+        *reinterpret_cast<f32x4*>(lg + ((rt0 + rt) * 16 + r16) * sl + t * 16 + kq * 4) = acc[i][rt];
     }
   }
 }
@@ -356,7 +399,7 @@ struct BigShape {
 };
 
 template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB>
-__global__ __launch_bounds__(NW * 64, MINB) void policy_bf16_k(MlpParams m, const float* __restrict__ obs,
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MINB / 4 > 0 ? NW * MINB / 4 : 1))) void policy_bf16_k(MlpParams m, const float* __restrict__ obs,
                                                                uint64_t seed, uint32_t step,
                                                                uint8_t* __restrict__ act,
                                                                float* __restrict__ logp,
@@ -382,35 +425,13 @@ __global__ __launch_bounds__(NW * 64, MINB) void policy_bf16_k(MlpParams m, cons
     *reinterpret_cast<uint32_t*>(xs + r * Sh::SX + f) = pack_bf16(v0, v1);
   }
   __syncthreads();
-  {
-    f32x4 acc[(H1 / 16 + NW - 1) / NW][RT];
-    mma_t<FP, H1, RT, NW>(xs, Sh::SX, static_cast<const uint16_t*>(m.w1), m.b1, acc);
-    store_hidden_t<H1, RT, NW>(acc, hs, Sh::SH);
-  }
+  hidden_layer<FP, H1, RT, NW, false>(xs, Sh::SX, static_cast<const uint16_t*>(m.w1), m.b1, hs,
+                                      Sh::SH);
   __syncthreads();
-  {
-    f32x4 acc[(H2 / 16 + NW - 1) / NW][RT];
-    mma_t<H1, H2, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w2), m.b2, acc);
-    __syncthreads();  // every wave has finished reading h1
-    store_hidden_t<H2, RT, NW>(acc, hs, Sh::SH);
-  }
+  hidden_layer<H1, H2, RT, NW, true>(hs, Sh::SH, static_cast<const uint16_t*>(m.w2), m.b2, hs,
+                                     Sh::SH);
   __syncthreads();
-  {
-    constexpr int NT = AP / 16, CTW = (NT + NW - 1) / NW;
-    f32x4 acc[CTW][RT];
-    mma_t<H2, AP, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w3), m.b3, acc);
-    __syncthreads();  // every wave has finished reading h2
-    const int lane = tid & 63, wave = tid >> 6, r16 = lane & 15, kq = lane >> 4;
-#pragma unroll
-    for (int c = 0; c < CTW; ++c) {
-      const int ot = wave + NW * c;
-      if (ot >= NT) continue;
-      const int u0 = ot * 16 + kq * 4;
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-        *reinterpret_cast<f32x4*>(lg + (rt * 16 + r16) * Sh::SL + u0) = acc[c][rt];
-    }
-  }
+  output_layer<H2, AP, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w3), m.b3, lg, Sh::SL);
   __syncthreads();
   // sampling: G lanes per environment row (an aligned group of G lanes), each over a
   // contiguous slice of the actions whose exponentials it keeps in registers; max, prefix
