@@ -224,6 +224,49 @@ int ppo_minibatch_grad(sim_ctx* ctx, const void* d_weights, int32_t T, const flo
 /* Number of fp32 gradient values written by ppo_minibatch_grad (no device work).       */
 int sim_ppo_grad_count(const sim_cfg* cfg, int64_t* h_count);
 
+/* REINFORCE with a learned baseline (Sec. 4.3) on one minibatch: as ppo_minibatch_grad, with
+ * the policy term -mean(A log pi(a|s)) (A held constant) and no old log-probabilities; the
+ * caller passes A = G - V and R = G (returns_gae with lambda = 1 gives both).            */
+int reinforce_minibatch_grad(sim_ctx* ctx, const void* d_weights, int32_t T, const float* d_obs,
+                             const uint8_t* d_actions, const double* d_adv, const double* d_ret,
+                             int32_t M, uint64_t seed, float c_value, float c_entropy,
+                             float* d_grads, double* d_loss, int64_t* d_index);
+
+/* Master parameters from a weights buffer: d_params (device, sim_ppo_grad_count fp32 values
+ * in the gradient layout) receives the values d_weights holds.                          */
+int sim_params_from_weights(sim_ctx* ctx, const void* d_weights, float* d_params);
+
+/* One Adam step (Kingma & Ba 2015, Algorithm 1) on the fp32 master parameters, in place:
+ *   m = b1 m + (1-b1) g,  v = b2 v + (1-b2) g^2,  p -= lr (m/(1-b1^t)) / (sqrt(v/(1-b2^t)) + eps)
+ * with t = step >= 1 (the step being taken); d_m, d_v are the caller's moment buffers (zero
+ * before the first step). With d_weights non-NULL the policy's weights are then rewritten from
+ * the parameters (matrices rounded to bf16, nearest even, in bf16 configurations).        */
+int adam_update(sim_ctx* ctx, float* d_params, const float* d_grads, float* d_m, float* d_v,
+                int32_t step, float lr, float beta1, float beta2, float eps, void* d_weights);
+
+enum sim_algo { SIM_ALGO_PPO = 0, SIM_ALGO_REINFORCE = 1 };
+
+typedef struct sim_update_cfg {
+  int32_t algo;         /* SIM_ALGO_PPO or SIM_ALGO_REINFORCE */
+  int32_t epochs;       /* passes over the trajectory */
+  int32_t minibatches;  /* minibatches per epoch */
+  int32_t M;            /* samples per minibatch (multiple of 16) */
+  uint64_t seed;        /* minibatch b of epoch e: key seed + (e*minibatches + b)*0x9E3779B97F4A7C15 */
+  float clip;           /* PPO clip range epsilon */
+  float c_value, c_entropy;
+  float lr, beta1, beta2, eps;
+} sim_update_cfg;
+
+/* The policy update of Sec. 4.3 over one stored trajectory (d_obs [T][F][E], d_actions,
+ * d_logp_old (PPO only) [T][E], d_adv, d_ret [T][E] fp64): for each epoch and minibatch,
+ * the minibatch gradient and one Adam step, after which d_weights holds the new policy.
+ * *h_step is Adam's step count, advanced once per minibatch. d_losses (optional, device)
+ * receives [epochs*minibatches][4] fp64 loss terms, each from the weights before its step. */
+int sim_update(sim_ctx* ctx, const sim_update_cfg* cfg, void* d_weights, float* d_params,
+               float* d_m, float* d_v, int32_t* h_step, int32_t T, const float* d_obs,
+               const uint8_t* d_actions, const float* d_logp_old, const double* d_adv,
+               const double* d_ret, double* d_losses);
+
 /* Per-environment counters [2][SIM_NCNT][E] int64 and sums [2][SIM_NSUM][E] fp64 into
  * device buffers (either may be NULL).                                                  */
 int sim_counters(sim_ctx* ctx, int64_t* d_cnt, double* d_sum);
@@ -247,7 +290,7 @@ enum sim_kernel_class {
   SIM_KC_GAE = 3,     /* returns / GAE */
   SIM_KC_RESET = 4,   /* reset */
   SIM_KC_OTHER = 5,   /* weight repack / init, counters, totals */
-  SIM_KC_PPO = 6,     /* PPO minibatch gradient */
+  SIM_KC_PPO = 6,     /* policy update: minibatch gradients, Adam */
   SIM_KC_COUNT = 7
 };
 

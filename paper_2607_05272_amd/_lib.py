@@ -21,7 +21,9 @@ SYMBOLS = ("sim_last_error", "sim_abi_version", "sim_create", "sim_destroy", "si
            "sim_reset", "sim_obs", "sim_step", "sim_tick", "sim_weights_layout",
            "sim_init_weights", "sim_policy", "sim_rollout", "returns_gae", "sim_counters",
            "sim_checksums", "sim_stats", "sim_sync", "sim_set_timing", "sim_get_timing",
-           "ppo_minibatch_grad", "sim_ppo_grad_count")
+           "ppo_minibatch_grad", "sim_ppo_grad_count", "reinforce_minibatch_grad",
+           "sim_params_from_weights", "adam_update", "sim_update")
+ALGO_PPO, ALGO_REINFORCE = 0, 1
 KERNEL_CLASSES = ("policy", "step", "static", "gae", "reset", "other", "ppo")
 
 
@@ -54,6 +56,13 @@ class SimTraj(C.Structure):
     _fields_ = [("actions", C.c_void_p), ("logp", C.c_void_p), ("reward", C.c_void_p),
                 ("reward_shadow", C.c_void_p), ("value", C.c_void_p), ("obs", C.c_void_p),
                 ("rchk", C.c_void_p)]
+
+
+class SimUpdateCfg(C.Structure):
+    _fields_ = [("algo", C.c_int32), ("epochs", C.c_int32), ("minibatches", C.c_int32),
+                ("M", C.c_int32), ("seed", C.c_uint64), ("clip", C.c_float),
+                ("c_value", C.c_float), ("c_entropy", C.c_float), ("lr", C.c_float),
+                ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float)]
 
 
 class SimTotals(C.Structure):
@@ -93,6 +102,11 @@ def load():
         "ppo_minibatch_grad": [vp, vp, i32, vp, vp, vp, vp, vp, i32, u64, C.c_float, C.c_float,
                                C.c_float, vp, vp, vp],
         "sim_ppo_grad_count": [vp, vp],
+        "reinforce_minibatch_grad": [vp, vp, i32, vp, vp, vp, vp, i32, u64, C.c_float, C.c_float,
+                                     vp, vp, vp],
+        "sim_params_from_weights": [vp, vp, vp],
+        "adam_update": [vp, vp, vp, vp, vp, i32, C.c_float, C.c_float, C.c_float, C.c_float, vp],
+        "sim_update": [vp, vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, vp],
     }
     for name, args in sig.items():
         f = getattr(L, name)

@@ -95,8 +95,16 @@ bool policy_shape_supported(const MlpParams& m);
 hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t off[6], int T,
                       const float* obs, const uint8_t* act, const float* logp_old,
                       const double* adv, const double* ret, int M, uint64_t seed, float clip,
-                      float c_v, float c_h, float* scratch, double* loss_out, float* grads,
-                      int64_t* idx_out, uint32_t* err, hipStream_t st);
+                      float c_v, float c_h, int reinforce, float* scratch, double* loss_out,
+                      float* grads, int64_t* idx_out, uint32_t* err, hipStream_t st);
+// Adam on fp32 parameters (train_kernels.hip): one step, bias corrections bc1 = 1 - b1^t and
+// bc2 = 1 - b2^t computed by the caller; then the policy's weights from the parameters
+hipError_t launch_adam(float* params, const float* grads, float* m, float* v, size_t n, float lr,
+                       float b1, float b2, float eps, float bc1, float bc2, hipStream_t st);
+hipError_t launch_export_weights(const MlpParams& m, const float* params, void* d_weights,
+                                 const size_t off[6], hipStream_t st);
+hipError_t launch_import_weights(const MlpParams& m, const void* d_weights, const size_t off[6],
+                                 float* params, hipStream_t st);
 size_t ppo_scratch_floats(const MlpParams& m, int M);
 size_t ppo_lds_bytes(const MlpParams& m);   // at most 64 KiB is supported
 

@@ -1,5 +1,6 @@
-// ppo_kernels.hip -- one PPO minibatch (paper Sec. 4.3): gather, forward, clipped-surrogate
-// + value + entropy loss, and its gradient with respect to every policy weight.
+// ppo_kernels.hip -- one policy-gradient minibatch (paper Sec. 4.3): gather, forward, loss
+// (PPO clipped surrogate, or REINFORCE with a learned baseline) + value + entropy, and its
+// gradient with respect to every policy weight.
 //
 // M samples (t, env) are drawn with replacement: sample m takes u from the MINIBATCH block at
 // counter (m, 0xFFFFFFFD, MINIBATCH<<24, 0) and index floor(u * T * E). The forward repeats
@@ -7,7 +8,8 @@
 // arithmetic and saves pre-activations; gradients pass through the bf16 roundings as the
 // identity. Loss
 //   L = -mean(min(rho A, clip(rho, 1-eps, 1+eps) A)) + c_v mean((V - R)^2) - c_h mean(H),
-//   rho = exp(logp_new(a) - logp_old), H the entropy of the action distribution.
+//   rho = exp(logp_new(a) - logp_old), H the entropy of the action distribution; REINFORCE
+//   replaces the first term by -mean(A log pi(a|s)) with A held constant.
 // Work is split into: forward (16 samples per workgroup, one output unit per thread),
 // backward through the activations (same split, reading the out-major repacked weights so
 // that threads walk consecutive inputs), and weight gradients (one output element per
@@ -63,6 +65,7 @@ struct PpoArgs {
   const double* adv;
   const double* ret;
   uint64_t seed;
+  int reinforce;                     // 0: PPO clipped surrogate; 1: REINFORCE with baseline
   float clip, c_v, c_h;
   float* x; float* z1; float* h1; float* z2; float* h2; float* dout;
   float* dz1; float* dz2;
@@ -136,7 +139,7 @@ __global__ __launch_bounds__(kThr) void ppo_fwd_k(PpoArgs a) {
       tm[0] = tm[1] = tm[2] = 0.0;
       return;
     }
-    const float adv = (float)a.adv[ti], ret = (float)a.ret[ti], lpo = a.logp_old[ti];
+    const float adv = (float)a.adv[ti], ret = (float)a.ret[ti];
     float mx = l[0];
     for (int i = 1; i < a.A; ++i) mx = fmaxf(mx, l[i]);
     float S = 0.f;
@@ -148,13 +151,21 @@ __global__ __launch_bounds__(kThr) void ppo_fwd_k(PpoArgs a) {
       H -= expf(lp) * lp;
     }
     const float logp = (l[act] - mx) - lS;
-    const float rho = expf(logp - lpo);
-    const float lo = 1.0f - a.clip, hi = 1.0f + a.clip;
-    const float rc = fminf(fmaxf(rho, lo), hi);
-    const float s1 = rho * adv, s2 = rc * adv;
-    const float g_rho = s1 <= s2 ? adv : ((rho > lo && rho < hi) ? adv : 0.0f);
     const float invM = 1.0f / (float)a.M;
-    const float dlogp = -g_rho * rho * invM;
+    float dlogp, pterm;
+    if (a.reinforce) {
+      // -A log pi(a|s), the advantage held constant
+      dlogp = -adv * invM;
+      pterm = -adv * logp;
+    } else {
+      const float rho = expf(logp - a.logp_old[ti]);
+      const float lo = 1.0f - a.clip, hi = 1.0f + a.clip;
+      const float rc = fminf(fmaxf(rho, lo), hi);
+      const float s1 = rho * adv, s2 = rc * adv;
+      const float g_rho = s1 <= s2 ? adv : ((rho > lo && rho < hi) ? adv : 0.0f);
+      dlogp = -g_rho * rho * invM;
+      pterm = -fminf(s1, s2);
+    }
     for (int i = 0; i < a.A; ++i) {
       const float lp = (l[i] - mx) - lS;
       const float p = expf(lp);
@@ -164,7 +175,7 @@ __global__ __launch_bounds__(kThr) void ppo_fwd_k(PpoArgs a) {
     }
     const float v = l[a.A];
     d[a.A] = 2.0f * a.c_v * (v - ret) * invM;
-    tm[0] = -(double)fminf(s1, s2);
+    tm[0] = (double)pterm;
     tm[1] = (double)(v - ret) * (double)(v - ret);
     tm[2] = (double)H;
   }
@@ -260,8 +271,8 @@ size_t ppo_lds_bytes(const MlpParams& m) {
 hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t off[6], int T,
                       const float* obs, const uint8_t* act, const float* logp_old,
                       const double* adv, const double* ret, int M, uint64_t seed, float clip,
-                      float c_v, float c_h, float* scratch, double* loss_out, float* grads,
-                      int64_t* idx_out, uint32_t* err, hipStream_t st) {
+                      float c_v, float c_h, int reinforce, float* scratch, double* loss_out,
+                      float* grads, int64_t* idx_out, uint32_t* err, hipStream_t st) {
   const unsigned char* wb = static_cast<const unsigned char*>(d_weights);
   PpoArgs a;
   a.F = m.F; a.H1 = m.H1; a.H2 = m.H2; a.A = m.A; a.Ap = m.Ap; a.E = m.E; a.T = T; a.M = M;
@@ -270,7 +281,7 @@ hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t of
   a.w2 = wb + off[2]; a.b2 = reinterpret_cast<const float*>(wb + off[3]);
   a.w3 = wb + off[4]; a.b3 = reinterpret_cast<const float*>(wb + off[5]);
   a.obs = obs; a.act = act; a.logp_old = logp_old; a.adv = adv; a.ret = ret;
-  a.seed = seed; a.clip = clip; a.c_v = c_v; a.c_h = c_h;
+  a.seed = seed; a.clip = clip; a.c_v = c_v; a.c_h = c_h; a.reinforce = reinforce;
   a.idx_out = idx_out; a.err = err;
   float* p = scratch;
   a.x = p; p += (size_t)M * m.F;

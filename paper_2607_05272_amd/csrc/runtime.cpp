@@ -60,8 +60,9 @@ struct sim_ctx {
   void* arena = nullptr;   // all environment state
   size_t arena_bytes = 0;
   void* wpack = nullptr;   // repacked policy weights
-  void* ppo_scratch = nullptr;  // PPO minibatch activations, grown on demand
+  void* ppo_scratch = nullptr;  // minibatch activations, grown on demand
   size_t ppo_bytes = 0;
+  void* grads = nullptr;        // gradient + loss buffer of sim_update
   int64_t* d_tot_cnt = nullptr;
   double* d_tot_sum = nullptr;
   uint32_t tick = 0;
@@ -316,6 +317,7 @@ int sim_destroy(sim_ctx* x) {
   (void)hipFree(x->arena);
   (void)hipFree(x->wpack);
   (void)hipFree(x->ppo_scratch);
+  (void)hipFree(x->grads);
   delete x;
   return SIM_OK;
 }
@@ -506,21 +508,24 @@ int sim_ppo_grad_count(const sim_cfg* c, int64_t* h_count) {
   return SIM_OK;
 }
 
-int ppo_minibatch_grad(sim_ctx* x, const void* d_weights, int32_t T, const float* d_obs,
-                       const uint8_t* d_actions, const float* d_logp_old, const double* d_adv,
-                       const double* d_ret, int32_t M, uint64_t seed, float clip, float c_value,
-                       float c_entropy, float* d_grads, double* d_loss, int64_t* d_index) {
-  if (!x || !d_weights || !d_obs || !d_actions || !d_logp_old || !d_adv || !d_ret || !d_grads ||
-      !d_loss)
-    return fail(SIM_EINVAL, "NULL argument");
-  if (!x->cfg.value_head) return fail(SIM_EUNSUPPORTED, "ppo_minibatch_grad needs value_head = 1");
+// shared by the PPO and REINFORCE entry points
+static int pg_grad(sim_ctx* x, int reinforce, const void* d_weights, int32_t T, const float* d_obs,
+                   const uint8_t* d_actions, const float* d_logp_old, const double* d_adv,
+                   const double* d_ret, int32_t M, uint64_t seed, float clip, float c_value,
+                   float c_entropy, float* d_grads, double* d_loss, int64_t* d_index) {
+  const char* who = reinforce ? "reinforce_minibatch_grad" : "ppo_minibatch_grad";
+  if (!x || !d_weights || !d_obs || !d_actions || (!reinforce && !d_logp_old) || !d_adv ||
+      !d_ret || !d_grads || !d_loss)
+    return fail(SIM_EINVAL, "%s: NULL argument", who);
+  if (!x->cfg.value_head) return fail(SIM_EUNSUPPORTED, "%s needs value_head = 1", who);
   if (T < 1) return fail(SIM_EINVAL, "T must be >= 1");
   if (M < 16 || M % 16) return fail(SIM_EINVAL, "M = %d must be a positive multiple of 16", M);
   if ((int64_t)T * x->cfg.n_envs > 0x7FFFFFFFll)
     return fail(SIM_EINVAL, "T * E must stay below 2^31");
-  if (!(clip > 0.0f && clip < 1.0f)) return fail(SIM_EINVAL, "clip must lie in (0, 1)");
+  if (!reinforce && !(clip > 0.0f && clip < 1.0f))
+    return fail(SIM_EINVAL, "clip must lie in (0, 1)");
   if (ppo_lds_bytes(x->m) > 64 * 1024)
-    return fail(SIM_EUNSUPPORTED, "PPO forward needs %zu bytes of LDS (at most 65536)",
+    return fail(SIM_EUNSUPPORTED, "the minibatch forward needs %zu bytes of LDS (at most 65536)",
                 ppo_lds_bytes(x->m));
   const size_t need = ppo_scratch_floats(x->m, M) * sizeof(float);
   if (need > x->ppo_bytes) {
@@ -530,7 +535,7 @@ int ppo_minibatch_grad(sim_ctx* x, const void* d_weights, int32_t T, const float
     x->ppo_bytes = 0;
     hipError_t he = hipMalloc(&x->ppo_scratch, need);
     if (he != hipSuccess)
-      return fail(SIM_ENOMEM, "hipMalloc of %zu bytes of PPO scratch failed: %s", need,
+      return fail(SIM_ENOMEM, "hipMalloc of %zu bytes of minibatch scratch failed: %s", need,
                   hipGetErrorString(he));
     x->ppo_bytes = need;
   }
@@ -538,10 +543,95 @@ int ppo_minibatch_grad(sim_ctx* x, const void* d_weights, int32_t T, const float
   offsets(x->cfg, off);
   HIPCHK(x->timed(SIM_KC_PPO, [&] {
            return launch_ppo(x->m, d_weights, off, T, d_obs, d_actions, d_logp_old, d_adv, d_ret,
-                             M, seed, clip, c_value, c_entropy,
+                             M, seed, clip, c_value, c_entropy, reinforce,
                              static_cast<float*>(x->ppo_scratch), d_loss, d_grads, d_index,
                              x->s.err, x->stream);
-         }), "PPO kernel launch");
+         }), "minibatch gradient kernel launch");
+  return SIM_OK;
+}
+
+int ppo_minibatch_grad(sim_ctx* x, const void* d_weights, int32_t T, const float* d_obs,
+                       const uint8_t* d_actions, const float* d_logp_old, const double* d_adv,
+                       const double* d_ret, int32_t M, uint64_t seed, float clip, float c_value,
+                       float c_entropy, float* d_grads, double* d_loss, int64_t* d_index) {
+  return pg_grad(x, 0, d_weights, T, d_obs, d_actions, d_logp_old, d_adv, d_ret, M, seed, clip,
+                 c_value, c_entropy, d_grads, d_loss, d_index);
+}
+
+int reinforce_minibatch_grad(sim_ctx* x, const void* d_weights, int32_t T, const float* d_obs,
+                             const uint8_t* d_actions, const double* d_adv, const double* d_ret,
+                             int32_t M, uint64_t seed, float c_value, float c_entropy,
+                             float* d_grads, double* d_loss, int64_t* d_index) {
+  return pg_grad(x, 1, d_weights, T, d_obs, d_actions, nullptr, d_adv, d_ret, M, seed, 0.0f,
+                 c_value, c_entropy, d_grads, d_loss, d_index);
+}
+
+int sim_params_from_weights(sim_ctx* x, const void* d_weights, float* d_params) {
+  if (!x || !d_weights || !d_params) return fail(SIM_EINVAL, "NULL argument");
+  size_t off[6];
+  offsets(x->cfg, off);
+  HIPCHK(x->timed(SIM_KC_OTHER, [&] {
+           return launch_import_weights(x->m, d_weights, off, d_params, x->stream);
+         }), "weight import launch");
+  return SIM_OK;
+}
+
+int adam_update(sim_ctx* x, float* d_params, const float* d_grads, float* d_m, float* d_v,
+                int32_t step, float lr, float beta1, float beta2, float eps, void* d_weights) {
+  if (!x || !d_params || !d_grads || !d_m || !d_v) return fail(SIM_EINVAL, "NULL argument");
+  if (step < 1) return fail(SIM_EINVAL, "step = %d must be >= 1", step);
+  if (!(beta1 >= 0.0f && beta1 < 1.0f && beta2 >= 0.0f && beta2 < 1.0f && eps > 0.0f))
+    return fail(SIM_EINVAL, "need 0 <= beta1, beta2 < 1 and eps > 0");
+  int64_t n = 0;
+  sim_ppo_grad_count(&x->cfg, &n);
+  const float bc1 = (float)(1.0 - std::pow((double)beta1, (double)step));
+  const float bc2 = (float)(1.0 - std::pow((double)beta2, (double)step));
+  HIPCHK(x->timed(SIM_KC_PPO, [&] {
+           return launch_adam(d_params, d_grads, d_m, d_v, (size_t)n, lr, beta1, beta2, eps, bc1,
+                              bc2, x->stream);
+         }), "Adam kernel launch");
+  if (d_weights) {
+    size_t off[6];
+    offsets(x->cfg, off);
+    HIPCHK(x->timed(SIM_KC_PPO, [&] {
+             return launch_export_weights(x->m, d_params, d_weights, off, x->stream);
+           }), "weight export launch");
+  }
+  return SIM_OK;
+}
+
+int sim_update(sim_ctx* x, const sim_update_cfg* u, void* d_weights, float* d_params, float* d_m,
+               float* d_v, int32_t* h_step, int32_t T, const float* d_obs,
+               const uint8_t* d_actions, const float* d_logp_old, const double* d_adv,
+               const double* d_ret, double* d_losses) {
+  if (!x || !u || !d_weights || !d_params || !d_m || !d_v || !h_step)
+    return fail(SIM_EINVAL, "NULL argument");
+  if (u->algo != SIM_ALGO_PPO && u->algo != SIM_ALGO_REINFORCE)
+    return fail(SIM_EINVAL, "unknown algorithm %d", u->algo);
+  if (u->epochs < 1 || u->minibatches < 1) return fail(SIM_EINVAL, "epochs and minibatches >= 1");
+  int64_t n = 0;
+  sim_ppo_grad_count(&x->cfg, &n);
+  if (!x->grads) {
+    hipError_t he = hipMalloc(&x->grads, (size_t)(n + 2) * sizeof(float) + 4 * sizeof(double));
+    if (he != hipSuccess) return fail(SIM_ENOMEM, "hipMalloc of the gradient buffer failed");
+  }
+  float* g = static_cast<float*>(x->grads);
+  double* scratch_loss = reinterpret_cast<double*>(g + n + (n & 1));
+  for (int e = 0; e < u->epochs; ++e) {
+    for (int b = 0; b < u->minibatches; ++b) {
+      const uint64_t k = (uint64_t)e * (uint64_t)u->minibatches + (uint64_t)b;
+      const uint64_t seed = u->seed + k * 0x9E3779B97F4A7C15ull;
+      double* loss = d_losses ? d_losses + 4 * k : scratch_loss;
+      int rc = pg_grad(x, u->algo == SIM_ALGO_REINFORCE, d_weights, T, d_obs, d_actions,
+                       d_logp_old, d_adv, d_ret, u->M, seed, u->clip, u->c_value, u->c_entropy,
+                       g, loss, nullptr);
+      if (rc) return rc;
+      rc = adam_update(x, d_params, g, d_m, d_v, *h_step + 1, u->lr, u->beta1, u->beta2, u->eps,
+                       d_weights);
+      if (rc) return rc;
+      *h_step += 1;
+    }
+  }
   return SIM_OK;
 }
 

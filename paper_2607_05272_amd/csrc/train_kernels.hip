@@ -1,0 +1,114 @@
+// train_kernels.hip -- parameter update of the policy (paper Sec. 4.3): Adam on fp32 master
+// parameters (Kingma & Ba, "Adam: a method for stochastic optimization", ICLR 2015,
+// Algorithm 1) and the conversions between the master parameters and the policy's weights.
+//
+// The master parameters use the gradient layout: W1 [F][H1], b1 [H1], W2 [H1][H2], b2 [H2],
+// W3 [H2][A'], b3 [A'] back to back (fp32). The policy's weights are the ABI buffer (matrices
+// in the element type, bf16 by round-to-nearest-even or fp32; biases fp32; each block at its
+// layout offset).
+#include "devmath.hpp"
+#include "params.hpp"
+
+namespace bsim {
+namespace {
+
+__global__ __launch_bounds__(256) void adam_k(float* __restrict__ p, const float* __restrict__ g,
+                                              float* __restrict__ m, float* __restrict__ v, size_t n,
+                                              float lr, float b1, float b2, float eps, float bc1,
+                                              float bc2) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (size_t)gridDim.x * blockDim.x) {
+    const float gi = g[i];
+    const float mi = b1 * m[i] + (1.0f - b1) * gi;
+    const float vi = b2 * v[i] + (1.0f - b2) * (gi * gi);
+    m[i] = mi;
+    v[i] = vi;
+    const float mhat = mi / bc1, vhat = vi / bc2;
+    p[i] = p[i] - lr * mhat / (sqrtf(vhat) + eps);
+  }
+}
+
+struct Segs {
+  size_t poff[6];   // offset in the parameter vector
+  size_t woff[6];   // byte offset in the weight buffer
+  size_t len[6];
+  int matrix[6];
+};
+
+// one thread per parameter; seg found by a short scan of the six segment starts
+__device__ __forceinline__ int seg_of(const Segs& s, size_t i) {
+  int k = 0;
+#pragma unroll
+  for (int j = 1; j < 6; ++j)
+    if (i >= s.poff[j]) k = j;
+  return k;
+}
+
+__global__ __launch_bounds__(256) void export_k(Segs s, size_t n, int bf16,
+                                                const float* __restrict__ p,
+                                                unsigned char* __restrict__ w) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int k = seg_of(s, i);
+  const size_t j = i - s.poff[k];
+  if (s.matrix[k] && bf16) reinterpret_cast<uint16_t*>(w + s.woff[k])[j] = bf16_bits(p[i]);
+  else reinterpret_cast<float*>(w + s.woff[k])[j] = p[i];
+}
+
+__global__ __launch_bounds__(256) void import_k(Segs s, size_t n, int bf16,
+                                                const unsigned char* __restrict__ w,
+                                                float* __restrict__ p) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int k = seg_of(s, i);
+  const size_t j = i - s.poff[k];
+  if (s.matrix[k] && bf16) p[i] = bf16_to_f32(reinterpret_cast<const uint16_t*>(w + s.woff[k])[j]);
+  else p[i] = reinterpret_cast<const float*>(w + s.woff[k])[j];
+}
+
+Segs segments(const MlpParams& m, const size_t off[6]) {
+  Segs s;
+  const size_t len[6] = {(size_t)m.F * m.H1, (size_t)m.H1, (size_t)m.H1 * m.H2, (size_t)m.H2,
+                         (size_t)m.H2 * m.Ap, (size_t)m.Ap};
+  size_t acc = 0;
+  for (int k = 0; k < 6; ++k) {
+    s.poff[k] = acc;
+    s.woff[k] = off[k];
+    s.len[k] = len[k];
+    s.matrix[k] = (k % 2) == 0;
+    acc += len[k];
+  }
+  return s;
+}
+
+size_t total(const Segs& s) { return s.poff[5] + s.len[5]; }
+
+}  // namespace
+
+hipError_t launch_adam(float* params, const float* grads, float* m, float* v, size_t n, float lr,
+                       float b1, float b2, float eps, float bc1, float bc2, hipStream_t st) {
+  const unsigned blocks = (unsigned)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
+  hipLaunchKernelGGL(adam_k, dim3(blocks > 0 ? blocks : 1), dim3(256), 0, st, params, grads, m, v,
+                     n, lr, b1, b2, eps, bc1, bc2);
+  return hipGetLastError();
+}
+
+hipError_t launch_export_weights(const MlpParams& m, const float* params, void* d_weights,
+                                 const size_t off[6], hipStream_t st) {
+  const Segs s = segments(m, off);
+  const size_t n = total(s);
+  hipLaunchKernelGGL(export_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, s, n, m.bf16,
+                     params, static_cast<unsigned char*>(d_weights));
+  return hipGetLastError();
+}
+
+hipError_t launch_import_weights(const MlpParams& m, const void* d_weights, const size_t off[6],
+                                 float* params, hipStream_t st) {
+  const Segs s = segments(m, off);
+  const size_t n = total(s);
+  hipLaunchKernelGGL(import_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, s, n, m.bf16,
+                     static_cast<const unsigned char*>(d_weights), params);
+  return hipGetLastError();
+}
+
+}  // namespace bsim

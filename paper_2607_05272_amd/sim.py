@@ -221,6 +221,47 @@ class Sim:
                                             _p(idx)), "ppo_minibatch_grad")
         return grads, loss, idx
 
+    def reinforce_minibatch_grad(self, weights, obs, actions, adv, ret, M, seed, c_value=0.5,
+                                 c_entropy=0.01, want_index=False, grads=None, loss=None):
+        """REINFORCE with baseline on one minibatch (adv = G - V, ret = G)."""
+        T = actions.shape[0]
+        assert actions.shape[1] == self.E and obs.shape[1] == self.F and obs.shape[0] >= T
+        grads = (torch.empty(self.ppo_grad_count(), dtype=torch.float32, device=self.device)
+                 if grads is None else grads)
+        loss = torch.empty(4, dtype=torch.float64, device=self.device) if loss is None else loss
+        idx = torch.empty(M, dtype=torch.int64, device=self.device) if want_index else None
+        L.check(self.lib.reinforce_minibatch_grad(self._ctx, _p(weights), T, _p(obs), _p(actions),
+                                                  _p(adv), _p(ret), M, C.c_uint64(seed), c_value,
+                                                  c_entropy, _p(grads), _p(loss), _p(idx)),
+                "reinforce_minibatch_grad")
+        return grads, loss, idx
+
+    def params_from_weights(self, weights):
+        p = torch.empty(self.ppo_grad_count(), dtype=torch.float32, device=self.device)
+        L.check(self.lib.sim_params_from_weights(self._ctx, _p(weights), _p(p)),
+                "sim_params_from_weights")
+        return p
+
+    def adam_update(self, params, grads, m, v, step, lr, beta1=0.9, beta2=0.999, eps=1e-8,
+                    weights=None):
+        L.check(self.lib.adam_update(self._ctx, _p(params), _p(grads), _p(m), _p(v), step, lr,
+                                     beta1, beta2, eps, _p(weights)), "adam_update")
+
+    def update(self, weights, params, m, v, step, obs, actions, logp_old, adv, ret, algo,
+               epochs, minibatches, M, seed, lr, clip=0.2, c_value=0.5, c_entropy=0.01,
+               beta1=0.9, beta2=0.999, eps=1e-8, want_losses=True):
+        """sim_update: epochs x minibatches of gradient + Adam; returns (new step, losses)."""
+        T = actions.shape[0]
+        cfg = L.SimUpdateCfg(algo, epochs, minibatches, M, seed, clip, c_value, c_entropy, lr,
+                             beta1, beta2, eps)
+        st = C.c_int32(step)
+        losses = (torch.empty((epochs * minibatches, 4), dtype=torch.float64, device=self.device)
+                  if want_losses else None)
+        L.check(self.lib.sim_update(self._ctx, C.byref(cfg), _p(weights), _p(params), _p(m),
+                                    _p(v), C.byref(st), T, _p(obs), _p(actions), _p(logp_old),
+                                    _p(adv), _p(ret), _p(losses)), "sim_update")
+        return st.value, losses
+
     def unflatten_grads(self, g):
         """Split a flat gradient vector (host numpy) into W1,b1,W2,b2,W3,b3 arrays."""
         F, H1, H2, Ap = self.F, self.w["mlp_h1"], self.w["mlp_h2"], self.Ap

@@ -13,7 +13,7 @@ HEADER = os.path.join(ROOT, "include", "batchsim.h")
 def declared_functions():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(sim_[a-z_0-9]+|returns_gae|ppo_[a-z_0-9]+)\s*\(",
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z][a-z_0-9]*)\s*\(",
                                  src, flags=re.M)))
 
 
@@ -37,6 +37,7 @@ def test_struct_sizes_match_header_layout():
     assert C.sizeof(_lib.SimCfg) == 448
     assert C.sizeof(_lib.SimTraj) == 7 * 8
     assert C.sizeof(_lib.SimWLayout) == 7 * 8 + 8
+    assert C.sizeof(_lib.SimUpdateCfg) == 4 * 4 + 8 + 7 * 4 + 4  # padded to 8
 
 
 def test_invalid_config_is_rejected_without_device_work():
