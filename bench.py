@@ -195,6 +195,11 @@ def main():
     ap.add_argument("--config", default="C5", choices=sorted(DESCR))
     ap.add_argument("--ticks", type=int, default=0, help="override T (diagnostics only)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--train", default="none", choices=("none", "ppo", "reinforce"),
+                    help="add the policy update (epochs x minibatches of gradient + Adam over "
+                         "the stored trajectory) to every step")
+    ap.add_argument("--epochs", type=int, default=4)
+    ap.add_argument("--minibatches", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="only copy this many MiB device-to-device (HBM counter calibration)")
@@ -234,15 +239,25 @@ def main():
     seed = 0x5EED0000 + int(args.config[1])
     sim = bs.Sim(w)
     weights = sim.init_weights(seed)
-    ppo = w.get("ppo_minibatch", 0) > 0
+    ppo = w.get("ppo_minibatch", 0) > 0 and args.train == "none"
+    train = args.train != "none"
     traj = bs.Trajectory(T, E, F, dev, value=bool(w["value_head"]), shadow=bool(w["shadow"]),
-                         obs=ppo)
+                         obs=ppo or train)
+    if train:
+        params = sim.params_from_weights(weights)
+        adam_m = torch.zeros_like(params)
+        adam_v = torch.zeros_like(params)
+        adam_t = [0]
+        mb = w.get("ppo_minibatch", 0) or 8192
+        algo = bs.ALGO_PPO if args.train == "ppo" else bs.ALGO_REINFORCE
     grads = torch.empty(sim.ppo_grad_count(), dtype=torch.float32, device=dev) if ppo else None
     ploss = torch.empty(4, dtype=torch.float64, device=dev) if ppo else None
     adv = torch.empty((T, E), dtype=torch.float64, device=dev)
     ret = torch.empty((T, E), dtype=torch.float64, device=dev)
     gae = bool(w["value_head"])
     lam = w["lam"] if gae else 1.0
+    if args.train == "reinforce":
+        lam = 1.0  # A = G - V, R = G
 
     def one_step(i):
         sim.reset(seed + i)
@@ -251,6 +266,10 @@ def main():
         if ppo:
             sim.ppo_minibatch_grad(weights, traj.obs, traj.actions, traj.logp, adv, ret,
                                    w["ppo_minibatch"], seed + i, grads=grads, loss=ploss)
+        if train:
+            adam_t[0], _ = sim.update(weights, params, adam_m, adam_v, adam_t[0], traj.obs,
+                                      traj.actions, traj.logp, adv, ret, algo, args.epochs,
+                                      args.minibatches, mb, seed + i, 3e-4, want_losses=False)
         return sim.stats()
 
     for i in range(args.warmup):
@@ -305,8 +324,11 @@ def main():
                      "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("gae", args.config),
                      "work_per_launch": by}
     if "ppo" in kern:
-        fl = ppo_flops(w)
-        ach = fl / (kern["ppo"]["avg_us"] * 1e-6) / 1e12
+        # minibatch gradients per step (one, or epochs x minibatches when training), each
+        # with its share of Adam
+        n_grad = args.epochs * args.minibatches if train else 1
+        fl = ppo_flops(dict(w, ppo_minibatch=w.get("ppo_minibatch", 0) or 8192)) * n_grad
+        ach = fl / (kern["ppo"]["total_ms_per_step"] * 1e-3) / 1e12
         rl["ppo"] = {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS,
                      "unit": "TFLOP/s", "frac": ach / PEAK_FP32_VALU_TFLOPS,
                      "traffic": traffic_for("ppo", args.config), "work_per_launch": fl}
@@ -322,7 +344,9 @@ def main():
         "scaling": "weak", "vs_baseline": None,
         "dtype": "f64 simulator + bf16 MLP (fp32 accumulate)" if w["mlp_bf16"] else "f64 simulator + f32 MLP",
         "data": "synthetic (seeded workload generator; untrained Xavier policy)",
-        "config": {"workload": DESCR[args.config] if not args.ticks else DESCR[args.config] + f" [T={T}]",
+        "config": {"workload": (DESCR[args.config] if not args.ticks else DESCR[args.config] + f" [T={T}]")
+                   + ("" if not train else f"; + {args.train} update, {args.epochs} epochs x "
+                      f"{args.minibatches} minibatches of {mb} samples, Adam"),
                    "envs": E, "ticks": T, "env_steps_per_step": E * T},
         "roofline": roof,
         "kernels": {k: dict(v, **{kk: vv for kk, vv in rl.get(k, {}).items()

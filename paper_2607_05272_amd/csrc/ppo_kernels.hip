@@ -11,9 +11,8 @@
 //   rho = exp(logp_new(a) - logp_old), H the entropy of the action distribution; REINFORCE
 //   replaces the first term by -mean(A log pi(a|s)) with A held constant.
 // Work is split into: forward (16 samples per workgroup, one output unit per thread),
-// backward through the activations (same split, reading the out-major repacked weights so
-// that threads walk consecutive inputs), and weight gradients (one output element per
-// thread, fp64 accumulation over the samples in order, so results are deterministic).
+// backward through the activations (same split), and weight gradients (LDS-tiled products
+// over fixed sample chunks, fp32, summed in chunk order, so results are deterministic).
 #include "devmath.hpp"
 #include "params.hpp"
 
@@ -222,22 +221,55 @@ __global__ __launch_bounds__(kThr) void ppo_bwd_k(PpoArgs a) {
   }
 }
 
-// dW[i][j] = sum_m A[m][i] B[m][j] (fp64, samples in order); db[j] = sum_m B[m][j]
-__global__ __launch_bounds__(kThr) void ppo_wgrad_k(const float* __restrict__ Am, int K,
+// Weight gradients as one augmented product per layer: G = [A | 1]^T B, (K+1) x N, whose
+// first K rows are dW = A^T B and whose last row is db = sum_m B[m]. The samples are split
+// into chunks of kMC; workgroup (ti, tj, c) forms a 32 x 32 tile of chunk c's partial product
+// from LDS-staged 32-sample slices (fp32, each thread 2 x 2 outputs); a second pass adds the
+// chunks in order. The result does not depend on the launch, only on M.
+constexpr int kWT = 32, kMS = 32, kMC = 512;
+
+__global__ __launch_bounds__(256) void wgrad_part_k(const float* __restrict__ Am, int K,
                                                     const float* __restrict__ Bm, int N, int M,
-                                                    float* __restrict__ dW, float* __restrict__ db) {
-  const int idx = blockIdx.x * kThr + threadIdx.x;
-  if (idx < K * N) {
-    const int i = idx / N, j = idx % N;
-    double acc = 0.0;
-    for (int m = 0; m < M; ++m) acc += (double)Am[(size_t)m * K + i] * (double)Bm[(size_t)m * N + j];
-    dW[idx] = (float)acc;
-  } else if (idx < K * N + N) {
-    const int j = idx - K * N;
-    double acc = 0.0;
-    for (int m = 0; m < M; ++m) acc += (double)Bm[(size_t)m * N + j];
-    db[j] = (float)acc;
+                                                    float* __restrict__ part) {
+  __shared__ float As[kMS][kWT + 1], Bs[kMS][kWT + 1];
+  const int i0 = blockIdx.x * kWT, j0 = blockIdx.y * kWT, c = blockIdx.z;
+  const int m0 = c * kMC, m1 = m0 + kMC < M ? m0 + kMC : M;
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+  float acc00 = 0.f, acc01 = 0.f, acc10 = 0.f, acc11 = 0.f;
+  for (int ms = m0; ms < m1; ms += kMS) {
+    for (int q = threadIdx.x; q < kMS * kWT; q += 256) {
+      const int r = q / kWT, col = q % kWT, m = ms + r;
+      const int i = i0 + col, j = j0 + col;
+      As[r][col] = m < m1 ? (i < K ? Am[(size_t)m * K + i] : (i == K ? 1.0f : 0.0f)) : 0.0f;
+      Bs[r][col] = (m < m1 && j < N) ? Bm[(size_t)m * N + j] : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int r = 0; r < kMS; ++r) {
+      const float a0 = As[r][2 * ty], a1 = As[r][2 * ty + 1];
+      const float b0 = Bs[r][2 * tx], b1 = Bs[r][2 * tx + 1];
+      acc00 = fmaf(a0, b0, acc00);
+      acc01 = fmaf(a0, b1, acc01);
+      acc10 = fmaf(a1, b0, acc10);
+      acc11 = fmaf(a1, b1, acc11);
+    }
+    __syncthreads();
   }
+  const int i = i0 + 2 * ty, j = j0 + 2 * tx;
+  float* out = part + (size_t)c * (K + 1) * N;
+  if (i <= K && j < N) out[(size_t)i * N + j] = acc00;
+  if (i <= K && j + 1 < N) out[(size_t)i * N + j + 1] = acc01;
+  if (i + 1 <= K && j < N) out[(size_t)(i + 1) * N + j] = acc10;
+  if (i + 1 <= K && j + 1 < N) out[(size_t)(i + 1) * N + j + 1] = acc11;
+}
+
+__global__ __launch_bounds__(256) void wgrad_sum_k(const float* __restrict__ part, int nc,
+                                                   size_t n, float* __restrict__ g) {
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= n) return;
+  float s = 0.f;
+  for (int c = 0; c < nc; ++c) s += part[(size_t)c * n + idx];
+  g[idx] = s;
 }
 
 // loss terms summed in a fixed order by one workgroup
@@ -309,14 +341,22 @@ hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t of
   float* gw2 = gb1 + m.H1;
   float* gb2 = gw2 + (size_t)m.H1 * m.H2;
   float* gw3 = gb2 + m.H2;
-  float* gb3 = gw3 + (size_t)m.H2 * m.Ap;
-  const struct { const float* A; int K; const float* B; int N; float* dW; float* db; } g[3] = {
-      {a.x, m.F, a.dz1, m.H1, gw1, gb1}, {a.h1, m.H1, a.dz2, m.H2, gw2, gb2},
-      {a.h2, m.H2, a.dout, m.Ap, gw3, gb3}};
+  // the three augmented products [x|1]^T dz1, [h1|1]^T dz2, [h2|1]^T dout land on W,b pairs
+  // that are contiguous in the gradient layout
+  const struct { const float* A; int K; const float* B; int N; float* G; } g[3] = {
+      {a.x, m.F, a.dz1, m.H1, gw1}, {a.h1, m.H1, a.dz2, m.H2, gw2}, {a.h2, m.H2, a.dout, m.Ap, gw3}};
+  const int nc = (M + kMC - 1) / kMC;
+  float* part = reinterpret_cast<float*>(a.terms + (size_t)M * 3);
   for (int l = 0; l < 3; ++l) {
-    const int n = g[l].K * g[l].N + g[l].N;
-    hipLaunchKernelGGL(ppo_wgrad_k, dim3((n + kThr - 1) / kThr), dim3(kThr), 0, st, g[l].A, g[l].K,
-                       g[l].B, g[l].N, M, g[l].dW, g[l].db);
+    const dim3 grid((unsigned)((g[l].K + 1 + kWT - 1) / kWT), (unsigned)((g[l].N + kWT - 1) / kWT),
+                    (unsigned)nc);
+    hipLaunchKernelGGL(wgrad_part_k, grid, dim3(256), 0, st, g[l].A, g[l].K, g[l].B, g[l].N, M,
+                       part);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const size_t n = (size_t)(g[l].K + 1) * g[l].N;
+    hipLaunchKernelGGL(wgrad_sum_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, nc,
+                       n, g[l].G);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -325,7 +365,13 @@ hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t of
 }
 
 size_t ppo_scratch_floats(const MlpParams& m, int M) {
-  return (size_t)M * (m.F + 2 * m.H1 + 2 * m.H2 + m.Ap + m.H1 + m.H2) + (size_t)M * 3 * 2 + 64;
+  // activations, per-sample loss terms (fp64), then the chunked weight-gradient partials
+  const size_t nc = (size_t)(M + kMC - 1) / kMC;
+  size_t kn = (size_t)(m.F + 1) * m.H1;
+  if ((size_t)(m.H1 + 1) * m.H2 > kn) kn = (size_t)(m.H1 + 1) * m.H2;
+  if ((size_t)(m.H2 + 1) * m.Ap > kn) kn = (size_t)(m.H2 + 1) * m.Ap;
+  return (size_t)M * (m.F + 2 * m.H1 + 2 * m.H2 + m.Ap + m.H1 + m.H2) + (size_t)M * 3 * 2 +
+         nc * kn + 64;
 }
 
 }  // namespace bsim
