@@ -199,7 +199,8 @@ static void derive(const orc_cfg* c, derived* d) {
    * embedded jump chain is uniform over the other states (R11) */
   double mdw[ORC_MAX_S], tot = 0.0;
   for (int i = 0; i < c->n_states; i++) {
-    if (c->dwell_kind[i] == ORC_DWELL_EXP) mdw[i] = c->dwell_mean[i];
+    if (c->dwell_kind[i] == ORC_DWELL_EXP || c->dwell_kind[i] == ORC_DWELL_DET)
+      mdw[i] = c->dwell_mean[i];
     else if (c->dwell_kind[i] == ORC_DWELL_PARETO)
       mdw[i] = c->pareto_alpha[i] * c->pareto_xm[i] / (c->pareto_alpha[i] - 1.0);
     else mdw[i] = 1.0;
@@ -235,6 +236,7 @@ typedef struct sys_t {
   int q[ORC_MAX_C], head[ORC_MAX_C];
   double ring[ORC_MAX_C][ORC_MAX_N];
   /* servers */
+  int rr;                        /* round-robin pointer of the static system (R23) */
   double busy[ORC_MAX_K];
   int inflight[ORC_MAX_K], last_b[ORC_MAX_K], last_cls[ORC_MAX_K];
   double ewma[4];
@@ -254,7 +256,7 @@ typedef struct tick_ctx {
   uint32_t env;
   uint64_t seed;
   uint32_t k;
-  uint32_t j_arr, j_proc, j_svc;
+  uint32_t j_arr, j_proc, j_svc, j_route;
   int n_k, ndisp, A_k;
   double Lw;
   orc_out* out;
@@ -273,6 +275,7 @@ static double dwell_draw(const tick_ctx* t, int state, double u) {
   if (c->dwell_kind[state] == ORC_DWELL_EXP) return -det_log(u) * c->dwell_mean[state];
   if (c->dwell_kind[state] == ORC_DWELL_PARETO)
     return c->pareto_xm[state] * det_exp(-det_log(u) * t->d->inv_alpha[state]);
+  if (c->dwell_kind[state] == ORC_DWELL_DET) return c->dwell_mean[state];  /* square wave (R24) */
   return INFINITY;
 }
 
@@ -350,6 +353,12 @@ static void batch(tick_ctx* t, sys_t* S, int j, int h, int n, double now) {
 
 /* Learned system (R2-R4): action a = 6 s + log2 b. Whenever server s is idle and the
  * head-of-line class holds at least b requests, exactly b of them are dispatched to s. */
+static int any_idle(const sys_t* S, int K, double now) {
+  for (int j = 0; j < K; j++)
+    if (S->busy[j] <= now) return 1;
+  return 0;
+}
+
 static void dispatch_learned(tick_ctx* t, sys_t* S, int action, double now) {
   int s = action / 6, b = 1 << (action % 6);
   int C = t->c->n_classes;
@@ -360,21 +369,45 @@ static void dispatch_learned(tick_ctx* t, sys_t* S, int action, double now) {
   }
 }
 
+/* Server for the static system's next batch among the idle ones (R23): the lowest index;
+ * uniformly at random (the idx-th idle server in index order, idx = floor(u * n_idle) with
+ * u from ROUTE block j_route of (env, tick, system 1)); or round robin (the first idle
+ * server at or after the pointer, cyclically; the pointer then moves past it). */
+static int route_static(tick_ctx* t, sys_t* S, double now) {
+  const orc_cfg* c = t->c;
+  int idle[ORC_MAX_K], n_idle = 0;
+  for (int i = 0; i < c->n_servers; i++)
+    if (S->busy[i] <= now) idle[n_idle++] = i;
+  if (n_idle == 0) return -1;
+  if (c->static_route == ORC_ROUTE_RANDOM) {
+    uint32_t w[4];
+    draw(t->seed, t->env, t->k, ORC_P_ROUTE, t->j_route++, 1, w);
+    int idx = (int)(u01(w[0], w[1]) * (double)n_idle);
+    return idle[idx < n_idle ? idx : n_idle - 1];
+  }
+  if (c->static_route == ORC_ROUTE_ROUND_ROBIN) {
+    for (int d = 0; d < c->n_servers; d++) {
+      int i = (S->rr + d) % c->n_servers;
+      if (S->busy[i] <= now) return i;
+    }
+  }
+  return idle[0];
+}
+
 /* Static timeout rule (Sec. 1's "wait T or until B requests accumulate", R18): while some
- * server is idle and requests wait, take the lowest idle server; dispatch min(B, Q_h) of
- * the head-of-line class if Q_h >= B or its head has waited at least T. */
+ * server is idle and requests wait, dispatch min(B, Q_h) of the head-of-line class if
+ * Q_h >= B or its head has waited at least T, to the server route_static chooses. */
 static void dispatch_static(tick_ctx* t, sys_t* S, double now) {
   const orc_cfg* c = t->c;
   for (;;) {
-    int j = -1;
-    for (int i = 0; i < c->n_servers; i++)
-      if (S->busy[i] <= now) { j = i; break; }
-    if (j < 0 || sumq(S, c->n_classes) == 0) return;
+    if (!any_idle(S, c->n_servers, now) || sumq(S, c->n_classes) == 0) return;
     int h = hol(S, c->n_classes);
     double head_ts = S->ring[h][S->head[h]];
     if (S->q[h] >= c->static_bmax || now >= head_ts + c->static_timeout) {
       int n = S->q[h] < c->static_bmax ? S->q[h] : c->static_bmax;
+      int j = route_static(t, S, now);
       batch(t, S, j, h, n, now);
+      S->rr = (j + 1) % c->n_servers;
     } else {
       return;
     }
@@ -452,17 +485,11 @@ static void process_arrival(tick_ctx* t, sys_t* S, double now) {
   }
 }
 
-static int any_idle(const sys_t* S, int K, double now) {
-  for (int j = 0; j < K; j++)
-    if (S->busy[j] <= now) return 1;
-  return 0;
-}
-
 /* One tick [t_k, t_{k+1}) of one system (R1, R2, R9, R10). */
 static double tick(tick_ctx* t, sys_t* S, int action) {
   const orc_cfg* c = t->c;
   double t0 = (double)t->k * c->tick_s, t1 = (double)(t->k + 1) * c->tick_s;
-  t->j_arr = 0; t->j_proc = 0; t->j_svc = 0;
+  t->j_arr = 0; t->j_proc = 0; t->j_svc = 0; t->j_route = 0;
   t->n_k = 0; t->ndisp = 0; t->A_k = 0; t->Lw = 0.0;
   double now = t0;
   do_dispatch(t, S, action, now);
@@ -562,7 +589,11 @@ static void reset_sys(const orc_cfg* c, const derived* d, const orc_trace* tr, i
   tick_ctx t;
   memset(&t, 0, sizeof(t));
   t.c = c; t.d = d;
-  if (c->n_states > 1) {
+  if (c->n_states > 1 && c->dwell_kind[0] == ORC_DWELL_DET) {
+    /* a square wave starts in state 0 with its full dwell: same phase everywhere (R24) */
+    S->proc = 0;
+    S->next_sw = c->dwell_mean[0];
+  } else if (c->n_states > 1) {
     draw(seed, env, ORC_STEP_RESET, ORC_P_PROCESS, 0, 0, w);
     double us = u01(w[2], w[3]);
     int s = 0;

@@ -34,10 +34,11 @@
 #define ORC_MAX_N 255
 
 enum { ORC_ARR_MODULATED = 0, ORC_ARR_TRACE = 1 };
-enum { ORC_DWELL_INF = 0, ORC_DWELL_EXP = 1, ORC_DWELL_PARETO = 2 };
+enum { ORC_DWELL_INF = 0, ORC_DWELL_EXP = 1, ORC_DWELL_PARETO = 2, ORC_DWELL_DET = 3 };
+enum { ORC_ROUTE_LOWEST = 0, ORC_ROUTE_RANDOM = 1, ORC_ROUTE_ROUND_ROBIN = 2 };
 enum { ORC_SVC_DET = 0, ORC_SVC_LOGN = 1, ORC_SVC_EXP = 2 };
 enum { ORC_P_ARRIVAL = 1, ORC_P_PROCESS = 2, ORC_P_SERVICE = 3, ORC_P_ACTION = 4,
-       ORC_P_WEIGHTS = 5, ORC_P_MINIBATCH = 6 };
+       ORC_P_WEIGHTS = 5, ORC_P_MINIBATCH = 6, ORC_P_ROUTE = 7 };
 #define ORC_STEP_RESET 0xFFFFFFFFu
 
 typedef struct orc_cfg {
@@ -58,6 +59,7 @@ typedef struct orc_cfg {
   double static_timeout;
   int32_t static_bmax;
   int32_t mlp_h1, mlp_h2, mlp_bf16, value_head;
+  int32_t static_route;          /* ORC_ROUTE_*: server choice of the static system (R23) */
 } orc_cfg;
 
 /* Explicit arrivals for ORC_ARR_TRACE: times [n_env][max_len] (seconds, nondecreasing),

@@ -16,6 +16,11 @@ ARR_TRACE = 1       # explicit per-env arrival list (tests / trace replay)
 DWELL_INF = 0
 DWELL_EXP = 1
 DWELL_PARETO = 2
+DWELL_DET = 3       # fixed dwell (square wave), R24
+# server choice of the static shadow system (R23)
+ROUTE_LOWEST = 0
+ROUTE_RANDOM = 1
+ROUTE_ROUND_ROBIN = 2
 # service kinds
 SVC_DET = 0
 SVC_LOGN = 1
@@ -33,7 +38,7 @@ _BASE = dict(
     svc_sigma=0.0,
     w_thr=0.01, w_class=[1.0], reward_sum=0,
     obs_tw=0.010, lambda_ref=500.0,
-    shadow=0, static_timeout=0.010, static_bmax=32,
+    shadow=0, static_timeout=0.010, static_bmax=32, static_route=ROUTE_LOWEST,
     mlp_h1=64, mlp_h2=64, mlp_bf16=0, value_head=0,
     gamma=0.99, lam=1.0, ppo_minibatch=0,
 )
@@ -104,6 +109,29 @@ def preset(name, **override):
     """A deep copy of preset `name` with fields overridden (e.g. n_envs, T)."""
     d = copy.deepcopy(PRESETS[name])
     d.update(override)
+    return d
+
+
+def burst_preset(**kw):
+    """The paper's Extreme Burst workload (Sec. 3.2): arrivals switch squarely between
+    100 req/s and 0 every 200 steps (0.2 s of 1 ms ticks), starting high (R24); one server
+    and class as C1, with a static shadow system for the baseline rules."""
+    d = _mk(name="burst", rates=[100.0, 0.0], dwell_kind=[DWELL_DET, DWELL_DET],
+            dwell_mean=[0.2, 0.2], pareto_alpha=[0.0, 0.0], pareto_xm=[0.0, 0.0],
+            lambda_ref=100.0, shadow=1)
+    d.update(kw)
+    return d
+
+
+def baseline_preset(rule, base="C3", **kw):
+    """A workload whose shadow system runs one of the paper's baselines (Sec. 5.1):
+    'static8' (fixed batch 8 with the timeout of R18), 'random' or 'round_robin' routing of
+    the static rule's batches (R23)."""
+    extra = dict(static8=dict(static_bmax=8),
+                 random=dict(static_route=ROUTE_RANDOM),
+                 round_robin=dict(static_route=ROUTE_ROUND_ROBIN))[rule]
+    d = preset(base, shadow=1, **extra)
+    d.update(kw)
     return d
 
 
