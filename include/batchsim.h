@@ -47,7 +47,8 @@ enum sim_status {
 };
 
 enum { SIM_ARR_MODULATED = 0, SIM_ARR_TRACE = 1 };
-enum { SIM_DWELL_INF = 0, SIM_DWELL_EXP = 1, SIM_DWELL_PARETO = 2 };
+enum { SIM_DWELL_INF = 0, SIM_DWELL_EXP = 1, SIM_DWELL_PARETO = 2, SIM_DWELL_DET = 3 };
+enum { SIM_ROUTE_LOWEST = 0, SIM_ROUTE_RANDOM = 1, SIM_ROUTE_ROUND_ROBIN = 2 };
 enum { SIM_SVC_DET = 0, SIM_SVC_LOGN = 1, SIM_SVC_EXP = 2 };
 
 #define SIM_MAX_SERVERS 16
@@ -65,8 +66,10 @@ enum { SIM_SVC_DET = 0, SIM_SVC_LOGN = 1, SIM_SVC_EXP = 2 };
  *  arrival_kind    SIM_ARR_MODULATED (Poisson / MMPP / ON-OFF) or SIM_ARR_TRACE
  *  n_states        states of the modulating process (1 = plain Poisson)
  *  rate[i]         arrival rate in state i (0 = no arrivals)
- *  dwell_kind[i]   law of the time spent in state i: INF, EXP(mean dwell_mean[i]) or
- *                  PARETO(pareto_alpha[i], pareto_xm[i])
+ *  dwell_kind[i]   law of the time spent in state i: INF, EXP(mean dwell_mean[i]),
+ *                  PARETO(pareto_alpha[i], pareto_xm[i]) or DET (exactly dwell_mean[i]; a
+ *                  process whose state 0 is DET starts in state 0 at t = 0, the square
+ *                  wave of the Extreme Burst workload, Sec. 3.2)
  *  class_mix[c]    probability that an arrival is of class c
  *  service_kind[c] DET: alpha + beta*n; LOGN: median*exp(sigma*Z) + beta*n;
  *                  EXP: Exp with mean alpha + beta*n (Sec. 3.1 execution model)
@@ -80,7 +83,11 @@ enum { SIM_SVC_DET = 0, SIM_SVC_LOGN = 1, SIM_SVC_EXP = 2 };
  *  mlp_h1, mlp_h2  hidden widths of the policy MLP; mlp_bf16 = 1 for bf16 weights and
  *                  activations with fp32 accumulation, 0 for fp32 throughout
  *  value_head      1 adds a value output column (Sec. 4.2 value head)
- *  trace_max_len   per-environment capacity of the arrays given to sim_set_trace        */
+ *  trace_max_len   per-environment capacity of the arrays given to sim_set_trace
+ *  static_route    server that takes a batch of the static rule: SIM_ROUTE_LOWEST idle
+ *                  index, SIM_ROUTE_RANDOM (uniform over the idle servers) or
+ *                  SIM_ROUTE_ROUND_ROBIN (first idle server from a per-environment
+ *                  pointer); the Random and Round-Robin baselines of Sec. 5.1            */
 typedef struct sim_cfg {
   uint32_t abi_version; /* BATCHSIM_ABI_VERSION */
   uint32_t struct_size; /* sizeof(sim_cfg) */
@@ -102,6 +109,7 @@ typedef struct sim_cfg {
   int32_t static_bmax;
   int32_t mlp_h1, mlp_h2, mlp_bf16, value_head;
   int32_t trace_max_len;
+  int32_t static_route;
 } sim_cfg;
 
 /* Byte offsets of the policy weights inside one caller-owned device buffer. Weights are

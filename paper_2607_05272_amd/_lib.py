@@ -42,7 +42,7 @@ class SimCfg(C.Structure):
         ("reward_sum", C.c_int32), ("obs_tw", C.c_double), ("lambda_ref", C.c_double),
         ("shadow", C.c_int32), ("static_timeout", C.c_double), ("static_bmax", C.c_int32),
         ("mlp_h1", C.c_int32), ("mlp_h2", C.c_int32), ("mlp_bf16", C.c_int32),
-        ("value_head", C.c_int32), ("trace_max_len", C.c_int32),
+        ("value_head", C.c_int32), ("trace_max_len", C.c_int32), ("static_route", C.c_int32),
     ]
 
 
@@ -144,4 +144,5 @@ def make_cfg(w, n_envs=None):
     c.static_timeout = w["static_timeout"]; c.static_bmax = w["static_bmax"]
     c.mlp_h1 = w["mlp_h1"]; c.mlp_h2 = w["mlp_h2"]; c.mlp_bf16 = w["mlp_bf16"]
     c.value_head = w["value_head"]; c.trace_max_len = w.get("trace_max_len", 0)
+    c.static_route = w.get("static_route", 0)
     return c

@@ -31,7 +31,7 @@ __device__ __forceinline__ u32x4 philox(uint32_t c0, uint32_t c1, uint32_t c2, u
 }
 
 enum : uint32_t { P_ARRIVAL = 1, P_PROCESS = 2, P_SERVICE = 3, P_ACTION = 4, P_WEIGHTS = 5,
-                  P_MINIBATCH = 6 };
+                  P_MINIBATCH = 6, P_ROUTE = 7 };
 constexpr uint32_t STEP_RESET = 0xFFFFFFFFu;
 
 // Draw block j of `purpose` for (env, step, system) under `seed`.

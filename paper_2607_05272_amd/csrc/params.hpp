@@ -16,6 +16,7 @@ enum : uint32_t { ERR_ACTION = 1u, ERR_EVENTS = 2u, ERR_TRACE = 4u };
 struct SimParams {
   int E, K, C, N, F, S;
   int arrival_kind, shadow, bmax, reward_sum;
+  int route;                             // server choice of the static rule (SIM_ROUTE_*)
   double dt;
   double rate[kMaxS], mean_gap[kMaxS], dwell_mean[kMaxS], inv_alpha[kMaxS], xm[kMaxS];
   int dwell_kind[kMaxS];
@@ -48,6 +49,7 @@ struct SysState {
   double* next_sw;   // [E]     next modulating-state switch
   double* next_arr;  // [E]     next arrival
   uint32_t* tr_idx;  // [E]     next trace arrival index
+  uint32_t* rr;      // [E]     round-robin pointer (static system)
 };
 
 struct EnvState {

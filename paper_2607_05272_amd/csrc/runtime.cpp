@@ -136,10 +136,10 @@ static int validate(const sim_cfg* c) {
     for (int i = 0; i < c->n_states; ++i) {
       if (!(c->rate[i] >= 0.0)) return fail(SIM_EINVAL, "rate[%d] must be >= 0", i);
       const int k = c->dwell_kind[i];
-      if (k < 0 || k > 2) return fail(SIM_EINVAL, "dwell_kind[%d]", i);
+      if (k < 0 || k > 3) return fail(SIM_EINVAL, "dwell_kind[%d]", i);
       if (c->n_states > 1 && k == SIM_DWELL_INF)
         return fail(SIM_EINVAL, "dwell_kind[%d] must be finite with several states", i);
-      if (k == SIM_DWELL_EXP && !(c->dwell_mean[i] > 0.0))
+      if ((k == SIM_DWELL_EXP || k == SIM_DWELL_DET) && !(c->dwell_mean[i] > 0.0))
         return fail(SIM_EINVAL, "dwell_mean[%d] must be > 0", i);
       if (k == SIM_DWELL_PARETO && (!(c->pareto_alpha[i] > 1.0) || !(c->pareto_xm[i] > 0.0)))
         return fail(SIM_EINVAL, "pareto_alpha[%d] must be > 1 and pareto_xm > 0", i);
@@ -163,6 +163,8 @@ static int validate(const sim_cfg* c) {
   if (std::fabs(mix - 1.0) > 1e-9) return fail(SIM_EINVAL, "class_mix must sum to 1");
   if (!(c->obs_tw > 0.0) || !(c->lambda_ref > 0.0))
     return fail(SIM_EINVAL, "obs_tw and lambda_ref must be > 0");
+  if (c->static_route < SIM_ROUTE_LOWEST || c->static_route > SIM_ROUTE_ROUND_ROBIN)
+    return fail(SIM_EINVAL, "static_route");
   if (c->shadow && (c->static_bmax < 1 || c->static_bmax > 255 || !(c->static_timeout >= 0.0)))
     return fail(SIM_EINVAL, "static rule needs 1 <= static_bmax <= 255, static_timeout >= 0");
   return SIM_OK;
@@ -174,6 +176,7 @@ static void derive(sim_ctx* x) {
   p.E = c.n_envs; p.K = c.n_servers; p.C = c.n_classes; p.N = c.queue_cap;
   p.F = c.obs_dim; p.S = c.arrival_kind == SIM_ARR_TRACE ? 1 : c.n_states;
   p.arrival_kind = c.arrival_kind; p.shadow = c.shadow; p.bmax = c.static_bmax;
+  p.route = c.static_route;
   p.reward_sum = c.reward_sum; p.dt = c.tick_s;
   double mdw[kMaxS], tot = 0.0;
   for (int i = 0; i < kMaxS; ++i) {
@@ -186,7 +189,8 @@ static void derive(sim_ctx* x) {
     p.xm[i] = on ? c.pareto_xm[i] : 0.0;
     if (on) {
       // stationary time share of a state is proportional to its mean dwell
-      if (c.dwell_kind[i] == SIM_DWELL_EXP) mdw[i] = c.dwell_mean[i];
+      if (c.dwell_kind[i] == SIM_DWELL_EXP || c.dwell_kind[i] == SIM_DWELL_DET)
+        mdw[i] = c.dwell_mean[i];
       else if (c.dwell_kind[i] == SIM_DWELL_PARETO)
         mdw[i] = c.pareto_alpha[i] * c.pareto_xm[i] / (c.pareto_alpha[i] - 1.0);
       else mdw[i] = 1.0;
@@ -258,6 +262,7 @@ int sim_create(const sim_cfg* cfg, void* hip_stream, sim_ctx** out) {
     parts.push_back({(void**)&g.next_sw, 8 * E});
     parts.push_back({(void**)&g.next_arr, 8 * E});
     parts.push_back({(void**)&g.tr_idx, 4 * E});
+    parts.push_back({(void**)&g.rr, 4 * E});
   }
   parts.push_back({(void**)&x->s.ewma, 8 * 4 * E});
   parts.push_back({(void**)&x->s.obs, 4 * (size_t)cfg->obs_dim * E});

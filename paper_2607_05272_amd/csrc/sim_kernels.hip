@@ -172,6 +172,7 @@ __device__ __forceinline__ double dwell(const SimParams& p, int st, double u) {
   const int kind = pick<kMaxS>(p.dwell_kind, st);
   if (kind == 1) return -dlog(u) * pick<kMaxS>(p.dwell_mean, st);
   if (kind == 2) return pick<kMaxS>(p.xm, st) * dexp(-dlog(u) * pick<kMaxS>(p.inv_alpha, st));
+  if (kind == 3) return pick<kMaxS>(p.dwell_mean, st);  // fixed dwell: square wave
   return kInf;
 }
 
@@ -650,6 +651,28 @@ struct ServerBytes {
 };
 static_assert(kMaxK <= 16, "ServerBytes holds 16 servers");
 
+// Server for the static rule's next batch among the idle ones: the lowest index; uniformly
+// at random (the idx-th idle server in index order, idx = floor(u * n_idle), u from ROUTE
+// block jroute of (env, tick, system 1)); or round robin (the first idle server at or after
+// the pointer rr, cyclically).
+__device__ __forceinline__ int route_pick(uint32_t idle, int route, uint32_t rr, uint64_t seed,
+                                          int e, uint32_t k, uint32_t& jroute) {
+  if (route == 1) {
+    const int n_idle = __popc(idle);
+    const u32x4 w = draw(seed, (uint32_t)e, k, P_ROUTE, jroute++, 1);
+    int idx = (int)(unit(w.x, w.y) * (double)n_idle);
+    if (idx > n_idle - 1) idx = n_idle - 1;
+    uint32_t m = idle;
+    for (int i = 0; i < idx; ++i) m &= m - 1u;  // drop the idx lowest idle servers
+    return __builtin_ctz(m);
+  }
+  if (route == 2) {
+    const uint32_t at_or_after = idle & ~((1u << rr) - 1u);
+    return __builtin_ctz(at_or_after ? at_or_after : idle);
+  }
+  return __builtin_ctz(idle);
+}
+
 template <int KM, int CM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void static_k(SimParams p, EnvState g, uint64_t seed, uint32_t k,
                                                 double* __restrict__ rew) {
@@ -679,6 +702,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     if (j < p.K) infl.set(j, G.meta[(size_t)j * E + ee] & 0xffu);
   }
   uint32_t dirty = 0;
+  uint32_t rr = p.route == 2 ? G.rr[ee] : 0u, jroute = 0;
 
   const double t0 = (double)k * p.dt, t1 = (double)(k + 1) * p.dt;
   int A_k = 0;
@@ -727,14 +751,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       }
     }
     if (go || (first && !done)) {
-      // lowest idle server; min(B, Q_h) of the HoL class if Q_h >= B or its head waited T
+      // min(B, Q_h) of the HoL class if Q_h >= B or its head waited T, to the routed server
       while (idle != 0u && Q.qsum > 0) {
-        const int j = __builtin_ctz(idle);
         double ts;
         const int h = hol(Q, p, ts);
         const int qh = Q.q(h);
         if (!(qh >= p.bmax || now >= ts + p.static_timeout)) break;
         const int n = qh < p.bmax ? qh : p.bmax;
+        const int j = route_pick(idle, p.route, rr, seed, ee, k, jroute);
+        if (p.route == 2) rr = (uint32_t)((j + 1) % p.K);
         C.c[C_DONE] += infl.get(j);  // the previous batch on j finished at busy_j <= now
         infl.set(j, (uint32_t)n);
         const double sv = service<CM>(C, p, seed, ee, k, 1, h, n);
@@ -773,6 +798,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 #pragma unroll
   for (int j = 0; j < KM; ++j)
     if (dirty & (1u << j)) G.busy[(size_t)j * E + e] = busy[j];
+  if (p.route == 2) G.rr[e] = rr;
   store_queue(Q, G, p, e);
   store_count(C, G, p, e);
   store_arrivals(A, G, p, e);
@@ -795,7 +821,11 @@ __global__ __launch_bounds__(256) void reset_k(SimParams p, EnvState g, uint64_t
     if (bad) atomicOr(g.err, ERR_TRACE);
     next_arr = n > 0 ? p.tr_times[(size_t)e * p.tr_len] : kInf;
   } else {
-    if (p.S > 1) {
+    if (p.S > 1 && p.dwell_kind[0] == 3) {
+      // a square wave starts in state 0 with its full dwell: the same phase everywhere
+      proc = 0;
+      next_sw = p.dwell_mean[0];
+    } else if (p.S > 1) {
       const u32x4 w = draw(seed, (uint32_t)e, STEP_RESET, P_PROCESS, 0, 0);
       const double us = unit(w.z, w.w);
       int st = p.S - 1;
@@ -828,6 +858,7 @@ __global__ __launch_bounds__(256) void reset_k(SimParams p, EnvState g, uint64_t
     s.next_sw[e] = next_sw;
     s.next_arr[e] = next_arr;
     s.tr_idx[e] = 0u;
+    s.rr[e] = 0u;
   }
   for (int r = 0; r < 4; ++r) g.ewma[(size_t)r * E + e] = 0.0;
   // obs_0 is all zeros: empty queues, idle servers, no last batch (class feature

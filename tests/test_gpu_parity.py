@@ -8,7 +8,7 @@ import sys
 import numpy as np
 import pytest
 
-from workloads import preset, trace_preset
+from workloads import preset, trace_preset, burst_preset, baseline_preset
 from workloads.gen import seeded_actions, seeded_obs, seeded_rewards_values
 
 torch = pytest.importorskip("torch")
@@ -100,6 +100,31 @@ def test_sim_step_parity_small(bs, orc, name):
     assert np.array_equal(g["tot"]["cnt"][0], g["cnt"][0].sum(axis=1))
     if nsys == 2:
         assert np.array_equal(g["tot"]["cnt"][1], g["cnt"][1].sum(axis=1))
+
+
+BASELINES = {
+    "burst": lambda: burst_preset(),
+    "static8_C3": lambda: baseline_preset("static8", "C3"),
+    "random_C3": lambda: baseline_preset("random", "C3"),
+    "round_robin_C3": lambda: baseline_preset("round_robin", "C3"),
+    "random_C5": lambda: baseline_preset("random", "C5"),
+    "round_robin_C4": lambda: baseline_preset("round_robin", "C4"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(BASELINES))
+def test_baselines_and_burst_parity(bs, orc, name):
+    """The paper's baselines on the shadow system (Static-8, random and round-robin routing,
+    R23) and the Extreme Burst square wave (R24): 300 envs x 600 ticks, bit-exact integer
+    state and rewards against the oracle."""
+    w = BASELINES[name]()
+    E, T, seed = 300, 600, 0xBA5E + len(name)
+    acts = seeded_actions(seed, T, E, 6 * w["n_servers"], small_bias=0.5)
+    say(f"[baselines] {name} E={E} T={T}")
+    g = gpu_run_actions(bs, w, E, T, seed, acts)
+    r = orc.rollout(w, seed, T, np.arange(E), actions=acts)
+    compare_sim(r, g, w, np.arange(E), 2)
+    assert g["cnt"][1, 3].sum() > 0
 
 
 def _step_actions(seed, k, E, A):
