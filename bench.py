@@ -33,7 +33,23 @@ DESCR = {
     "C3": "C3: 16384 envs x 2048 ticks, 4 servers, Poisson 3000/s, 2 classes 70/30, obs 32, MLP 32-256-256-24 bf16, GAE",
     "C4": "C4: 65536 envs x 1024 ticks, 8 servers, 3-state MMPP, 4 classes lognormal, obs 64, MLP 64-256-256-48 bf16, GAE",
     "C5": "C5: 262144 envs x 4096 ticks, 16 servers, Pareto ON/OFF bursts 20000/s, 4 classes 50/30/15/5 lognormal, static shadow, obs 96, MLP 96-512-512-96 bf16, GAE",
+    "burst": "Extreme Burst: 65536 envs x 1000 ticks, square wave 100 <-> 0 req/s every 200 ticks, 1 server, DET 5ms+0.5ms*b, static shadow (B=32, T=10ms), MLP 8-64-64-6 fp32",
+    "C3-static8": "C3 with a Static-8 shadow (fixed batch 8, 10 ms timeout, lowest idle server)",
+    "C3-random": "C3 with a static shadow routing each batch to a uniformly random idle server",
+    "C3-round_robin": "C3 with a static shadow routing batches round-robin over the idle servers",
+    "C5-random": "C5 with the static shadow routing each batch to a uniformly random idle server",
 }
+
+
+def workload_of(name):
+    """The workload dict of a bench configuration name."""
+    from workloads import preset, burst_preset, baseline_preset
+    if name == "burst":
+        return burst_preset(n_envs=65536, T=1000)
+    if "-" in name:
+        base, rule = name.split("-", 1)
+        return baseline_preset(rule, base)
+    return preset(name)
 
 
 def mlp_flops(w):
@@ -229,14 +245,12 @@ def main():
         sys.exit(2)
     import torch
     import paper_2607_05272_amd as bs
-    from workloads import preset
-
-    w = preset(args.config)
+    w = workload_of(args.config)
     if args.ticks:
         w["T"] = args.ticks
     E, T, F = w["n_envs"], w["T"], w["obs_dim"]
     dev = torch.device("cuda")
-    seed = 0x5EED0000 + int(args.config[1])
+    seed = 0x5EED0000 + (int(args.config[1]) if args.config[0] == "C" else 9)
     sim = bs.Sim(w)
     weights = sim.init_weights(seed)
     ppo = w.get("ppo_minibatch", 0) > 0 and args.train == "none"
