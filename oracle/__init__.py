@@ -39,6 +39,8 @@ class OrcCfg(C.Structure):
         ("shadow", C.c_int32), ("static_timeout", C.c_double), ("static_bmax", C.c_int32),
         ("mlp_h1", C.c_int32), ("mlp_h2", C.c_int32), ("mlp_bf16", C.c_int32),
         ("value_head", C.c_int32), ("static_route", C.c_int32),
+        ("policy_kind", C.c_int32), ("attn_tokens", C.c_int32), ("attn_embed", C.c_int32),
+        ("attn_heads", C.c_int32),
     ]
 
 
@@ -47,8 +49,14 @@ class OrcTrace(C.Structure):
                 ("max_len", C.c_int32)]
 
 
+MLP_KEYS = ("w1", "b1", "w2", "b2", "w3", "b3")
+ATTN_KEYS = ("w_in", "b_in", "w_qkv", "b_qkv", "w_o", "b_o", "wp1", "bp1", "wp2", "bp2",
+             "wv1", "bv1", "wv2", "bv2")
+POLICY_MLP, POLICY_ATTN = 0, 1
+
+
 class OrcWeights(C.Structure):
-    _fields_ = [(n, C.c_void_p) for n in ("w1", "b1", "w2", "b2", "w3", "b3")]
+    _fields_ = [(n, C.c_void_p) for n in MLP_KEYS + ATTN_KEYS]
 
 
 class OrcDisp(C.Structure):
@@ -89,6 +97,9 @@ def lib():
             L.orc_n_out.argtypes = [vp]
             L.orc_init_weights.argtypes = [vp, u64, vp, vp, vp, vp, vp, vp]
             L.orc_policy.argtypes = [vp, vp, u64, u32, i32, vp, vp, vp, vp, vp, vp]
+            L.orc_policy.restype = i32
+            L.orc_init_weights_attn.argtypes = [vp, u64, vp]
+            L.orc_init_weights_attn.restype = i32
             L.orc_rollout.argtypes = [vp, u64, i32, i32, vp, vp, vp, vp, vp]
             L.orc_rollout.restype = i32
             L.orc_gae.argtypes = [i32, i32, vp, vp, dbl, dbl, vp, vp]
@@ -125,6 +136,10 @@ def make_cfg(w):
     c.mlp_h1 = w["mlp_h1"]; c.mlp_h2 = w["mlp_h2"]; c.mlp_bf16 = w["mlp_bf16"]
     c.value_head = w["value_head"]
     c.static_route = w.get("static_route", 0)
+    c.policy_kind = w.get("policy_kind", POLICY_MLP)
+    c.attn_tokens = w.get("attn_tokens", 0)
+    c.attn_embed = w.get("attn_embed", 0)
+    c.attn_heads = w.get("attn_heads", 0)
     return c
 
 
@@ -193,9 +208,24 @@ def n_out(w):
     return 6 * w["n_servers"] + (1 if w["value_head"] else 0)
 
 
+def attn_shapes(w):
+    """Shapes of the attention policy's parameters (R26), in ATTN_KEYS order."""
+    F, D, A = w["obs_dim"], w["attn_embed"], 6 * w["n_servers"]
+    Hp, Hv = w["mlp_h1"], w["mlp_h2"]
+    return dict(w_in=(F, D), b_in=(D,), w_qkv=(D, 3 * D), b_qkv=(3 * D,), w_o=(D, D), b_o=(D,),
+                wp1=(D, Hp), bp1=(Hp,), wp2=(Hp, A), bp2=(A,), wv1=(D, Hv), bv1=(Hv,),
+                wv2=(Hv, 1), bv2=(1,))
+
+
 def init_weights(w, seed):
     """Xavier-uniform weights from the seed as fp64 arrays of the rounded values."""
     c = make_cfg(w)
+    if w.get("policy_kind", POLICY_MLP) == POLICY_ATTN:
+        arrs = {k: np.empty(sh) for k, sh in attn_shapes(w).items()}
+        ptrs = (C.c_void_p * 14)(*[arrs[k].ctypes.data for k in ATTN_KEYS])
+        if lib().orc_init_weights_attn(C.byref(c), seed, ptrs) != 0:
+            raise ValueError("attention shape not supported by the oracle")
+        return arrs
     F, H1, H2, A = w["obs_dim"], w["mlp_h1"], w["mlp_h2"], n_out(w)
     arrs = dict(w1=np.empty((F, H1)), b1=np.empty(H1), w2=np.empty((H1, H2)), b2=np.empty(H2),
                 w3=np.empty((H2, A)), b3=np.empty(A))
@@ -207,7 +237,9 @@ def init_weights(w, seed):
 def _weights_struct(wts):
     ws = OrcWeights()
     keep = {}
-    for k in ("w1", "b1", "w2", "b2", "w3", "b3"):
+    for k in wts:
+        if k not in MLP_KEYS + ATTN_KEYS:
+            continue
         a = np.ascontiguousarray(wts[k], dtype=np.float64)
         keep[k] = a
         setattr(ws, k, a.ctypes.data)
@@ -224,8 +256,9 @@ def policy(w, wts, seed, k, obs, env_ids):
     A = n_out(w)
     logits = np.empty((n, A)); act = np.empty(n, np.uint8)
     logp = np.empty(n); margin = np.empty(n)
-    lib().orc_policy(C.byref(c), C.byref(ws), seed, k, n, _p(ids), _p(obs), _p(logits),
-                     _p(act), _p(logp), _p(margin))
+    if lib().orc_policy(C.byref(c), C.byref(ws), seed, k, n, _p(ids), _p(obs), _p(logits),
+                        _p(act), _p(logp), _p(margin)) != 0:
+        raise ValueError("policy shape not supported by the oracle")
     return dict(logits=logits, actions=act, logp=logp, margin=margin)
 
 

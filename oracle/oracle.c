@@ -654,6 +654,101 @@ static void mlp_forward(const orc_cfg* c, const orc_weights* w, const float* obs
   }
 }
 
+/* The attention policy of Sec. 4.2 (R26), one observation, fp64, in the order the
+ * definitions are stated:
+ *   tokens    e_g = b_in + sum over the features i of group g of x_i W_in[i,:]
+ *             (F features in attn_tokens = L contiguous groups of F/L),
+ *   attention q_g, k_g, v_g = e_g W_qkv + b_qkv (query, key, value column blocks); head h
+ *             takes columns [h dh, (h+1) dh) with dh = D / attn_heads and gives
+ *             o_{g,h} = sum_g' softmax_g'(q_{g,h} . k_{g',h} / sqrt(dh)) v_{g',h}
+ *             (scaled dot-product attention, Vaswani et al. 2017); y_g = concat_h o_{g,h}
+ *             W_o + b_o,
+ *   pooling   p = mean over g of y_g,
+ *   heads     logits = GELU(p W_p1 + b_p1) W_p2 + b_p2 and
+ *             V = GELU(p W_v1 + b_v1) W_v2 + b_v2 (a separate value MLP).
+ * out[0..A) are the logits, out[A] = V when value_head = 1. */
+static void attn_forward(const orc_cfg* c, const orc_weights* w, const float* obs, double* out) {
+  const int F = c->obs_dim, L = c->attn_tokens, D = c->attn_embed, NH = c->attn_heads;
+  const int G = F / L, dh = D / NH, A = 6 * c->n_servers;
+  const int Hp = c->mlp_h1, Hv = c->mlp_h2;
+  double e[ORC_ATTN_MAX_L][ORC_ATTN_MAX_D];
+  double q[ORC_ATTN_MAX_L][ORC_ATTN_MAX_D], k[ORC_ATTN_MAX_L][ORC_ATTN_MAX_D];
+  double v[ORC_ATTN_MAX_L][ORC_ATTN_MAX_D], o[ORC_ATTN_MAX_L][ORC_ATTN_MAX_D];
+  double pool[ORC_ATTN_MAX_D];
+  for (int g = 0; g < L; g++)
+    for (int d = 0; d < D; d++) {
+      double acc = w->b_in[d];
+      for (int i = g * G; i < (g + 1) * G; i++) acc = acc + (double)obs[i] * w->w_in[i * D + d];
+      e[g][d] = acc;
+    }
+  for (int g = 0; g < L; g++)
+    for (int d = 0; d < D; d++) {
+      double aq = w->b_qkv[d], ak = w->b_qkv[D + d], av = w->b_qkv[2 * D + d];
+      for (int i = 0; i < D; i++) {
+        aq = aq + e[g][i] * w->w_qkv[i * 3 * D + d];
+        ak = ak + e[g][i] * w->w_qkv[i * 3 * D + D + d];
+        av = av + e[g][i] * w->w_qkv[i * 3 * D + 2 * D + d];
+      }
+      q[g][d] = aq; k[g][d] = ak; v[g][d] = av;
+    }
+  const double scale = 1.0 / sqrt((double)dh);
+  for (int h = 0; h < NH; h++)
+    for (int g = 0; g < L; g++) {
+      double sc[ORC_ATTN_MAX_L];
+      double mx = -INFINITY;
+      for (int j = 0; j < L; j++) {
+        double dot = 0.0;
+        for (int t = h * dh; t < (h + 1) * dh; t++) dot = dot + q[g][t] * k[j][t];
+        sc[j] = dot * scale;
+        if (sc[j] > mx) mx = sc[j];
+      }
+      double S = 0.0;
+      for (int j = 0; j < L; j++) { sc[j] = exp(sc[j] - mx); S = S + sc[j]; }
+      for (int t = h * dh; t < (h + 1) * dh; t++) {
+        double acc = 0.0;
+        for (int j = 0; j < L; j++) acc = acc + (sc[j] / S) * v[j][t];
+        o[g][t] = acc;
+      }
+    }
+  for (int d = 0; d < D; d++) pool[d] = 0.0;
+  for (int g = 0; g < L; g++)
+    for (int d = 0; d < D; d++) {
+      double y = w->b_o[d];
+      for (int i = 0; i < D; i++) y = y + o[g][i] * w->w_o[i * D + d];
+      pool[d] = pool[d] + y;
+    }
+  for (int d = 0; d < D; d++) pool[d] = pool[d] / (double)L;
+  for (int a = 0; a < A; a++) out[a] = w->bp2[a];
+  for (int j = 0; j < Hp; j++) {
+    double z = w->bp1[j];
+    for (int d = 0; d < D; d++) z = z + pool[d] * w->wp1[d * Hp + j];
+    const double h = gelu(z);
+    for (int a = 0; a < A; a++) out[a] = out[a] + h * w->wp2[j * A + a];
+  }
+  if (c->value_head) {
+    double V = w->bv2[0];
+    for (int j = 0; j < Hv; j++) {
+      double z = w->bv1[j];
+      for (int d = 0; d < D; d++) z = z + pool[d] * w->wv1[d * Hv + j];
+      V = V + gelu(z) * w->wv2[j];
+    }
+    out[A] = V;
+  }
+}
+
+static void policy_forward(const orc_cfg* c, const orc_weights* w, const float* obs, double* out,
+                           double* h1, double* h2) {
+  if (c->policy_kind == ORC_POLICY_ATTN) attn_forward(c, w, obs, out);
+  else mlp_forward(c, w, obs, out, h1, h2);
+}
+
+static int attn_shape_ok(const orc_cfg* c) {
+  return c->attn_tokens >= 1 && c->attn_tokens <= ORC_ATTN_MAX_L && c->attn_embed >= 1 &&
+         c->attn_embed <= ORC_ATTN_MAX_D && c->attn_heads >= 1 &&
+         c->attn_embed % c->attn_heads == 0 && c->obs_dim % c->attn_tokens == 0 &&
+         c->mlp_h1 >= 1 && c->mlp_h2 >= 1 && !c->mlp_bf16;
+}
+
 /* Action uniform (R13, R17): 23 bits of the first word of the ACTION block, centred. */
 static double action_u(uint64_t seed, uint32_t env, uint32_t k) {
   uint32_t w[4];
@@ -761,17 +856,42 @@ void orc_init_weights(const orc_cfg* c, uint64_t seed, double* w1, double* b1, d
   }
 }
 
-/* MLP forward + sampler on a batch of observations [n][F]; the uniform of row i is that
+/* Xavier-uniform weights of the attention policy (R26): its seven matrices in the order
+ * W_in [F][D], W_qkv [D][3D], W_o [D][D], W_p1 [D][H1], W_p2 [H1][A], W_v1 [D][H2],
+ * W_v2 [H2][1] take layer indices 0..6 of the same counter scheme as the MLP (element i of
+ * matrix l from the WEIGHTS block at (i, 0xFFFFFFFE, WEIGHTS<<24 | l, 0)), limits
+ * sqrt(6 / (fan_in + fan_out)), rounded to fp32; the seven biases are zero. p[14] receives
+ * w_in, b_in, w_qkv, b_qkv, w_o, b_o, wp1, bp1, wp2, bp2, wv1, bv1, wv2, bv2. Returns -1 for
+ * a shape it does not support. */
+int orc_init_weights_attn(const orc_cfg* c, uint64_t seed, double* const* p) {
+  if (!attn_shape_ok(c)) return -1;
+  const int F = c->obs_dim, D = c->attn_embed, A = 6 * c->n_servers;
+  const int fin[7] = {F, D, D, D, c->mlp_h1, D, c->mlp_h2};
+  const int fout[7] = {D, 3 * D, D, c->mlp_h1, A, c->mlp_h2, 1};
+  for (int l = 0; l < 7; l++) {
+    double lim = sqrt(6.0 / (double)(fin[l] + fout[l]));
+    for (int64_t i = 0; i < (int64_t)fin[l] * fout[l]; i++) {
+      uint32_t wd[4];
+      draw(seed, (uint32_t)i, 0xFFFFFFFEu, ORC_P_WEIGHTS, (uint32_t)l, 0, wd);
+      p[2 * l][i] = (double)(float)((2.0 * u01(wd[0], wd[1]) - 1.0) * lim);
+    }
+    for (int j = 0; j < fout[l]; j++) p[2 * l + 1][j] = 0.0;
+  }
+  return 0;
+}
+
+/* Policy forward + sampler on a batch of observations [n][F]; the uniform of row i is that
  * of env env_ids[i] at step k. Outputs: logits [n][A'], actions, logp, margin. */
-void orc_policy(const orc_cfg* c, const orc_weights* w, uint64_t seed, uint32_t k, int32_t n,
+int orc_policy(const orc_cfg* c, const orc_weights* w, uint64_t seed, uint32_t k, int32_t n,
                 const uint32_t* env_ids, const float* obs, double* logits, uint8_t* actions,
                 double* logp, double* margin) {
   int A = 6 * c->n_servers, Ap = n_out(c);
+  if (c->policy_kind == ORC_POLICY_ATTN && !attn_shape_ok(c)) return -1;
   double* h1 = (double*)malloc(sizeof(double) * (size_t)c->mlp_h1);
   double* h2 = (double*)malloc(sizeof(double) * (size_t)c->mlp_h2);
   double* l = (double*)malloc(sizeof(double) * (size_t)Ap);
   for (int32_t i = 0; i < n; i++) {
-    mlp_forward(c, w, obs + (int64_t)i * c->obs_dim, l, h1, h2);
+    policy_forward(c, w, obs + (int64_t)i * c->obs_dim, l, h1, h2);
     if (logits) memcpy(logits + (int64_t)i * Ap, l, sizeof(double) * (size_t)Ap);
     double lp, mg;
     int a = sample_action(l, A, action_u(seed, env_ids[i], k), &lp, &mg);
@@ -780,6 +900,7 @@ void orc_policy(const orc_cfg* c, const orc_weights* w, uint64_t seed, uint32_t 
     if (margin) margin[i] = mg;
   }
   free(h1); free(h2); free(l);
+  return 0;
 }
 
 /* The rollout: T ticks of each listed env, one env at a time. With actions != NULL the
@@ -793,6 +914,7 @@ int orc_rollout(const orc_cfg* c, uint64_t seed, int32_t T, int32_t n, const uin
     return -1;
   if (c->arrival_kind == ORC_ARR_TRACE && !tr) return -1;
   if (!actions && !w) return -1;
+  if (!actions && c->policy_kind == ORC_POLICY_ATTN && !attn_shape_ok(c)) return -1;
   if (c->n_states < 1 || c->n_states > ORC_MAX_S) return -1;
   /* observation width of R15 must fit in obs_dim */
   int need = 2 + c->n_servers * (c->n_servers > 1 ? 4 : 2) + (c->n_classes > 1 ? 2 * c->n_classes : 0) + 4;
@@ -818,7 +940,7 @@ int orc_rollout(const orc_cfg* c, uint64_t seed, int32_t T, int32_t n, const uin
       if (actions) {
         a = actions[(int64_t)k * n + i];
       } else {
-        mlp_forward(c, w, ob, l, h1, h2);
+        policy_forward(c, w, ob, l, h1, h2);
         double lp, mg;
         a = sample_action(l, A, action_u(seed, env, (uint32_t)k), &lp, &mg);
         if (out && out->actions) out->actions[(int64_t)k * n + i] = (uint8_t)a;
@@ -853,7 +975,7 @@ int orc_rollout(const orc_cfg* c, uint64_t seed, int32_t T, int32_t n, const uin
       if (out && out->rchk) out->rchk[(int64_t)k * n + i] = S[0].chk;
     }
     if (!actions && out && out->value && c->value_head) {
-      mlp_forward(c, w, ob, l, h1, h2);
+      policy_forward(c, w, ob, l, h1, h2);
       out->value[(int64_t)T * n + i] = (float)l[A];
     }
     for (int s = 0; s < nsys; s++) {

@@ -10,9 +10,11 @@
  *     central dispatcher), driven by the workloads of Sec. 3.2;
  *   - the MDP of Sec. 4.1 (state vector, batch/routing action, reward of throughput minus
  *     weighted latency);
- *   - the policy MLP of Sec. 4.2 (GELU hidden layers, categorical head, value column);
+ *   - the policy networks of Sec. 4.2: the MLP (GELU hidden layers, categorical head,
+ *     value column) and the attention policy (input projection to tokens, multi-head
+ *     self-attention, mean pooling, GELU policy head and a separate GELU value head);
  *   - discounted returns (REINFORCE) and GAE (PPO) of Sec. 4.3.
- * Every reading of a point the paper leaves open is numbered R1..R22 in the design doc; the
+ * Every reading of a point the paper leaves open is numbered R1..R26 in the design doc; the
  * comments in oracle.c name them.
  *
  * Every function runs one environment at a time, event by event, in fp64 with no
@@ -20,7 +22,9 @@
  *   pinned:   Philox structure (vs numpy's Philox4x64), det_log/det_exp/det_cos (vs libm),
  *             samplers (KS / chi-square vs scipy), queue dynamics (M/D/1, M/M/1, M/M/1/K,
  *             M/M/c closed forms), Little's law (exact sample-path identity), conservation,
- *             hand-enumerated traces, MLP (vs torch fp64), GAE (closed forms).
+ *             hand-enumerated traces, MLP (vs torch fp64), attention policy (vs
+ *             torch.nn.MultiheadAttention in fp64, one-token and uniform-attention closed
+ *             forms, feature-permutation invariance), GAE (closed forms).
  *   unpinned: the Philox4x32 multipliers (no known-answer vectors available here; pinned
  *             only statistically and by GPU/CPU bit identity).
  */
@@ -37,6 +41,9 @@ enum { ORC_ARR_MODULATED = 0, ORC_ARR_TRACE = 1 };
 enum { ORC_DWELL_INF = 0, ORC_DWELL_EXP = 1, ORC_DWELL_PARETO = 2, ORC_DWELL_DET = 3 };
 enum { ORC_ROUTE_LOWEST = 0, ORC_ROUTE_RANDOM = 1, ORC_ROUTE_ROUND_ROBIN = 2 };
 enum { ORC_SVC_DET = 0, ORC_SVC_LOGN = 1, ORC_SVC_EXP = 2 };
+enum { ORC_POLICY_MLP = 0, ORC_POLICY_ATTN = 1 };
+#define ORC_ATTN_MAX_L 16   /* tokens */
+#define ORC_ATTN_MAX_D 16   /* embedding width */
 enum { ORC_P_ARRIVAL = 1, ORC_P_PROCESS = 2, ORC_P_SERVICE = 3, ORC_P_ACTION = 4,
        ORC_P_WEIGHTS = 5, ORC_P_MINIBATCH = 6, ORC_P_ROUTE = 7 };
 #define ORC_STEP_RESET 0xFFFFFFFFu
@@ -60,6 +67,10 @@ typedef struct orc_cfg {
   int32_t static_bmax;
   int32_t mlp_h1, mlp_h2, mlp_bf16, value_head;
   int32_t static_route;          /* ORC_ROUTE_*: server choice of the static system (R23) */
+  /* policy network (R16, R26): the MLP, or the attention policy of Sec. 4.2 with
+   * attn_tokens tokens of width attn_embed and attn_heads heads; its policy head has
+   * mlp_h1 hidden units and its value head mlp_h2 */
+  int32_t policy_kind, attn_tokens, attn_embed, attn_heads;
 } orc_cfg;
 
 /* Explicit arrivals for ORC_ARR_TRACE: times [n_env][max_len] (seconds, nondecreasing),
@@ -72,9 +83,15 @@ typedef struct orc_trace {
 } orc_trace;
 
 /* Policy weights in fp64 (each value already rounded to the layer's storage precision).
- * W_l is [in][out] row-major. A' = 6K + value_head. */
+ * W_l is [in][out] row-major. A' = 6K + value_head.
+ * MLP: w1 [F][H1], w2 [H1][H2], w3 [H2][A'].
+ * Attention (R26, D = attn_embed, A = 6K): w_in [F][D], w_qkv [D][3D] (columns: query,
+ * key, value), w_o [D][D], wp1 [D][mlp_h1], wp2 [mlp_h1][A], wv1 [D][mlp_h2], wv2
+ * [mlp_h2][1], each with its bias. */
 typedef struct orc_weights {
   const double *w1, *b1, *w2, *b2, *w3, *b3;
+  const double *w_in, *b_in, *w_qkv, *b_qkv, *w_o, *b_o;
+  const double *wp1, *bp1, *wp2, *bp2, *wv1, *bv1, *wv2, *bv2;
 } orc_weights;
 
 #define ORC_REC_W 10   /* n_k, dispatches, sumQ, A_k, dropped(cum), completed(cum), Q[0..3] */

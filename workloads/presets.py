@@ -21,6 +21,9 @@ DWELL_DET = 3       # fixed dwell (square wave), R24
 ROUTE_LOWEST = 0
 ROUTE_RANDOM = 1
 ROUTE_ROUND_ROBIN = 2
+# policy network (R16, R26)
+POLICY_MLP = 0
+POLICY_ATTN = 1
 # service kinds
 SVC_DET = 0
 SVC_LOGN = 1
@@ -40,6 +43,7 @@ _BASE = dict(
     obs_tw=0.010, lambda_ref=500.0,
     shadow=0, static_timeout=0.010, static_bmax=32, static_route=ROUTE_LOWEST,
     mlp_h1=64, mlp_h2=64, mlp_bf16=0, value_head=0,
+    policy_kind=POLICY_MLP, attn_tokens=0, attn_embed=0, attn_heads=0,
     gamma=0.99, lam=1.0, ppo_minibatch=0,
 )
 
@@ -131,6 +135,17 @@ def baseline_preset(rule, base="C3", **kw):
                  random=dict(static_route=ROUTE_RANDOM),
                  round_robin=dict(static_route=ROUTE_ROUND_ROBIN))[rule]
     d = preset(base, shadow=1, **extra)
+    d.update(kw)
+    return d
+
+
+def attn_preset(**kw):
+    """The paper's own policy network (Sec. 4.2) on C1's single-server system: the 8 state
+    features as 8 tokens through the 8 -> 4 input projection, self-attention with 2 heads of
+    embedding 4, mean pooling, a GELU policy head of 64 units and a separate GELU value head
+    of 64 (R26), fp32; REINFORCE with the learned baseline (lambda = 1)."""
+    d = _mk(name="attn", policy_kind=POLICY_ATTN, attn_tokens=8, attn_embed=4, attn_heads=2,
+            mlp_h1=64, mlp_h2=64, value_head=1)
     d.update(kw)
     return d
 
