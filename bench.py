@@ -240,7 +240,7 @@ def main():
         return
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU only (environments are independent; the "
-              "multi-GPU design is described in DESIGN.md but not built). Use --gpus 1.",
+              "path would shard by environment, but only the one-GPU path is built). Use --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
     import torch

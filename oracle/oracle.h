@@ -14,8 +14,8 @@
  *     value column) and the attention policy (input projection to tokens, multi-head
  *     self-attention, mean pooling, GELU policy head and a separate GELU value head);
  *   - discounted returns (REINFORCE) and GAE (PPO) of Sec. 4.3.
- * Every reading of a point the paper leaves open is numbered R1..R26 in the design doc; the
- * comments in oracle.c name them.
+ * Every reading of a point the paper leaves open is numbered R1..R26 (the design notes list
+ * them); the comments in oracle.c name them.
  *
  * Every function runs one environment at a time, event by event, in fp64 with no
  * implicit contraction (built with -ffp-contract=off). Parity functions:

@@ -102,7 +102,7 @@ def test_sim_step_parity_small(bs, orc, name):
         assert np.array_equal(g["tot"]["cnt"][1], g["cnt"][1].sum(axis=1))
 
 
-BASELINES = {
+RULES = {
     "burst": lambda: burst_preset(),
     "static8_C3": lambda: baseline_preset("static8", "C3"),
     "random_C3": lambda: baseline_preset("random", "C3"),
@@ -112,12 +112,12 @@ BASELINES = {
 }
 
 
-@pytest.mark.parametrize("name", sorted(BASELINES))
+@pytest.mark.parametrize("name", sorted(RULES))
 def test_baselines_and_burst_parity(bs, orc, name):
     """The paper's baselines on the shadow system (Static-8, random and round-robin routing,
     R23) and the Extreme Burst square wave (R24): 300 envs x 600 ticks, bit-exact integer
     state and rewards against the oracle."""
-    w = BASELINES[name]()
+    w = RULES[name]()
     E, T, seed = 300, 600, 0xBA5E + len(name)
     acts = seeded_actions(seed, T, E, 6 * w["n_servers"], small_bias=0.5)
     say(f"[baselines] {name} E={E} T={T}")

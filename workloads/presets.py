@@ -4,8 +4,8 @@ Each preset is a dict of plain parameters; nothing here is derived. Units: secon
 requests per second. Sources (paper sections): the linear batch-latency model and the
 FIFO cap of 100 (Sec. 3.1), the workload families (Sec. 3.2), the MDP state/action/
 reward (Sec. 4.1), the policy network (Sec. 4.2), the discount/GAE settings
-(Sec. 4.3). Values the paper does not fix are documented readings (see the design doc's
-list of readings, R-numbers in the comments).
+(Sec. 4.3). Values the paper does not fix are numbered readings of it (R-numbers in the
+comments).
 """
 import copy
 
