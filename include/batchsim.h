@@ -49,6 +49,8 @@ enum sim_status {
 enum { SIM_ARR_MODULATED = 0, SIM_ARR_TRACE = 1 };
 enum { SIM_DWELL_INF = 0, SIM_DWELL_EXP = 1, SIM_DWELL_PARETO = 2, SIM_DWELL_DET = 3 };
 enum { SIM_ROUTE_LOWEST = 0, SIM_ROUTE_RANDOM = 1, SIM_ROUTE_ROUND_ROBIN = 2 };
+/* policy network (Sec. 4.2) */
+enum { SIM_POLICY_MLP = 0, SIM_POLICY_ATTN = 1 };
 enum { SIM_SVC_DET = 0, SIM_SVC_LOGN = 1, SIM_SVC_EXP = 2 };
 
 #define SIM_MAX_SERVERS 16
@@ -87,7 +89,16 @@ enum { SIM_SVC_DET = 0, SIM_SVC_LOGN = 1, SIM_SVC_EXP = 2 };
  *  static_route    server that takes a batch of the static rule: SIM_ROUTE_LOWEST idle
  *                  index, SIM_ROUTE_RANDOM (uniform over the idle servers) or
  *                  SIM_ROUTE_ROUND_ROBIN (first idle server from a per-environment
- *                  pointer); the Random and Round-Robin baselines of Sec. 5.1            */
+ *                  pointer); the Random and Round-Robin baselines of Sec. 5.1
+ *  policy_kind     SIM_POLICY_MLP (the MLP above) or SIM_POLICY_ATTN, the attention
+ *                  policy of Sec. 4.2: the obs_dim features split into attn_tokens
+ *                  contiguous groups, each group's terms of the input projection summed
+ *                  into one token of width attn_embed; multi-head self-attention with
+ *                  attn_heads heads; the mean of the tokens feeds a policy head with
+ *                  mlp_h1 GELU units and, with value_head = 1, a separate value head with
+ *                  mlp_h2 GELU units. fp32 only (mlp_bf16 = 0). Built shapes:
+ *                  attn_embed = 4, attn_heads in {1, 2, 4}, attn_tokens in {1, 2, 4, 8}
+ *                  dividing obs_dim <= 64, n_servers in {1, 2, 4}, mlp_h1, mlp_h2 <= 256 */
 typedef struct sim_cfg {
   uint32_t abi_version; /* BATCHSIM_ABI_VERSION */
   uint32_t struct_size; /* sizeof(sim_cfg) */
@@ -110,17 +121,31 @@ typedef struct sim_cfg {
   int32_t mlp_h1, mlp_h2, mlp_bf16, value_head;
   int32_t trace_max_len;
   int32_t static_route;
+  int32_t policy_kind, attn_tokens, attn_embed, attn_heads;
 } sim_cfg;
 
 /* Byte offsets of the policy weights inside one caller-owned device buffer. Weights are
  * [in][out] row-major; W1 is [F][H1], W2 [H1][H2], W3 [H2][A'] with A' = 6K + value_head.
  * Matrices are fp32, or bf16 (raw 16-bit patterns) when mlp_bf16 = 1; biases are fp32.  */
 typedef struct sim_wlayout {
-  size_t w1, b1, w2, b2, w3, b3; /* offsets in bytes, 256-byte aligned */
-  size_t bytes;                  /* total size of the buffer */
+  size_t w1, b1, w2, b2, w3, b3; /* offsets in bytes, 256-byte aligned (MLP policy only;
+                                    zero for the attention policy) */
+  size_t bytes;                  /* total size of the buffer (either policy) */
   int32_t n_out;                 /* A' */
   int32_t elem_bytes;            /* 4 (fp32) or 2 (bf16) */
 } sim_wlayout;
+
+/* Byte offsets of the attention policy's weights (policy_kind = SIM_POLICY_ATTN) in one
+ * caller-owned device buffer of sim_wlayout.bytes bytes, all fp32, [in][out] row-major
+ * (D = attn_embed, A = 6K): w_in [F][D] and b_in [D] (input projection), w_qkv [D][3D]
+ * (columns: query, key, value) and b_qkv [3D], w_o [D][D] and b_o [D] (attention output),
+ * wp1 [D][mlp_h1], bp1, wp2 [mlp_h1][A], bp2 (policy head), wv1 [D][mlp_h2], bv1,
+ * wv2 [mlp_h2][1], bv2 [1] (value head). Offsets are 256-byte aligned.                  */
+typedef struct sim_attn_layout {
+  size_t w_in, b_in, w_qkv, b_qkv, w_o, b_o;
+  size_t wp1, bp1, wp2, bp2, wv1, bv1, wv2, bv2;
+  size_t bytes;
+} sim_attn_layout;
 
 /* Caller-owned device buffers filled by sim_rollout. Only `actions` is required; any
  * other pointer may be NULL to skip that output.                                       */
@@ -185,13 +210,19 @@ int sim_tick(sim_ctx* ctx, int32_t* h_tick);
 /* Layout of the weights buffer for this configuration (no device work).                */
 int sim_weights_layout(const sim_cfg* cfg, sim_wlayout* out);
 
+/* Offsets of the attention policy's weights (Sec. 4.2); SIM_EINVAL unless
+ * cfg->policy_kind = SIM_POLICY_ATTN with a valid attention shape.                      */
+int sim_attn_weights_layout(const sim_cfg* cfg, sim_attn_layout* out);
+
 /* Writes Xavier-uniform weights drawn from `seed` and zero biases into d_weights
- * (layout of sim_weights_layout).                                                      */
+ * (layout of sim_weights_layout, or of sim_attn_weights_layout for the attention policy,
+ * whose seven matrices take weight-stream layers 0..6 in layout order).                 */
 int sim_init_weights(sim_ctx* ctx, uint64_t seed, void* d_weights);
 
-/* Policy on one batch of observations d_obs [F][E]: MLP forward, then an action sampled
- * from the softmax of the logits with the ACTION uniform of (env, step). Outputs (any may
- * be NULL): d_act [E], d_logp [E], d_value [E] (value head), d_logits [A'][E] fp32.     */
+/* Policy on one batch of observations d_obs [F][E]: MLP (or attention) forward, then an
+ * action sampled from the softmax of the logits with the ACTION uniform of (env, step).
+ * Outputs (any may be NULL): d_act [E], d_logp [E], d_value [E] (value head),
+ * d_logits [A'][E] fp32.                                                                */
 int sim_policy(sim_ctx* ctx, const void* d_weights, const float* d_obs, uint32_t step,
                uint8_t* d_act, float* d_logp, float* d_value, float* d_logits);
 

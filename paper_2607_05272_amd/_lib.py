@@ -22,7 +22,7 @@ SYMBOLS = ("sim_last_error", "sim_abi_version", "sim_create", "sim_destroy", "si
            "sim_init_weights", "sim_policy", "sim_rollout", "returns_gae", "sim_counters",
            "sim_checksums", "sim_stats", "sim_sync", "sim_set_timing", "sim_get_timing",
            "ppo_minibatch_grad", "sim_ppo_grad_count", "reinforce_minibatch_grad",
-           "sim_params_from_weights", "adam_update", "sim_update")
+           "sim_params_from_weights", "adam_update", "sim_update", "sim_attn_weights_layout")
 ALGO_PPO, ALGO_REINFORCE = 0, 1
 KERNEL_CLASSES = ("policy", "step", "static", "gae", "reset", "other", "ppo")
 
@@ -43,6 +43,8 @@ class SimCfg(C.Structure):
         ("shadow", C.c_int32), ("static_timeout", C.c_double), ("static_bmax", C.c_int32),
         ("mlp_h1", C.c_int32), ("mlp_h2", C.c_int32), ("mlp_bf16", C.c_int32),
         ("value_head", C.c_int32), ("trace_max_len", C.c_int32), ("static_route", C.c_int32),
+        ("policy_kind", C.c_int32), ("attn_tokens", C.c_int32), ("attn_embed", C.c_int32),
+        ("attn_heads", C.c_int32),
     ]
 
 
@@ -50,6 +52,15 @@ class SimWLayout(C.Structure):
     _fields_ = [("w1", C.c_size_t), ("b1", C.c_size_t), ("w2", C.c_size_t), ("b2", C.c_size_t),
                 ("w3", C.c_size_t), ("b3", C.c_size_t), ("bytes", C.c_size_t),
                 ("n_out", C.c_int32), ("elem_bytes", C.c_int32)]
+
+
+ATTN_KEYS = ("w_in", "b_in", "w_qkv", "b_qkv", "w_o", "b_o", "wp1", "bp1", "wp2", "bp2",
+             "wv1", "bv1", "wv2", "bv2")
+POLICY_MLP, POLICY_ATTN = 0, 1
+
+
+class SimAttnLayout(C.Structure):
+    _fields_ = [(k, C.c_size_t) for k in ATTN_KEYS] + [("bytes", C.c_size_t)]
 
 
 class SimTraj(C.Structure):
@@ -107,6 +118,7 @@ def load():
         "sim_params_from_weights": [vp, vp, vp],
         "adam_update": [vp, vp, vp, vp, vp, i32, C.c_float, C.c_float, C.c_float, C.c_float, vp],
         "sim_update": [vp, vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, vp],
+        "sim_attn_weights_layout": [vp, vp],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -145,4 +157,8 @@ def make_cfg(w, n_envs=None):
     c.mlp_h1 = w["mlp_h1"]; c.mlp_h2 = w["mlp_h2"]; c.mlp_bf16 = w["mlp_bf16"]
     c.value_head = w["value_head"]; c.trace_max_len = w.get("trace_max_len", 0)
     c.static_route = w.get("static_route", 0)
+    c.policy_kind = w.get("policy_kind", POLICY_MLP)
+    c.attn_tokens = w.get("attn_tokens", 0)
+    c.attn_embed = w.get("attn_embed", 0)
+    c.attn_heads = w.get("attn_heads", 0)
     return c

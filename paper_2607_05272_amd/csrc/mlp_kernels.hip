@@ -606,4 +606,20 @@ hipError_t launch_init_weights(int F, int H1, int H2, int Ap, int bf16, uint64_t
   return hipSuccess;
 }
 
+hipError_t launch_init_attn(uint64_t seed, void* d_weights, const size_t off[14], const int fin[7],
+                            const int fout[7], hipStream_t st) {
+  unsigned char* dst = static_cast<unsigned char*>(d_weights);
+  for (int l = 0; l < 7; ++l) {
+    const size_t n = (size_t)fin[l] * fout[l];
+    const double lim = sqrt(6.0 / (double)(fin[l] + fout[l]));
+    hipLaunchKernelGGL(init_w_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, seed, l, n,
+                       lim, 0, dst + off[2 * l]);
+    hipLaunchKernelGGL(zero_f32_k, dim3((fout[l] + 255) / 256), dim3(256), 0, st,
+                       reinterpret_cast<float*>(dst + off[2 * l + 1]), fout[l]);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 }  // namespace bsim

@@ -93,6 +93,22 @@ hipError_t launch_policy(const MlpParams& m, const float* obs, uint64_t seed, ui
 hipError_t launch_init_weights(int F, int H1, int H2, int Ap, int bf16, uint64_t seed,
                                void* d_weights, const size_t off[6], hipStream_t st);
 bool policy_shape_supported(const MlpParams& m);
+
+// The attention policy (attn_kernels.hip): fp32 weights [in][out] inside the caller's
+// buffer; D = 4 embedding, NH heads, L tokens over F features, heads of Hp and Hv units.
+struct AttnParams {
+  int E, F, L, D, NH, Hp, Hv, A, value_head;
+  const float *w_in, *b_in, *w_qkv, *b_qkv, *w_o, *b_o;
+  const float *wp1, *bp1, *wp2, *bp2, *wv1, *bv1, *wv2, *bv2;
+};
+bool attn_shape_supported(const AttnParams& p);
+hipError_t launch_attn_policy(const AttnParams& p, const float* obs, uint64_t seed, uint32_t step,
+                              uint8_t* act, float* logp, float* value, float* logits,
+                              hipStream_t st);
+// Xavier init of the attention policy's seven matrices (layers 0..6) and zero biases;
+// off[14] are the byte offsets of w_in, b_in, ..., wv2, bv2; fin/fout the matrix shapes
+hipError_t launch_init_attn(uint64_t seed, void* d_weights, const size_t off[14], const int fin[7],
+                            const int fout[7], hipStream_t st);
 // PPO minibatch gradient (ppo_kernels.hip); M a multiple of 16, value head required
 hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t off[6], int T,
                       const float* obs, const uint8_t* act, const float* logp_old,

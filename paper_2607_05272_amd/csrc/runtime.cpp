@@ -57,6 +57,7 @@ struct sim_ctx {
   SimParams p{};
   EnvState s{};
   MlpParams m{};
+  AttnParams a{};          // attention policy (policy_kind = SIM_POLICY_ATTN)
   void* arena = nullptr;   // all environment state
   size_t arena_bytes = 0;
   void* wpack = nullptr;   // repacked policy weights
@@ -125,6 +126,18 @@ static int validate(const sim_cfg* c) {
     return fail(SIM_EINVAL, "n_classes must be in 1..%d", SIM_MAX_CLASSES);
   if (c->queue_cap < 1 || c->queue_cap > SIM_MAX_QUEUE)
     return fail(SIM_EINVAL, "queue_cap must be in 1..%d", SIM_MAX_QUEUE);
+  if (c->policy_kind != SIM_POLICY_MLP && c->policy_kind != SIM_POLICY_ATTN)
+    return fail(SIM_EINVAL, "policy_kind");
+  if (c->policy_kind == SIM_POLICY_ATTN) {
+    if (c->attn_tokens < 1 || c->attn_embed < 1 || c->attn_heads < 1)
+      return fail(SIM_EINVAL, "attn_tokens, attn_embed and attn_heads must be >= 1");
+    if (c->obs_dim % c->attn_tokens)
+      return fail(SIM_EINVAL, "attn_tokens must divide obs_dim");
+    if (c->attn_embed % c->attn_heads)
+      return fail(SIM_EINVAL, "attn_heads must divide attn_embed");
+    if (c->mlp_bf16) return fail(SIM_EINVAL, "the attention policy is fp32 (mlp_bf16 = 0)");
+    if (c->mlp_h1 < 1 || c->mlp_h2 < 1) return fail(SIM_EINVAL, "head widths must be >= 1");
+  }
   if (c->obs_dim < obs_width(*c))
     return fail(SIM_EINVAL, "obs_dim %d is below the state width %d", c->obs_dim, obs_width(*c));
   if (!(c->tick_s > 0.0)) return fail(SIM_EINVAL, "tick_s must be > 0");
@@ -230,6 +243,10 @@ static void derive(sim_ctx* x) {
   m.bf16 = c.mlp_bf16; m.value_head = c.value_head;
   m.FP = pad_to(c.obs_dim, c.mlp_bf16 ? 32 : 4);
   m.AP = pad_to(m.Ap, 16);
+
+  AttnParams& a = x->a;
+  a.E = c.n_envs; a.F = c.obs_dim; a.L = c.attn_tokens; a.D = c.attn_embed; a.NH = c.attn_heads;
+  a.Hp = c.mlp_h1; a.Hv = c.mlp_h2; a.A = 6 * c.n_servers; a.value_head = c.value_head;
 }
 
 int sim_create(const sim_cfg* cfg, void* hip_stream, sim_ctx** out) {
@@ -389,8 +406,39 @@ int sim_tick(sim_ctx* x, int32_t* h_tick) {
   return SIM_OK;
 }
 
+int sim_attn_weights_layout(const sim_cfg* c, sim_attn_layout* o) {
+  if (!c || !o) return fail(SIM_EINVAL, "NULL argument");
+  if (c->policy_kind != SIM_POLICY_ATTN) return fail(SIM_EINVAL, "policy_kind is not SIM_POLICY_ATTN");
+  if (c->attn_embed < 1 || c->attn_heads < 1 || c->attn_tokens < 1 || c->obs_dim < 1 ||
+      c->mlp_h1 < 1 || c->mlp_h2 < 1 || c->n_servers < 1)
+    return fail(SIM_EINVAL, "attention dimensions must be positive");
+  const size_t F = c->obs_dim, D = c->attn_embed, Hp = c->mlp_h1, Hv = c->mlp_h2;
+  const size_t A = 6 * (size_t)c->n_servers;
+  size_t off = 0;
+  size_t* dst[14] = {&o->w_in, &o->b_in, &o->w_qkv, &o->b_qkv, &o->w_o, &o->b_o, &o->wp1,
+                     &o->bp1, &o->wp2, &o->bp2, &o->wv1, &o->bv1, &o->wv2, &o->bv2};
+  const size_t n[14] = {F * D, D, D * 3 * D, 3 * D, D * D, D, D * Hp, Hp, Hp * A, A, D * Hv, Hv,
+                        Hv, 1};
+  for (int i = 0; i < 14; ++i) {
+    *dst[i] = off;
+    off += align256(4 * n[i]);
+  }
+  o->bytes = off;
+  return SIM_OK;
+}
+
 int sim_weights_layout(const sim_cfg* c, sim_wlayout* o) {
   if (!c || !o) return fail(SIM_EINVAL, "NULL argument");
+  if (c->policy_kind == SIM_POLICY_ATTN) {
+    sim_attn_layout al;
+    int rc = sim_attn_weights_layout(c, &al);
+    if (rc) return rc;
+    o->w1 = o->b1 = o->w2 = o->b2 = o->w3 = o->b3 = 0;
+    o->bytes = al.bytes;
+    o->n_out = 6 * c->n_servers + (c->value_head ? 1 : 0);
+    o->elem_bytes = 4;
+    return SIM_OK;
+  }
   if (c->mlp_h1 < 1 || c->mlp_h2 < 1 || c->obs_dim < 1 || c->n_servers < 1)
     return fail(SIM_EINVAL, "MLP dimensions must be positive");
   const size_t eb = c->mlp_bf16 ? 2 : 4;
@@ -415,8 +463,27 @@ static void offsets(const sim_cfg& c, size_t off[6]) {
   off[0] = L.w1; off[1] = L.b1; off[2] = L.w2; off[3] = L.b2; off[4] = L.w3; off[5] = L.b3;
 }
 
+static void attn_offsets(const sim_cfg& c, size_t off[14]) {
+  sim_attn_layout L;
+  sim_attn_weights_layout(&c, &L);
+  const size_t v[14] = {L.w_in, L.b_in, L.w_qkv, L.b_qkv, L.w_o, L.b_o, L.wp1,
+                        L.bp1, L.wp2, L.bp2, L.wv1, L.bv1, L.wv2, L.bv2};
+  for (int i = 0; i < 14; ++i) off[i] = v[i];
+}
+
 int sim_init_weights(sim_ctx* x, uint64_t seed, void* d_weights) {
   if (!x || !d_weights) return fail(SIM_EINVAL, "NULL argument");
+  if (x->cfg.policy_kind == SIM_POLICY_ATTN) {
+    size_t off[14];
+    attn_offsets(x->cfg, off);
+    const int F = x->cfg.obs_dim, D = x->cfg.attn_embed, Hp = x->cfg.mlp_h1, Hv = x->cfg.mlp_h2;
+    const int A = 6 * x->cfg.n_servers;
+    const int fin[7] = {F, D, D, D, Hp, D, Hv}, fout[7] = {D, 3 * D, D, Hp, A, Hv, 1};
+    HIPCHK(x->timed(SIM_KC_OTHER, [&] {
+             return launch_init_attn(seed, d_weights, off, fin, fout, x->stream);
+           }), "attention weight init launch");
+    return SIM_OK;
+  }
   size_t off[6];
   offsets(x->cfg, off);
   HIPCHK(x->timed(SIM_KC_OTHER, [&] {
@@ -439,11 +506,33 @@ static int repack_weights(sim_ctx* x, const void* d_weights) {
 }
 
 static int prepare_policy(sim_ctx* x, const void* d_weights) {
+  if (x->cfg.policy_kind == SIM_POLICY_ATTN) {
+    AttnParams& a = x->a;
+    if (!attn_shape_supported(a))
+      return fail(SIM_EUNSUPPORTED,
+                  "attention shape (tokens=%d, embed=%d, heads=%d, actions=%d) is not compiled",
+                  a.L, a.D, a.NH, a.A);
+    size_t off[14];
+    attn_offsets(x->cfg, off);
+    const float* b = static_cast<const float*>(d_weights);
+    const float** dst[14] = {&a.w_in, &a.b_in, &a.w_qkv, &a.b_qkv, &a.w_o, &a.b_o, &a.wp1,
+                             &a.bp1, &a.wp2, &a.bp2, &a.wv1, &a.bv1, &a.wv2, &a.bv2};
+    for (int i = 0; i < 14; ++i) *dst[i] = b + off[i] / 4;
+    return SIM_OK;
+  }
   if (!policy_shape_supported(x->m))
     return fail(SIM_EUNSUPPORTED,
                 "policy shape (bf16=%d, F_pad=%d, H1=%d, H2=%d, A_pad=%d) is not compiled",
                 x->m.bf16, x->m.FP, x->m.H1, x->m.H2, x->m.AP);
   return repack_weights(x, d_weights);
+}
+
+// the policy kernel of the configured network (after prepare_policy)
+static hipError_t policy_launch(sim_ctx* x, const float* obs, uint32_t step, uint8_t* act,
+                                float* logp, float* value, float* logits) {
+  if (x->cfg.policy_kind == SIM_POLICY_ATTN)
+    return launch_attn_policy(x->a, obs, x->seed, step, act, logp, value, logits, x->stream);
+  return launch_policy(x->m, obs, x->seed, step, act, logp, value, logits, x->stream);
 }
 
 int sim_policy(sim_ctx* x, const void* d_weights, const float* d_obs, uint32_t step,
@@ -453,8 +542,7 @@ int sim_policy(sim_ctx* x, const void* d_weights, const float* d_obs, uint32_t s
   int rc = prepare_policy(x, d_weights);
   if (rc) return rc;
   HIPCHK(x->timed(SIM_KC_POLICY, [&] {
-           return launch_policy(x->m, d_obs, x->seed, step, d_act, d_logp, d_value, d_logits,
-                                x->stream);
+           return policy_launch(x, d_obs, step, d_act, d_logp, d_value, d_logits);
          }), "policy kernel launch");
   return SIM_OK;
 }
@@ -476,9 +564,9 @@ int sim_rollout(sim_ctx* x, const void* d_weights, int32_t T, const sim_traj* tr
   for (int32_t k = 0; k < T; ++k) {
     const size_t row = (size_t)k * E;
     HIPCHK(x->timed(SIM_KC_POLICY, [&] {
-             return launch_policy(x->m, x->s.obs, x->seed, x->tick, tr->actions + row,
+             return policy_launch(x, x->s.obs, x->tick, tr->actions + row,
                                   tr->logp ? tr->logp + row : nullptr,
-                                  tr->value ? tr->value + row : nullptr, nullptr, x->stream);
+                                  tr->value ? tr->value + row : nullptr, nullptr);
            }), "policy kernel launch");
     rc = enqueue_tick(x, tr->actions + row, tr->obs ? tr->obs + (size_t)(k + 1) * F * E : nullptr,
                       tr->reward ? tr->reward + row : nullptr,
@@ -489,8 +577,8 @@ int sim_rollout(sim_ctx* x, const void* d_weights, int32_t T, const sim_traj* tr
   }
   if (tr->value)
     HIPCHK(x->timed(SIM_KC_POLICY, [&] {
-             return launch_policy(x->m, x->s.obs, x->seed, x->tick, nullptr, nullptr,
-                                  tr->value + (size_t)T * E, nullptr, x->stream);
+             return policy_launch(x, x->s.obs, x->tick, nullptr, nullptr,
+                                  tr->value + (size_t)T * E, nullptr);
            }), "policy kernel launch (final value)");
   return SIM_OK;
 }
@@ -522,6 +610,8 @@ static int pg_grad(sim_ctx* x, int reinforce, const void* d_weights, int32_t T, 
   if (!x || !d_weights || !d_obs || !d_actions || (!reinforce && !d_logp_old) || !d_adv ||
       !d_ret || !d_grads || !d_loss)
     return fail(SIM_EINVAL, "%s: NULL argument", who);
+  if (x->cfg.policy_kind != SIM_POLICY_MLP)
+    return fail(SIM_EUNSUPPORTED, "%s: built for the MLP policy only", who);
   if (!x->cfg.value_head) return fail(SIM_EUNSUPPORTED, "%s needs value_head = 1", who);
   if (T < 1) return fail(SIM_EINVAL, "T must be >= 1");
   if (M < 16 || M % 16) return fail(SIM_EINVAL, "M = %d must be a positive multiple of 16", M);
@@ -573,6 +663,8 @@ int reinforce_minibatch_grad(sim_ctx* x, const void* d_weights, int32_t T, const
 
 int sim_params_from_weights(sim_ctx* x, const void* d_weights, float* d_params) {
   if (!x || !d_weights || !d_params) return fail(SIM_EINVAL, "NULL argument");
+  if (x->cfg.policy_kind != SIM_POLICY_MLP)
+    return fail(SIM_EUNSUPPORTED, "sim_params_from_weights: built for the MLP policy only");
   size_t off[6];
   offsets(x->cfg, off);
   HIPCHK(x->timed(SIM_KC_OTHER, [&] {
@@ -614,6 +706,8 @@ int sim_update(sim_ctx* x, const sim_update_cfg* u, void* d_weights, float* d_pa
   if (u->algo != SIM_ALGO_PPO && u->algo != SIM_ALGO_REINFORCE)
     return fail(SIM_EINVAL, "unknown algorithm %d", u->algo);
   if (u->epochs < 1 || u->minibatches < 1) return fail(SIM_EINVAL, "epochs and minibatches >= 1");
+  if (x->cfg.policy_kind != SIM_POLICY_MLP)
+    return fail(SIM_EUNSUPPORTED, "sim_update: built for the MLP policy only");
   int64_t n = 0;
   sim_ppo_grad_count(&x->cfg, &n);
   if (!x->grads) {

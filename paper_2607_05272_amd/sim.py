@@ -26,13 +26,44 @@ def weights_layout(w):
                 bytes=lay.bytes, n_out=lay.n_out, elem_bytes=lay.elem_bytes)
 
 
+def attn_layout(w):
+    """Byte offsets of the attention policy's weights (sim_attn_weights_layout) and their
+    shapes ([in][out] matrices, vectors)."""
+    lib = L.load()
+    cfg = L.make_cfg(w, n_envs=max(1, w.get("n_envs", 1)))
+    lay = L.SimAttnLayout()
+    L.check(lib.sim_attn_weights_layout(C.byref(cfg), C.byref(lay)), "sim_attn_weights_layout")
+    F, D, A = w["obs_dim"], w["attn_embed"], 6 * w["n_servers"]
+    Hp, Hv = w["mlp_h1"], w["mlp_h2"]
+    shapes = dict(w_in=(F, D), b_in=(D,), w_qkv=(D, 3 * D), b_qkv=(3 * D,), w_o=(D, D),
+                  b_o=(D,), wp1=(D, Hp), bp1=(Hp,), wp2=(Hp, A), bp2=(A,), wv1=(D, Hv),
+                  bv1=(Hv,), wv2=(Hv, 1), bv2=(1,))
+    return {k: getattr(lay, k) for k in L.ATTN_KEYS}, shapes, lay.bytes
+
+
+def _is_attn(w):
+    return w.get("policy_kind", L.POLICY_MLP) == L.POLICY_ATTN
+
+
 def _dims(w, n_out):
     return [w["obs_dim"], w["mlp_h1"], w["mlp_h2"], n_out]
 
 
 def pack_weights(w, arrays):
     """Host bytes of the ABI weight buffer from arrays w1,b1,w2,b2,w3,b3 ([in][out]).
-    Matrices must hold fp32 values (bf16-representable ones in bf16 mode)."""
+    Matrices must hold fp32 values (bf16-representable ones in bf16 mode). For the attention
+    policy: the fp32 arrays named by sim_attn_weights_layout."""
+    if _is_attn(w):
+        off, shapes, nbytes = attn_layout(w)
+        buf = np.zeros(nbytes, np.uint8)
+        for k in L.ATTN_KEYS:
+            a = np.ascontiguousarray(arrays[k], dtype=np.float64).reshape(shapes[k])
+            f32 = a.astype(np.float32)
+            if not np.array_equal(f32.astype(np.float64), a):
+                raise ValueError(f"{k} is not fp32-representable")
+            raw = f32.tobytes()
+            buf[off[k]:off[k] + len(raw)] = np.frombuffer(raw, np.uint8)
+        return buf
     lay = weights_layout(w)
     buf = np.zeros(lay["bytes"], np.uint8)
     dims = _dims(w, lay["n_out"])
@@ -58,6 +89,15 @@ def pack_weights(w, arrays):
 
 def unpack_weights(w, buf):
     """fp64 arrays of the values held in an ABI weight buffer (host bytes)."""
+    if _is_attn(w):
+        off, shapes, _ = attn_layout(w)
+        buf = np.asarray(buf, dtype=np.uint8)
+        out = {}
+        for k in L.ATTN_KEYS:
+            n = int(np.prod(shapes[k]))
+            out[k] = np.frombuffer(buf[off[k]:off[k] + 4 * n].tobytes(),
+                                   np.float32).astype(np.float64).reshape(shapes[k])
+        return out
     lay = weights_layout(w)
     buf = np.asarray(buf, dtype=np.uint8)
     dims = _dims(w, lay["n_out"])

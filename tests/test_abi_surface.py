@@ -33,8 +33,8 @@ def test_library_exports_every_declared_symbol():
 
 def test_struct_sizes_match_header_layout():
     # sizes implied by the header's field list on x86-64 (natural alignment)
-    # 456 by the header's field list; sim_create also rejects a struct_size mismatch
-    assert C.sizeof(_lib.SimCfg) == 456
+    # 472 by the header's field list; sim_create also rejects a struct_size mismatch
+    assert C.sizeof(_lib.SimCfg) == 472
     assert C.sizeof(_lib.SimTraj) == 7 * 8
     assert C.sizeof(_lib.SimWLayout) == 7 * 8 + 8
     assert C.sizeof(_lib.SimUpdateCfg) == 4 * 4 + 8 + 7 * 4 + 4  # padded to 8

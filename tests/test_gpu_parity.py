@@ -8,7 +8,7 @@ import sys
 import numpy as np
 import pytest
 
-from workloads import preset, trace_preset, burst_preset, baseline_preset
+from workloads import preset, trace_preset, burst_preset, baseline_preset, attn_preset
 from workloads.gen import seeded_actions, seeded_obs, seeded_rewards_values
 
 torch = pytest.importorskip("torch")
@@ -17,6 +17,20 @@ pytestmark = pytest.mark.gpu
 GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "hand_traces.json")))
 NAMES = ["C1", "C2", "C3", "C4", "C5"]
 RTOL = 1e-9
+# the attention policy of Sec. 4.2 in the variants the kernel is built for
+ATTN = {
+    "attn": dict(),                                        # 8 tokens, 2 heads, 6 actions
+    "attn_L1": dict(attn_tokens=1),                        # the plain input projection
+    "attn_L4_H4": dict(attn_tokens=4, attn_heads=4),
+    "attn_L2_H1": dict(attn_tokens=2, attn_heads=1),
+    "attn_K4": dict(n_servers=4, obs_dim=2 + 16 + 6, n_classes=1, attn_tokens=8),
+}
+
+
+def workload(name, **kw):
+    if name in ATTN:
+        return attn_preset(**dict(ATTN[name], **kw))
+    return preset(name, **kw)
 
 
 def say(*a):
@@ -234,15 +248,16 @@ def test_hand_traces_on_gpu(bs, orc, tr):
     sim.close()
 
 
-@pytest.mark.parametrize("name", NAMES)
+@pytest.mark.parametrize("name", NAMES + ["attn", "attn_K4"])
 def test_init_weights_bit_identical(bs, orc, name):
-    w = preset(name)
+    w = workload(name)
     sim = bs.Sim(w, n_envs=64)
     buf = sim.init_weights(1234)
     torch.cuda.synchronize()
     got = bs.unpack_weights(w, buf.cpu().numpy())
     ref = orc.init_weights(w, 1234)
-    for k in ("w1", "b1", "w2", "b2", "w3", "b3"):
+    assert set(got) == set(ref)
+    for k in ref:
         assert np.array_equal(got[k], ref[k]), k
     sim.close()
 
@@ -275,11 +290,88 @@ def mlp_tol(w, wts, obs):
     return scale * 2.0 ** -6 + gelu_term[None, :]
 
 
+def attn_tol(w, W, obs):
+    """Per-output tolerance of the fp32 attention kernel against the fp64 oracle, from a
+    forward error analysis in fp64 over the exact intermediates (u = 2^-24):
+    * a fp32 dot product with fma over n terms plus a bias is off by at most (n + 1) u times
+      the sum of its terms' magnitudes (local rounding), and an input error e propagates
+      as |W|^T e;
+    * a score error ds changes the softmax weights by at most 2 max|ds| in L1 (exp, sum and
+      the division add (L + 2) u), so the weighted values move by that times max|v| plus the
+      weights' average of the values' errors;
+    * the mean pool adds L u of the mean magnitude; GELU has slope at most 1.13 and erff is
+      good to a few ulps (8 u |z|).
+    The tolerance is four times the bound (margin for the first-order treatment)."""
+    u = 2.0 ** -24
+    x = np.asarray(obs, np.float64)
+    n, F = x.shape
+    L, D, NH = w["attn_tokens"], w["attn_embed"], w["attn_heads"]
+    G, dh = F // L, D // NH
+    Wa = {k: np.abs(v) for k, v in W.items()}
+
+    def lin(inp, err, k_w, k_b):
+        """value, error of inp @ W + b given inp's error."""
+        val = inp @ W[k_w] + W[k_b]
+        nt = W[k_w].shape[0]
+        e = err @ Wa[k_w] + (nt + 1) * u * (np.abs(inp) @ Wa[k_w] + Wa[k_b])
+        return val, e
+
+    xt = x.reshape(n, L, G)
+    win = W["w_in"].reshape(L, G, D)
+    tok = np.einsum("nlg,lgd->nld", xt, win) + W["b_in"]
+    e_tok = (G + 1) * u * (np.einsum("nlg,lgd->nld", np.abs(xt), np.abs(win)) + Wa["b_in"])
+    qkv, e_qkv = lin(tok, e_tok, "w_qkv", "b_qkv")
+    q, k, v = qkv[..., :D], qkv[..., D:2 * D], qkv[..., 2 * D:]
+    eq, ek, ev = e_qkv[..., :D], e_qkv[..., D:2 * D], e_qkv[..., 2 * D:]
+    o = np.zeros((n, L, D))
+    eo = np.zeros((n, L, D))
+    for h in range(NH):
+        c = slice(h * dh, (h + 1) * dh)
+        sc = np.einsum("ngt,njt->ngj", q[..., c], k[..., c]) / np.sqrt(dh)
+        esc = (np.einsum("ngt,njt->ngj", eq[..., c], np.abs(k[..., c])) +
+               np.einsum("ngt,njt->ngj", np.abs(q[..., c]), ek[..., c]) +
+               (dh + 1) * u * np.einsum("ngt,njt->ngj", np.abs(q[..., c]), np.abs(k[..., c])))
+        esc = esc / np.sqrt(dh)
+        a = np.exp(sc - sc.max(axis=2, keepdims=True))
+        a = a / a.sum(axis=2, keepdims=True)
+        ea = 2.0 * esc.max(axis=2) + (L + 2) * u                        # [n][g], L1 over j
+        vmax = np.abs(v[..., c]).max(axis=1)                            # [n][t]
+        o[..., c] = np.einsum("ngj,njt->ngt", a, v[..., c])
+        eo[..., c] = (ea[..., None] * vmax[:, None, :] + np.einsum("ngj,njt->ngt", a, ev[..., c])
+                      + L * u * np.einsum("ngj,njt->ngt", a, np.abs(v[..., c])))
+    y, ey = lin(o, eo, "w_o", "b_o")
+    p = y.mean(axis=1)
+    ep = ey.mean(axis=1) + L * u * np.abs(y).mean(axis=1)
+
+    def head(k1, b1, k2, b2):
+        z, ez = lin(p, ep, k1, b1)
+        hz = 0.5 * z * (1.0 + np.vectorize(__import__("math").erf)(z / np.sqrt(2.0)))
+        eh = 1.13 * ez + 8 * u * np.abs(z)
+        return lin(hz, eh, k2, b2)[1]
+
+    cols = [head("wp1", "bp1", "wp2", "bp2")]
+    if w["value_head"]:
+        cols.append(head("wv1", "bv1", "wv2", "bv2"))
+    return 4.0 * np.concatenate(cols, axis=1)
+
+
+def attn_weights(orc, w, seed):
+    """Random fp32 weights of the attention policy with nonzero biases (Xavier-initialised
+    weights have zero biases, which would leave the bias terms untested)."""
+    rng = np.random.default_rng(seed)
+    out = {}
+    for k, sh in orc.attn_shapes(w).items():
+        sc = 0.6 if k.startswith("w") else 0.2
+        out[k] = (rng.standard_normal(sh) * sc).astype(np.float32).astype(np.float64)
+    return out
+
+
 def check_policy(bs, orc, w, E, ids, step=17, seed=0x5EED):
     """Policy on E seeded observations through the C ABI; the oracle evaluates rows `ids`.
     MLP logits/value within the derived tolerance; sampled actions identical wherever the
     oracle's uniform is farther than 2*max|dlogit| from a CDF boundary; logp close."""
-    wts = orc.init_weights(w, 99)
+    attn = w.get("policy_kind", 0) == 1
+    wts = attn_weights(orc, w, 99) if attn else orc.init_weights(w, 99)
     obs = seeded_obs(21, E, w["obs_dim"])
     sim = bs.Sim(w, n_envs=E)
     sim.reset(seed)
@@ -290,7 +382,7 @@ def check_policy(bs, orc, w, E, ids, step=17, seed=0x5EED):
     act = out["actions"].cpu().numpy()[ids]
     logp = out["logp"].cpu().numpy().astype(np.float64)[ids]
     ref = orc.policy(w, wts, seed, step, obs[ids], ids)
-    tol = mlp_tol(w, wts, obs[ids])
+    tol = (attn_tol if attn else mlp_tol)(w, wts, obs[ids])
     err = np.abs(lg - ref["logits"])
     assert np.all(err <= tol), f"max err/tol {np.max(err / tol):.3g}"
     A = 6 * w["n_servers"]
@@ -324,6 +416,31 @@ def test_policy_parity_large_batch(bs, orc, name):
     check_policy(bs, orc, preset(name), E, ids)
 
 
+@pytest.mark.parametrize("name", sorted(ATTN))
+def test_attention_policy_parity(bs, orc, name):
+    """The attention policy kernel on 1000 seeded observations (several workgroups and a
+    ragged last one) and, for the paper's shape, on 64 * 512 + 77 with sampled rows."""
+    say(f"[attn policy] {name}")
+    check_policy(bs, orc, workload(name), 1000, np.arange(1000))
+    if name == "attn":
+        E = 64 * 512 + 77
+        rng = np.random.default_rng(8)
+        ids = np.unique(np.concatenate([np.arange(64), np.arange(E - 100, E),
+                                        rng.integers(0, E, 256)])).astype(np.int64)
+        check_policy(bs, orc, workload(name), E, ids)
+
+
+def test_attention_update_is_refused(bs):
+    """The update entry points are built for the MLP policy: the attention policy gets a
+    clear SIM_EUNSUPPORTED instead of a wrong gradient."""
+    w = workload("attn")
+    sim = bs.Sim(w, n_envs=64)
+    wb = sim.init_weights(1)
+    with pytest.raises(bs.SimError, match="MLP policy only"):
+        sim.params_from_weights(wb)
+    sim.close()
+
+
 @pytest.mark.parametrize("name", ["C1", "C3", "C5"])
 def test_gae_bit_exact(bs, orc, name):
     w = preset(name)
@@ -341,7 +458,7 @@ def test_gae_bit_exact(bs, orc, name):
     sim.close()
 
 
-@pytest.mark.parametrize("name", NAMES)
+@pytest.mark.parametrize("name", NAMES + ["attn", "attn_K4"])
 def test_rollout_parity_and_validity(bs, orc, name):
     """sim_rollout (policy + sampler + simulator, T ticks) checked three ways:
     (1) the oracle's own policy rollout with the same weights agrees exactly, per env, on
@@ -351,8 +468,8 @@ def test_rollout_parity_and_validity(bs, orc, name):
         the same running checksums, rewards and observations at every tick;
     (3) validity of every decision: on the rollout's observations the oracle policy picks
         the same action wherever its uniform is outside the tie band."""
-    w = preset(name)
-    E, T, seed = 300, 100, 0xC0FFEE + 10 + NAMES.index(name)
+    w = workload(name)
+    E, T, seed = 300, 100, 0xC0FFEE + 10 + (NAMES + ["attn", "attn_K4"]).index(name)
     A = 6 * w["n_servers"]
     wts = orc.init_weights(w, 7)
     say(f"[rollout] {name}")
