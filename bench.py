@@ -38,12 +38,15 @@ DESCR = {
     "C3-random": "C3 with a static shadow routing each batch to a uniformly random idle server",
     "C3-round_robin": "C3 with a static shadow routing batches round-robin over the idle servers",
     "C5-random": "C5 with the static shadow routing each batch to a uniformly random idle server",
+    "attn": "attention policy (Sec. 4.2): 262144 envs x 1000 ticks, C1's system (1 server, Poisson 500/s, DET 5ms+0.5ms*b), 8 features as 8 tokens, 8->4 projection, 2-head self-attention, mean pool, GELU heads of 64 (policy) and 64 (value), fp32, REINFORCE with baseline returns",
 }
 
 
 def workload_of(name):
     """The workload dict of a bench configuration name."""
-    from workloads import preset, burst_preset, baseline_preset
+    from workloads import preset, burst_preset, baseline_preset, attn_preset
+    if name == "attn":
+        return attn_preset(n_envs=262144, T=1000)
     if name == "burst":
         return burst_preset(n_envs=65536, T=1000)
     if "-" in name:
@@ -55,6 +58,17 @@ def workload_of(name):
 def mlp_flops(w):
     A1 = 6 * w["n_servers"] + (1 if w["value_head"] else 0)
     return 2 * (w["obs_dim"] * w["mlp_h1"] + w["mlp_h1"] * w["mlp_h2"] + w["mlp_h2"] * A1)
+
+
+def attn_flops(w):
+    """Multiply-adds (x2) of one attention-policy forward (Sec. 4.2): tokens, q/k/v,
+    scores and weighted values per head, output projection, both heads."""
+    F, L, D, NH = w["obs_dim"], w["attn_tokens"], w["attn_embed"], w["attn_heads"]
+    A, Hp, Hv = 6 * w["n_servers"], w["mlp_h1"], w["mlp_h2"]
+    dh = D // NH
+    mac = (F * D + L * D * 3 * D + 2 * NH * L * L * dh + L * D * D + D * Hp + Hp * A
+           + (D * Hv + Hv if w["value_head"] else 0))
+    return 2 * mac
 
 
 def ppo_flops(w):
@@ -199,7 +213,8 @@ def cpu_baseline(w, name, budget_s, seed):
         t.join()
     dt = time.perf_counter() - t0
     return {"value": n_env * T / dt, "unit": "env-steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n_env} envs (evenly spaced ids) x {T} ticks of {name}, fp64 policy MLP + "
+            "sample": f"{n_env} envs (evenly spaced ids) x {T} ticks of {name}, fp64 "
+                      f"{'attention policy' if w.get('policy_kind', 0) == 1 else 'policy MLP'} + "
                       f"sampler + simulator, {dt:.1f} s wall on {threads} threads"}
 
 
@@ -312,7 +327,13 @@ def main():
                        "avg_us": 1000.0 * ms / n}
     # roofline of each hot kernel class
     rl = {}
-    if "policy" in kern:
+    if "policy" in kern and w.get("policy_kind", 0) == 1:
+        fl = attn_flops(w) * E
+        ach = fl / (kern["policy"]["avg_us"] * 1e-6) / 1e12
+        rl["policy"] = {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS,
+                        "unit": "TFLOP/s", "frac": ach / PEAK_FP32_VALU_TFLOPS,
+                        "traffic": traffic_for("policy", args.config), "work_per_launch": fl}
+    elif "policy" in kern:
         fl = mlp_flops(w) * E
         ach = fl / (kern["policy"]["avg_us"] * 1e-6) / 1e12
         peak = PEAK_BF16_TFLOPS if w["mlp_bf16"] else PEAK_FP32_TFLOPS

@@ -28,6 +28,8 @@ __device__ __forceinline__ float gelu_exact(float x) {
   return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
 }
 
+// Scores are kept in base-2 units: the queries carry the factor log2(e) / sqrt(D/NH), so each
+// softmax weight is one exp2 of (score - max).
 template <int L, int NH, int A>
 __global__ __launch_bounds__(kBlock) void attn_policy_k(AttnParams p, const float* __restrict__ obs,
                                                         uint64_t seed, uint32_t step,
@@ -36,7 +38,8 @@ __global__ __launch_bounds__(kBlock) void attn_policy_k(AttnParams p, const floa
                                                         float* __restrict__ value,
                                                         float* __restrict__ logits) {
   constexpr int DH = kD / NH;
-  const float scale = DH == 1 ? 1.0f : DH == 2 ? 0.70710678118654752f : 0.5f;
+  constexpr float kLog2e = 1.4426950408889634f;
+  const float qscale = (DH == 1 ? 1.0f : DH == 2 ? 0.70710678118654752f : 0.5f) * kLog2e;
   const int e = blockIdx.x * kBlock + threadIdx.x;
   if (e >= p.E) return;
   const size_t E = (size_t)p.E;
@@ -67,7 +70,7 @@ __global__ __launch_bounds__(kBlock) void attn_policy_k(AttnParams p, const floa
         ak = fmaf(tok[g][i], p.w_qkv[i * 3 * kD + kD + d], ak);
         av = fmaf(tok[g][i], p.w_qkv[i * 3 * kD + 2 * kD + d], av);
       }
-      q[g][d] = aq;
+      q[g][d] = aq * qscale;
       k[g][d] = ak;
       v[g][d] = av;
     }
@@ -86,16 +89,16 @@ __global__ __launch_bounds__(kBlock) void attn_policy_k(AttnParams p, const floa
         float dot = 0.f;
 #pragma unroll
         for (int t = h * DH; t < (h + 1) * DH; ++t) dot = fmaf(q[g][t], k[j][t], dot);
-        sc[j] = dot * scale;
+        sc[j] = dot;
         mx = fmaxf(mx, sc[j]);
       }
       float S = 0.f;
 #pragma unroll
       for (int j = 0; j < L; ++j) {
-        sc[j] = expf(sc[j] - mx);
+        sc[j] = __builtin_amdgcn_exp2f(sc[j] - mx);
         S += sc[j];
       }
-      const float inv = 1.0f / S;
+      const float inv = __builtin_amdgcn_rcpf(S);
 #pragma unroll
       for (int t = h * DH; t < (h + 1) * DH; ++t) {
         float acc = 0.f;
@@ -119,6 +122,8 @@ __global__ __launch_bounds__(kBlock) void attn_policy_k(AttnParams p, const floa
   float lg[A];
 #pragma unroll
   for (int a = 0; a < A; ++a) lg[a] = p.bp2[a];
+  // unrolled so that the scalar weight loads of several units are in flight together
+#pragma unroll 8
   for (int j = 0; j < p.Hp; ++j) {
     float z = p.bp1[j];
 #pragma unroll
@@ -132,6 +137,7 @@ __global__ __launch_bounds__(kBlock) void attn_policy_k(AttnParams p, const floa
   float V = 0.f;
   if (p.value_head) {
     V = p.bv2[0];
+#pragma unroll 8
     for (int j = 0; j < p.Hv; ++j) {
       float z = p.bv1[j];
 #pragma unroll
