@@ -95,14 +95,18 @@ def step_bytes(w, tot, E, T):
     return fixed + var
 
 
-def static_bytes(w, tot, E, T):
-    """Same for the static shadow kernel (no action, observation or rates)."""
+def static_bytes(w, tot, E, T, ticks_per_launch):
+    """Algorithmic HBM bytes per environment of one launch of the static shadow kernel,
+    which runs `ticks_per_launch` ticks with the state in registers: the state read and
+    written once (queues, counters, arrival process, servers), then per tick the reward and
+    the ring entries of accepted arrivals and dispatched requests, and per dispatch the
+    server's meta word and busy time."""
     K, C = w["n_servers"], w["n_classes"]
     state_rw = 4 + 4 + 8 * C + 4 * 6 + 16 + 8 + 4 + 8 + 8
-    fixed = 2 * state_rw + 12 * K + 8
     n = E * T
     c = tot["cnt"][1]
-    return fixed + 8.0 * (c[1] + c[3]) / n + 16.0 * c[4] / n
+    per_tick = 8 + 8.0 * (c[1] + c[3]) / n + 12.0 * c[4] / n
+    return 2 * state_rw + 12 * K + ticks_per_launch * per_tick
 
 
 def kernel_hash():
@@ -347,7 +351,7 @@ def main():
                       "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("step", args.config),
                       "work_per_launch": by}
     if "static" in kern:
-        by = static_bytes(w, tot, E, T) * E
+        by = static_bytes(w, tot, E, T, T / kern["static"]["launches_per_step"]) * E
         ach = by / (kern["static"]["avg_us"] * 1e-6) / 1e9
         rl["static"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("static", args.config),

@@ -64,8 +64,9 @@ hipError_t launch_reset(const SimParams& p, const EnvState& s, uint64_t seed, hi
 hipError_t launch_step(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
                        const uint8_t* act, float* obs_out, double* rew, uint64_t* rchk,
                        hipStream_t st);
+// ticks k .. k + nt - 1 of the static shadow system; rew_sh [nt][E] or NULL
 hipError_t launch_static(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
-                         double* rew_sh, hipStream_t st);
+                         int nt, double* rew_sh, hipStream_t st);
 hipError_t launch_counters(const SimParams& p, const EnvState& s, int64_t* cnt, double* sums,
                            hipStream_t st);
 hipError_t launch_totals(const SimParams& p, const EnvState& s, int64_t* d_tot_cnt,

@@ -377,15 +377,31 @@ int sim_obs(sim_ctx* x, float* d_obs) {
   return SIM_OK;
 }
 
+// the learned system's tick and, if `shadow`, the static system's
 static int enqueue_tick(sim_ctx* x, const uint8_t* act, float* obs_out, double* rew,
-                        double* rew_sh, uint64_t* rchk) {
+                        double* rew_sh, uint64_t* rchk, bool shadow) {
   HIPCHK(x->timed(SIM_KC_STEP, [&] {
            return launch_step(x->p, x->s, x->seed, x->tick, act, obs_out, rew, rchk, x->stream);
          }), "step kernel launch");
-  if (x->cfg.shadow)
+  if (shadow && x->cfg.shadow)
     HIPCHK(x->timed(SIM_KC_STATIC, [&] {
-             return launch_static(x->p, x->s, x->seed, x->tick, rew_sh, x->stream);
+             return launch_static(x->p, x->s, x->seed, x->tick, 1, rew_sh, x->stream);
            }), "static kernel launch");
+  return SIM_OK;
+}
+
+// The static shadow system over ticks k0 .. k0 + T - 1 in launches of kStaticChunk ticks
+// (it does not depend on the learned system, so its ticks need not interleave with it).
+constexpr int32_t kStaticChunk = 256;
+static int run_static(sim_ctx* x, uint32_t k0, int32_t T, double* rew_sh) {
+  const size_t E = (size_t)x->cfg.n_envs;
+  for (int32_t c = 0; c < T; c += kStaticChunk) {
+    const int nt = T - c < kStaticChunk ? T - c : kStaticChunk;
+    HIPCHK(x->timed(SIM_KC_STATIC, [&] {
+             return launch_static(x->p, x->s, x->seed, k0 + (uint32_t)c, nt,
+                                  rew_sh ? rew_sh + (size_t)c * E : nullptr, x->stream);
+           }), "static kernel launch");
+  }
   return SIM_OK;
 }
 
@@ -394,7 +410,7 @@ int sim_step(sim_ctx* x, const uint8_t* d_actions, float* d_obs_next, double* d_
   if (!x || !d_actions) return fail(SIM_EINVAL, "NULL argument");
   if (!x->reset_done) return fail(SIM_ESTATE, "sim_step before sim_reset");
   if (x->tick == 0xFFFFFFFEu) return fail(SIM_ESTATE, "tick counter exhausted");
-  int rc = enqueue_tick(x, d_actions, d_obs_next, d_reward, d_reward_shadow, nullptr);
+  int rc = enqueue_tick(x, d_actions, d_obs_next, d_reward, d_reward_shadow, nullptr, true);
   if (rc) return rc;
   x->tick++;
   return SIM_OK;
@@ -561,6 +577,10 @@ int sim_rollout(sim_ctx* x, const void* d_weights, int32_t T, const sim_traj* tr
   if (tr->obs)
     HIPCHK(hipMemcpyAsync(tr->obs, x->s.obs, 4 * F * E, hipMemcpyDeviceToDevice, x->stream),
            "hipMemcpyAsync obs_0");
+  if (x->cfg.shadow) {
+    rc = run_static(x, x->tick, T, tr->reward_shadow);
+    if (rc) return rc;
+  }
   for (int32_t k = 0; k < T; ++k) {
     const size_t row = (size_t)k * E;
     HIPCHK(x->timed(SIM_KC_POLICY, [&] {
@@ -569,9 +589,8 @@ int sim_rollout(sim_ctx* x, const void* d_weights, int32_t T, const sim_traj* tr
                                   tr->value ? tr->value + row : nullptr, nullptr);
            }), "policy kernel launch");
     rc = enqueue_tick(x, tr->actions + row, tr->obs ? tr->obs + (size_t)(k + 1) * F * E : nullptr,
-                      tr->reward ? tr->reward + row : nullptr,
-                      tr->reward_shadow ? tr->reward_shadow + row : nullptr,
-                      tr->rchk ? tr->rchk + row : nullptr);
+                      tr->reward ? tr->reward + row : nullptr, nullptr,
+                      tr->rchk ? tr->rchk + row : nullptr, false);
     if (rc) return rc;
     x->tick++;
   }

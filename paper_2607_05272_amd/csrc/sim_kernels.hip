@@ -673,37 +673,26 @@ __device__ __forceinline__ int route_pick(uint32_t idle, int route, uint32_t rr,
   return __builtin_ctz(idle);
 }
 
+// One tick [t_k, t_{k+1}) of the static system of one environment whose state is held in
+// registers: arrivals, the static rule's dispatches to the routed server, completions, and
+// the tick's reward (into rew_row[e] when given). A dispatch stores its server's meta word at
+// once; a completion clears the in-flight byte only in registers and marks the server in
+// `clear`, and `dirty` marks servers whose busy-until time changed; the caller writes both
+// back. Lanes without an environment (live = false) take part in the wave's ballots only.
 template <int KM, int CM>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void static_k(SimParams p, EnvState g, uint64_t seed, uint32_t k,
-                                                double* __restrict__ rew) {
-  __shared__ Stage stage[4];
-  const int lane = threadIdx.x & 63;
-  Stage& st = stage[threadIdx.x >> 6];
-  const int e_lane0 = blockIdx.x * blockDim.x + (threadIdx.x & ~63);
-  const int e = e_lane0 + lane;
-  const bool live = e < p.E;
-  if (__ballot(live) == 0ull) return;
-  const int ee = live ? e : 0;
+__device__ __forceinline__ void static_tick(const SimParams& p, const SysState& G, uint32_t* err,
+                                            uint64_t seed, uint32_t k, bool live, int e, int ee,
+                                            int e_lane0, int lane, Stage& st, Queue<CM>& Q,
+                                            Count& C, Arrivals& A, double (&busy)[KM],
+                                            ServerBytes& infl, uint32_t& dirty, uint32_t& clear,
+                                            uint32_t& rr, double* __restrict__ rew_row) {
   const size_t E = (size_t)p.E;
-  const SysState& G = g.sys[1];
-  Queue<CM> Q;
-  load_queue(Q, G, p, ee);
-  Count C;
-  load_count(C, G, p, ee);
-  Arrivals A;
-  load_arrivals(A, G, p, ee);
-  // busy-until times in registers; of each server's meta word only the in-flight count
-  // (low byte) is kept, eight servers to a 64-bit register (the word is stored at dispatch)
-  double busy[KM];
-  ServerBytes infl;
-#pragma unroll
-  for (int j = 0; j < KM; ++j) {
-    busy[j] = j < p.K ? G.busy[(size_t)j * E + ee] : kInf;
-    if (j < p.K) infl.set(j, G.meta[(size_t)j * E + ee] & 0xffu);
-  }
-  uint32_t dirty = 0;
-  uint32_t rr = p.route == 2 ? G.rr[ee] : 0u, jroute = 0;
-
+  C.n_k = 0;
+  C.Lw = 0.0;
+  C.jsvc = 0;
+  A.jarr = 0;
+  A.jproc = 0;
+  uint32_t jroute = 0;
   const double t0 = (double)k * p.dt, t1 = (double)(k + 1) * p.dt;
   int A_k = 0;
   double now = t0;
@@ -730,7 +719,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
       if (!(te < t1)) {
         done = true;
       } else if (it > kMaxEventsPerTick) {
-        atomicOr(g.err, ERR_EVENTS);
+        atomicOr(err, ERR_EVENTS);
         done = true;
       } else {
         need = p.arrival_kind != 1 && (A.next_sw == te || A.next_arr == te) &&
@@ -777,24 +766,67 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     if (__ballot(!done) == 0ull) break;
   }
   if (!live) return;
-  // completions before t1: count them and clear the in-flight byte of the stored word
-  uint32_t clear = 0;
+  // completions before t1
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
     const uint32_t n = infl.get(j);
     if (j < p.K && n > 0 && busy[j] < t1) {
       C.c[C_DONE] += n;
       clear |= 1u << j;
+      infl.set(j, 0u);
     }
   }
+  const double r = close_tick(Q, C, p, A.proc, A_k);
+  if (rew_row) rew_row[e] = r;
+}
+
+// Ticks k0 .. k0 + nt - 1 of the static shadow system. The static rule never looks at the
+// learned system, so one launch may cover many ticks: the state is loaded once, kept in
+// registers from tick to tick, and stored once; each wave advances at its own pace instead of
+// waiting at every tick for the slowest wave of the grid. rew [nt][E] (optional) receives the
+// rewards; nt = 1 is the per-tick kernel of the step interface.
+template <int KM, int CM>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void static_k(
+    SimParams p, EnvState g, uint64_t seed, uint32_t k0, int nt, double* __restrict__ rew) {
+  __shared__ Stage stage[4];
+  const int lane = threadIdx.x & 63;
+  Stage& st = stage[threadIdx.x >> 6];
+  const int e_lane0 = blockIdx.x * blockDim.x + (threadIdx.x & ~63);
+  const int e = e_lane0 + lane;
+  const bool live = e < p.E;
+  if (__ballot(live) == 0ull) return;
+  const int ee = live ? e : 0;
+  const size_t E = (size_t)p.E;
+  const SysState& G = g.sys[1];
+  Queue<CM> Q;
+  load_queue(Q, G, p, ee);
+  Count C;
+  load_count(C, G, p, ee);
+  Arrivals A;
+  load_arrivals(A, G, p, ee);
+  // busy-until times in registers; of each server's meta word only the in-flight count
+  // (low byte) is kept, eight servers to a 64-bit register (the word is stored at dispatch)
+  double busy[KM];
+  ServerBytes infl;
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    busy[j] = j < p.K ? G.busy[(size_t)j * E + ee] : kInf;
+    if (j < p.K) infl.set(j, G.meta[(size_t)j * E + ee] & 0xffu);
+  }
+  uint32_t dirty = 0, clear = 0;
+  uint32_t rr = p.route == 2 ? G.rr[ee] : 0u;
+  for (int i = 0; i < nt; ++i)
+    static_tick<KM, CM>(p, G, g.err, seed, k0 + (uint32_t)i, live, e, ee, e_lane0, lane, st, Q,
+                        C, A, busy, infl, dirty, clear, rr, rew ? rew + (size_t)i * E : nullptr);
+  if (!live) return;
+  // servers whose last batch completed: clear the in-flight byte of the stored meta word
   uint32_t m[KM];
 #pragma unroll
-  for (int j = 0; j < KM; ++j) m[j] = (clear >> j) & 1u ? G.meta[(size_t)j * E + e] : 0u;
+  for (int j = 0; j < KM; ++j)
+    m[j] = ((clear >> j) & 1u) && infl.get(j) == 0u ? G.meta[(size_t)j * E + e] : 0u;
 #pragma unroll
   for (int j = 0; j < KM; ++j)
-    if ((clear >> j) & 1u) G.meta[(size_t)j * E + e] = m[j] & ~0xffu;
-  const double r = close_tick(Q, C, p, A.proc, A_k);
-  if (rew) rew[e] = r;
+    if (((clear >> j) & 1u) && infl.get(j) == 0u) G.meta[(size_t)j * E + e] = m[j] & ~0xffu;
 #pragma unroll
   for (int j = 0; j < KM; ++j)
     if (dirty & (1u << j)) G.busy[(size_t)j * E + e] = busy[j];
@@ -920,13 +952,13 @@ __global__ __launch_bounds__(256) void totals_k(SimParams p, EnvState g, int64_t
 }
 
 template <int CM>
-void launch_static_c(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
+void launch_static_c(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k, int nt,
                      double* rew_sh, hipStream_t st) {
   const dim3 grid((p.E + 255) / 256), block(256);
-  if (p.K <= 1) hipLaunchKernelGGL((static_k<1, CM>), grid, block, 0, st, p, s, seed, k, rew_sh);
-  else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM>), grid, block, 0, st, p, s, seed, k, rew_sh);
-  else if (p.K <= 8) hipLaunchKernelGGL((static_k<8, CM>), grid, block, 0, st, p, s, seed, k, rew_sh);
-  else hipLaunchKernelGGL((static_k<16, CM>), grid, block, 0, st, p, s, seed, k, rew_sh);
+  if (p.K <= 1) hipLaunchKernelGGL((static_k<1, CM>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
+  else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
+  else if (p.K <= 8) hipLaunchKernelGGL((static_k<8, CM>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
+  else hipLaunchKernelGGL((static_k<16, CM>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
 }
 
 }  // namespace
@@ -950,10 +982,11 @@ hipError_t launch_step(const SimParams& p, const EnvState& s, uint64_t seed, uin
 }
 
 hipError_t launch_static(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
-                         double* rew_sh, hipStream_t st) {
-  if (p.C <= 1) launch_static_c<1>(p, s, seed, k, rew_sh, st);
-  else if (p.C <= 2) launch_static_c<2>(p, s, seed, k, rew_sh, st);
-  else launch_static_c<4>(p, s, seed, k, rew_sh, st);
+                         int nt, double* rew_sh, hipStream_t st) {
+  if (nt < 1) return hipErrorInvalidValue;
+  if (p.C <= 1) launch_static_c<1>(p, s, seed, k, nt, rew_sh, st);
+  else if (p.C <= 2) launch_static_c<2>(p, s, seed, k, nt, rew_sh, st);
+  else launch_static_c<4>(p, s, seed, k, nt, rew_sh, st);
   return hipGetLastError();
 }
 

@@ -521,6 +521,50 @@ def test_rollout_parity_and_validity(bs, orc, name):
     sim.close()
 
 
+SHADOWED = {
+    "C5": lambda: preset("C5"),
+    "burst": lambda: burst_preset(),
+    "static8_C3": lambda: baseline_preset("static8", "C3"),
+    "random_C5": lambda: baseline_preset("random", "C5"),
+    "round_robin_C4": lambda: baseline_preset("round_robin", "C4"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SHADOWED))
+def test_rollout_static_chunks_then_steps(bs, orc, name):
+    """sim_rollout runs the static shadow system in launches of 256 ticks with its state in
+    registers; 600 ticks (chunks of 256, 256, 88) followed by 20 sim_step calls (the per-tick
+    kernel) must equal the oracle's replay of the same 620 ticks, bit for bit in the integer
+    state and checksums."""
+    w = SHADOWED[name]()
+    E, T, T2 = 300, 600, 20
+    seed = 0x5EED5 + len(name)
+    say(f"[static chunks] {name}")
+    sim = bs.Sim(w, n_envs=E)
+    sim.reset(seed)
+    wb = sim.init_weights(3)
+    tr = sim.rollout(wb, T)
+    acts2 = seeded_actions(seed, T2, E, 6 * w["n_servers"], small_bias=0.5)
+    a2 = torch.from_numpy(np.ascontiguousarray(acts2)).cuda()
+    rsh2 = []
+    for k in range(T2):
+        _, _, rs = sim.step(a2[k], want_obs=False)
+        rsh2.append(rs)
+    sim.sync()
+    acts = np.concatenate([tr.actions.cpu().numpy(), acts2], axis=0)
+    rsh = np.concatenate([tr.reward_shadow.cpu().numpy(), torch.stack(rsh2).cpu().numpy()])
+    cnt, sums = sim.counters()
+    chk = sim.checksums().cpu().numpy().view(np.uint64)
+    ref = orc.rollout(w, seed, T + T2, np.arange(E), actions=acts, want_obs=False, want_rec=False)
+    assert_close_rel(rsh, ref["reward_shadow"], "reward_shadow")
+    for s_ in (0, 1):
+        assert np.array_equal(chk[s_], ref["chk"][:, s_]), f"checksum sys {s_}"
+        assert np.array_equal(cnt.cpu().numpy()[s_].T, ref["counters"][:, s_]), f"counters sys {s_}"
+        assert_close_rel(sums.cpu().numpy()[s_].T, ref["sums"][:, s_, :2], f"sums sys {s_}")
+    assert ref["counters"][:, 1, 4].sum() > 0
+    sim.close()
+
+
 def test_action_out_of_range_is_latched(bs):
     w = preset("C1")
     sim = bs.Sim(w, n_envs=70)
