@@ -353,6 +353,101 @@ __device__ __forceinline__ void hidden_layer(const uint16_t* __restrict__ act, i
   }
 }
 
+// TPW output tiles (16 units each, tiles tile0 + i * tstride) of a layer for RTN consecutive
+// environment tiles from rt0 in one pass over k: every activation fragment read from LDS feeds
+// TPW MFMAs (the LDS traffic of a layer falls by that factor against one tile per pass), and
+// a ring of D k-steps of weight fragments of all TPW tiles is kept in flight. The bias is the
+// accumulators' initial value.
+template <int K, int TPW, int RTN>
+__device__ __forceinline__ void mma_group(const uint16_t* __restrict__ act, int sa,
+                                          const uint16_t* __restrict__ W,
+                                          const float* __restrict__ bias, int tile0, int tstride,
+                                          int rt0, f32x4 (&acc)[TPW][RTN]) {
+  constexpr int KS = K / 32, D = KS < 3 ? KS : 3, S = D + 1;
+  const int lane = threadIdx.x & 63, r16 = lane & 15, kq = lane >> 4;
+  const uint16_t* brow = act + (rt0 * 16 + r16) * sa + kq * 8;
+  const uint16_t* wp[TPW];
+#pragma unroll
+  for (int i = 0; i < TPW; ++i) {
+    const int tile = tile0 + i * tstride;
+    wp[i] = W + (size_t)tile * KS * 512 + lane * 8;  // fragment order
+    const f32x4 bv = *reinterpret_cast<const f32x4*>(bias + tile * 16 + kq * 4);
+#pragma unroll
+    for (int rt = 0; rt < RTN; ++rt) acc[i][rt] = bv;
+  }
+  bf16x8 w[S][TPW];
+#pragma unroll
+  for (int s = 0; s < D; ++s)
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) w[s][i] = *reinterpret_cast<const bf16x8*>(wp[i] + s * 512);
+  // software pipeline: the activation fragments of k-step ks + 1 and the weight fragments of
+  // ks + D are issued before the MFMAs of ks; scheduling barriers keep the compiler from
+  // sinking those loads next to their first use, where every step would wait out the L2 and
+  // LDS latency
+  bf16x8 b[2][RTN];
+#pragma unroll
+  for (int rt = 0; rt < RTN; ++rt) b[0][rt] = *reinterpret_cast<const bf16x8*>(brow + rt * 16 * sa);
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    if (ks + 1 < KS) {
+#pragma unroll
+      for (int rt = 0; rt < RTN; ++rt)
+        b[(ks + 1) & 1][rt] = *reinterpret_cast<const bf16x8*>(brow + rt * 16 * sa + (ks + 1) * 32);
+    }
+    if (ks + D < KS) {
+#pragma unroll
+      for (int i = 0; i < TPW; ++i)
+        w[(ks + D) % S][i] = *reinterpret_cast<const bf16x8*>(wp[i] + (ks + D) * 512);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int rt = 0; rt < RTN; ++rt)
+#pragma unroll
+      for (int i = 0; i < TPW; ++i)
+        acc[i][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[ks % S][i], b[ks & 1][rt], acc[i][rt], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// Hidden layer with TPW tiles per pass (see mma_group): the wave's CTW tiles wave, wave + NW,
+// ... in CTW / TPW passes, each followed by its GELU epilogue; in place, the packed results
+// wait in registers until every wave has finished reading act.
+template <int K, int N, int RT, int NW, int TPW, bool kInPlace>
+__device__ __forceinline__ void hidden_layer_g(const uint16_t* __restrict__ act, int sa,
+                                               const uint16_t* __restrict__ W,
+                                               const float* __restrict__ bias, uint16_t* out,
+                                               int so) {
+  constexpr int NT = N / 16, CTW = NT / NW, NG = CTW / TPW;
+  static_assert(NT % NW == 0 && CTW % TPW == 0, "tiles divide evenly over waves and passes");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, kq = lane >> 4;
+  u32x2 pk[kInPlace ? CTW : 1][RT];
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    f32x4 acc[TPW][RT];
+    mma_group<K, TPW, RT>(act, sa, W, bias, wave + NW * TPW * g, NW, 0, acc);
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+      const int c = g * TPW + i;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const u32x2 v = gelu_pack4(acc[i][rt]);
+        if (kInPlace) pk[kInPlace ? c : 0][rt] = v;
+        else *reinterpret_cast<u32x2*>(out + (rt * 16 + r16) * so + (wave + NW * c) * 16 + kq * 4) = v;
+      }
+    }
+  }
+  if (kInPlace) {
+    __syncthreads();  // every wave has finished reading act
+#pragma unroll
+    for (int c = 0; c < CTW; ++c)
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+        *reinterpret_cast<u32x2*>(out + (rt * 16 + r16) * so + (wave + NW * c) * 16 + kq * 4) =
+            pk[kInPlace ? c : 0][rt];
+  }
+}
+
 __host__ __device__ constexpr int pow2_floor(int v) { return v >= 8 ? 8 : v >= 4 ? 4 : v >= 2 ? 2 : 1; }
 
 // Output layer (logits and value, fp32 into lg, which aliases act): NT tiles x G groups of
@@ -398,7 +493,7 @@ struct BigShape {
   static constexpr size_t LDS = X_BYTES + HREG;
 };
 
-template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB>
+template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MINB / 4 > 0 ? NW * MINB / 4 : 1))) void policy_bf16_k(MlpParams m, const float* __restrict__ obs,
                                                                uint64_t seed, uint32_t step,
                                                                uint8_t* __restrict__ act,
@@ -425,11 +520,19 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
     *reinterpret_cast<uint32_t*>(xs + r * Sh::SX + f) = pack_bf16(v0, v1);
   }
   __syncthreads();
-  hidden_layer<FP, H1, RT, NW, false>(xs, Sh::SX, static_cast<const uint16_t*>(m.w1), m.b1, hs,
-                                      Sh::SH);
-  __syncthreads();
-  hidden_layer<H1, H2, RT, NW, true>(hs, Sh::SH, static_cast<const uint16_t*>(m.w2), m.b2, hs,
-                                     Sh::SH);
+  if constexpr (TPW == 1) {
+    hidden_layer<FP, H1, RT, NW, false>(xs, Sh::SX, static_cast<const uint16_t*>(m.w1), m.b1, hs,
+                                        Sh::SH);
+    __syncthreads();
+    hidden_layer<H1, H2, RT, NW, true>(hs, Sh::SH, static_cast<const uint16_t*>(m.w2), m.b2, hs,
+                                       Sh::SH);
+  } else {
+    hidden_layer_g<FP, H1, RT, NW, TPW, false>(xs, Sh::SX, static_cast<const uint16_t*>(m.w1),
+                                               m.b1, hs, Sh::SH);
+    __syncthreads();
+    hidden_layer_g<H1, H2, RT, NW, TPW, true>(hs, Sh::SH, static_cast<const uint16_t*>(m.w2),
+                                              m.b2, hs, Sh::SH);
+  }
   __syncthreads();
   output_layer<H2, AP, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w3), m.b3, lg, Sh::SL);
   __syncthreads();
@@ -489,12 +592,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
   }
 }
 
-template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB>
+template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW = 1>
 hipError_t run_policy_bf16(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
                            uint8_t* act, float* logp, float* value, float* logits, hipStream_t st) {
   typedef BigShape<FP, H1, H2, AP, RT, NW> Sh;
   static_assert(Sh::LDS <= 160 * 1024, "LDS budget");
-  auto kern = policy_bf16_k<FP, H1, H2, AP, RT, NW, MINB>;
+  auto kern = policy_bf16_k<FP, H1, H2, AP, RT, NW, MINB, TPW>;
   static bool attr = false;
   if (!attr) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -561,7 +664,7 @@ hipError_t launch_policy(const MlpParams& m, const float* obs, uint64_t seed, ui
     return big ? run_policy_bf16<64, 256, 256, 64, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, st)
                : run_policy_bf16<64, 256, 256, 64, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, st);
   if (m.bf16 && m.FP == 96 && m.H1 == 512 && m.H2 == 512 && m.AP == 112)
-    return big ? run_policy_bf16<96, 512, 512, 112, 8, 16, 1>(m, obs, seed, step, act, logp, value, logits, st)
+    return big ? run_policy_bf16<96, 512, 512, 112, 4, 8, 2, 2>(m, obs, seed, step, act, logp, value, logits, st)
                : run_policy_bf16<96, 512, 512, 112, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, st);
   return hipErrorInvalidValue;
 }
