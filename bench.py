@@ -366,7 +366,11 @@ def main():
         # minibatch gradients per step (one, or epochs x minibatches when training), each
         # with its share of Adam
         n_grad = args.epochs * args.minibatches if train else 1
-        fl = ppo_flops(dict(w, ppo_minibatch=w.get("ppo_minibatch", 0) or 8192)) * n_grad
+        if w.get("policy_kind", 0) == 1:
+            # forward and backward of the attention network: about three forwards per sample
+            fl = 3 * attn_flops(w) * (w.get("ppo_minibatch", 0) or 8192) * n_grad
+        else:
+            fl = ppo_flops(dict(w, ppo_minibatch=w.get("ppo_minibatch", 0) or 8192)) * n_grad
         ach = fl / (kern["ppo"]["total_ms_per_step"] * 1e-3) / 1e12
         rl["ppo"] = {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS,
                      "unit": "TFLOP/s", "frac": ach / PEAK_FP32_VALU_TFLOPS,

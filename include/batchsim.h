@@ -254,13 +254,19 @@ int returns_gae(sim_ctx* ctx, int32_t T, const double* d_r, const float* d_v, do
  * value and entropy terms; d_index [M] int64 (t E + env) or NULL. Requires value_head = 1,
  * M > 0 and a multiple of 16. Scratch of about 4 M (F + 3 H1 + 3 H2 + A') bytes is held by
  * the context after the first call. A stored action out of range latches SIM_ESTATE
- * (reported by sim_sync); that sample then contributes nothing.                         */
+ * (reported by sim_sync); that sample then contributes nothing.
+ * For the attention policy (policy_kind = SIM_POLICY_ATTN) the forward is fp32 with exact
+ * GELU and d_grads holds the fourteen arrays of sim_attn_layout in its order (w_in, b_in,
+ * w_qkv, b_qkv, w_o, b_o, wp1, bp1, wp2, bp2, wv1, bv1, wv2, bv2), each [in][out] as in the
+ * weights; per-sample gradient terms are summed over the minibatch in a fixed order (the
+ * scratch then holds 4 M P + 24 M bytes, P = sim_ppo_grad_count).                        */
 int ppo_minibatch_grad(sim_ctx* ctx, const void* d_weights, int32_t T, const float* d_obs,
                        const uint8_t* d_actions, const float* d_logp_old, const double* d_adv,
                        const double* d_ret, int32_t M, uint64_t seed, float clip, float c_value,
                        float c_entropy, float* d_grads, double* d_loss, int64_t* d_index);
 
-/* Number of fp32 gradient values written by ppo_minibatch_grad (no device work).       */
+/* Number of fp32 gradient values written by ppo_minibatch_grad (no device work), for either
+ * policy network.                                                                       */
 int sim_ppo_grad_count(const sim_cfg* cfg, int64_t* h_count);
 
 /* REINFORCE with a learned baseline (Sec. 4.3) on one minibatch: as ppo_minibatch_grad, with
@@ -279,7 +285,8 @@ int sim_params_from_weights(sim_ctx* ctx, const void* d_weights, float* d_params
  *   m = b1 m + (1-b1) g,  v = b2 v + (1-b2) g^2,  p -= lr (m/(1-b1^t)) / (sqrt(v/(1-b2^t)) + eps)
  * with t = step >= 1 (the step being taken); d_m, d_v are the caller's moment buffers (zero
  * before the first step). With d_weights non-NULL the policy's weights are then rewritten from
- * the parameters (matrices rounded to bf16, nearest even, in bf16 configurations).        */
+ * the parameters (matrices rounded to bf16, nearest even, in bf16 configurations; copied as
+ * they are for the fp32 attention policy).                                              */
 int adam_update(sim_ctx* ctx, float* d_params, const float* d_grads, float* d_m, float* d_v,
                 int32_t step, float lr, float beta1, float beta2, float eps, void* d_weights);
 

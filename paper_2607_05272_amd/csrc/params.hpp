@@ -106,6 +106,25 @@ bool attn_shape_supported(const AttnParams& p);
 hipError_t launch_attn_policy(const AttnParams& p, const float* obs, uint64_t seed, uint32_t step,
                               uint8_t* act, float* logp, float* value, float* logits,
                               hipStream_t st);
+// Minibatch gradient of the attention policy (REINFORCE with baseline or PPO): indices drawn
+// as for the MLP; grads in the order w_in, b_in, w_qkv, b_qkv, w_o, b_o, wp1, bp1, wp2, bp2,
+// wv1, bv1, wv2, bv2 (fp32); loss_out[4] total, policy, value, entropy (fp64); scratch of
+// attn_grad_scratch_bytes bytes
+int attn_param_count(const AttnParams& p, int off[14]);
+size_t attn_grad_scratch_bytes(const AttnParams& p, int M);
+hipError_t launch_attn_grad(const AttnParams& p, int T, const float* obs, const uint8_t* act,
+                            const float* logp_old, const double* adv, const double* ret, int M,
+                            uint64_t seed, float clip, float c_v, float c_h, int reinforce,
+                            void* scratch, double* loss_out, float* grads, int64_t* idx_out,
+                            uint32_t* err, hipStream_t st);
+// the attention policy's weights from / to fp32 parameters in gradient order (plain copies)
+hipError_t launch_export_attn(const AttnParams& p, const float* params, void* d_weights,
+                              const size_t off[14], hipStream_t st);
+hipError_t launch_import_attn(const AttnParams& p, const void* d_weights, const size_t off[14],
+                              float* params, hipStream_t st);
+// the four loss terms from per-sample [M][3] fp64 terms, summed in a fixed order
+hipError_t launch_pg_loss(const double* terms, int M, float c_v, float c_h, double* out,
+                          hipStream_t st);
 // Xavier init of the attention policy's seven matrices (layers 0..6) and zero biases;
 // off[14] are the byte offsets of w_in, b_in, ..., wv2, bv2; fin/fout the matrix shapes
 hipError_t launch_init_attn(uint64_t seed, void* d_weights, const size_t off[14], const int fin[7],

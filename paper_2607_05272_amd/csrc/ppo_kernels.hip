@@ -364,6 +364,12 @@ hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t of
   return hipGetLastError();
 }
 
+hipError_t launch_pg_loss(const double* terms, int M, float c_v, float c_h, double* out,
+                          hipStream_t st) {
+  hipLaunchKernelGGL(ppo_loss_k, dim3(1), dim3(kThr), 0, st, terms, M, c_v, c_h, out);
+  return hipGetLastError();
+}
+
 size_t ppo_scratch_floats(const MlpParams& m, int M) {
   // activations, per-sample loss terms (fp64), then the chunked weight-gradient partials
   const size_t nc = (size_t)(M + kMC - 1) / kMC;

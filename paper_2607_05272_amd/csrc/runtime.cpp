@@ -614,6 +614,13 @@ int returns_gae(sim_ctx* x, int32_t T, const double* d_r, const float* d_v, doub
 
 int sim_ppo_grad_count(const sim_cfg* c, int64_t* h_count) {
   if (!c || !h_count) return fail(SIM_EINVAL, "NULL argument");
+  if (c->policy_kind == SIM_POLICY_ATTN) {
+    AttnParams a{};
+    a.F = c->obs_dim; a.L = c->attn_tokens; a.D = c->attn_embed; a.NH = c->attn_heads;
+    a.Hp = c->mlp_h1; a.Hv = c->mlp_h2; a.A = 6 * c->n_servers;
+    *h_count = attn_param_count(a, nullptr);
+    return SIM_OK;
+  }
   const int64_t F = c->obs_dim, H1 = c->mlp_h1, H2 = c->mlp_h2;
   const int64_t Ap = 6 * (int64_t)c->n_servers + (c->value_head ? 1 : 0);
   *h_count = F * H1 + H1 + H1 * H2 + H2 + H2 * Ap + Ap;
@@ -629,8 +636,6 @@ static int pg_grad(sim_ctx* x, int reinforce, const void* d_weights, int32_t T, 
   if (!x || !d_weights || !d_obs || !d_actions || (!reinforce && !d_logp_old) || !d_adv ||
       !d_ret || !d_grads || !d_loss)
     return fail(SIM_EINVAL, "%s: NULL argument", who);
-  if (x->cfg.policy_kind != SIM_POLICY_MLP)
-    return fail(SIM_EUNSUPPORTED, "%s: built for the MLP policy only", who);
   if (!x->cfg.value_head) return fail(SIM_EUNSUPPORTED, "%s needs value_head = 1", who);
   if (T < 1) return fail(SIM_EINVAL, "T must be >= 1");
   if (M < 16 || M % 16) return fail(SIM_EINVAL, "M = %d must be a positive multiple of 16", M);
@@ -638,6 +643,28 @@ static int pg_grad(sim_ctx* x, int reinforce, const void* d_weights, int32_t T, 
     return fail(SIM_EINVAL, "T * E must stay below 2^31");
   if (!reinforce && !(clip > 0.0f && clip < 1.0f))
     return fail(SIM_EINVAL, "clip must lie in (0, 1)");
+  if (x->cfg.policy_kind == SIM_POLICY_ATTN) {
+    int rc = prepare_policy(x, d_weights);  // shape check and weight pointers
+    if (rc) return rc;
+    const size_t need = attn_grad_scratch_bytes(x->a, M);
+    if (need > x->ppo_bytes) {
+      (void)hipStreamSynchronize(x->stream);
+      (void)hipFree(x->ppo_scratch);
+      x->ppo_scratch = nullptr;
+      x->ppo_bytes = 0;
+      hipError_t he = hipMalloc(&x->ppo_scratch, need);
+      if (he != hipSuccess)
+        return fail(SIM_ENOMEM, "hipMalloc of %zu bytes of minibatch scratch failed: %s", need,
+                    hipGetErrorString(he));
+      x->ppo_bytes = need;
+    }
+    HIPCHK(x->timed(SIM_KC_PPO, [&] {
+             return launch_attn_grad(x->a, T, d_obs, d_actions, d_logp_old, d_adv, d_ret, M, seed,
+                                     clip, c_value, c_entropy, reinforce, x->ppo_scratch, d_loss,
+                                     d_grads, d_index, x->s.err, x->stream);
+           }), "attention minibatch gradient kernel launch");
+    return SIM_OK;
+  }
   if (ppo_lds_bytes(x->m) > 64 * 1024)
     return fail(SIM_EUNSUPPORTED, "the minibatch forward needs %zu bytes of LDS (at most 65536)",
                 ppo_lds_bytes(x->m));
@@ -682,8 +709,14 @@ int reinforce_minibatch_grad(sim_ctx* x, const void* d_weights, int32_t T, const
 
 int sim_params_from_weights(sim_ctx* x, const void* d_weights, float* d_params) {
   if (!x || !d_weights || !d_params) return fail(SIM_EINVAL, "NULL argument");
-  if (x->cfg.policy_kind != SIM_POLICY_MLP)
-    return fail(SIM_EUNSUPPORTED, "sim_params_from_weights: built for the MLP policy only");
+  if (x->cfg.policy_kind == SIM_POLICY_ATTN) {
+    size_t off[14];
+    attn_offsets(x->cfg, off);
+    HIPCHK(x->timed(SIM_KC_OTHER, [&] {
+             return launch_import_attn(x->a, d_weights, off, d_params, x->stream);
+           }), "weight import launch");
+    return SIM_OK;
+  }
   size_t off[6];
   offsets(x->cfg, off);
   HIPCHK(x->timed(SIM_KC_OTHER, [&] {
@@ -706,7 +739,13 @@ int adam_update(sim_ctx* x, float* d_params, const float* d_grads, float* d_m, f
            return launch_adam(d_params, d_grads, d_m, d_v, (size_t)n, lr, beta1, beta2, eps, bc1,
                               bc2, x->stream);
          }), "Adam kernel launch");
-  if (d_weights) {
+  if (d_weights && x->cfg.policy_kind == SIM_POLICY_ATTN) {
+    size_t off[14];
+    attn_offsets(x->cfg, off);
+    HIPCHK(x->timed(SIM_KC_PPO, [&] {
+             return launch_export_attn(x->a, d_params, d_weights, off, x->stream);
+           }), "weight export launch");
+  } else if (d_weights) {
     size_t off[6];
     offsets(x->cfg, off);
     HIPCHK(x->timed(SIM_KC_PPO, [&] {
@@ -725,8 +764,6 @@ int sim_update(sim_ctx* x, const sim_update_cfg* u, void* d_weights, float* d_pa
   if (u->algo != SIM_ALGO_PPO && u->algo != SIM_ALGO_REINFORCE)
     return fail(SIM_EINVAL, "unknown algorithm %d", u->algo);
   if (u->epochs < 1 || u->minibatches < 1) return fail(SIM_EINVAL, "epochs and minibatches >= 1");
-  if (x->cfg.policy_kind != SIM_POLICY_MLP)
-    return fail(SIM_EUNSUPPORTED, "sim_update: built for the MLP policy only");
   int64_t n = 0;
   sim_ppo_grad_count(&x->cfg, &n);
   if (!x->grads) {

@@ -28,19 +28,21 @@ __global__ __launch_bounds__(256) void adam_k(float* __restrict__ p, const float
   }
 }
 
+constexpr int kMaxSegs = 14;
 struct Segs {
-  size_t poff[6];   // offset in the parameter vector
-  size_t woff[6];   // byte offset in the weight buffer
-  size_t len[6];
-  int matrix[6];
+  int n;                   // segments in use (6 for the MLP, 14 for the attention policy)
+  size_t poff[kMaxSegs];   // offset in the parameter vector
+  size_t woff[kMaxSegs];   // byte offset in the weight buffer
+  size_t len[kMaxSegs];
+  int matrix[kMaxSegs];
 };
 
-// one thread per parameter; seg found by a short scan of the six segment starts
+// one thread per parameter; seg found by a short scan of the segment starts
 __device__ __forceinline__ int seg_of(const Segs& s, size_t i) {
   int k = 0;
 #pragma unroll
-  for (int j = 1; j < 6; ++j)
-    if (i >= s.poff[j]) k = j;
+  for (int j = 1; j < kMaxSegs; ++j)
+    if (j < s.n && i >= s.poff[j]) k = j;
   return k;
 }
 
@@ -68,6 +70,7 @@ __global__ __launch_bounds__(256) void import_k(Segs s, size_t n, int bf16,
 
 Segs segments(const MlpParams& m, const size_t off[6]) {
   Segs s;
+  s.n = 6;
   const size_t len[6] = {(size_t)m.F * m.H1, (size_t)m.H1, (size_t)m.H1 * m.H2, (size_t)m.H2,
                          (size_t)m.H2 * m.Ap, (size_t)m.Ap};
   size_t acc = 0;
@@ -81,7 +84,22 @@ Segs segments(const MlpParams& m, const size_t off[6]) {
   return s;
 }
 
-size_t total(const Segs& s) { return s.poff[5] + s.len[5]; }
+// the attention policy: fourteen fp32 arrays (nothing is rounded to bf16)
+Segs attn_segments(const AttnParams& p, const size_t off[14]) {
+  Segs s;
+  s.n = 14;
+  int po[14];
+  const int P = attn_param_count(p, po);
+  for (int k = 0; k < 14; ++k) {
+    s.poff[k] = (size_t)po[k];
+    s.woff[k] = off[k];
+    s.len[k] = (size_t)((k < 13 ? po[k + 1] : P) - po[k]);
+    s.matrix[k] = 0;
+  }
+  return s;
+}
+
+size_t total(const Segs& s) { return s.poff[s.n - 1] + s.len[s.n - 1]; }
 
 }  // namespace
 
@@ -99,6 +117,24 @@ hipError_t launch_export_weights(const MlpParams& m, const float* params, void* 
   const size_t n = total(s);
   hipLaunchKernelGGL(export_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, s, n, m.bf16,
                      params, static_cast<unsigned char*>(d_weights));
+  return hipGetLastError();
+}
+
+hipError_t launch_export_attn(const AttnParams& p, const float* params, void* d_weights,
+                              const size_t off[14], hipStream_t st) {
+  const Segs s = attn_segments(p, off);
+  const size_t n = total(s);
+  hipLaunchKernelGGL(export_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, s, n, 0,
+                     params, static_cast<unsigned char*>(d_weights));
+  return hipGetLastError();
+}
+
+hipError_t launch_import_attn(const AttnParams& p, const void* d_weights, const size_t off[14],
+                              float* params, hipStream_t st) {
+  const Segs s = attn_segments(p, off);
+  const size_t n = total(s);
+  hipLaunchKernelGGL(import_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, s, n, 0,
+                     static_cast<const unsigned char*>(d_weights), params);
   return hipGetLastError();
 }
 

@@ -303,10 +303,15 @@ class Sim:
         return st.value, losses
 
     def unflatten_grads(self, g):
-        """Split a flat gradient vector (host numpy) into W1,b1,W2,b2,W3,b3 arrays."""
-        F, H1, H2, Ap = self.F, self.w["mlp_h1"], self.w["mlp_h2"], self.Ap
-        shapes = [("w1", (F, H1)), ("b1", (H1,)), ("w2", (H1, H2)), ("b2", (H2,)),
-                  ("w3", (H2, Ap)), ("b3", (Ap,))]
+        """Split a flat gradient vector (host numpy) into the policy's arrays (W1,b1,W2,b2,W3,b3,
+        or the attention policy's fourteen in sim_attn_layout order)."""
+        if _is_attn(self.w):
+            _, sh, _ = attn_layout(self.w)
+            shapes = [(k, sh[k]) for k in L.ATTN_KEYS]
+        else:
+            F, H1, H2, Ap = self.F, self.w["mlp_h1"], self.w["mlp_h2"], self.Ap
+            shapes = [("w1", (F, H1)), ("b1", (H1,)), ("w2", (H1, H2)), ("b2", (H2,)),
+                      ("w3", (H2, Ap)), ("b3", (Ap,))]
         out, o = {}, 0
         for k, sh in shapes:
             n = int(np.prod(sh))

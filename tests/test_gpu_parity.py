@@ -430,14 +430,19 @@ def test_attention_policy_parity(bs, orc, name):
         check_policy(bs, orc, workload(name), E, ids)
 
 
-def test_attention_update_is_refused(bs):
-    """The update entry points are built for the MLP policy: the attention policy gets a
-    clear SIM_EUNSUPPORTED instead of a wrong gradient."""
-    w = workload("attn")
-    sim = bs.Sim(w, n_envs=64)
+def test_attention_gradient_needs_value_head(bs):
+    """The minibatch gradient uses the value head's output in its loss: without a value head
+    the attention policy's gradient is refused with a clear error."""
+    w = workload("attn", value_head=0)
+    E, T = 64, 3
+    sim = bs.Sim(w, n_envs=E)
     wb = sim.init_weights(1)
-    with pytest.raises(bs.SimError, match="MLP policy only"):
-        sim.params_from_weights(wb)
+    dev = torch.device("cuda")
+    obs = torch.zeros((T, w["obs_dim"], E), dtype=torch.float32, device=dev)
+    act = torch.zeros((T, E), dtype=torch.uint8, device=dev)
+    z = torch.zeros((T, E), dtype=torch.float64, device=dev)
+    with pytest.raises(bs.SimError, match="value_head"):
+        sim.reinforce_minibatch_grad(wb, obs, act, z, z, 64, 1)
     sim.close()
 
 
