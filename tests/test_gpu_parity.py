@@ -570,6 +570,84 @@ def test_rollout_static_chunks_then_steps(bs, orc, name):
     sim.close()
 
 
+FULL_ROLLOUT = {"C5": lambda: preset("C5"), "attn": lambda: attn_preset(n_envs=262144)}
+
+
+@pytest.mark.parametrize("name", sorted(FULL_ROLLOUT))
+def test_rollout_full_size_sampled(bs, orc, name):
+    """sim_rollout at the full environment count in the launch configuration the bench times
+    (large-batch policy kernel, learned tick, static shadow system in 256-tick launches), 300
+    ticks so that the shadow system crosses a launch boundary. For sampled environments the
+    oracle replays the rollout's actions: running checksums, rewards (both systems), final
+    checksums and counters agree exactly; and every sampled decision equals the oracle
+    policy's on the replayed observation outside the tie band (logits from the same GPU
+    policy kernel on those observations)."""
+    w = FULL_ROLLOUT[name]()
+    E, T = w["n_envs"], 300
+    seed = 0xF011 + len(name)
+    rng = np.random.default_rng(seed)
+    cols = np.unique(np.concatenate([[0, 1, 63, 64, E - 1], rng.choice(E, 28, replace=False)]))
+    say(f"[rollout-full] {name} E={E} T={T} sampled={len(cols)}")
+    sim = bs.Sim(w)
+    sim.reset(seed)
+    wb = sim.init_weights(seed + 1)
+    tr = sim.rollout(wb, T, rchk=True)
+    sim.sync()
+    c = torch.from_numpy(cols).cuda()
+    ga = tr.actions[:, c].cpu().numpy()
+    gr = tr.reward[:, c].cpu().numpy()
+    grs = tr.reward_shadow[:, c].cpu().numpy() if w["shadow"] else None
+    grchk = tr.rchk[:, c].cpu().numpy().view(np.uint64)
+    cnt, sums = sim.counters()
+    chk = sim.checksums().cpu().numpy().view(np.uint64)[:, cols]
+    cnt = cnt.cpu().numpy()[:, :, cols]
+    wts = bs.unpack_weights(w, wb.cpu().numpy())
+    sim.close()
+    del tr
+    rep = orc.rollout(w, seed, T, cols, actions=ga, want_rchk=True, want_rec=False)
+    assert np.array_equal(rep["rchk"], grchk), "running checksums differ"
+    assert_close_rel(gr, rep["reward"], "reward")
+    nsys = 2 if w["shadow"] else 1
+    if nsys == 2:
+        assert_close_rel(grs, rep["reward_shadow"], "reward_shadow")
+    for s_ in range(nsys):
+        assert np.array_equal(chk[s_], rep["chk"][:, s_]), f"checksum sys {s_}"
+        assert np.array_equal(cnt[s_].T, rep["counters"][:, s_]), f"counters sys {s_}"
+    # decisions: GPU logits of the replayed observations from the same policy kernel (a
+    # context of 64 * 512 environments selects the large-batch variant; the sampled rows are
+    # its first columns, and logits do not depend on the environment index) against the
+    # oracle policy with the true env ids
+    A = 6 * w["n_servers"]
+    n = len(cols)
+    Ec = 64 * 512
+    small = bs.Sim(w, n_envs=Ec)
+    small.reset(1)
+    wsm = small.upload_weights(wts)
+    ob = torch.zeros((w["obs_dim"], Ec), dtype=torch.float32, device="cuda")
+    ties = near = 0
+    for t in range(T):
+        ob[:, :n] = torch.from_numpy(np.ascontiguousarray(rep["obs"][t].T)).cuda()
+        out = small.policy(wsm, ob, t, want_logits=True)
+        glg = out["logits"][:, :n].cpu().numpy().T.astype(np.float64)
+        ref = orc.policy(w, wts, seed, t, rep["obs"][t], cols)
+        tol = (attn_tol if w.get("policy_kind", 0) == 1 else mlp_tol)(w, wts, rep["obs"][t])
+        assert np.all(np.abs(glg - ref["logits"]) <= tol), f"tick {t}: logits"
+        err = np.abs(glg - ref["logits"])[:, :A].max(axis=1)
+        sure = ref["margin"] > 2 * err + 1e-5
+        ties += int(np.sum(~sure))
+        assert np.array_equal(ga[t][sure], ref["actions"][sure]), f"tick {t}: decision differs"
+        # the sampler alone: the oracle's inverse CDF on the GPU's own logits with the same
+        # uniform; only fp32-versus-fp64 rounding of the sums separates the two
+        for i, e in enumerate(cols):
+            a_ref, _, mg = orc.sample_logits(glg[i, :A], orc.action_u(seed, int(e), t))
+            if mg > 1e-5:
+                assert ga[t][i] == a_ref, f"tick {t} env {e}: sampler"
+            else:
+                near += 1
+    small.close()
+    say(f"  decisions in the tie band {ties}/{n * T}; sampler-only near-ties {near}")
+
+
 def test_action_out_of_range_is_latched(bs):
     w = preset("C1")
     sim = bs.Sim(w, n_envs=70)
