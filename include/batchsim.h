@@ -328,6 +328,22 @@ int sim_stats(sim_ctx* ctx, sim_totals* h_out);
  * clears it), with the reason in sim_last_error().                                     */
 int sim_sync(sim_ctx* ctx);
 
+/* Checkpoint and resume of the simulation: a snapshot holds every environment's state of both
+ * systems (queues and timestamp rings, servers, counters, sums and checksums, arrival
+ * processes, arrival-rate averages, the current observation, latched error flags) and the
+ * context's tick counter and seed, behind a 256-byte header. sim_get_state with buf = NULL
+ * stores the snapshot size in *bytes; otherwise *bytes must be at least that size and buf
+ * (device or host memory) receives the snapshot after the work already enqueued on the
+ * stream; the copy is complete when the call returns. sim_set_state restores a snapshot
+ * into a context whose configuration has the same layout (n_envs, n_servers, n_classes,
+ * queue_cap, obs_dim, shadow; SIM_EINVAL otherwise, or for a buffer that is not a snapshot
+ * of this library version). Trace arrivals (sim_set_trace) are caller memory and not part
+ * of the snapshot: set the same trace again before resuming. Continuing from a restored
+ * snapshot reproduces the original continuation bit for bit (the counter-based random
+ * draws depend only on the seed, the environment and the tick).                          */
+int sim_get_state(sim_ctx* ctx, void* buf, size_t* bytes);
+int sim_set_state(sim_ctx* ctx, const void* buf, size_t bytes);
+
 /* Kernel classes for tracing. */
 enum sim_kernel_class {
   SIM_KC_POLICY = 0,  /* policy MLP + sampler */

@@ -847,6 +847,76 @@ int sim_sync(sim_ctx* x) {
   return SIM_OK;
 }
 
+// ---- checkpoint / resume ---------------------------------------------------------------------
+namespace {
+constexpr uint64_t kSnapMagic = 0x50414e534d495342ull;  // "BSIMSNAP"
+constexpr size_t kSnapHeader = 256;
+struct SnapHeader {
+  uint64_t magic;
+  uint32_t abi, header_bytes;
+  int32_t n_envs, n_servers, n_classes, queue_cap, obs_dim, shadow;
+  uint64_t arena_bytes;
+  uint64_t seed;
+  uint32_t tick, reset_done;
+};
+static_assert(sizeof(SnapHeader) <= kSnapHeader, "snapshot header");
+}  // namespace
+
+int sim_get_state(sim_ctx* x, void* buf, size_t* bytes) {
+  if (!x || !bytes) return fail(SIM_EINVAL, "NULL argument");
+  const size_t need = kSnapHeader + x->arena_bytes;
+  if (!buf) {
+    *bytes = need;
+    return SIM_OK;
+  }
+  if (*bytes < need) return fail(SIM_EINVAL, "snapshot needs %zu bytes, buffer has %zu", need, *bytes);
+  unsigned char hdr[kSnapHeader] = {};
+  SnapHeader h;
+  h.magic = kSnapMagic;
+  h.abi = BATCHSIM_ABI_VERSION;
+  h.header_bytes = (uint32_t)kSnapHeader;
+  h.n_envs = x->cfg.n_envs; h.n_servers = x->cfg.n_servers; h.n_classes = x->cfg.n_classes;
+  h.queue_cap = x->cfg.queue_cap; h.obs_dim = x->cfg.obs_dim; h.shadow = x->cfg.shadow;
+  h.arena_bytes = x->arena_bytes;
+  h.seed = x->seed;
+  h.tick = x->tick;
+  h.reset_done = x->reset_done ? 1u : 0u;
+  std::memcpy(hdr, &h, sizeof(h));
+  HIPCHK(hipStreamSynchronize(x->stream), "stream synchronize before the snapshot");
+  unsigned char* dst = static_cast<unsigned char*>(buf);
+  HIPCHK(hipMemcpy(dst, hdr, kSnapHeader, hipMemcpyDefault), "snapshot header copy");
+  HIPCHK(hipMemcpy(dst + kSnapHeader, x->arena, x->arena_bytes, hipMemcpyDefault),
+         "snapshot state copy");
+  *bytes = need;
+  return SIM_OK;
+}
+
+int sim_set_state(sim_ctx* x, const void* buf, size_t bytes) {
+  if (!x || !buf) return fail(SIM_EINVAL, "NULL argument");
+  if (bytes < kSnapHeader) return fail(SIM_EINVAL, "buffer of %zu bytes is not a snapshot", bytes);
+  HIPCHK(hipStreamSynchronize(x->stream), "stream synchronize before the restore");
+  const unsigned char* src = static_cast<const unsigned char*>(buf);
+  SnapHeader h;
+  HIPCHK(hipMemcpy(&h, src, sizeof(h), hipMemcpyDefault), "snapshot header copy");
+  if (h.magic != kSnapMagic || h.abi != BATCHSIM_ABI_VERSION || h.header_bytes != kSnapHeader)
+    return fail(SIM_EINVAL, "buffer is not a snapshot of this library version");
+  if (h.n_envs != x->cfg.n_envs || h.n_servers != x->cfg.n_servers ||
+      h.n_classes != x->cfg.n_classes || h.queue_cap != x->cfg.queue_cap ||
+      h.obs_dim != x->cfg.obs_dim || h.shadow != x->cfg.shadow || h.arena_bytes != x->arena_bytes)
+    return fail(SIM_EINVAL, "snapshot layout (E=%d, K=%d, C=%d, N=%d, F=%d, shadow=%d) differs "
+                "from the context's", h.n_envs, h.n_servers, h.n_classes, h.queue_cap,
+                h.obs_dim, h.shadow);
+  if (bytes < kSnapHeader + h.arena_bytes)
+    return fail(SIM_EINVAL, "snapshot truncated: %zu of %zu bytes", bytes,
+                (size_t)(kSnapHeader + h.arena_bytes));
+  HIPCHK(hipMemcpy(x->arena, src + kSnapHeader, x->arena_bytes, hipMemcpyDefault),
+         "snapshot state copy");
+  x->seed = h.seed;
+  x->tick = h.tick;
+  x->reset_done = h.reset_done != 0;
+  return SIM_OK;
+}
+
 int sim_set_timing(sim_ctx* x, int32_t on) {
   if (!x) return fail(SIM_EINVAL, "ctx is NULL");
   x->timing = on != 0;

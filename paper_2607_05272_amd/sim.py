@@ -319,6 +319,19 @@ class Sim:
             o += n
         return out
 
+    # -- checkpoint / resume ------------------------------------------------------------
+    def get_state(self, device=True):
+        """Snapshot of every environment's state, the tick counter and the seed, as a uint8
+        tensor on the device (or in host memory)."""
+        n = C.c_size_t()
+        L.check(self.lib.sim_get_state(self._ctx, None, C.byref(n)), "sim_get_state")
+        buf = torch.empty(n.value, dtype=torch.uint8, device=self.device if device else "cpu")
+        L.check(self.lib.sim_get_state(self._ctx, _p(buf), C.byref(n)), "sim_get_state")
+        return buf
+
+    def set_state(self, buf):
+        L.check(self.lib.sim_set_state(self._ctx, _p(buf), buf.numel()), "sim_set_state")
+
     # -- statistics -------------------------------------------------------------------
     def counters(self):
         cnt = torch.empty((2, L.NCNT, self.E), dtype=torch.int64, device=self.device)
