@@ -15,6 +15,7 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import threading
 import time
@@ -109,10 +110,19 @@ def static_bytes(w, tot, E, T, ticks_per_launch):
     return 2 * state_rw + 12 * K + ticks_per_launch * per_tick
 
 
-def kernel_hash():
+# the source of each kernel class (with the shared device headers)
+KERNEL_SOURCE = {"policy": "mlp_kernels.hip", "step": "sim_kernels.hip",
+                 "static": "sim_kernels.hip", "gae": "gae_kernels.hip", "ppo": "ppo_kernels.hip"}
+
+
+def kernel_hash(cls=None):
+    """Hash of the sources a kernel class is built from (all kernel sources without a class)."""
+    d = os.path.join(ROOT, "paper_2607_05272_amd", "csrc")
+    files = ([KERNEL_SOURCE[cls], "devmath.hpp", "params.hpp"] if cls in KERNEL_SOURCE else
+             sorted(f for f in os.listdir(d) if f.endswith((".hip", ".hpp"))))
     h = hashlib.sha256()
-    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2607_05272_amd", "csrc"))):
-        h.update(open(os.path.join(ROOT, "paper_2607_05272_amd", "csrc", f), "rb").read())
+    for f in files:
+        h.update(open(os.path.join(d, f), "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -125,7 +135,7 @@ def traffic_for(kernel, cfg_name):
     except (OSError, ValueError):
         return None
     ent = d.get(f"{cfg_name}:{kernel}")
-    if not ent or ent.get("kernel_hash") != kernel_hash():
+    if not ent or ent.get("kernel_hash") != kernel_hash(kernel):
         return None
     return ent.get("bytes_per_launch")
 
@@ -183,9 +193,65 @@ def write_traffic(d, cfg_name):
         out[f"{cfg_name}:{cls}"] = {
             "bytes_per_launch": fk * 1024.0 * f_fac + wk * 1024.0 * w_fac,
             "fetch_kib_raw": fk, "write_kib_raw": wk, "dispatches": [nf, nw],
-            "fetch_factor": f_fac, "write_factor": w_fac, "kernel_hash": kernel_hash()}
+            "fetch_factor": f_fac, "write_factor": w_fac, "kernel_hash": kernel_hash(cls)}
     json.dump(out, open(path, "w"), indent=1, sort_keys=True)
     print(json.dumps(out, indent=1, sort_keys=True))
+
+
+def copy_ceiling(mib=1024, reps=5):
+    """Measured HBM ceiling: a device-to-device copy of `mib` MiB (read + write bytes per
+    second, best of `reps`)."""
+    import torch
+    n = mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    best = 0.0
+    for _ in range(reps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        dst.copy_(src)
+        b.record()
+        b.synchronize()
+        best = max(best, 2.0 * n / (a.elapsed_time(b) * 1e-3) / 1e9)
+    del src, dst
+    return best
+
+
+def cpu_baseline_sim_only(w, name, budget_s, seed):
+    """The oracle's simulator alone (replayed uniform actions, no MLP) on the host cores."""
+    import numpy as np
+    import oracle
+    threads = max(1, min(16, os.cpu_count() or 1))
+    T = min(w["T"], 256)
+    A = 6 * w["n_servers"]
+    cal_ids = np.linspace(0, w["n_envs"] - 1, 16).astype(np.uint32)
+    cal_act = np.random.default_rng(seed).integers(0, A, (64, 16)).astype(np.uint8)
+    oracle.rollout(w, seed, 8, cal_ids, actions=cal_act[:8], want_obs=False, want_rec=False)
+    t0 = time.perf_counter()
+    oracle.rollout(w, seed, 64, cal_ids, actions=cal_act, want_obs=False, want_rec=False)
+    per_step = (time.perf_counter() - t0) / (64 * 16)
+    n_env = max(threads, int(budget_s * threads / (per_step * T)))
+    n_env = min(n_env, w["n_envs"])
+    ids = np.linspace(0, w["n_envs"] - 1, n_env).astype(np.uint32)
+    acts = np.random.default_rng(seed).integers(0, A, (T, n_env)).astype(np.uint8)
+    chunks = np.array_split(np.arange(n_env), threads)
+
+    def work(c):
+        if len(c):
+            oracle.rollout(w, seed, T, ids[c], actions=np.ascontiguousarray(acts[:, c]),
+                           want_obs=False, want_rec=False)
+
+    t0 = time.perf_counter()
+    th = [threading.Thread(target=work, args=(c,)) for c in chunks]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    dt = time.perf_counter() - t0
+    return {"value": n_env * T / dt, "unit": "env-steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_env} envs x {T} ticks of {name}, simulator only (uniform random "
+                      f"actions replayed), {dt:.1f} s wall on {threads} threads"}
 
 
 def cpu_baseline(w, name, budget_s, seed):
@@ -225,7 +291,7 @@ def cpu_baseline(w, name, budget_s, seed):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", default="C5", choices=sorted(DESCR))
     ap.add_argument("--ticks", type=int, default=0, help="override T (diagnostics only)")
@@ -292,9 +358,17 @@ def main():
     if args.train == "reinforce":
         lam = 1.0  # A = G - V, R = G
 
-    def one_step(i):
+    marks = []   # per timed step: events before reset, around the rollout, at the end
+
+    def one_step(i, ev=None):
+        if ev:
+            ev[0].record(sim.stream)
         sim.reset(seed + i)
+        if ev:
+            ev[1].record(sim.stream)
         sim.rollout(weights, T, traj=traj)
+        if ev:
+            ev[2].record(sim.stream)
         sim.returns_gae(traj.reward, traj.value if gae else None, w["gamma"], lam, adv, ret)
         if ppo:
             sim.ppo_minibatch_grad(weights, traj.obs, traj.actions, traj.logp, adv, ret,
@@ -303,6 +377,8 @@ def main():
             adam_t[0], _ = sim.update(weights, params, adam_m, adam_v, adam_t[0], traj.obs,
                                       traj.actions, traj.logp, adv, ret, algo, args.epochs,
                                       args.minibatches, mb, seed + i, 3e-4, want_losses=False)
+        if ev:
+            ev[3].record(sim.stream)
         return sim.stats()
 
     for i in range(args.warmup):
@@ -315,9 +391,13 @@ def main():
     t0 = time.perf_counter()
     tot = None
     for i in range(args.steps):
-        tot = one_step(1000 + i)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        marks.append(ev)
+        tot = one_step(1000 + i, ev)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    step_ms = [ev[0].elapsed_time(ev[3]) for ev in marks]
+    rollout_ms = [ev[1].elapsed_time(ev[2]) for ev in marks]
     sim.sync()
     timing = sim.get_timing(clear=True)
     sim.set_timing(False)
@@ -397,9 +477,18 @@ def main():
         "work_per_launch": work,
         "totals": {"arrivals": int(tot["cnt"][0][0]), "dropped": int(tot["cnt"][0][2]),
                    "dispatched": int(tot["cnt"][0][3]), "batches": int(tot["cnt"][0][4])},
+        # per-step event times on the library's stream: the median step, and the rollout
+        # alone (policy + sampling + simulator; reset and returns reported apart)
+        "step_ms": {"median": statistics.median(step_ms), "min": min(step_ms),
+                    "max": max(step_ms)},
+        "rollout_only": {"median_ms": statistics.median(rollout_ms),
+                         "env_steps_per_s": E * T / (statistics.median(rollout_ms) / 1000.0)},
+        "hbm_copy_ceiling_GBs": copy_ceiling(),
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.config, args.cpu_seconds, seed)
+        line["cpu_baseline_sim_only"] = cpu_baseline_sim_only(w, args.config,
+                                                              args.cpu_seconds / 3, seed)
     sim.close()
     print(json.dumps(line), flush=True)
 
