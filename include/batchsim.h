@@ -344,6 +344,22 @@ int sim_sync(sim_ctx* ctx);
 int sim_get_state(sim_ctx* ctx, void* buf, size_t* bytes);
 int sim_set_state(sim_ctx* ctx, const void* buf, size_t bytes);
 
+/* Diagnostics: one of the library's device primitives evaluated elementwise on n inputs, so
+ * that its bit identity with a host implementation can be checked directly (the parity of
+ * whole rollouts depends on it). All arrays are device memory owned by the caller; the work
+ * is enqueued on hip_stream (NULL: the default stream) and complete after it synchronizes.
+ *   SIM_PRIM_PHILOX  d_in uint32 [n][4] counters, d_out uint32 [n][4]: the Philox4x32-10
+ *                    block of each counter under the 64-bit key (low word first) (R13)
+ *   SIM_PRIM_LOG, SIM_PRIM_EXP, SIM_PRIM_COS  fp64 [n] -> fp64 [n]: the deterministic
+ *                    logarithm, exponential and cosine of the arrival and service draws (R14)
+ *   SIM_PRIM_SQRT    fp64 [n] -> fp64 [n], correctly rounded square root
+ *   SIM_PRIM_DIV     fp64 [n][2] -> fp64 [n], the first of each pair divided by the second
+ * SIM_EINVAL for an unknown kind, n < 0 or NULL arrays with n > 0.                          */
+enum { SIM_PRIM_PHILOX = 0, SIM_PRIM_LOG = 1, SIM_PRIM_EXP = 2, SIM_PRIM_COS = 3,
+       SIM_PRIM_SQRT = 4, SIM_PRIM_DIV = 5 };
+int sim_device_primitive(int32_t kind, int64_t n, uint64_t key, const void* d_in, void* d_out,
+                         void* hip_stream);
+
 /* Kernel classes for tracing. */
 enum sim_kernel_class {
   SIM_KC_POLICY = 0,  /* policy MLP + sampler */

@@ -87,6 +87,7 @@ def lib():
                                            C.c_uint64, C.c_double)
             L.orc_philox4x32.argtypes = [vp, vp, vp]
             L.orc_philox4x64.argtypes = [vp, vp, vp]
+            L.orc_philox4x32_batch.argtypes = [i64, vp, vp, vp]
             L.orc_philox_constants.argtypes = [vp]
             L.orc_draw.argtypes = [u64, u32, u32, u32, u32, u32, vp]
             L.orc_u01.argtypes = [u32, u32]
@@ -151,6 +152,15 @@ def philox4x32(ctr, key):
     o = np.zeros(4, np.uint32)
     lib().orc_philox4x32(_p(c), _p(k), _p(o))
     return o
+
+
+def philox4x32_batch(ctr, key):
+    """Philox4x32-10 blocks of counters [n][4] (uint32) under a 64-bit key (low word first)."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint32).reshape(-1, 4)
+    k = np.array([key & 0xFFFFFFFF, key >> 32], dtype=np.uint32)
+    out = np.empty_like(c)
+    lib().orc_philox4x32_batch(c.shape[0], _p(c), _p(k), _p(out))
+    return out
 
 
 def philox4x64(ctr, key):

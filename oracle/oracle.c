@@ -788,6 +788,10 @@ static int sample_action(const double* l, int A, double u, double* logp, double*
 void orc_philox4x32(const uint32_t* ctr, const uint32_t* key, uint32_t* out) {
   philox4x32_10(ctr, key, out);
 }
+/* n counters [n][4] under one key (two words) -> [n][4] blocks */
+void orc_philox4x32_batch(int64_t n, const uint32_t* ctr, const uint32_t* key, uint32_t* out) {
+  for (int64_t i = 0; i < n; i++) philox4x32_10(ctr + 4 * i, key, out + 4 * i);
+}
 void orc_philox4x64(const uint64_t* ctr, const uint64_t* key, uint64_t* out) {
   philox4x64_10(ctr, key, out);
 }

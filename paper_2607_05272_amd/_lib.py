@@ -23,7 +23,7 @@ SYMBOLS = ("sim_last_error", "sim_abi_version", "sim_create", "sim_destroy", "si
            "sim_checksums", "sim_stats", "sim_sync", "sim_set_timing", "sim_get_timing",
            "ppo_minibatch_grad", "sim_ppo_grad_count", "reinforce_minibatch_grad",
            "sim_params_from_weights", "adam_update", "sim_update", "sim_attn_weights_layout",
-           "sim_get_state", "sim_set_state")
+           "sim_get_state", "sim_set_state", "sim_device_primitive")
 ALGO_PPO, ALGO_REINFORCE = 0, 1
 KERNEL_CLASSES = ("policy", "step", "static", "gae", "reset", "other", "ppo")
 
@@ -121,6 +121,7 @@ def load():
         "sim_update": [vp, vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, vp],
         "sim_attn_weights_layout": [vp, vp],
         "sim_get_state": [vp, vp, vp], "sim_set_state": [vp, vp, C.c_size_t],
+        "sim_device_primitive": [i32, C.c_int64, u64, vp, vp, vp],
     }
     for name, args in sig.items():
         f = getattr(L, name)

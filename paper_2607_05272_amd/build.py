@@ -14,7 +14,8 @@ ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libbatchsim.so")
 BUILD = os.path.join(HERE, "_build")
 SOURCES = ["runtime.cpp", "sim_kernels.hip", "mlp_kernels.hip", "gae_kernels.hip",
-           "ppo_kernels.hip", "train_kernels.hip", "attn_kernels.hip"]
+           "ppo_kernels.hip", "train_kernels.hip", "attn_kernels.hip",
+           "prim_kernels.hip"]
 HEADERS = ["devmath.hpp", "params.hpp"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",
          "-fno-fast-math", "-Wall", "-Wno-unused-function",

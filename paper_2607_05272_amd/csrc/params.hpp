@@ -122,6 +122,10 @@ hipError_t launch_export_attn(const AttnParams& p, const float* params, void* d_
                               const size_t off[14], hipStream_t st);
 hipError_t launch_import_attn(const AttnParams& p, const void* d_weights, const size_t off[14],
                               float* params, hipStream_t st);
+// device primitives evaluated elementwise (prim_kernels.hip); kinds as in the ABI
+enum { PRIM_PHILOX = 0, PRIM_LOG = 1, PRIM_EXP = 2, PRIM_COS = 3, PRIM_SQRT = 4, PRIM_DIV = 5 };
+hipError_t launch_primitive(int kind, int64_t n, uint64_t key, const void* in, void* out,
+                            hipStream_t st);
 // the four loss terms from per-sample [M][3] fp64 terms, summed in a fixed order
 hipError_t launch_pg_loss(const double* terms, int M, float c_v, float c_h, double* out,
                           hipStream_t st);

@@ -917,6 +917,20 @@ int sim_set_state(sim_ctx* x, const void* buf, size_t bytes) {
   return SIM_OK;
 }
 
+static_assert(SIM_PRIM_PHILOX == PRIM_PHILOX && SIM_PRIM_LOG == PRIM_LOG && SIM_PRIM_EXP == PRIM_EXP &&
+                  SIM_PRIM_COS == PRIM_COS && SIM_PRIM_SQRT == PRIM_SQRT && SIM_PRIM_DIV == PRIM_DIV,
+              "primitive kinds");
+
+int sim_device_primitive(int32_t kind, int64_t n, uint64_t key, const void* d_in, void* d_out,
+                         void* hip_stream) {
+  if (kind < SIM_PRIM_PHILOX || kind > SIM_PRIM_DIV) return fail(SIM_EINVAL, "unknown primitive %d", kind);
+  if (n < 0) return fail(SIM_EINVAL, "n must be >= 0");
+  if (n > 0 && (!d_in || !d_out)) return fail(SIM_EINVAL, "NULL argument");
+  HIPCHK(launch_primitive(kind, n, key, d_in, d_out, static_cast<hipStream_t>(hip_stream)),
+         "primitive kernel launch");
+  return SIM_OK;
+}
+
 int sim_set_timing(sim_ctx* x, int32_t on) {
   if (!x) return fail(SIM_EINVAL, "ctx is NULL");
   x->timing = on != 0;
