@@ -252,8 +252,11 @@ int returns_gae(sim_ctx* ctx, int32_t T, const double* d_r, const float* d_v, do
  * W1 [F][H1], b1 [H1], W2 [H1][H2], b2 [H2], W3 [H2][A'], b3 [A'] packed back to back
  * (A' = 6K + 1; sim_ppo_grad_count gives the total); d_loss [4] fp64 = total, policy,
  * value and entropy terms; d_index [M] int64 (t E + env) or NULL. Requires value_head = 1,
- * M > 0 and a multiple of 16. Scratch of about 4 M (F + 3 H1 + 3 H2 + A') bytes is held by
- * the context after the first call. A stored action out of range latches SIM_ESTATE
+ * M > 0 and a multiple of 16. The dense products run in rocBLAS (bf16 x bf16 -> fp32 forward
+ * for a bf16 policy, fp32 otherwise; fp32 backward) with its atomics disabled, so repeated
+ * calls return identical results. Scratch of about 4 M (F + 3 H1 + 3 H2 + 2 A') bytes, plus
+ * 2 M (F + H1 + H2) and fp32 copies of W2 and W3 for a bf16 policy, and the library handle
+ * are held by the context after the first call. A stored action out of range latches SIM_ESTATE
  * (reported by sim_sync); that sample then contributes nothing.
  * For the attention policy (policy_kind = SIM_POLICY_ATTN) the forward is fp32 with exact
  * GELU and d_grads holds the fourteen arrays of sim_attn_layout in its order (w_in, b_in,

@@ -21,6 +21,8 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=o
          "-fno-fast-math", "-Wall", "-Wno-unused-function",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", os.path.join(ROOT, "include")]
+# the MLP minibatch's plain GEMMs run in rocBLAS
+LINK = ["-L/opt/rocm/lib", "-lrocblas", "-Wl,-rpath,/opt/rocm/lib"]
 
 
 def _hipcc():
@@ -59,7 +61,7 @@ def build(force=True, verbose=False):
     if failed:
         raise RuntimeError("HIP build failed:\n" + "\n\n".join(f"[{s}]\n{o}" for s, o in failed))
     tmp = LIB + ".tmp"
-    subprocess.run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp],
+    subprocess.run([hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, *LINK, "-o", tmp],
                    check=True)
     os.replace(tmp, LIB)
     return LIB

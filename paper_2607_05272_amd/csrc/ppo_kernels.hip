@@ -1,27 +1,38 @@
-// ppo_kernels.hip -- one policy-gradient minibatch (paper Sec. 4.3): gather, forward, loss
-// (PPO clipped surrogate, or REINFORCE with a learned baseline) + value + entropy, and its
-// gradient with respect to every policy weight.
+// ppo_kernels.hip -- one policy-gradient minibatch of the MLP policy (paper Sec. 4.3): gather,
+// forward, loss (PPO clipped surrogate, or REINFORCE with a learned baseline) + value +
+// entropy, and its gradient with respect to every policy weight.
 //
 // M samples (t, env) are drawn with replacement: sample m takes u from the MINIBATCH block at
 // counter (m, 0xFFFFFFFD, MINIBATCH<<24, 0) and index floor(u * T * E). The forward repeats
 // the rollout policy's rounding points (every layer input rounded to bf16) with fp32
-// arithmetic and saves pre-activations; gradients pass through the bf16 roundings as the
+// sums and saves pre-activations; gradients pass through the bf16 roundings as the
 // identity. Loss
 //   L = -mean(min(rho A, clip(rho, 1-eps, 1+eps) A)) + c_v mean((V - R)^2) - c_h mean(H),
 //   rho = exp(logp_new(a) - logp_old), H the entropy of the action distribution; REINFORCE
 //   replaces the first term by -mean(A log pi(a|s)) with A held constant.
-// Work is split into: forward (16 samples per workgroup, one output unit per thread),
-// backward through the activations (same split), and weight gradients (LDS-tiled products
-// over fixed sample chunks, fp32, summed in chunk order, so results are deterministic).
+//
+// The dense products are plain GEMMs and run in rocBLAS: the forward as bf16 x bf16 -> fp32
+// products when the policy is bf16 (the products of bf16 values are exact, the sums fp32, as in
+// the rollout kernel), as fp32 products otherwise; the backward through the activations and the
+// weight gradients as fp32 products against fp32 copies of the weights. A layer's weight and
+// bias gradients come out of one product [A | 1]^T dZ (the saved activations carry a ones
+// column), whose K+1 rows land on the contiguous W, b pair of the gradient layout. The library
+// runs with atomics disabled, so its sums are taken in an order fixed by the shapes and the
+// gradients are deterministic. The elementwise steps around the products (index draw and
+// gather, bias + GELU + bf16 rounding, the per-sample loss and its gradient, GELU') are the
+// small kernels below.
+#include <rocblas/rocblas.h>
+
+#include <cstdio>
+
 #include "devmath.hpp"
 #include "params.hpp"
 
 namespace bsim {
 namespace {
 
-constexpr int kSpb = 16;   // samples per workgroup
 constexpr int kThr = 256;
-constexpr size_t kMaxLds = 64 * 1024;  // dynamic LDS per workgroup used by the forward
+constexpr int kGs = 64;   // samples per workgroup of the gather
 
 __device__ __forceinline__ float bf16_round(float f) { return bf16_to_f32(bf16_bits(f)); }
 __device__ __forceinline__ float gelu_exact(float z) {
@@ -31,245 +42,156 @@ __device__ __forceinline__ float gelu_grad(float z) {
   return 0.5f * (1.0f + erff(z * 0.70710678118654752f)) + z * expf(-0.5f * z * z) * 0.39894228040143268f;
 }
 
-__device__ __forceinline__ float wval(const void* w, size_t i, int bf16) {
-  return bf16 ? bf16_to_f32(static_cast<const uint16_t*>(w)[i]) : static_cast<const float*>(w)[i];
-}
-
-// out[s][j] = sum_i in[s][i] W[i][j] + b[j] for the workgroup's samples; W is [K][N] in-major
-__device__ void dense_fwd(const float* in, int K, const void* W, const float* b, int N, int bf16,
-                          float* out) {
-  for (int j = threadIdx.x; j < N; j += kThr) {
-    float acc[kSpb];
-#pragma unroll
-    for (int s = 0; s < kSpb; ++s) acc[s] = b[j];
-    for (int i = 0; i < K; ++i) {
-      const float wv = wval(W, (size_t)i * N + j, bf16);
-#pragma unroll
-      for (int s = 0; s < kSpb; ++s) acc[s] = fmaf(in[s * K + i], wv, acc[s]);
+// Index draw and gather: the first kGs threads draw their sample's index, then the workgroup
+// copies the samples' observations (bf16-rounded in bf16 mode) into xa [M][F+1], whose last
+// column is 1, and their bf16 bits into xb [M][F].
+__global__ __launch_bounds__(kThr) void mb_gather_k(uint64_t seed, int M, int T, int E, int F,
+                                                    int bf16, const float* __restrict__ obs,
+                                                    int64_t* __restrict__ idx,
+                                                    int64_t* __restrict__ idx_out,
+                                                    float* __restrict__ xa,
+                                                    uint16_t* __restrict__ xb) {
+  __shared__ int ts_[kGs], es_[kGs];
+  const int m0 = blockIdx.x * kGs;
+  const int ns = M - m0 < kGs ? M - m0 : kGs;
+  if ((int)threadIdx.x < ns) {
+    const int m = m0 + threadIdx.x;
+    const u32x4 w = draw(seed, (uint32_t)m, 0xFFFFFFFDu, P_MINIBATCH, 0, 0);
+    const double n = (double)T * (double)E;
+    long long i = (long long)(unit(w.x, w.y) * n);
+    if (i > (long long)T * E - 1) i = (long long)T * E - 1;
+    ts_[threadIdx.x] = (int)(i / E);
+    es_[threadIdx.x] = (int)(i % E);
+    idx[m] = i;
+    if (idx_out) idx_out[m] = i;
+  }
+  __syncthreads();
+  for (int q = threadIdx.x; q < ns * (F + 1); q += kThr) {
+    const int s = q / (F + 1), f = q % (F + 1);
+    const size_t m = (size_t)(m0 + s);
+    if (f == F) {
+      xa[m * (F + 1) + F] = 1.0f;
+      continue;
     }
-#pragma unroll
-    for (int s = 0; s < kSpb; ++s) out[s * N + j] = acc[s];
+    float v = obs[((size_t)ts_[s] * F + f) * E + es_[s]];
+    if (bf16) {
+      v = bf16_round(v);
+      xb[m * F + f] = bf16_bits(v);
+    }
+    xa[m * (F + 1) + f] = v;
   }
 }
 
-struct PpoArgs {
-  int F, H1, H2, A, Ap, E, T, M, bf16;
-  const void* w1; const float* b1;   // ABI weights, in-major
-  const void* w2; const float* b2;
-  const void* w3; const float* b3;
-  int AP;
-  const float* obs;                  // [T(+1)][F][E]
+// z [M][N] holds x W; adds the bias in place, then h = GELU(z) (bf16-rounded in bf16 mode)
+// into ha [M][N+1] with a ones column and, in bf16 mode, its bits into hb [M][N].
+__global__ __launch_bounds__(kThr) void mb_bias_gelu_k(int M, int N, int bf16,
+                                                       const float* __restrict__ b,
+                                                       float* __restrict__ z,
+                                                       float* __restrict__ ha,
+                                                       uint16_t* __restrict__ hb) {
+  const uint32_t n = (uint32_t)M * (uint32_t)(N + 1);
+  for (uint32_t q = blockIdx.x * kThr + threadIdx.x; q < n; q += gridDim.x * kThr) {
+    const uint32_t m = q / (uint32_t)(N + 1), j = q % (uint32_t)(N + 1);
+    if (j == (uint32_t)N) {
+      ha[q] = 1.0f;
+      continue;
+    }
+    const uint32_t zi = m * (uint32_t)N + j;
+    const float v = z[zi] + b[j];
+    z[zi] = v;
+    float h = gelu_exact(v);
+    if (bf16) {
+      h = bf16_round(h);
+      hb[zi] = bf16_bits(h);
+    }
+    ha[q] = h;
+  }
+}
+
+struct LossArgs {
+  int A, Ap, M, reinforce;
+  float clip, c_v, c_h;
+  float* out;                        // [M][Ap]: h2 W3 on entry, the outputs (with b3) on exit
+  const float* b3;
+  const int64_t* idx;                // [M] sampled t * E + env
   const uint8_t* act;
   const float* logp_old;
   const double* adv;
   const double* ret;
-  uint64_t seed;
-  int reinforce;                     // 0: PPO clipped surrogate; 1: REINFORCE with baseline
-  float clip, c_v, c_h;
-  float* x; float* z1; float* h1; float* z2; float* h2; float* dout;
-  float* dz1; float* dz2;
+  float* dout;                       // [M][Ap] dL/d(output)
   double* terms;                     // [M][3] policy, value, entropy per sample
-  int64_t* idx_out;                  // optional [M] sampled t * E + env
-  uint32_t* err;                     // device error flags
+  uint32_t* err;
 };
 
-__global__ __launch_bounds__(kThr) void ppo_fwd_k(PpoArgs a) {
-  extern __shared__ float sm[];
-  float* xs = sm;                          // [kSpb][F]
-  float* h1s = xs + kSpb * a.F;            // [kSpb][H1]
-  float* h2s = h1s + kSpb * a.H1;          // [kSpb][H2]
-  float* os = h2s + kSpb * a.H2;           // [kSpb][Ap]
-  __shared__ int ts_[kSpb], es_[kSpb];
-  const int m0 = blockIdx.x * kSpb;
-  if (threadIdx.x < kSpb) {
-    const int m = m0 + threadIdx.x;
-    const u32x4 w = draw(a.seed, (uint32_t)m, 0xFFFFFFFDu, P_MINIBATCH, 0, 0);
-    const double n = (double)a.T * (double)a.E;
-    long long i = (long long)(unit(w.x, w.y) * n);
-    if (i > (long long)a.T * a.E - 1) i = (long long)a.T * a.E - 1;
-    ts_[threadIdx.x] = (int)(i / a.E);
-    es_[threadIdx.x] = (int)(i % a.E);
-    if (a.idx_out) a.idx_out[m] = i;
+// loss terms and the loss gradient with respect to the outputs, one thread per sample
+__global__ __launch_bounds__(kThr) void mb_loss_k(LossArgs a) {
+  const int m = blockIdx.x * kThr + threadIdx.x;
+  if (m >= a.M) return;
+  float* l = a.out + (size_t)m * a.Ap;
+  float* d = a.dout + (size_t)m * a.Ap;
+  double* tm = a.terms + (size_t)m * 3;
+  for (int i = 0; i < a.Ap; ++i) l[i] += a.b3[i];
+  const size_t ti = (size_t)a.idx[m];
+  const int act = a.act[ti];
+  if (act >= a.A) {  // invalid stored action: flag it, the sample contributes nothing
+    atomicOr(a.err, ERR_ACTION);
+    for (int i = 0; i < a.Ap; ++i) d[i] = 0.0f;
+    tm[0] = tm[1] = tm[2] = 0.0;
+    return;
   }
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < kSpb * a.F; idx += kThr) {
-    const int s = idx / a.F, f = idx % a.F;
-    float v = a.obs[((size_t)ts_[s] * a.F + f) * a.E + es_[s]];
-    if (a.bf16) v = bf16_round(v);
-    xs[idx] = v;
-    a.x[(size_t)(m0 + s) * a.F + f] = v;
+  const float adv = (float)a.adv[ti], ret = (float)a.ret[ti];
+  float mx = l[0];
+  for (int i = 1; i < a.A; ++i) mx = fmaxf(mx, l[i]);
+  float S = 0.f;
+  for (int i = 0; i < a.A; ++i) S += expf(l[i] - mx);
+  const float lS = logf(S);
+  float H = 0.f;
+  for (int i = 0; i < a.A; ++i) {
+    const float lp = (l[i] - mx) - lS;
+    H -= expf(lp) * lp;
   }
-  __syncthreads();
-  dense_fwd(xs, a.F, a.w1, a.b1, a.H1, a.bf16, h1s);
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < kSpb * a.H1; idx += kThr) {
-    const float z = h1s[idx];
-    float h = gelu_exact(z);
-    if (a.bf16) h = bf16_round(h);
-    a.z1[(size_t)m0 * a.H1 + idx] = z;
-    a.h1[(size_t)m0 * a.H1 + idx] = h;
-    h1s[idx] = h;
+  const float logp = (l[act] - mx) - lS;
+  const float invM = 1.0f / (float)a.M;
+  float dlogp, pterm;
+  if (a.reinforce) {
+    // -A log pi(a|s), the advantage held constant
+    dlogp = -adv * invM;
+    pterm = -adv * logp;
+  } else {
+    const float rho = expf(logp - a.logp_old[ti]);
+    const float lo = 1.0f - a.clip, hi = 1.0f + a.clip;
+    const float rc = fminf(fmaxf(rho, lo), hi);
+    const float s1 = rho * adv, s2 = rc * adv;
+    const float g_rho = s1 <= s2 ? adv : ((rho > lo && rho < hi) ? adv : 0.0f);
+    dlogp = -g_rho * rho * invM;
+    pterm = -fminf(s1, s2);
   }
-  __syncthreads();
-  dense_fwd(h1s, a.H1, a.w2, a.b2, a.H2, a.bf16, h2s);
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < kSpb * a.H2; idx += kThr) {
-    const float z = h2s[idx];
-    float h = gelu_exact(z);
-    if (a.bf16) h = bf16_round(h);
-    a.z2[(size_t)m0 * a.H2 + idx] = z;
-    a.h2[(size_t)m0 * a.H2 + idx] = h;
-    h2s[idx] = h;
+  for (int i = 0; i < a.A; ++i) {
+    const float lp = (l[i] - mx) - lS;
+    const float p = expf(lp);
+    float g = -dlogp * p + a.c_h * invM * p * (lp + H);
+    if (i == act) g += dlogp;
+    d[i] = g;
   }
-  __syncthreads();
-  dense_fwd(h2s, a.H2, a.w3, a.b3, a.Ap, a.bf16, os);
-  __syncthreads();
-  // loss gradient with respect to the outputs, one thread per sample
-  if (threadIdx.x < kSpb) {
-    const int s = threadIdx.x, m = m0 + s;
-    const float* l = os + s * a.Ap;
-    float* d = a.dout + (size_t)m * a.Ap;
-    const size_t ti = (size_t)ts_[s] * a.E + es_[s];
-    const int act = a.act[ti];
-    double* tm = a.terms + (size_t)m * 3;
-    if (act >= a.A) {  // invalid stored action: flag it, the sample contributes nothing
-      atomicOr(a.err, ERR_ACTION);
-      for (int i = 0; i < a.Ap; ++i) d[i] = 0.0f;
-      tm[0] = tm[1] = tm[2] = 0.0;
-      return;
-    }
-    const float adv = (float)a.adv[ti], ret = (float)a.ret[ti];
-    float mx = l[0];
-    for (int i = 1; i < a.A; ++i) mx = fmaxf(mx, l[i]);
-    float S = 0.f;
-    for (int i = 0; i < a.A; ++i) S += expf(l[i] - mx);
-    const float lS = logf(S);
-    float H = 0.f;
-    for (int i = 0; i < a.A; ++i) {
-      const float lp = (l[i] - mx) - lS;
-      H -= expf(lp) * lp;
-    }
-    const float logp = (l[act] - mx) - lS;
-    const float invM = 1.0f / (float)a.M;
-    float dlogp, pterm;
-    if (a.reinforce) {
-      // -A log pi(a|s), the advantage held constant
-      dlogp = -adv * invM;
-      pterm = -adv * logp;
-    } else {
-      const float rho = expf(logp - a.logp_old[ti]);
-      const float lo = 1.0f - a.clip, hi = 1.0f + a.clip;
-      const float rc = fminf(fmaxf(rho, lo), hi);
-      const float s1 = rho * adv, s2 = rc * adv;
-      const float g_rho = s1 <= s2 ? adv : ((rho > lo && rho < hi) ? adv : 0.0f);
-      dlogp = -g_rho * rho * invM;
-      pterm = -fminf(s1, s2);
-    }
-    for (int i = 0; i < a.A; ++i) {
-      const float lp = (l[i] - mx) - lS;
-      const float p = expf(lp);
-      float g = -dlogp * p + a.c_h * invM * p * (lp + H);
-      if (i == act) g += dlogp;
-      d[i] = g;
-    }
-    const float v = l[a.A];
-    d[a.A] = 2.0f * a.c_v * (v - ret) * invM;
-    tm[0] = (double)pterm;
-    tm[1] = (double)(v - ret) * (double)(v - ret);
-    tm[2] = (double)H;
-  }
+  const float v = l[a.A];
+  d[a.A] = 2.0f * a.c_v * (v - ret) * invM;
+  tm[0] = (double)pterm;
+  tm[1] = (double)(v - ret) * (double)(v - ret);
+  tm[2] = (double)H;
 }
 
-// dz2 = (dout W3^T) * gelu'(z2); dz1 = (dz2 W2^T) * gelu'(z1); thread j walks row j of the
-// in-major weights.
-__global__ __launch_bounds__(kThr) void ppo_bwd_k(PpoArgs a) {
-  extern __shared__ float sm[];
-  float* ds = sm;                          // [kSpb][Ap]
-  float* d2 = ds + kSpb * a.Ap;            // [kSpb][H2]
-  const int m0 = blockIdx.x * kSpb;
-  for (int idx = threadIdx.x; idx < kSpb * a.Ap; idx += kThr) ds[idx] = a.dout[(size_t)m0 * a.Ap + idx];
-  __syncthreads();
-  for (int j = threadIdx.x; j < a.H2; j += kThr) {
-    float acc[kSpb];
-#pragma unroll
-    for (int s = 0; s < kSpb; ++s) acc[s] = 0.f;
-    for (int o = 0; o < a.Ap; ++o) {
-      const float wv = wval(a.w3, (size_t)j * a.Ap + o, a.bf16);
-#pragma unroll
-      for (int s = 0; s < kSpb; ++s) acc[s] = fmaf(ds[s * a.Ap + o], wv, acc[s]);
-    }
-#pragma unroll
-    for (int s = 0; s < kSpb; ++s) {
-      const float g = acc[s] * gelu_grad(a.z2[(size_t)(m0 + s) * a.H2 + j]);
-      d2[s * a.H2 + j] = g;
-      a.dz2[(size_t)(m0 + s) * a.H2 + j] = g;
-    }
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < a.H1; i += kThr) {
-    float acc[kSpb];
-#pragma unroll
-    for (int s = 0; s < kSpb; ++s) acc[s] = 0.f;
-    for (int j = 0; j < a.H2; ++j) {
-      const float wv = wval(a.w2, (size_t)i * a.H2 + j, a.bf16);
-#pragma unroll
-      for (int s = 0; s < kSpb; ++s) acc[s] = fmaf(d2[s * a.H2 + j], wv, acc[s]);
-    }
-#pragma unroll
-    for (int s = 0; s < kSpb; ++s)
-      a.dz1[(size_t)(m0 + s) * a.H1 + i] = acc[s] * gelu_grad(a.z1[(size_t)(m0 + s) * a.H1 + i]);
-  }
+// d *= GELU'(z), elementwise over n entries
+__global__ __launch_bounds__(kThr) void mb_gelu_bwd_k(uint32_t n, const float* __restrict__ z,
+                                                      float* __restrict__ d) {
+  for (uint32_t q = blockIdx.x * kThr + threadIdx.x; q < n; q += gridDim.x * kThr)
+    d[q] = d[q] * gelu_grad(z[q]);
 }
 
-// Weight gradients as one augmented product per layer: G = [A | 1]^T B, (K+1) x N, whose
-// first K rows are dW = A^T B and whose last row is db = sum_m B[m]. The samples are split
-// into chunks of kMC; workgroup (ti, tj, c) forms a 32 x 32 tile of chunk c's partial product
-// from LDS-staged 32-sample slices (fp32, each thread 2 x 2 outputs); a second pass adds the
-// chunks in order. The result does not depend on the launch, only on M.
-constexpr int kWT = 32, kMS = 32, kMC = 512;
-
-__global__ __launch_bounds__(256) void wgrad_part_k(const float* __restrict__ Am, int K,
-                                                    const float* __restrict__ Bm, int N, int M,
-                                                    float* __restrict__ part) {
-  __shared__ float As[kMS][kWT + 1], Bs[kMS][kWT + 1];
-  const int i0 = blockIdx.x * kWT, j0 = blockIdx.y * kWT, c = blockIdx.z;
-  const int m0 = c * kMC, m1 = m0 + kMC < M ? m0 + kMC : M;
-  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
-  float acc00 = 0.f, acc01 = 0.f, acc10 = 0.f, acc11 = 0.f;
-  for (int ms = m0; ms < m1; ms += kMS) {
-    for (int q = threadIdx.x; q < kMS * kWT; q += 256) {
-      const int r = q / kWT, col = q % kWT, m = ms + r;
-      const int i = i0 + col, j = j0 + col;
-      As[r][col] = m < m1 ? (i < K ? Am[(size_t)m * K + i] : (i == K ? 1.0f : 0.0f)) : 0.0f;
-      Bs[r][col] = (m < m1 && j < N) ? Bm[(size_t)m * N + j] : 0.0f;
-    }
-    __syncthreads();
-#pragma unroll 8
-    for (int r = 0; r < kMS; ++r) {
-      const float a0 = As[r][2 * ty], a1 = As[r][2 * ty + 1];
-      const float b0 = Bs[r][2 * tx], b1 = Bs[r][2 * tx + 1];
-      acc00 = fmaf(a0, b0, acc00);
-      acc01 = fmaf(a0, b1, acc01);
-      acc10 = fmaf(a1, b0, acc10);
-      acc11 = fmaf(a1, b1, acc11);
-    }
-    __syncthreads();
-  }
-  const int i = i0 + 2 * ty, j = j0 + 2 * tx;
-  float* out = part + (size_t)c * (K + 1) * N;
-  if (i <= K && j < N) out[(size_t)i * N + j] = acc00;
-  if (i <= K && j + 1 < N) out[(size_t)i * N + j + 1] = acc01;
-  if (i + 1 <= K && j < N) out[(size_t)(i + 1) * N + j] = acc10;
-  if (i + 1 <= K && j + 1 < N) out[(size_t)(i + 1) * N + j + 1] = acc11;
-}
-
-__global__ __launch_bounds__(256) void wgrad_sum_k(const float* __restrict__ part, int nc,
-                                                   size_t n, float* __restrict__ g) {
-  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= n) return;
-  float s = 0.f;
-  for (int c = 0; c < nc; ++c) s += part[(size_t)c * n + idx];
-  g[idx] = s;
+// fp32 copy of bf16 weights
+__global__ __launch_bounds__(kThr) void mb_widen_k(uint32_t n, const uint16_t* __restrict__ w,
+                                                   float* __restrict__ o) {
+  for (uint32_t q = blockIdx.x * kThr + threadIdx.x; q < n; q += gridDim.x * kThr)
+    o[q] = bf16_to_f32(w[q]);
 }
 
 // loss terms summed in a fixed order by one workgroup
@@ -294,90 +216,209 @@ __global__ __launch_bounds__(kThr) void ppo_loss_k(const double* terms, int M, f
   }
 }
 
+unsigned grid_for(size_t n) {
+  const size_t g = (n + kThr - 1) / kThr;
+  return (unsigned)(g < 4096 ? (g ? g : 1) : 4096);
+}
+
+// the scratch carve-up; every piece starts on a 256-byte boundary
+struct MbScratch {
+  int64_t* idx;
+  float *xa, *h1a, *h2a, *z1, *z2, *out, *dout, *d1, *d2, *w2f, *w3f;
+  uint16_t *xb, *h1b, *h2b;
+  double* terms;
+};
+
+size_t carve(const MlpParams& m, int M, void* base, MbScratch* s) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    void* p = base ? static_cast<unsigned char*>(base) + off : nullptr;
+    off += (bytes + 255) & ~(size_t)255;
+    return p;
+  };
+  const size_t Ms = (size_t)M;
+  MbScratch t;
+  t.idx = static_cast<int64_t*>(take(Ms * sizeof(int64_t)));
+  t.xa = static_cast<float*>(take(Ms * (m.F + 1) * sizeof(float)));
+  t.h1a = static_cast<float*>(take(Ms * (m.H1 + 1) * sizeof(float)));
+  t.h2a = static_cast<float*>(take(Ms * (m.H2 + 1) * sizeof(float)));
+  t.z1 = static_cast<float*>(take(Ms * m.H1 * sizeof(float)));
+  t.z2 = static_cast<float*>(take(Ms * m.H2 * sizeof(float)));
+  t.out = static_cast<float*>(take(Ms * m.Ap * sizeof(float)));
+  t.dout = static_cast<float*>(take(Ms * m.Ap * sizeof(float)));
+  t.d1 = static_cast<float*>(take(Ms * m.H1 * sizeof(float)));
+  t.d2 = static_cast<float*>(take(Ms * m.H2 * sizeof(float)));
+  t.terms = static_cast<double*>(take(Ms * 3 * sizeof(double)));
+  if (m.bf16) {
+    t.xb = static_cast<uint16_t*>(take(Ms * m.F * sizeof(uint16_t)));
+    t.h1b = static_cast<uint16_t*>(take(Ms * m.H1 * sizeof(uint16_t)));
+    t.h2b = static_cast<uint16_t*>(take(Ms * m.H2 * sizeof(uint16_t)));
+    t.w2f = static_cast<float*>(take((size_t)m.H1 * m.H2 * sizeof(float)));
+    t.w3f = static_cast<float*>(take((size_t)m.H2 * m.Ap * sizeof(float)));
+  } else {
+    t.xb = t.h1b = t.h2b = nullptr;
+    t.w2f = t.w3f = nullptr;
+  }
+  if (s) *s = t;
+  return off;
+}
+
+// rocBLAS is column-major: a row-major [R][C] array with leading dimension ld is its C x R
+// column-major view, so each row-major product below is issued with its factors swapped.
+struct Gemm {
+  rocblas_handle h;
+  const char* failed = nullptr;   // the product that failed
+  rocblas_status status = rocblas_status_success;
+
+  bool ok(rocblas_status s, const char* what) {
+    if (s != rocblas_status_success && !failed) {
+      failed = what;
+      status = s;
+    }
+    return s == rocblas_status_success;
+  }
+  // Z [M][N] = In [M][K] (leading dimension ldi) W [K][N]
+  bool fwd(bool bf16, int M, int K, int N, const void* in, int ldi, const void* w, float* z,
+           const char* what) {
+    const float one = 1.0f, zero = 0.0f;
+    if (bf16)
+      return ok(rocblas_gemm_ex(h, rocblas_operation_none, rocblas_operation_none, N, M, K, &one, w,
+                                rocblas_datatype_bf16_r, N, in, rocblas_datatype_bf16_r, ldi, &zero,
+                                z, rocblas_datatype_f32_r, N, z, rocblas_datatype_f32_r, N,
+                                rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0,
+                                rocblas_gemm_flags_none),
+                what);
+    return ok(rocblas_sgemm(h, rocblas_operation_none, rocblas_operation_none, N, M, K, &one,
+                            static_cast<const float*>(w), N, static_cast<const float*>(in), ldi,
+                            &zero, z, N),
+              what);
+  }
+  // dIn [M][K] = dZ [M][N] W^T, W [K][N]
+  bool bwd(int M, int K, int N, const float* dz, const float* w, float* din, const char* what) {
+    const float one = 1.0f, zero = 0.0f;
+    return ok(rocblas_sgemm(h, rocblas_operation_transpose, rocblas_operation_none, K, M, N, &one,
+                            w, N, dz, N, &zero, din, K),
+              what);
+  }
+  // G [K+1][N] = Aaug^T dZ, Aaug [M][K+1] (the activations and a ones column), dZ [M][N]
+  bool wgrad(int M, int K, int N, const float* aaug, const float* dz, float* g, const char* what) {
+    const float one = 1.0f, zero = 0.0f;
+    return ok(rocblas_sgemm(h, rocblas_operation_none, rocblas_operation_transpose, N, K + 1, M,
+                            &one, dz, N, aaug, K + 1, &zero, g, N),
+              what);
+  }
+};
+
+thread_local char g_blas_msg[192];
+
 }  // namespace
 
-size_t ppo_lds_bytes(const MlpParams& m) {
-  return (size_t)kSpb * (m.F + m.H1 + m.H2 + m.Ap) * sizeof(float);
+void* mb_blas_create(const char** why) {
+  rocblas_handle h = nullptr;
+  rocblas_status s = rocblas_create_handle(&h);
+  if (s == rocblas_status_success) s = rocblas_set_atomics_mode(h, rocblas_atomics_not_allowed);
+  if (s == rocblas_status_success) s = rocblas_set_pointer_mode(h, rocblas_pointer_mode_host);
+  if (s != rocblas_status_success) {
+    if (h) (void)rocblas_destroy_handle(h);
+    std::snprintf(g_blas_msg, sizeof g_blas_msg, "rocBLAS handle set-up failed: %s",
+                  rocblas_status_to_string(s));
+    if (why) *why = g_blas_msg;
+    return nullptr;
+  }
+  return h;
 }
+
+void mb_blas_destroy(void* blas) {
+  if (blas) (void)rocblas_destroy_handle(static_cast<rocblas_handle>(blas));
+}
+
+size_t ppo_scratch_bytes(const MlpParams& m, int M) { return carve(m, M, nullptr, nullptr); }
 
 hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t off[6], int T,
                       const float* obs, const uint8_t* act, const float* logp_old,
                       const double* adv, const double* ret, int M, uint64_t seed, float clip,
-                      float c_v, float c_h, int reinforce, float* scratch, double* loss_out,
-                      float* grads, int64_t* idx_out, uint32_t* err, hipStream_t st) {
+                      float c_v, float c_h, int reinforce, void* scratch, double* loss_out,
+                      float* grads, int64_t* idx_out, uint32_t* err, void* blas,
+                      const char** why, hipStream_t st) {
+  if (M < 1 || !blas) return hipErrorInvalidValue;
   const unsigned char* wb = static_cast<const unsigned char*>(d_weights);
-  PpoArgs a;
-  a.F = m.F; a.H1 = m.H1; a.H2 = m.H2; a.A = m.A; a.Ap = m.Ap; a.E = m.E; a.T = T; a.M = M;
-  a.bf16 = m.bf16; a.AP = m.AP;
-  a.w1 = wb + off[0]; a.b1 = reinterpret_cast<const float*>(wb + off[1]);
-  a.w2 = wb + off[2]; a.b2 = reinterpret_cast<const float*>(wb + off[3]);
-  a.w3 = wb + off[4]; a.b3 = reinterpret_cast<const float*>(wb + off[5]);
-  a.obs = obs; a.act = act; a.logp_old = logp_old; a.adv = adv; a.ret = ret;
-  a.seed = seed; a.clip = clip; a.c_v = c_v; a.c_h = c_h; a.reinforce = reinforce;
-  a.idx_out = idx_out; a.err = err;
-  float* p = scratch;
-  a.x = p; p += (size_t)M * m.F;
-  a.z1 = p; p += (size_t)M * m.H1;
-  a.h1 = p; p += (size_t)M * m.H1;
-  a.z2 = p; p += (size_t)M * m.H2;
-  a.h2 = p; p += (size_t)M * m.H2;
-  a.dout = p; p += (size_t)M * m.Ap;
-  a.dz1 = p; p += (size_t)M * m.H1;
-  a.dz2 = p; p += (size_t)M * m.H2;
-  a.terms = reinterpret_cast<double*>(p);
-  const int blocks = M / kSpb;
-  const size_t lds_f = ppo_lds_bytes(m);
-  if (lds_f > kMaxLds || M % kSpb) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(ppo_fwd_k, dim3(blocks), dim3(kThr), lds_f, st, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const size_t lds_b = (size_t)kSpb * (m.Ap + m.H2) * sizeof(float);
-  hipLaunchKernelGGL(ppo_bwd_k, dim3(blocks), dim3(kThr), lds_b, st, a);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  // gradient layout: W1 [F][H1], b1, W2 [H1][H2], b2, W3 [H2][Ap], b3 (fp32, contiguous)
-  float* gw1 = grads;
-  float* gb1 = gw1 + (size_t)m.F * m.H1;
-  float* gw2 = gb1 + m.H1;
-  float* gb2 = gw2 + (size_t)m.H1 * m.H2;
-  float* gw3 = gb2 + m.H2;
-  // the three augmented products [x|1]^T dz1, [h1|1]^T dz2, [h2|1]^T dout land on W,b pairs
-  // that are contiguous in the gradient layout
-  const struct { const float* A; int K; const float* B; int N; float* G; } g[3] = {
-      {a.x, m.F, a.dz1, m.H1, gw1}, {a.h1, m.H1, a.dz2, m.H2, gw2}, {a.h2, m.H2, a.dout, m.Ap, gw3}};
-  const int nc = (M + kMC - 1) / kMC;
-  float* part = reinterpret_cast<float*>(a.terms + (size_t)M * 3);
-  for (int l = 0; l < 3; ++l) {
-    const dim3 grid((unsigned)((g[l].K + 1 + kWT - 1) / kWT), (unsigned)((g[l].N + kWT - 1) / kWT),
-                    (unsigned)nc);
-    hipLaunchKernelGGL(wgrad_part_k, grid, dim3(256), 0, st, g[l].A, g[l].K, g[l].B, g[l].N, M,
-                       part);
-    e = hipGetLastError();
+  const void* w1 = wb + off[0];
+  const float* b1 = reinterpret_cast<const float*>(wb + off[1]);
+  const void* w2 = wb + off[2];
+  const float* b2 = reinterpret_cast<const float*>(wb + off[3]);
+  const void* w3 = wb + off[4];
+  const float* b3 = reinterpret_cast<const float*>(wb + off[5]);
+  MbScratch s;
+  carve(m, M, scratch, &s);
+  const bool bf = m.bf16 != 0;
+  Gemm g{static_cast<rocblas_handle>(blas)};
+  if (!g.ok(rocblas_set_stream(g.h, st), "set_stream")) goto blas_fail;
+  {
+    hipLaunchKernelGGL(mb_gather_k, dim3((unsigned)((M + kGs - 1) / kGs)), dim3(kThr), 0, st, seed,
+                       M, T, m.E, m.F, m.bf16, obs, s.idx, idx_out, s.xa, s.xb);
+    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const size_t n = (size_t)(g[l].K + 1) * g[l].N;
-    hipLaunchKernelGGL(wgrad_sum_k, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, nc,
-                       n, g[l].G);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if (bf) {
+      const uint32_t n2 = (uint32_t)m.H1 * m.H2, n3 = (uint32_t)m.H2 * m.Ap;
+      hipLaunchKernelGGL(mb_widen_k, dim3(grid_for(n2)), dim3(kThr), 0, st, n2,
+                         static_cast<const uint16_t*>(w2), s.w2f);
+      hipLaunchKernelGGL(mb_widen_k, dim3(grid_for(n3)), dim3(kThr), 0, st, n3,
+                         static_cast<const uint16_t*>(w3), s.w3f);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    const float* w2f = bf ? s.w2f : static_cast<const float*>(w2);
+    const float* w3f = bf ? s.w3f : static_cast<const float*>(w3);
+    // forward: three products, each followed by its bias (and GELU)
+    if (!g.fwd(bf, M, m.F, m.H1, bf ? (const void*)s.xb : s.xa, bf ? m.F : m.F + 1, w1, s.z1,
+               "forward layer 1"))
+      goto blas_fail;
+    hipLaunchKernelGGL(mb_bias_gelu_k, dim3(grid_for((size_t)M * (m.H1 + 1))), dim3(kThr), 0, st,
+                       M, m.H1, m.bf16, b1, s.z1, s.h1a, s.h1b);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (!g.fwd(bf, M, m.H1, m.H2, bf ? (const void*)s.h1b : s.h1a, bf ? m.H1 : m.H1 + 1, w2, s.z2,
+               "forward layer 2"))
+      goto blas_fail;
+    hipLaunchKernelGGL(mb_bias_gelu_k, dim3(grid_for((size_t)M * (m.H2 + 1))), dim3(kThr), 0, st,
+                       M, m.H2, m.bf16, b2, s.z2, s.h2a, s.h2b);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (!g.fwd(bf, M, m.H2, m.Ap, bf ? (const void*)s.h2b : s.h2a, bf ? m.H2 : m.H2 + 1, w3, s.out,
+               "forward layer 3"))
+      goto blas_fail;
+    LossArgs la;
+    la.A = m.A; la.Ap = m.Ap; la.M = M; la.reinforce = reinforce;
+    la.clip = clip; la.c_v = c_v; la.c_h = c_h;
+    la.out = s.out; la.b3 = b3; la.idx = s.idx; la.act = act; la.logp_old = logp_old;
+    la.adv = adv; la.ret = ret; la.dout = s.dout; la.terms = s.terms; la.err = err;
+    hipLaunchKernelGGL(mb_loss_k, dim3((unsigned)((M + kThr - 1) / kThr)), dim3(kThr), 0, st, la);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // gradient layout: W1 [F][H1], b1, W2 [H1][H2], b2, W3 [H2][Ap], b3 (fp32, contiguous)
+    float* gw1 = grads;
+    float* gw2 = gw1 + (size_t)(m.F + 1) * m.H1;
+    float* gw3 = gw2 + (size_t)(m.H1 + 1) * m.H2;
+    if (!g.wgrad(M, m.H2, m.Ap, s.h2a, s.dout, gw3, "weight gradient layer 3")) goto blas_fail;
+    if (!g.bwd(M, m.H2, m.Ap, s.dout, w3f, s.d2, "backward layer 3")) goto blas_fail;
+    const uint32_t n2 = (uint32_t)M * m.H2, n1 = (uint32_t)M * m.H1;
+    hipLaunchKernelGGL(mb_gelu_bwd_k, dim3(grid_for(n2)), dim3(kThr), 0, st, n2, s.z2, s.d2);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (!g.wgrad(M, m.H1, m.H2, s.h1a, s.d2, gw2, "weight gradient layer 2")) goto blas_fail;
+    if (!g.bwd(M, m.H1, m.H2, s.d2, w2f, s.d1, "backward layer 2")) goto blas_fail;
+    hipLaunchKernelGGL(mb_gelu_bwd_k, dim3(grid_for(n1)), dim3(kThr), 0, st, n1, s.z1, s.d1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (!g.wgrad(M, m.F, m.H1, s.xa, s.d1, gw1, "weight gradient layer 1")) goto blas_fail;
+    hipLaunchKernelGGL(ppo_loss_k, dim3(1), dim3(kThr), 0, st, s.terms, M, c_v, c_h, loss_out);
+    return hipGetLastError();
   }
-  hipLaunchKernelGGL(ppo_loss_k, dim3(1), dim3(kThr), 0, st, a.terms, M, c_v, c_h, loss_out);
-  return hipGetLastError();
+blas_fail:
+  std::snprintf(g_blas_msg, sizeof g_blas_msg, "rocBLAS %s: %s", g.failed ? g.failed : "?",
+                rocblas_status_to_string(g.status));
+  if (why) *why = g_blas_msg;
+  return hipErrorLaunchFailure;
 }
 
 hipError_t launch_pg_loss(const double* terms, int M, float c_v, float c_h, double* out,
                           hipStream_t st) {
   hipLaunchKernelGGL(ppo_loss_k, dim3(1), dim3(kThr), 0, st, terms, M, c_v, c_h, out);
   return hipGetLastError();
-}
-
-size_t ppo_scratch_floats(const MlpParams& m, int M) {
-  // activations, per-sample loss terms (fp64), then the chunked weight-gradient partials
-  const size_t nc = (size_t)(M + kMC - 1) / kMC;
-  size_t kn = (size_t)(m.F + 1) * m.H1;
-  if ((size_t)(m.H1 + 1) * m.H2 > kn) kn = (size_t)(m.H1 + 1) * m.H2;
-  if ((size_t)(m.H2 + 1) * m.Ap > kn) kn = (size_t)(m.H2 + 1) * m.Ap;
-  return (size_t)M * (m.F + 2 * m.H1 + 2 * m.H2 + m.Ap + m.H1 + m.H2) + (size_t)M * 3 * 2 +
-         nc * kn + 64;
 }
 
 }  // namespace bsim
