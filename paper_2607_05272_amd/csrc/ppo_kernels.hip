@@ -32,7 +32,7 @@ namespace bsim {
 namespace {
 
 constexpr int kThr = 256;
-constexpr int kGs = 64;   // samples per workgroup of the gather
+constexpr int kGs = 16;   // samples per workgroup of the gather
 
 __device__ __forceinline__ float bf16_round(float f) { return bf16_to_f32(bf16_bits(f)); }
 __device__ __forceinline__ float gelu_exact(float z) {
@@ -123,34 +123,56 @@ struct LossArgs {
   uint32_t* err;
 };
 
-// loss terms and the loss gradient with respect to the outputs, one thread per sample
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Loss terms and the loss gradient with respect to the outputs, one wavefront per sample:
+// lane i holds outputs i and i + 64 (A' <= 128), max and sums are butterfly reductions.
+constexpr int kLossWaves = kThr / 64;
 __global__ __launch_bounds__(kThr) void mb_loss_k(LossArgs a) {
-  const int m = blockIdx.x * kThr + threadIdx.x;
-  if (m >= a.M) return;
+  const int m = blockIdx.x * kLossWaves + threadIdx.x / 64;
+  const int lane = threadIdx.x % 64;
+  if (m >= a.M) return;   // uniform per wavefront
   float* l = a.out + (size_t)m * a.Ap;
   float* d = a.dout + (size_t)m * a.Ap;
   double* tm = a.terms + (size_t)m * 3;
-  for (int i = 0; i < a.Ap; ++i) l[i] += a.b3[i];
+  const int i0 = lane, i1 = lane + 64;
+  const float v0 = i0 < a.Ap ? l[i0] + a.b3[i0] : 0.0f;
+  const float v1 = i1 < a.Ap ? l[i1] + a.b3[i1] : 0.0f;
+  if (i0 < a.Ap) l[i0] = v0;
+  if (i1 < a.Ap) l[i1] = v1;
   const size_t ti = (size_t)a.idx[m];
   const int act = a.act[ti];
   if (act >= a.A) {  // invalid stored action: flag it, the sample contributes nothing
-    atomicOr(a.err, ERR_ACTION);
-    for (int i = 0; i < a.Ap; ++i) d[i] = 0.0f;
-    tm[0] = tm[1] = tm[2] = 0.0;
+    if (lane == 0) {
+      atomicOr(a.err, ERR_ACTION);
+      tm[0] = tm[1] = tm[2] = 0.0;
+    }
+    if (i0 < a.Ap) d[i0] = 0.0f;
+    if (i1 < a.Ap) d[i1] = 0.0f;
     return;
   }
+  const bool in0 = i0 < a.A, in1 = i1 < a.A;
   const float adv = (float)a.adv[ti], ret = (float)a.ret[ti];
-  float mx = l[0];
-  for (int i = 1; i < a.A; ++i) mx = fmaxf(mx, l[i]);
-  float S = 0.f;
-  for (int i = 0; i < a.A; ++i) S += expf(l[i] - mx);
+  const float mx = wave_max(fmaxf(in0 ? v0 : -INFINITY, in1 ? v1 : -INFINITY));
+  const float S = wave_sum((in0 ? expf(v0 - mx) : 0.0f) + (in1 ? expf(v1 - mx) : 0.0f));
   const float lS = logf(S);
-  float H = 0.f;
-  for (int i = 0; i < a.A; ++i) {
-    const float lp = (l[i] - mx) - lS;
-    H -= expf(lp) * lp;
-  }
-  const float logp = (l[act] - mx) - lS;
+  const float lp0 = (v0 - mx) - lS, lp1 = (v1 - mx) - lS;
+  const float p0 = in0 ? expf(lp0) : 0.0f, p1 = in1 ? expf(lp1) : 0.0f;
+  const float H = -wave_sum(p0 * (in0 ? lp0 : 0.0f) + p1 * (in1 ? lp1 : 0.0f));
+  // the taken action's logit and the value output, broadcast from the lanes that hold them
+  const float la0 = __shfl(v0, act & 63, 64), la1 = __shfl(v1, act & 63, 64);
+  const float logp = ((act < 64 ? la0 : la1) - mx) - lS;
+  const float va0 = __shfl(v0, a.A & 63, 64), va1 = __shfl(v1, a.A & 63, 64);
+  const float v = a.A < 64 ? va0 : va1;
   const float invM = 1.0f / (float)a.M;
   float dlogp, pterm;
   if (a.reinforce) {
@@ -166,18 +188,22 @@ __global__ __launch_bounds__(kThr) void mb_loss_k(LossArgs a) {
     dlogp = -g_rho * rho * invM;
     pterm = -fminf(s1, s2);
   }
-  for (int i = 0; i < a.A; ++i) {
-    const float lp = (l[i] - mx) - lS;
-    const float p = expf(lp);
-    float g = -dlogp * p + a.c_h * invM * p * (lp + H);
-    if (i == act) g += dlogp;
-    d[i] = g;
+  const float dv = 2.0f * a.c_v * (v - ret) * invM;
+  if (i0 < a.Ap) {
+    float g = in0 ? -dlogp * p0 + a.c_h * invM * p0 * (lp0 + H) : dv;
+    if (i0 == act) g += dlogp;
+    d[i0] = g;
   }
-  const float v = l[a.A];
-  d[a.A] = 2.0f * a.c_v * (v - ret) * invM;
-  tm[0] = (double)pterm;
-  tm[1] = (double)(v - ret) * (double)(v - ret);
-  tm[2] = (double)H;
+  if (i1 < a.Ap) {
+    float g = in1 ? -dlogp * p1 + a.c_h * invM * p1 * (lp1 + H) : dv;
+    if (i1 == act) g += dlogp;
+    d[i1] = g;
+  }
+  if (lane == 0) {
+    tm[0] = (double)pterm;
+    tm[1] = (double)(v - ret) * (double)(v - ret);
+    tm[2] = (double)H;
+  }
 }
 
 // d *= GELU'(z), elementwise over n entries
@@ -194,21 +220,33 @@ __global__ __launch_bounds__(kThr) void mb_widen_k(uint32_t n, const uint16_t* _
     o[q] = bf16_to_f32(w[q]);
 }
 
-// loss terms summed in a fixed order by one workgroup
-__global__ __launch_bounds__(kThr) void ppo_loss_k(const double* terms, int M, float c_v, float c_h,
-                                                   double* out) {
-  __shared__ double part[3][kThr];
-  for (int c = 0; c < 3; ++c) {
-    double s = 0.0;
-    for (int m = threadIdx.x; m < M; m += kThr) s += terms[(size_t)m * 3 + c];
-    part[c][threadIdx.x] = s;
+// loss terms summed in a fixed order by one workgroup: each thread adds a contiguous run of
+// samples in order, then a pairwise tree combines the threads' partial sums
+constexpr int kSumThr = 1024;
+__global__ __launch_bounds__(kSumThr) void ppo_loss_k(const double* terms, int M, float c_v,
+                                                      float c_h, double* out) {
+  __shared__ double part[3][kSumThr];
+  const int per = (M + kSumThr - 1) / kSumThr;
+  const int m0 = threadIdx.x * per;
+  const int m1 = m0 + per < M ? m0 + per : M;
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0;
+#pragma unroll 4
+  for (int m = m0; m < m1; ++m) {
+    s0 += terms[(size_t)m * 3];
+    s1 += terms[(size_t)m * 3 + 1];
+    s2 += terms[(size_t)m * 3 + 2];
   }
+  part[0][threadIdx.x] = s0;
+  part[1][threadIdx.x] = s1;
+  part[2][threadIdx.x] = s2;
   __syncthreads();
+  for (int w = kSumThr / 2; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w)
+      for (int c = 0; c < 3; ++c) part[c][threadIdx.x] += part[c][threadIdx.x + w];
+    __syncthreads();
+  }
   if (threadIdx.x == 0) {
-    double t[3] = {0.0, 0.0, 0.0};
-    for (int c = 0; c < 3; ++c)
-      for (int i = 0; i < kThr; ++i) t[c] += part[c][i];
-    const double pi = t[0] / M, v = c_v * t[1] / M, h = -c_h * t[2] / M;
+    const double pi = part[0][0] / M, v = c_v * part[1][0] / M, h = -c_h * part[2][0] / M;
     out[0] = pi + v + h;
     out[1] = pi;
     out[2] = v;
@@ -340,7 +378,7 @@ hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t of
                       float c_v, float c_h, int reinforce, void* scratch, double* loss_out,
                       float* grads, int64_t* idx_out, uint32_t* err, void* blas,
                       const char** why, hipStream_t st) {
-  if (M < 1 || !blas) return hipErrorInvalidValue;
+  if (M < 1 || !blas || m.Ap > 128) return hipErrorInvalidValue;
   const unsigned char* wb = static_cast<const unsigned char*>(d_weights);
   const void* w1 = wb + off[0];
   const float* b1 = reinterpret_cast<const float*>(wb + off[1]);
@@ -389,7 +427,8 @@ hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t of
     la.clip = clip; la.c_v = c_v; la.c_h = c_h;
     la.out = s.out; la.b3 = b3; la.idx = s.idx; la.act = act; la.logp_old = logp_old;
     la.adv = adv; la.ret = ret; la.dout = s.dout; la.terms = s.terms; la.err = err;
-    hipLaunchKernelGGL(mb_loss_k, dim3((unsigned)((M + kThr - 1) / kThr)), dim3(kThr), 0, st, la);
+    hipLaunchKernelGGL(mb_loss_k, dim3((unsigned)((M + kLossWaves - 1) / kLossWaves)), dim3(kThr), 0,
+                       st, la);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // gradient layout: W1 [F][H1], b1, W2 [H1][H2], b2, W3 [H2][Ap], b3 (fp32, contiguous)
     float* gw1 = grads;
@@ -405,7 +444,7 @@ hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t of
     hipLaunchKernelGGL(mb_gelu_bwd_k, dim3(grid_for(n1)), dim3(kThr), 0, st, n1, s.z1, s.d1);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (!g.wgrad(M, m.F, m.H1, s.xa, s.d1, gw1, "weight gradient layer 1")) goto blas_fail;
-    hipLaunchKernelGGL(ppo_loss_k, dim3(1), dim3(kThr), 0, st, s.terms, M, c_v, c_h, loss_out);
+    hipLaunchKernelGGL(ppo_loss_k, dim3(1), dim3(kSumThr), 0, st, s.terms, M, c_v, c_h, loss_out);
     return hipGetLastError();
   }
 blas_fail:
@@ -417,7 +456,7 @@ blas_fail:
 
 hipError_t launch_pg_loss(const double* terms, int M, float c_v, float c_h, double* out,
                           hipStream_t st) {
-  hipLaunchKernelGGL(ppo_loss_k, dim3(1), dim3(kThr), 0, st, terms, M, c_v, c_h, out);
+  hipLaunchKernelGGL(ppo_loss_k, dim3(1), dim3(kSumThr), 0, st, terms, M, c_v, c_h, out);
   return hipGetLastError();
 }
 
