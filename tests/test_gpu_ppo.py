@@ -10,8 +10,9 @@ about sqrt(2^-8) * 2^-8 = 2^-12 relative in norm and the gradients, sums of per-
 products, by about as much: the norm bound is 2^-9 (a factor of 8 margin) and the
 elementwise bound 2^-8 of the tensor's largest entry. fp32 mode differs only in fp32
 rounding (sums of at most 64 terms over three layers, erf/exp to an ulp or two: about
-2^-16 relative per sample), with fp64 accumulation over the samples: 2^-13 for both
-bounds (a factor of 8 margin). The clip decision of the surrogate is taken away from its
+2^-16 relative per sample), summed over the M <= 4096 samples of the parity cases in fp32
+GEMMs (sign-mixed sums whose rounding error grows about as sqrt(M) u, about 2^-18): 2^-13 for
+both bounds (a factor of 8 margin). The clip decision of the surrogate is taken away from its
 boundaries by construction: logp_old = logp_new - d with |d - ln(1 +- clip)| >= 0.01, far
 beyond any logit difference the tolerances allow."""
 import sys
