@@ -2,16 +2,16 @@
 //
 // obs [F][E] -> h1 = GELU(x W1 + b1) -> h2 = GELU(h1 W2 + b2) -> out = h2 W3 + b3, where
 // out[0..A) are the logits of the categorical action distribution and out[A] (when the
-// value head is on) is V(s). In bf16 mode each layer's input is rounded to bf16 (RNE) and
-// multiplied by bf16 weights with fp32 accumulation (v_mfma_f32_16x16x32_bf16); bias and
-// GELU are fp32. In fp32 mode the products use v_mfma_f32_16x16x4_f32.
+// value head is on) is V(s). The epilogue of the last layer samples the action by inverse CDF
+// of the fp32 softmax with the ACTION uniform of (env, step) and writes action,
+// log-probability and value.
 //
-// One workgroup (4 waves) owns 64 environments. Activations of its 64 rows live in LDS
-// (x, then h1, then h2); each wave produces a quarter of the output columns of every layer
-// for all 64 rows, reading weight fragments (16 bytes per lane in bf16 mode) straight from
-// the repacked out-major weights, which stay resident in L2. The epilogue of the last
-// layer samples the action by inverse CDF of the fp32 softmax with the ACTION uniform of
-// (env, step) and writes action, log-probability and value.
+// Two kernels. policy_k (fp32 policies, v_mfma_f32_16x16x4_f32): one workgroup of 4 waves owns
+// 64 environments whose activations live in LDS; each wave produces a quarter of the output
+// columns of every layer, reading weight fragments straight from the repacked weights in L2.
+// policy_bf16_k (bf16 policies): every layer's input rounded to bf16 (RNE), bf16 weights,
+// fp32 accumulation (v_mfma_f32_16x16x32_bf16), bias and GELU in fp32; its layout and
+// scheduling are described above the kernel.
 #include "devmath.hpp"
 #include "params.hpp"
 
@@ -23,19 +23,6 @@ typedef __attribute__((ext_vector_type(4))) float f32x4;
 
 constexpr int kRows = 64;      // environments per workgroup
 constexpr int kThreads = 256;  // 4 waves
-
-struct Bf16Mode {
-  typedef uint16_t elem;
-  typedef bf16x8 frag;
-  static constexpr int KS = 32;   // K per MFMA
-  static constexpr int KL = 8;    // K elements per lane
-  static constexpr int PAD = 8;   // LDS row padding (elements)
-  __device__ static frag load(const elem* p) { return *reinterpret_cast<const frag*>(p); }
-  __device__ static f32x4 mfma(frag a, frag b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-  }
-  __device__ static elem from_f32(float f) { return bf16_bits(f); }
-};
 
 struct F32Mode {
   typedef float elem;
