@@ -234,7 +234,6 @@ struct Stage {
   uint8_t cls[kStage][64];
   uint32_t owner[64];
   uint32_t j0[64];
-  uint32_t k[64];   // the tick of the owner's blocks (lanes of the static system may differ)
 };
 
 __device__ __forceinline__ void wave_sync_lds() {
@@ -243,10 +242,10 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Called by all 64 lanes of the wave. Lanes with `need` get blocks [jneed, jneed + KS) of
-// their tick kneed: fill(owner lane, tick, j) computes one block into the stage.
+// Called by all 64 lanes of the wave. Lanes with `need` get blocks [jneed, jneed + KS):
+// fill(owner lane, j) computes one block into the stage.
 template <int KS, class Fill>
-__device__ __forceinline__ void wave_refill(Stage& st, bool need, uint32_t jneed, uint32_t kneed,
+__device__ __forceinline__ void wave_refill(Stage& st, bool need, uint32_t jneed,
                                             uint32_t& staged_hi, int lane, Fill&& fill) {
   const uint64_t mask = __ballot(need);
   const int nneed = __popcll(mask);
@@ -254,12 +253,11 @@ __device__ __forceinline__ void wave_refill(Stage& st, bool need, uint32_t jneed
     const int rank = __popcll(mask & ((1ull << lane) - 1ull));
     st.owner[rank] = (uint32_t)lane;
     st.j0[rank] = jneed;
-    st.k[rank] = kneed;
   }
   wave_sync_lds();
   for (int w = lane; w < KS * nneed; w += 64) {
     const int r = w / KS;
-    fill(st.owner[r], st.k[r], st.j0[r] + (uint32_t)(w % KS));
+    fill(st.owner[r], st.j0[r] + (uint32_t)(w % KS));
   }
   wave_sync_lds();
   if (need) staged_hi = jneed + KS;
@@ -269,9 +267,8 @@ template <int CM>
 __device__ __forceinline__ void refill_arrivals(Stage& st, const SimParams& p, bool need,
                                                 uint32_t jneed, uint32_t& staged_hi,
                                                 uint64_t seed, int e_lane0, uint32_t k, int lane) {
-  wave_refill<kStage>(st, need, jneed, k, staged_hi, lane, [&](uint32_t own, uint32_t kown,
-                                                               uint32_t j) {
-    const u32x4 d = draw(seed, (uint32_t)(e_lane0 + (int)own), kown, P_ARRIVAL, j, 0);
+  wave_refill<kStage>(st, need, jneed, staged_hi, lane, [&](uint32_t own, uint32_t j) {
+    const u32x4 d = draw(seed, (uint32_t)(e_lane0 + (int)own), k, P_ARRIVAL, j, 0);
     st.E[j % kStage][own] = -dlog(unit(d.x, d.y));
     const double uc = unit(d.z, d.w);
     int cls = CM - 1;
@@ -676,55 +673,41 @@ __device__ __forceinline__ int route_pick(uint32_t idle, int route, uint32_t rr,
   return __builtin_ctz(idle);
 }
 
-// Ticks k0 .. k0 + nt - 1 of the static system of one environment whose state is held in
-// registers: in each tick [t_k, t_{k+1}) arrivals, the static rule's dispatches to the routed
-// server, completions, and the tick's reward (into rew[(k - k0) E + e] when given). Every lane
-// runs through its own ticks: a lane whose tick has no event left closes it (completions,
-// reward) and opens the next one, with its dispatch at the opening instant, in the same loop
-// iteration. A wave therefore takes as many iterations as its busiest environment has events
-// over the nt ticks, rather than the sum over ticks of each tick's busiest environment (an
-// environment in a burst no longer holds the others at every tick boundary). The lanes meet
-// only in the ballots of the arrival refill and of the loop's end. A dispatch stores its
-// server's meta word at once; a completion clears the in-flight byte only in registers and
-// marks the server in `clear`, and `dirty` marks servers whose busy-until time changed; the
-// caller writes both back. Lanes without an environment (live = false) take part in the
-// wave's ballots only.
+// One tick [t_k, t_{k+1}) of the static system of one environment whose state is held in
+// registers: arrivals, the static rule's dispatches to the routed server, completions, and
+// the tick's reward (into rew_row[e] when given). A dispatch stores its server's meta word at
+// once; a completion clears the in-flight byte only in registers and marks the server in
+// `clear`, and `dirty` marks servers whose busy-until time changed; the caller writes both
+// back. Lanes without an environment (live = false) take part in the wave's ballots only.
 template <int KM, int CM>
-__device__ __forceinline__ void static_run(const SimParams& p, const SysState& G, uint32_t* err,
-                                           uint64_t seed, uint32_t k0, int nt, bool live, int e,
-                                           int ee, int e_lane0, int lane, Stage& st, Queue<CM>& Q,
-                                           Count& C, Arrivals& A, double (&busy)[KM],
-                                           ServerBytes& infl, uint32_t& dirty, uint32_t& clear,
-                                           uint32_t& rr, double* __restrict__ rew) {
+__device__ __forceinline__ void static_tick(const SimParams& p, const SysState& G, uint32_t* err,
+                                            uint64_t seed, uint32_t k, bool live, int e, int ee,
+                                            int e_lane0, int lane, Stage& st, Queue<CM>& Q,
+                                            Count& C, Arrivals& A, double (&busy)[KM],
+                                            ServerBytes& infl, uint32_t& dirty, uint32_t& clear,
+                                            uint32_t& rr, double* __restrict__ rew_row) {
   const size_t E = (size_t)p.E;
-  const uint32_t k_end = k0 + (uint32_t)nt;
-  uint32_t k = k0;
-  bool active = live && nt > 0;
-  // the open tick's state
-  uint32_t jroute = 0, staged_hi = 0, it = 0, idle = 0u;
+  C.n_k = 0;
+  C.Lw = 0.0;
+  C.jsvc = 0;
+  A.jarr = 0;
+  A.jproc = 0;
+  uint32_t jroute = 0;
+  const double t0 = (double)k * p.dt, t1 = (double)(k + 1) * p.dt;
   int A_k = 0;
-  double now = 0.0, t1 = 0.0, next_done = kInf;
-  auto open_tick = [&]() {
-    C.n_k = 0;
-    C.Lw = 0.0;
-    C.jsvc = 0;
-    A.jarr = 0;
-    A.jproc = 0;
-    jroute = 0;
-    staged_hi = 0;
-    it = 0;
-    A_k = 0;
-    now = (double)k * p.dt;
-    t1 = (double)(k + 1) * p.dt;
-    server_scan(busy, p.K, now, idle, next_done);
-  };
-  if (active) open_tick();
-  bool opening = active;  // the dispatch at the opening instant of the tick is due
+  double now = t0;
+  uint32_t idle;
+  double next_done;
+  server_scan(busy, p.K, now, idle, next_done);
+  uint32_t staged_hi = 0;
+  bool done = !live;
+  uint32_t it = 0;
+  bool first = true;
   for (;;) {
     bool go = false;
     bool need = false;
     double te = now;
-    if (active && !opening) {
+    if (!done && !first) {
       te = A.next_sw < A.next_arr ? A.next_sw : A.next_arr;
       if (next_done < te) te = next_done;
       if (Q.qsum > 0 && idle != 0u) {
@@ -733,28 +716,11 @@ __device__ __forceinline__ void static_run(const SimParams& p, const SysState& G
         const double tout = ts + p.static_timeout;
         if (tout > now && tout < te) te = tout;
       }
-      const bool over = te < t1 && it > kMaxEventsPerTick;
-      if (over) atomicOr(err, ERR_EVENTS);
-      if (!(te < t1) || over) {
-        // close the tick: completions before t1, reward
-#pragma unroll
-        for (int j = 0; j < KM; ++j) {
-          const uint32_t n = infl.get(j);
-          if (j < p.K && n > 0 && busy[j] < t1) {
-            C.c[C_DONE] += n;
-            clear |= 1u << j;
-            infl.set(j, 0u);
-          }
-        }
-        const double r = close_tick(Q, C, p, A.proc, A_k);
-        if (rew) rew[(size_t)(k - k0) * E + e] = r;
-        ++k;
-        if (k == k_end) {
-          active = false;
-        } else {
-          open_tick();
-          opening = true;
-        }
+      if (!(te < t1)) {
+        done = true;
+      } else if (it > kMaxEventsPerTick) {
+        atomicOr(err, ERR_EVENTS);
+        done = true;
       } else {
         need = p.arrival_kind != 1 && (A.next_sw == te || A.next_arr == te) &&
                A.jarr + 2u > staged_hi;
@@ -773,7 +739,7 @@ __device__ __forceinline__ void static_run(const SimParams& p, const SysState& G
         enqueue(Q, C, p, cls, now);
       }
     }
-    if (go || opening) {
+    if (go || (first && !done)) {
       // min(B, Q_h) of the HoL class if Q_h >= B or its head waited T, to the routed server
       while (idle != 0u && Q.qsum > 0) {
         double ts;
@@ -796,15 +762,28 @@ __device__ __forceinline__ void static_run(const SimParams& p, const SysState& G
         }
       }
     }
-    opening = false;
-    if (__ballot(active) == 0ull) break;
+    first = false;
+    if (__ballot(!done) == 0ull) break;
   }
+  if (!live) return;
+  // completions before t1
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    const uint32_t n = infl.get(j);
+    if (j < p.K && n > 0 && busy[j] < t1) {
+      C.c[C_DONE] += n;
+      clear |= 1u << j;
+      infl.set(j, 0u);
+    }
+  }
+  const double r = close_tick(Q, C, p, A.proc, A_k);
+  if (rew_row) rew_row[e] = r;
 }
 
 // Ticks k0 .. k0 + nt - 1 of the static shadow system. The static rule never looks at the
 // learned system, so one launch may cover many ticks: the state is loaded once, kept in
-// registers from tick to tick, and stored once; each wave, and each lane within it (see
-// static_run), advances at its own pace instead of waiting at every tick for the slowest. rew [nt][E] (optional) receives the
+// registers from tick to tick, and stored once; each wave advances at its own pace instead of
+// waiting at every tick for the slowest wave of the grid. rew [nt][E] (optional) receives the
 // rewards; nt = 1 is the per-tick kernel of the step interface.
 template <int KM, int CM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void static_k(
@@ -836,8 +815,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   }
   uint32_t dirty = 0, clear = 0;
   uint32_t rr = p.route == 2 ? G.rr[ee] : 0u;
-  static_run<KM, CM>(p, G, g.err, seed, k0, nt, live, e, ee, e_lane0, lane, st, Q, C, A, busy,
-                     infl, dirty, clear, rr, rew);
+  for (int i = 0; i < nt; ++i)
+    static_tick<KM, CM>(p, G, g.err, seed, k0 + (uint32_t)i, live, e, ee, e_lane0, lane, st, Q,
+                        C, A, busy, infl, dirty, clear, rr, rew ? rew + (size_t)i * E : nullptr);
   if (!live) return;
   // servers whose last batch completed: clear the in-flight byte of the stored meta word
   uint32_t m[KM];
