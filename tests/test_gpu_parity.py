@@ -116,6 +116,54 @@ def test_sim_step_parity_small(bs, orc, name):
         assert np.array_equal(g["tot"]["cnt"][1], g["cnt"][1].sum(axis=1))
 
 
+def _edge(name):
+    from workloads.presets import DWELL_EXP, DWELL_INF, SVC_EXP
+    if name == "queue255_states4":   # capacity and modulation states at their limits, overload
+        return preset("C4", queue_cap=255, rates=[200.0, 2000.0, 20000.0, 60000.0],
+                      dwell_kind=[DWELL_EXP] * 4, dwell_mean=[0.05, 0.02, 0.01, 0.005],
+                      pareto_alpha=[0.0] * 4, pareto_xm=[0.0] * 4, shadow=1)
+    if name == "no_arrivals":        # a process that never fires
+        return preset("C3", rates=[0.0], dwell_kind=[DWELL_INF], dwell_mean=[0.0],
+                      pareto_alpha=[0.0], pareto_xm=[0.0])
+    if name == "cap1_overload":      # one waiting slot, ten times the service capacity
+        return preset("C1", queue_cap=1, rates=[5000.0])
+    if name == "exp_service_K16":    # exponential service on the 16-server system
+        return preset("C5", service_kind=[SVC_EXP] * 4, svc_alpha=[1e-3, 5e-3, 2e-2, 8e-2])
+    raise KeyError(name)
+
+
+EDGE = ["queue255_states4", "no_arrivals", "cap1_overload", "exp_service_K16"]
+
+
+@pytest.mark.parametrize("name", EDGE)
+def test_edge_workloads_parity(bs, orc, name):
+    """Configurations at the ABI's limits and the method's degenerate cases, 300 envs (a
+    ragged tail) x 150 ticks, bit-exact against the oracle; plus the expected degenerate
+    behaviour (nothing counted without arrivals; drops under overload)."""
+    w = _edge(name)
+    E, T, seed = 300, 150, 0xED6E + EDGE.index(name)
+    acts = seeded_actions(seed, T, E, 6 * w["n_servers"], small_bias=0.5)
+    say(f"[edge] {name} E={E} T={T}")
+    g = gpu_run_actions(bs, w, E, T, seed, acts)
+    r = orc.rollout(w, seed, T, np.arange(E), actions=acts)
+    nsys = 2 if w["shadow"] else 1
+    compare_sim(r, g, w, np.arange(E), nsys)
+    if name == "no_arrivals":
+        assert not g["cnt"].any() and not g["reward"].any()
+    if name in ("queue255_states4", "cap1_overload"):
+        assert g["cnt"][0, 2].sum() > 0          # dropped requests (counter 2)
+
+
+def test_single_tick_and_single_env(bs, orc):
+    """T = 1 on one environment and on 65 (one wave and one lane), against the oracle."""
+    w = preset("C4")
+    for E in (1, 65):
+        acts = seeded_actions(3, 1, E, 6 * w["n_servers"])
+        g = gpu_run_actions(bs, w, E, 1, 5, acts)
+        r = orc.rollout(w, 5, 1, np.arange(E), actions=acts)
+        compare_sim(r, g, w, np.arange(E), 1)
+
+
 RULES = {
     "burst": lambda: burst_preset(),
     "static8_C3": lambda: baseline_preset("static8", "C3"),
