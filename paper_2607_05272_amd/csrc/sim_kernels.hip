@@ -608,10 +608,10 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
     if (obs_out) put_obs(obs_out, E, i, e, fr);
     ++i;
   }
-  for (; i < p.F; ++i) {
-    obs[(size_t)i * E + e] = 0.0f;
-    if (obs_out) obs_out[(size_t)i * E + e] = 0.0f;
-  }
+  // the padding rows past the observation's width: zero in the current observation since the
+  // reset (nothing else writes them), so only a trajectory row needs them
+  if (obs_out)
+    for (; i < p.F; ++i) obs_out[(size_t)i * E + e] = 0.0f;
 
   store_queue(Q, G, p, e);
   store_count(C, G, p, e);
