@@ -140,8 +140,9 @@ def traffic_for(kernel, cfg_name):
     return ent.get("bytes_per_launch")
 
 
-KERNEL_OF = {"policy": "policy_", "step": "learned_k", "static": "static_k", "gae": "gae_k",
-             "ppo": "ppo_"}
+# kernel classes whose HBM traffic is taken from counters (the minibatch gradient, a sequence of
+# library GEMMs and small kernels, has no single kernel to attribute it to)
+KERNEL_OF = {"policy": "policy_", "step": "learned_k", "static": "static_k", "gae": "gae_k"}
 
 
 def _pmc_rows(d):
@@ -153,18 +154,14 @@ def _pmc_rows(d):
     return rows
 
 
-def _per_dispatch(rows, counter, match, launch=None):
-    """Counter total over the kernels that `match`, per launch (a launch counted once per
-    dispatch of the kernels that `launch` matches, default `match`)."""
-    launch = launch or match
+def _per_dispatch(rows, counter, match):
+    """Counter total over the kernels that `match`, per dispatch of them."""
     tot, disp = 0.0, set()
     for r in rows:
-        if r["Counter_Name"] != counter:
+        if r["Counter_Name"] != counter or not match(r["Kernel_Name"]):
             continue
-        if match(r["Kernel_Name"]):
-            tot += float(r["Counter_Value"])
-        if launch(r["Kernel_Name"]):
-            disp.add(r.get("Dispatch_Id") or r.get("Correlation_Id"))
+        tot += float(r["Counter_Value"])
+        disp.add(r.get("Dispatch_Id") or r.get("Correlation_Id"))
     return (tot / len(disp), len(disp)) if disp else (None, 0)
 
 
@@ -185,9 +182,8 @@ def write_traffic(d, cfg_name):
     except (OSError, ValueError):
         out = {}
     for cls, pat in KERNEL_OF.items():
-        first = (lambda k: "ppo_fwd_k" in k) if cls == "ppo" else None
-        fk, nf = _per_dispatch(fr, "FETCH_SIZE", lambda k, p=pat: p in k, first)
-        wk, nw = _per_dispatch(wr, "WRITE_SIZE", lambda k, p=pat: p in k, first)
+        fk, nf = _per_dispatch(fr, "FETCH_SIZE", lambda k, p=pat: p in k)
+        wk, nw = _per_dispatch(wr, "WRITE_SIZE", lambda k, p=pat: p in k)
         if fk is None or wk is None:
             continue
         out[f"{cfg_name}:{cls}"] = {
