@@ -622,16 +622,38 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
 // The set of idle servers {j : busy_j <= now} and the next completion min{busy_j > now} only
 // change at a completion instant or a dispatch, so they are kept as a bit mask and a time and
 // recomputed by one scan of the servers at those points (not at every arrival).
+// Busy-until times of the static system's servers: the first kBusyRegs in registers, the rest
+// in the wave's slab of LDS, one double per lane, so that a 16-server system does not spill
+// them inside the event loop (four workgroups of four waves fill the CU's 160 KiB exactly:
+// 20 KiB of arrival stages and 20 KiB of busy times each). Loops over j with a compile-time bound resolve each
+// access to a register or an LDS word at a fixed offset.
+constexpr int kBusyRegs = 6;
 template <int KM>
-__device__ __forceinline__ void server_scan(const double (&busy)[KM], int K, double now,
+struct BusyTimes {
+  static constexpr int KR = KM > 8 ? kBusyRegs : KM;
+  double r[KR];
+  double* slab;   // [KM - KR][64] in LDS (unused when KM <= 8)
+  int lane;
+  __device__ __forceinline__ double get(int j) const {
+    return j < KR ? r[j < KR ? j : 0] : slab[(j - KR) * 64 + lane];
+  }
+  __device__ __forceinline__ void set(int j, double v) {
+    if (KM <= KR || j < KR) put<KR>(r, j, v);
+    else slab[(j - KR) * 64 + lane] = v;
+  }
+};
+
+template <int KM>
+__device__ __forceinline__ void server_scan(const BusyTimes<KM>& busy, int K, double now,
                                             uint32_t& idle, double& next_done) {
   idle = 0u;
   next_done = kInf;
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
     if (j < K) {
-      if (busy[j] <= now) idle |= 1u << j;
-      else if (busy[j] < next_done) next_done = busy[j];
+      const double b = busy.get(j);
+      if (b <= now) idle |= 1u << j;
+      else if (b < next_done) next_done = b;
     }
   }
 }
@@ -683,7 +705,7 @@ template <int KM, int CM>
 __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& G, uint32_t* err,
                                             uint64_t seed, uint32_t k, bool live, int e, int ee,
                                             int e_lane0, int lane, Stage& st, Queue<CM>& Q,
-                                            Count& C, Arrivals& A, double (&busy)[KM],
+                                            Count& C, Arrivals& A, BusyTimes<KM>& busy,
                                             ServerBytes& infl, uint32_t& dirty, uint32_t& clear,
                                             uint32_t& rr, double* __restrict__ rew_row) {
   const size_t E = (size_t)p.E;
@@ -753,7 +775,7 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
         infl.set(j, (uint32_t)n);
         const double sv = service<CM>(C, p, seed, ee, k, 1, h, n);
         const double cdone = pop_batch(Q, C, p, k, j, h, n, now, sv);
-        put<KM>(busy, j, cdone);
+        busy.set(j, cdone);
         G.meta[(size_t)j * E + ee] = (uint32_t)n | ((uint32_t)n << 8) | ((uint32_t)h << 16);
         dirty |= 1u << j;
         if (cdone > now) {
@@ -770,7 +792,7 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
     const uint32_t n = infl.get(j);
-    if (j < p.K && n > 0 && busy[j] < t1) {
+    if (j < p.K && n > 0 && busy.get(j) < t1) {
       C.c[C_DONE] += n;
       clear |= 1u << j;
       infl.set(j, 0u);
@@ -789,6 +811,7 @@ template <int KM, int CM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void static_k(
     SimParams p, EnvState g, uint64_t seed, uint32_t k0, int nt, double* __restrict__ rew) {
   __shared__ Stage stage[4];
+  __shared__ double busy_lds[4][KM > 8 ? KM - kBusyRegs : 1][64];
   const int lane = threadIdx.x & 63;
   Stage& st = stage[threadIdx.x >> 6];
   const int e_lane0 = blockIdx.x * blockDim.x + (threadIdx.x & ~63);
@@ -806,11 +829,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   load_arrivals(A, G, p, ee);
   // busy-until times in registers; of each server's meta word only the in-flight count
   // (low byte) is kept, eight servers to a 64-bit register (the word is stored at dispatch)
-  double busy[KM];
+  BusyTimes<KM> busy;
+  busy.slab = &busy_lds[threadIdx.x >> 6][0][0];
+  busy.lane = lane;
   ServerBytes infl;
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
-    busy[j] = j < p.K ? G.busy[(size_t)j * E + ee] : kInf;
+    busy.set(j, j < p.K ? G.busy[(size_t)j * E + ee] : kInf);
     if (j < p.K) infl.set(j, G.meta[(size_t)j * E + ee] & 0xffu);
   }
   uint32_t dirty = 0, clear = 0;
@@ -829,7 +854,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     if (((clear >> j) & 1u) && infl.get(j) == 0u) G.meta[(size_t)j * E + e] = m[j] & ~0xffu;
 #pragma unroll
   for (int j = 0; j < KM; ++j)
-    if (dirty & (1u << j)) G.busy[(size_t)j * E + e] = busy[j];
+    if (dirty & (1u << j)) G.busy[(size_t)j * E + e] = busy.get(j);
   if (p.route == 2) G.rr[e] = rr;
   store_queue(Q, G, p, e);
   store_count(C, G, p, e);
