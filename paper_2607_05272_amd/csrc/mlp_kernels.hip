@@ -350,7 +350,7 @@ __device__ __forceinline__ void mma_group(const uint16_t* __restrict__ act, int 
                                           const uint16_t* __restrict__ W,
                                           const float* __restrict__ bias, int tile0, int tstride,
                                           int rt0, f32x4 (&acc)[TPW][RTN]) {
-  constexpr int KS = K / 32, D = KS < 3 ? KS : 3, S = D + 1;
+  constexpr int KS = K / 32, D = KS < 2 ? KS : 2, S = D + 1;
   const int lane = threadIdx.x & 63, r16 = lane & 15, kq = lane >> 4;
   const uint16_t* brow = act + (rt0 * 16 + r16) * sa + kq * 8;
   const uint16_t* wp[TPW];
