@@ -340,10 +340,10 @@ __device__ __forceinline__ void enqueue(Queue<CM>& Q, Count& C, const SimParams&
 
 // Service time of a batch of n requests of class h. kind 0: alpha + beta n; kind 1:
 // median * exp(sigma Z) + beta n with Z = sqrt(-2 log u1) cos(2 pi u2) (Box-Muller); kind 2:
-// -log(u1) (alpha + beta n), with u1, u2 from SERVICE block j of (env, tick, system). The
-// learned tick inlines it (it has registers to spare: a call saves and restores registers
-// through scratch); the static kernel, at its register budget, calls the out-of-line copy.
-__device__ __forceinline__ double service_draw_body(int kind, double al, double be, double med,
+// -log(u1) (alpha + beta n), with u1, u2 from SERVICE block j of (env, tick, system). Inline in
+// both tick kernels: as a call it saved and restored registers through scratch memory at every
+// dispatch (its fp64 elementary functions stay out of line, see devmath.hpp).
+__device__ __forceinline__ double service_draw(int kind, double al, double be, double med,
                                             double sigma, int n, uint64_t seed, uint32_t env,
                                             uint32_t k, uint32_t j, uint32_t sys) {
   const u32x4 w = draw(seed, env, k, P_SERVICE, j, sys);
@@ -353,22 +353,13 @@ __device__ __forceinline__ double service_draw_body(int kind, double al, double 
   const double z = sqrt(-2.0 * dlog(u1)) * dcos(kTwoPi * u2);
   return med * dexp(sigma * z) + be * (double)n;
 }
-__device__ __noinline__ double service_draw(int kind, double al, double be, double med,
-                                            double sigma, int n, uint64_t seed, uint32_t env,
-                                            uint32_t k, uint32_t j, uint32_t sys) {
-  return service_draw_body(kind, al, be, med, sigma, n, seed, env, k, j, sys);
-}
 
-// INL: draw inline rather than through the out-of-line copy
-template <int CM, bool INL = false>
+template <int CM>
 __device__ __forceinline__ double service(Count& C, const SimParams& p, uint64_t seed, int e,
                                           uint32_t k, int sys, int h, int n) {
   const int kind = pick<CM>(p.svc_kind, h);
   const double al = pick<CM>(p.svc_alpha, h), be = pick<CM>(p.svc_beta, h);
   if (kind == 0) return al + be * (double)n;
-  if (INL)
-    return service_draw_body(kind, al, be, pick<CM>(p.svc_median, h), p.svc_sigma, n, seed,
-                             (uint32_t)e, k, C.jsvc++, (uint32_t)sys);
   return service_draw(kind, al, be, pick<CM>(p.svc_median, h), p.svc_sigma, n, seed,
                       (uint32_t)e, k, C.jsvc++, (uint32_t)sys);
 }
@@ -520,7 +511,7 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
         const int h = hol(Q, p, ts);
         if (Q.q(h) < b) break;
         C.c[C_DONE] += meta_s & 0xffu;  // the previous batch on s finished at busy_s <= now
-        const double sv = service<CM, true>(C, p, seed, ee, k, 0, h, b);
+        const double sv = service<CM>(C, p, seed, ee, k, 0, h, b);
         busy_s = pop_batch(Q, C, p, k, s, h, b, now, sv);
         meta_s = (uint32_t)b | ((uint32_t)b << 8) | ((uint32_t)h << 16);
         dirty_s = true;
