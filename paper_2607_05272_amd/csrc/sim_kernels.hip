@@ -522,42 +522,62 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
   }
   if (!live) return;
 
-  // end of tick: completions before t1 and the per-server part of obs_{k+1}
+  // end of tick: completions before t1 and the per-server part of obs_{k+1}. The server rows
+  // are read kEndChunk at a time, all loads of a chunk issued before any of its stores (the
+  // compiler cannot reorder them across the stores, which it must assume may alias), so a
+  // chunk costs one memory round trip instead of two per server.
   float* obs = g.obs;
   const int per = p.K > 1 ? 4 : 2;
-  for (int j = 0; j < p.K; ++j) {
-    const bool mine = j == s;
-    const double bu = mine ? busy_s : G.busy[(size_t)j * E + e];
-    uint32_t m = mine ? meta_s : G.meta[(size_t)j * E + e];
-    bool dirty = mine && dirty_s;
-    const uint32_t infl = m & 0xffu;
-    if (infl > 0 && bu < t1) {
-      C.c[C_DONE] += infl;
-      m &= ~0xffu;
-      dirty = true;
+  constexpr int kEndChunk = 8;
+  for (int j0 = 0; j0 < p.K; j0 += kEndChunk) {
+    double brow[kEndChunk];
+    uint32_t mrow[kEndChunk];
+#pragma unroll
+    for (int i = 0; i < kEndChunk; ++i) {
+      brow[i] = 0.0;
+      mrow[i] = 0u;
+      if (j0 + i < p.K) {
+        brow[i] = G.busy[(size_t)(j0 + i) * E + e];
+        mrow[i] = G.meta[(size_t)(j0 + i) * E + e];
+      }
     }
-    if (dirty) {
-      if (mine) G.busy[(size_t)j * E + e] = bu;
-      G.meta[(size_t)j * E + e] = m;
-    }
-    const int base = 2 + per * j;
-    const double bflag = bu > t1 ? 1.0 : 0.0;
-    const double lb = (double)((m >> 8) & 0xffu) * 0.03125;
-    put_obs(obs, E, base, e, bflag);
-    put_obs(obs, E, base + 1, e, lb);
-    if (obs_out) {
-      put_obs(obs_out, E, base, e, bflag);
-      put_obs(obs_out, E, base + 1, e, lb);
-    }
-    if (p.K > 1) {
-      const double rem = (bu > t1 ? bu - t1 : 0.0) * p.inv_tw;
-      const uint32_t lc = (m >> 16) & 0xffu;
-      const double lcv = (double)((lc == 0xffu ? -1 : (int)lc) + 1) * p.inv_c;
-      put_obs(obs, E, base + 2, e, rem);
-      put_obs(obs, E, base + 3, e, lcv);
+#pragma unroll
+    for (int i = 0; i < kEndChunk; ++i) {
+      const int j = j0 + i;
+      if (j >= p.K) break;
+      const bool mine = j == s;
+      const double bu = mine ? busy_s : brow[i];
+      uint32_t m = mine ? meta_s : mrow[i];
+      bool dirty = mine && dirty_s;
+      const uint32_t infl = m & 0xffu;
+      if (infl > 0 && bu < t1) {
+        C.c[C_DONE] += infl;
+        m &= ~0xffu;
+        dirty = true;
+      }
+      if (dirty) {
+        if (mine) G.busy[(size_t)j * E + e] = bu;
+        G.meta[(size_t)j * E + e] = m;
+      }
+      const int base = 2 + per * j;
+      const double bflag = bu > t1 ? 1.0 : 0.0;
+      const double lb = (double)((m >> 8) & 0xffu) * 0.03125;
+      put_obs(obs, E, base, e, bflag);
+      put_obs(obs, E, base + 1, e, lb);
       if (obs_out) {
-        put_obs(obs_out, E, base + 2, e, rem);
-        put_obs(obs_out, E, base + 3, e, lcv);
+        put_obs(obs_out, E, base, e, bflag);
+        put_obs(obs_out, E, base + 1, e, lb);
+      }
+      if (p.K > 1) {
+        const double rem = (bu > t1 ? bu - t1 : 0.0) * p.inv_tw;
+        const uint32_t lc = (m >> 16) & 0xffu;
+        const double lcv = (double)((lc == 0xffu ? -1 : (int)lc) + 1) * p.inv_c;
+        put_obs(obs, E, base + 2, e, rem);
+        put_obs(obs, E, base + 3, e, lcv);
+        if (obs_out) {
+          put_obs(obs_out, E, base + 2, e, rem);
+          put_obs(obs_out, E, base + 3, e, lcv);
+        }
       }
     }
   }
@@ -566,12 +586,14 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
   if (rchk) rchk[e] = C.chk;
 
   // rates: exponentially weighted arrival counts with weights 1, 1/4, 1/16, 1/64
+  // (all four read before the first store, for the same reason as the server rows)
   double ew[4];
   const double ewc[4] = {1.0, 0.25, 0.0625, 0.015625};
 #pragma unroll
+  for (int i = 0; i < 4; ++i) ew[i] = g.ewma[(size_t)i * E + e];
+#pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const double v = g.ewma[(size_t)i * E + e];
-    ew[i] = v + ewc[i] * ((double)A_k - v);
+    ew[i] = ew[i] + ewc[i] * ((double)A_k - ew[i]);
     g.ewma[(size_t)i * E + e] = ew[i];
   }
   // queue part of obs_{k+1}
