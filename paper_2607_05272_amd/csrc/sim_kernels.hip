@@ -452,20 +452,22 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
   const int ee = live ? e : 0;
   const size_t E = (size_t)p.E;
   const SysState& G = g.sys[0];
-  int a = live ? act[ee] : 0;
-  if (a >= 6 * p.K) {
-    atomicOr(g.err, ERR_ACTION);
-    a = 0;
-  }
-  const int s = a / 6, b = 1 << (a % 6);
+  // the state loads are issued before the action is examined: a branch on the action (and
+  // the error flag's atomic, which may alias any state array) ahead of them would make every
+  // environment wait out the action load first
+  const int a_in = live ? act[ee] : 0;
   Queue<CM> Q;
   load_queue(Q, G, p, ee);
   Count C;
   load_count(C, G, p, ee);
   Arrivals A;
   load_arrivals(A, G, p, ee);
+  const bool bad_action = a_in >= 6 * p.K;
+  const int a = bad_action ? 0 : a_in;
+  const int s = a / 6, b = 1 << (a % 6);
   double busy_s = G.busy[(size_t)s * E + ee];
   uint32_t meta_s = G.meta[(size_t)s * E + ee];
+  if (bad_action) atomicOr(g.err, ERR_ACTION);
   bool dirty_s = false;
 
   const double t0 = (double)k * p.dt, t1 = (double)(k + 1) * p.dt;
