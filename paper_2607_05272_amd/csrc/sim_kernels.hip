@@ -57,36 +57,12 @@ struct Queue {
   uint32_t qp, hp;  // per-class length / ring head, one byte per class
   double hts[CM];   // arrival time of each class's head request
   int qsum;
+  int hh;           // head-of-line class (see hol), -1 when every queue is empty
+  double hts_h;     // arrival time of its head request
   double* ring;     // this environment's rings [C][N]
   __device__ __forceinline__ int q(int c) const { return (int)((qp >> (8 * c)) & 0xffu); }
   __device__ __forceinline__ int hd(int c) const { return (int)((hp >> (8 * c)) & 0xffu); }
 };
-
-template <int CM>
-__device__ __forceinline__ void load_queue(Queue<CM>& Q, const SysState& g, const SimParams& p,
-                                           int e) {
-  const size_t E = (size_t)p.E;
-  Q.qp = g.qpack[e];
-  Q.hp = g.hpack[e];
-  Q.qsum = 0;
-#pragma unroll
-  for (int c = 0; c < CM; ++c) {
-    Q.hts[c] = c < p.C ? g.hts[(size_t)c * E + e] : 0.0;
-    Q.qsum += Q.q(c);
-  }
-  Q.ring = g.ring + (size_t)e * p.C * p.N;
-}
-
-template <int CM>
-__device__ __forceinline__ void store_queue(const Queue<CM>& Q, const SysState& g,
-                                            const SimParams& p, int e) {
-  const size_t E = (size_t)p.E;
-  g.qpack[e] = Q.qp;
-  g.hpack[e] = Q.hp;
-#pragma unroll
-  for (int c = 0; c < CM; ++c)
-    if (c < p.C) g.hts[(size_t)c * E + e] = Q.hts[c];
-}
 
 // head-of-line class: oldest head request, ties to the lower class index; -1 if empty
 template <int CM>
@@ -102,6 +78,34 @@ __device__ __forceinline__ int hol(const Queue<CM>& Q, const SimParams& p, doubl
   }
   return h;
 }
+
+template <int CM>
+__device__ __forceinline__ void load_queue(Queue<CM>& Q, const SysState& g, const SimParams& p,
+                                           int e) {
+  const size_t E = (size_t)p.E;
+  Q.qp = g.qpack[e];
+  Q.hp = g.hpack[e];
+  Q.qsum = 0;
+#pragma unroll
+  for (int c = 0; c < CM; ++c) {
+    Q.hts[c] = c < p.C ? g.hts[(size_t)c * E + e] : 0.0;
+    Q.qsum += Q.q(c);
+  }
+  Q.ring = g.ring + (size_t)e * p.C * p.N;
+  Q.hh = hol(Q, p, Q.hts_h);
+}
+
+template <int CM>
+__device__ __forceinline__ void store_queue(const Queue<CM>& Q, const SysState& g,
+                                            const SimParams& p, int e) {
+  const size_t E = (size_t)p.E;
+  g.qpack[e] = Q.qp;
+  g.hpack[e] = Q.hp;
+#pragma unroll
+  for (int c = 0; c < CM; ++c)
+    if (c < p.C) g.hts[(size_t)c * E + e] = Q.hts[c];
+}
+
 
 // ---- counters of one system -----------------------------------------------------------------
 struct Count {
@@ -335,7 +339,15 @@ __device__ __forceinline__ void enqueue(Queue<CM>& Q, Count& C, const SimParams&
   int pos = Q.hd(cls) + qc;
   if (pos >= p.N) pos -= p.N;
   Q.ring[(size_t)cls * p.N + pos] = now;
-  if (qc == 0) put<CM>(Q.hts, cls, now);
+  if (qc == 0) {
+    put<CM>(Q.hts, cls, now);
+    // the new head is the newest request, so it is the head of line only when every queue
+    // was empty, or when it ties the current head of line's time from a lower class
+    if (Q.qsum == 0 || (now == Q.hts_h && cls < Q.hh)) {
+      Q.hh = cls;
+      Q.hts_h = now;
+    }
+  }
   Q.qp += 1u << (8 * cls);
   Q.qsum += 1;
   C.c[C_ACC] += 1u;
@@ -410,6 +422,7 @@ __device__ __forceinline__ double pop_batch(Queue<CM>& Q, Count& C, const SimPar
   Q.hp = (Q.hp & ~(0xffu << sh)) | ((uint32_t)pos << sh);
   Q.qsum -= n;
   if (qh > 0) put<CM>(Q.hts, h, next_head);
+  Q.hh = hol(Q, p, Q.hts_h);
   C.c[C_DISP] += (uint32_t)n;
   C.c[C_BATCH] += 1u;
   C.chk = fnv(C.chk, ((uint64_t)(k + 1) << 32) | ((uint64_t)j << 16) | ((uint64_t)h << 8) |
@@ -512,8 +525,7 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
     if (go || (first && !done)) {
       // exactly b requests of the head-of-line class whenever server s is idle
       while (busy_s <= now && Q.qsum > 0) {
-        double ts;
-        const int h = hol(Q, p, ts);
+        const int h = Q.hh;
         if (Q.q(h) < b) break;
         C.c[C_DONE] += meta_s & 0xffu;  // the previous batch on s finished at busy_s <= now
         const double sv = service<CM>(C, p, seed, ee, k, 0, h, b);
@@ -602,9 +614,8 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64
     g.ewma[(size_t)i * E + e] = ew[i];
   }
   // queue part of obs_{k+1}
-  double ts;
-  const int h = hol(Q, p, ts);
-  const double f0 = (double)Q.qsum * p.inv_n, f1 = (h >= 0 ? t1 - ts : 0.0) * p.inv_tw;
+  const int h = Q.hh;
+  const double f0 = (double)Q.qsum * p.inv_n, f1 = (h >= 0 ? t1 - Q.hts_h : 0.0) * p.inv_tw;
   put_obs(obs, E, 0, e, f0);
   put_obs(obs, E, 1, e, f1);
   if (obs_out) {
@@ -762,9 +773,7 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
       te = A.next_sw < A.next_arr ? A.next_sw : A.next_arr;
       if (next_done < te) te = next_done;
       if (Q.qsum > 0 && idle != 0u) {
-        double ts;
-        hol(Q, p, ts);
-        const double tout = ts + p.static_timeout;
+        const double tout = Q.hts_h + p.static_timeout;
         if (tout > now && tout < te) te = tout;
       }
       if (!(te < t1)) {
@@ -793,10 +802,9 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
     if (go || (first && !done)) {
       // min(B, Q_h) of the HoL class if Q_h >= B or its head waited T, to the routed server
       while (idle != 0u && Q.qsum > 0) {
-        double ts;
-        const int h = hol(Q, p, ts);
+        const int h = Q.hh;
         const int qh = Q.q(h);
-        if (!(qh >= p.bmax || now >= ts + p.static_timeout)) break;
+        if (!(qh >= p.bmax || now >= Q.hts_h + p.static_timeout)) break;
         const int n = qh < p.bmax ? qh : p.bmax;
         const int j = route_pick(idle, p.route, rr, seed, ee, k, jroute);
         if (p.route == 2) rr = (uint32_t)((j + 1) % p.K);
