@@ -143,6 +143,8 @@ __device__ __forceinline__ void store_count(const Count& C, const SysState& g, c
 struct Arrivals {
   uint32_t proc;
   double next_sw, next_arr;
+  double gap;  // mean gap of the current state (a per-lane indexed read of the parameters
+               // compiles to a memory load, which every arrival would otherwise wait for)
   uint32_t tr_idx;
   int tr_cnt;
   uint32_t jarr, jproc;
@@ -153,6 +155,7 @@ __device__ __forceinline__ void load_arrivals(Arrivals& A, const SysState& g, co
   A.proc = g.proc[e];
   A.next_sw = g.next_sw[e];
   A.next_arr = g.next_arr[e];
+  A.gap = pick<kMaxS>(p.mean_gap, (int)A.proc);
   A.tr_idx = 0;
   A.tr_cnt = 0;
   if (p.arrival_kind == 1) {
@@ -195,10 +198,11 @@ __device__ __forceinline__ int advance(Arrivals& A, const SimParams& p, uint64_t
       nxt = idx < (int)A.proc ? idx : idx + 1;
     }
     A.proc = (uint32_t)nxt;
+    A.gap = pick<kMaxS>(p.mean_gap, nxt);
     A.next_sw = now + dwell(p, nxt, unit(w.x, w.y));
     if (pick<kMaxS>(p.rate, nxt) > 0.0) {
       const u32x4 w2 = draw(seed, (uint32_t)e, k, P_ARRIVAL, A.jarr++, 0);
-      A.next_arr = now + -dlog(unit(w2.x, w2.y)) * pick<kMaxS>(p.mean_gap, nxt);
+      A.next_arr = now + -dlog(unit(w2.x, w2.y)) * A.gap;
     } else {
       A.next_arr = kInf;
     }
@@ -218,7 +222,7 @@ __device__ __forceinline__ int advance(Arrivals& A, const SimParams& p, uint64_t
 #pragma unroll
     for (int c = CM - 2; c >= 0; --c)
       if (uc < p.class_cum[c]) cls = c;
-    A.next_arr = now + -dlog(unit(w.x, w.y)) * pick<kMaxS>(p.mean_gap, (int)A.proc);
+    A.next_arr = now + -dlog(unit(w.x, w.y)) * A.gap;
   }
   return cls;
 }
@@ -302,10 +306,11 @@ __device__ __forceinline__ int advance_staged(Arrivals& A, const SimParams& p, c
       nxt = idx < (int)A.proc ? idx : idx + 1;
     }
     A.proc = (uint32_t)nxt;
+    A.gap = pick<kMaxS>(p.mean_gap, nxt);
     A.next_sw = now + dwell(p, nxt, unit(w.x, w.y));
     if (pick<kMaxS>(p.rate, nxt) > 0.0) {
       const uint32_t j = A.jarr++;
-      A.next_arr = now + st.E[j % KS][lane] * pick<kMaxS>(p.mean_gap, nxt);
+      A.next_arr = now + st.E[j % KS][lane] * A.gap;
     } else {
       A.next_arr = kInf;
     }
@@ -321,7 +326,7 @@ __device__ __forceinline__ int advance_staged(Arrivals& A, const SimParams& p, c
   } else {
     const uint32_t j = A.jarr++;
     cls = st.cls[j % KS][lane];
-    A.next_arr = now + st.E[j % KS][lane] * pick<kMaxS>(p.mean_gap, (int)A.proc);
+    A.next_arr = now + st.E[j % KS][lane] * A.gap;
   }
   return cls;
 }
