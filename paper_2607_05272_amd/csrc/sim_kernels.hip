@@ -183,50 +183,6 @@ __device__ __forceinline__ double dwell(const SimParams& p, int st, double u) {
   return kInf;
 }
 
-// Processes the switch and/or arrival due at `now` (switch first: it redraws the pending
-// arrival from the switch instant). Returns the class of an arrival at `now`, or -1.
-template <int CM>
-__device__ __forceinline__ int advance(Arrivals& A, const SimParams& p, uint64_t seed, int e,
-                                       uint32_t k, double now) {
-  if (A.next_sw == now) {
-    const u32x4 w = draw(seed, (uint32_t)e, k, P_PROCESS, A.jproc++, 0);
-    int nxt;
-    if (p.S == 2) {
-      nxt = 1 - (int)A.proc;
-    } else {
-      const int idx = (int)(unit(w.z, w.w) * (double)(p.S - 1));
-      nxt = idx < (int)A.proc ? idx : idx + 1;
-    }
-    A.proc = (uint32_t)nxt;
-    A.gap = pick<kMaxS>(p.mean_gap, nxt);
-    A.next_sw = now + dwell(p, nxt, unit(w.x, w.y));
-    if (pick<kMaxS>(p.rate, nxt) > 0.0) {
-      const u32x4 w2 = draw(seed, (uint32_t)e, k, P_ARRIVAL, A.jarr++, 0);
-      A.next_arr = now + -dlog(unit(w2.x, w2.y)) * A.gap;
-    } else {
-      A.next_arr = kInf;
-    }
-  }
-  if (!(A.next_arr == now)) return -1;
-  int cls;
-  if (p.arrival_kind == 1) {
-    const size_t base = (size_t)e * p.tr_len;
-    cls = p.tr_cls[base + A.tr_idx];
-    if (cls >= p.C) cls = p.C - 1;  // reset validated every class id; never index past C
-    ++A.tr_idx;
-    A.next_arr = (int)A.tr_idx < A.tr_cnt ? p.tr_times[base + A.tr_idx] : kInf;
-  } else {
-    const u32x4 w = draw(seed, (uint32_t)e, k, P_ARRIVAL, A.jarr++, 0);
-    const double uc = unit(w.z, w.w);
-    cls = CM - 1;
-#pragma unroll
-    for (int c = CM - 2; c >= 0; --c)
-      if (uc < p.class_cum[c]) cls = c;
-    A.next_arr = now + -dlog(unit(w.x, w.y)) * A.gap;
-  }
-  return cls;
-}
-
 // ---- wave-cooperative staging of ARRIVAL draws ---------------------------------------------
 // Block j of purpose ARRIVAL for (env, tick) gives the exponential variate E_j = -log u(w0,w1)
 // and, through the class mix, the class of uc_j = u(w2,w3); neither depends on the
@@ -290,8 +246,10 @@ __device__ __forceinline__ void refill_arrivals(Stage<KS>& st, const SimParams& 
   });
 }
 
-// As `advance`, with ARRIVAL blocks read from the stage (the caller guarantees that the two
-// blocks an instant can consume, a switch redraw and an arrival, are staged).
+// Processes the switch and/or arrival due at `now` (switch first: it redraws the pending
+// arrival from the switch instant). Returns the class of an arrival at `now`, or -1. ARRIVAL
+// blocks are read from the stage (the caller guarantees that the two blocks an instant can
+// consume, a switch redraw and an arrival, are staged).
 template <int CM, int KS>
 __device__ __forceinline__ int advance_staged(Arrivals& A, const SimParams& p, const Stage<KS>& st,
                                               int lane, uint64_t seed, int e, uint32_t k,
