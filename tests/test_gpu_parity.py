@@ -154,6 +154,67 @@ def test_edge_workloads_parity(bs, orc, name):
         assert g["cnt"][0, 2].sum() > 0          # dropped requests (counter 2)
 
 
+def _tie_traces(seed, E, L, C):
+    """Trace arrivals on a 0.25 ms grid, one to three per grid instant, classes drawn
+    independently and listed in random order: many instants where a lower class arrives after
+    a higher one at the same time, which decides the head of line between equal head times."""
+    rng = np.random.default_rng(seed)
+    times = np.zeros((E, L))
+    cls = np.zeros((E, L), np.uint8)
+    for e in range(E):
+        t, i = 0.0, 0
+        while i < L:
+            t += 0.25e-3 * int(rng.integers(1, 4))
+            for c in rng.integers(0, C, size=int(rng.integers(1, 4))):
+                if i < L:
+                    times[e, i], cls[e, i] = t, c
+                    i += 1
+    counts = np.full(E, L, np.int32)
+    counts[::7] = L // 2            # some environments run out of arrivals mid-rollout
+    return times, cls, counts
+
+
+def test_trace_ties_parity(bs, orc):
+    """Both systems against the oracle on trace arrivals with many simultaneous arrivals of
+    different classes (4 classes, 4 servers, 20 waiting slots, static batch 4 or 2 ms):
+    per-tick checksums, counters, sums and rewards bit-exact over 130 envs x 60 ticks."""
+    from workloads.presets import SVC_DET
+    E, T, L, C = 130, 60, 180, 4
+    w = trace_preset(n_servers=4, n_classes=C, queue_cap=20, obs_dim=32, shadow=1,
+                     static_bmax=4, static_timeout=2e-3, class_mix=[0.25] * C,
+                     service_kind=[SVC_DET] * C, svc_alpha=[0.3e-3, 1e-3, 2e-3, 4e-3],
+                     svc_beta=[0.1e-3, 0.2e-3, 0.5e-3, 1e-3], svc_median=[0.0] * C,
+                     w_class=[200.0, 100.0, 40.0, 20.0])
+    w["trace_max_len"] = L
+    times, cls, counts = _tie_traces(0x71E5, E, L, C)
+    acts = seeded_actions(0x71E5, T, E, 6 * w["n_servers"], small_bias=0.5)
+    say(f"[trace-ties] E={E} T={T} L={L}")
+    dev = torch.device("cuda")
+    sim = bs.Sim(w, n_envs=E)
+    sim.set_trace(torch.from_numpy(times).to(dev), torch.from_numpy(cls).to(dev),
+                  torch.from_numpy(counts).to(dev))
+    sim.reset(0)
+    a_dev = torch.from_numpy(acts).to(dev)
+    rew, rsh, rchk = [], [], []
+    for k in range(T):
+        _, r, rs = sim.step(a_dev[k], want_obs=False)
+        rew.append(r); rsh.append(rs)
+        rchk.append(sim.checksums()[0].clone())
+    sim.sync()
+    cnt, sums = sim.counters()
+    g = dict(reward=torch.stack(rew).cpu().numpy(), reward_shadow=torch.stack(rsh).cpu().numpy(),
+             cnt=cnt.cpu().numpy(), sums=sums.cpu().numpy(),
+             chk=sim.checksums().cpu().numpy().view(np.uint64))
+    g_rchk = torch.stack(rchk).cpu().numpy().view(np.uint64)
+    sim.close()
+    r = orc.rollout(w, 0, T, np.arange(E), actions=acts, want_obs=False, want_rchk=True,
+                    trace=dict(times=times, classes=cls, counts=counts))
+    assert np.array_equal(g_rchk, r["rchk"]), "learned-system checksums differ at some tick"
+    compare_sim(r, g, w, np.arange(E), 2)
+    assert g["cnt"][1, 4].sum() > 0 and g["cnt"][0, 4].sum() > 0   # both systems dispatched
+    assert g["cnt"][0, 2].sum() > 0                                  # and dropped
+
+
 def test_single_tick_and_single_env(bs, orc):
     """T = 1 on one environment and on 65 (one wave and one lane), against the oracle."""
     w = preset("C4")
