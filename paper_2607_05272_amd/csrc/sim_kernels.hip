@@ -209,32 +209,44 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Called by all 64 lanes of the wave. Lanes with `need` get blocks [jneed, jneed + KS):
+// Called by all 64 lanes of the wave. Lanes with `need` get blocks [jneed, jneed + n) with
+// n = KS when the arrival process can burst (`burst`: some state's rate exceeds KS / 4
+// arrivals per tick) or one of the lanes was already refilled in this tick, else KS / 2: at
+// low arrival rates most lanes need one or two blocks per tick, and the work of a pass is n
+// times the number of lanes served.
 // fill(owner lane, j) computes one block into the stage.
 template <int KS, class Fill>
-__device__ __forceinline__ void wave_refill(Stage<KS>& st, bool need, uint32_t jneed,
+__device__ __forceinline__ void wave_refill(Stage<KS>& st, bool need, bool burst, uint32_t jneed,
                                             uint32_t& staged_hi, int lane, Fill&& fill) {
   const uint64_t mask = __ballot(need);
   const int nneed = __popcll(mask);
+  static_assert(KS >= 4 && (KS & (KS - 1)) == 0, "stage size is a power of two");
+  const int lg = __ballot(need && (burst || staged_hi != 0u)) != 0ull ? __builtin_ctz(KS)
+                                                                       : __builtin_ctz(KS) - 1;
+  const int n = 1 << lg;
   if (need) {
     const int rank = __popcll(mask & ((1ull << lane) - 1ull));
     st.owner[rank] = (uint32_t)lane;
     st.j0[rank] = jneed;
   }
   wave_sync_lds();
-  for (int w = lane; w < KS * nneed; w += 64) {
-    const int r = w / KS;
-    fill(st.owner[r], st.j0[r] + (uint32_t)(w % KS));
+  for (int w = lane; w < n * nneed; w += 64) {
+    const int r = w >> lg;
+    fill(st.owner[r], st.j0[r] + (uint32_t)(w & (n - 1)));
   }
   wave_sync_lds();
-  if (need) staged_hi = jneed + KS;
+  if (need) staged_hi = jneed + (uint32_t)n;
 }
 
 template <int CM, int KS>
 __device__ __forceinline__ void refill_arrivals(Stage<KS>& st, const SimParams& p, bool need,
                                                 uint32_t jneed, uint32_t& staged_hi,
                                                 uint64_t seed, int e_lane0, uint32_t k, int lane) {
-  wave_refill<KS>(st, need, jneed, staged_hi, lane, [&](uint32_t own, uint32_t j) {
+  bool burst = false;
+#pragma unroll
+  for (int s = 0; s < kMaxS; ++s)
+    if (s < p.S && p.rate[s] * p.dt * 4.0 > (double)KS) burst = true;
+  wave_refill<KS>(st, need, burst, jneed, staged_hi, lane, [&](uint32_t own, uint32_t j) {
     const u32x4 d = draw(seed, (uint32_t)(e_lane0 + (int)own), k, P_ARRIVAL, j, 0);
     st.E[j % KS][own] = -dlog(unit(d.x, d.y));
     const double uc = unit(d.z, d.w);
