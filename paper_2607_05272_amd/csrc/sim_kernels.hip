@@ -192,7 +192,7 @@ __device__ __forceinline__ double dwell(const SimParams& p, int st, double u) {
 // logarithms of a few bursting environments are spread over all 64 lanes. (Service draws
 // are not staged: an environment dispatches a few batches per tick at most, and the lanes
 // dispatching at one instant already draw together.) The learned tick, whose LDS holds
-// nothing else, stages 16 slots (fewer refills in bursts: -2.3% per C5 launch against 8); the
+// nothing else, stages 16 slots (fewer refills in bursts: -2.5% per C5 launch against 8); the
 // static system shares the CU's LDS with its servers' busy times and stages 8.
 constexpr int kStageLearned = 16, kStageStatic = 8;
 template <int KS>
