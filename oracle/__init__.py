@@ -4,6 +4,7 @@ Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline leg may import 
 package. It shares no code with the HIP path; it reads workload parameter dicts (plain
 values from workloads.presets) and derives everything else itself in oracle.c.
 """
+import contextlib
 import ctypes as C
 import os
 import threading
@@ -74,42 +75,63 @@ class OrcOut(C.Structure):
                 ("logits", C.c_void_p), ("margin", C.c_void_p)]
 
 
+def _configure(path):
+    """Load an oracle library from `path` and declare its entry points."""
+    L = C.CDLL(path)
+    assert L.orc_sizeof_cfg() == C.sizeof(OrcCfg), "oracle cfg layout mismatch"
+    assert L.orc_sizeof_out() == C.sizeof(OrcOut), "oracle out layout mismatch"
+    assert L.orc_sizeof_disp() == C.sizeof(OrcDisp), "oracle disp layout mismatch"
+    vp, i32, i64, u32, u64, dbl = (C.c_void_p, C.c_int32, C.c_int64, C.c_uint32,
+                                   C.c_uint64, C.c_double)
+    L.orc_philox4x32.argtypes = [vp, vp, vp]
+    L.orc_philox4x64.argtypes = [vp, vp, vp]
+    L.orc_philox4x32_batch.argtypes = [i64, vp, vp, vp]
+    L.orc_philox_constants.argtypes = [vp]
+    L.orc_draw.argtypes = [u64, u32, u32, u32, u32, u32, vp]
+    L.orc_u01.argtypes = [u32, u32]
+    L.orc_u01.restype = dbl
+    for f in ("orc_det_log", "orc_det_exp", "orc_det_cos"):
+        getattr(L, f).argtypes = [vp, vp, i64]
+    L.orc_sample.argtypes = [i32, dbl, dbl, u64, i64, vp]
+    L.orc_n_out.argtypes = [vp]
+    L.orc_init_weights.argtypes = [vp, u64, vp, vp, vp, vp, vp, vp]
+    L.orc_policy.argtypes = [vp, vp, u64, u32, i32, vp, vp, vp, vp, vp, vp]
+    L.orc_policy.restype = i32
+    L.orc_init_weights_attn.argtypes = [vp, u64, vp]
+    L.orc_init_weights_attn.restype = i32
+    L.orc_rollout.argtypes = [vp, u64, i32, i32, vp, vp, vp, vp, vp]
+    L.orc_rollout.restype = i32
+    L.orc_gae.argtypes = [i32, i32, vp, vp, dbl, dbl, vp, vp]
+    L.orc_sample_logits.argtypes = [vp, i32, dbl, vp, vp]
+    L.orc_sample_logits.restype = i32
+    L.orc_action_u.argtypes = [u64, u32, u32]
+    L.orc_action_u.restype = dbl
+    L.orc_reset_probe.argtypes = [vp, u64, i32, vp, vp, vp, vp]
+    L.orc_reset_probe.restype = i32
+    return L
+
+
 def lib():
     global _lib
     with _lock:
         if _lib is None:
-            path = _build.build()
-            L = C.CDLL(path)
-            assert L.orc_sizeof_cfg() == C.sizeof(OrcCfg), "oracle cfg layout mismatch"
-            assert L.orc_sizeof_out() == C.sizeof(OrcOut), "oracle out layout mismatch"
-            assert L.orc_sizeof_disp() == C.sizeof(OrcDisp), "oracle disp layout mismatch"
-            vp, i32, i64, u32, u64, dbl = (C.c_void_p, C.c_int32, C.c_int64, C.c_uint32,
-                                           C.c_uint64, C.c_double)
-            L.orc_philox4x32.argtypes = [vp, vp, vp]
-            L.orc_philox4x64.argtypes = [vp, vp, vp]
-            L.orc_philox4x32_batch.argtypes = [i64, vp, vp, vp]
-            L.orc_philox_constants.argtypes = [vp]
-            L.orc_draw.argtypes = [u64, u32, u32, u32, u32, u32, vp]
-            L.orc_u01.argtypes = [u32, u32]
-            L.orc_u01.restype = dbl
-            for f in ("orc_det_log", "orc_det_exp", "orc_det_cos"):
-                getattr(L, f).argtypes = [vp, vp, i64]
-            L.orc_sample.argtypes = [i32, dbl, dbl, u64, i64, vp]
-            L.orc_n_out.argtypes = [vp]
-            L.orc_init_weights.argtypes = [vp, u64, vp, vp, vp, vp, vp, vp]
-            L.orc_policy.argtypes = [vp, vp, u64, u32, i32, vp, vp, vp, vp, vp, vp]
-            L.orc_policy.restype = i32
-            L.orc_init_weights_attn.argtypes = [vp, u64, vp]
-            L.orc_init_weights_attn.restype = i32
-            L.orc_rollout.argtypes = [vp, u64, i32, i32, vp, vp, vp, vp, vp]
-            L.orc_rollout.restype = i32
-            L.orc_gae.argtypes = [i32, i32, vp, vp, dbl, dbl, vp, vp]
-            L.orc_sample_logits.argtypes = [vp, i32, dbl, vp, vp]
-            L.orc_sample_logits.restype = i32
-            L.orc_action_u.argtypes = [u64, u32, u32]
-            L.orc_action_u.restype = dbl
-            _lib = L
+            _lib = _configure(_build.build())
     return _lib
+
+
+@contextlib.contextmanager
+def use_library(path):
+    """Run the oracle's Python entry points against another build of oracle.c (the tests'
+    deliberately broken copies, built on the CPU), restoring the real one afterwards."""
+    global _lib
+    real = lib()
+    with _lock:
+        _lib = _configure(path)
+    try:
+        yield
+    finally:
+        with _lock:
+            _lib = real
 
 
 def _p(a):
@@ -362,3 +384,15 @@ def sample_logits(logits, u):
 
 def action_u(seed, env, k):
     return lib().orc_action_u(seed, env, k)
+
+
+def reset_probe(w, seed, env_ids):
+    """Arrival process state right after reset (R11): modulating state, next switch and
+    first arrival, per listed env."""
+    c = make_cfg(w)
+    ids = np.ascontiguousarray(env_ids, dtype=np.uint32)
+    n = ids.size
+    proc = np.empty(n, np.int32); sw = np.empty(n); arr = np.empty(n)
+    if lib().orc_reset_probe(C.byref(c), seed, n, _p(ids), _p(proc), _p(sw), _p(arr)) != 0:
+        raise ValueError("reset_probe needs modulated arrivals")
+    return dict(proc=proc, next_sw=sw, next_arr=arr)

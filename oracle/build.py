@@ -25,3 +25,17 @@ def build(force=False):
 if __name__ == "__main__":
     build(force=True)
     print(LIB)
+
+
+def build_variant(source_text, lib_path):
+    """Compile `source_text` (a modified copy of oracle.c, written next to `lib_path`) with
+    the oracle's own flags into `lib_path`. The tests use this to check that each pin
+    rejects a deliberately broken oracle; the real library is untouched."""
+    src = os.path.splitext(lib_path)[0] + ".c"
+    with open(src, "w") as f:
+        f.write(source_text)
+    cmd = [a for a in CMD]
+    cmd[cmd.index(SRC)] = src
+    cmd[cmd.index(LIB)] = lib_path
+    subprocess.run(cmd + ["-I", HERE], check=True)
+    return lib_path

@@ -1039,3 +1039,23 @@ int32_t orc_sample_logits(const double* l, int32_t A, double u, double* logp, do
 
 /* The ACTION uniform of (env, step), for tests. */
 double orc_action_u(uint64_t seed, uint32_t env, uint32_t k) { return action_u(seed, env, k); }
+
+/* The arrival process of each listed env right after reset (R11, R21), for tests of the
+ * stationary start: modulating state, next switch instant and first arrival instant.
+ * Returns 0, or -1 on invalid arguments. */
+int orc_reset_probe(const orc_cfg* c, uint64_t seed, int32_t n, const uint32_t* env_ids,
+                    int32_t* proc, double* next_sw, double* next_arr) {
+  if (c->n_states < 1 || c->n_states > ORC_MAX_S || c->arrival_kind == ORC_ARR_TRACE) return -1;
+  derived d;
+  derive(c, &d);
+  sys_t* S = (sys_t*)malloc(sizeof(sys_t));
+  if (!S) return -1;
+  for (int32_t i = 0; i < n; i++) {
+    reset_sys(c, &d, NULL, i, env_ids[i], seed, 0, 1.0, S);
+    proc[i] = S->proc;
+    next_sw[i] = S->next_sw;
+    next_arr[i] = S->next_arr;
+  }
+  free(S);
+  return 0;
+}

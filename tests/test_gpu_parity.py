@@ -308,7 +308,7 @@ def _trace_tensors(g, dev):
     return times, cls, cnt, L
 
 
-@pytest.mark.parametrize("tr", ["T1", "T2", "T3"])
+@pytest.mark.parametrize("tr", ["T1", "T2", "T3", "T4"])
 def test_hand_traces_on_gpu(bs, orc, tr):
     g = GOLD[tr]
     w = trace_preset(**g["cfg"])
@@ -318,7 +318,7 @@ def test_hand_traces_on_gpu(bs, orc, tr):
     T = g["T"]
     if tr == "T1":
         acts = np.full((T, 1), g["action"], np.uint8)
-    elif tr == "T2":
+    elif tr in ("T2", "T4"):
         acts = np.array(g["actions"], np.uint8)[:, None]
     else:
         acts = np.zeros((T, 1), np.uint8)
@@ -337,7 +337,7 @@ def test_hand_traces_on_gpu(bs, orc, tr):
     rew = torch.stack(rews).cpu().numpy()[:, 0]
     cnt_, sums = sim.counters()
     cnt_ = cnt_.cpu().numpy(); sums = sums.cpu().numpy()
-    if tr in ("T1", "T2"):
+    if tr in ("T1", "T2", "T4"):
         for k, v in g["rewards"].items():
             assert abs(rew[int(k)] - v) <= 1e-9 * max(1.0, abs(v))
         nz = [k for k in range(T) if str(k) not in g["rewards"]]
@@ -346,6 +346,11 @@ def test_hand_traces_on_gpu(bs, orc, tr):
         o1 = obs[1].cpu().numpy()[:, 0]
         np.testing.assert_allclose(o1, np.array(g["obs1"], np.float32), rtol=1e-6)
         assert cnt_[0, 2, 0] == g["dropped_cum"][-1] and cnt_[0, 5, 0] == g["completed_cum"][-1]
+    if tr == "T4":
+        for k, v in g["obs"].items():
+            np.testing.assert_allclose(obs[int(k)].cpu().numpy()[:, 0], np.array(v, np.float32),
+                                       rtol=1e-6, atol=1e-9)
+        assert cnt_[0, 5, 0] == g["completed_cum"][-1]
     if tr == "T3":
         assert abs(sums[1, 0, 0] - g["shadow_latency_sum"]) < 1e-12
         assert cnt_[1, 4, 0] == len(g["shadow_dispatches"])
