@@ -226,6 +226,15 @@ int sim_init_weights(sim_ctx* ctx, uint64_t seed, void* d_weights);
 int sim_policy(sim_ctx* ctx, const void* d_weights, const float* d_obs, uint32_t step,
                uint8_t* d_act, float* d_logp, float* d_value, float* d_logits);
 
+/* Diagnostics for the parity tests of the policy MLP (Sec. 4.2): sim_policy, run by the same
+ * kernel source instantiated with extra stores, which also writes every hidden activation as
+ * the kernel hands it to the next layer: d_hidden [H1 + H2][E] fp32 (rows 0..H1-1 the first
+ * hidden layer, then the second; in bf16 configurations the bf16 values, widened). Its other
+ * outputs equal sim_policy's bit for bit. SIM_EUNSUPPORTED for the attention policy.       */
+int sim_policy_hidden(sim_ctx* ctx, const void* d_weights, const float* d_obs, uint32_t step,
+                      uint8_t* d_act, float* d_logp, float* d_value, float* d_logits,
+                      float* d_hidden);
+
 /* T ticks of policy + simulator from the current state (obs_k -> a_k -> obs_{k+1}),
  * writing the trajectory; with a value head, row T of traj->value holds V(obs_T).       */
 int sim_rollout(sim_ctx* ctx, const void* d_weights, int32_t T, const sim_traj* traj);

@@ -23,7 +23,7 @@ SYMBOLS = ("sim_last_error", "sim_abi_version", "sim_create", "sim_destroy", "si
            "sim_checksums", "sim_stats", "sim_sync", "sim_set_timing", "sim_get_timing",
            "ppo_minibatch_grad", "sim_ppo_grad_count", "reinforce_minibatch_grad",
            "sim_params_from_weights", "adam_update", "sim_update", "sim_attn_weights_layout",
-           "sim_get_state", "sim_set_state", "sim_device_primitive")
+           "sim_get_state", "sim_set_state", "sim_device_primitive", "sim_policy_hidden")
 ALGO_PPO, ALGO_REINFORCE = 0, 1
 KERNEL_CLASSES = ("policy", "step", "static", "gae", "reset", "other", "ppo")
 
@@ -108,6 +108,7 @@ def load():
         "sim_step": [vp, vp, vp, vp, vp], "sim_tick": [vp, vp],
         "sim_weights_layout": [vp, vp], "sim_init_weights": [vp, u64, vp],
         "sim_policy": [vp, vp, vp, u32, vp, vp, vp, vp], "sim_rollout": [vp, vp, i32, vp],
+        "sim_policy_hidden": [vp, vp, vp, u32, vp, vp, vp, vp, vp],
         "returns_gae": [vp, i32, vp, vp, dbl, dbl, vp, vp], "sim_counters": [vp, vp, vp],
         "sim_checksums": [vp, vp], "sim_stats": [vp, vp], "sim_sync": [vp],
         "sim_set_timing": [vp, i32], "sim_get_timing": [vp, vp, vp, i32],

@@ -39,14 +39,23 @@ struct F32Mode {
 
 __device__ __forceinline__ float gelu(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
 
+// Where a diagnostic instantiation (DBG = true) of the policy kernels also writes every hidden
+// activation it passes to the next layer: h [N][E] fp32 (bf16 values widened), for the
+// workgroup's environments e0 .. The production instantiations (DBG = false) compile without
+// these stores and are otherwise the same code.
+struct HidOut {
+  float* h;
+  int E, e0;
+};
+
 // out[64][N] = act_in[64][K] * W^T  (W packed out-major [N][K]); epilogue: +bias, then
 // GELU + rounding into act_out (hidden layers) or fp32 into lg (last layer).
-template <class M, int K, int N, bool LAST>
+template <class M, int K, int N, bool LAST, bool DBG = false>
 __device__ __forceinline__ void layer(const typename M::elem* __restrict__ in,
                                       const typename M::elem* __restrict__ W,
                                       const float* __restrict__ bias,
                                       typename M::elem* __restrict__ out, float* __restrict__ lg,
-                                      int lg_stride) {
+                                      int lg_stride, HidOut ho = {}) {
   constexpr int NT = N / 16;             // column tiles
   constexpr int NTW = (NT + 3) / 4;      // column tiles per wave
   constexpr int SIN = K + M::PAD;        // LDS row stride of the input
@@ -86,8 +95,14 @@ __device__ __forceinline__ void layer(const typename M::elem* __restrict__ in,
       for (int i = 0; i < 4; ++i) {
         const int row = rt * 16 + kq * 4 + i;
         const float v = acc[rt][c][i] + bv;
-        if (LAST) lg[row * lg_stride + col] = v;
-        else out[row * SOUT + col] = M::from_f32(gelu(v));
+        if (LAST) {
+          lg[row * lg_stride + col] = v;
+        } else {
+          const typename M::elem g = M::from_f32(gelu(v));
+          out[row * SOUT + col] = g;
+          if constexpr (DBG)
+            if (ho.e0 + row < ho.E) ho.h[(size_t)col * ho.E + ho.e0 + row] = (float)g;
+        }
       }
     }
   }
@@ -107,13 +122,14 @@ struct Shape {
   static constexpr size_t LDS = REGION_A + REGION_B;
 };
 
-template <class M, int FP, int H1, int H2, int AP>
+template <class M, int FP, int H1, int H2, int AP, bool DBG>
 __global__ __launch_bounds__(kThreads) void policy_k(MlpParams m, const float* __restrict__ obs,
                                                      uint64_t seed, uint32_t step,
                                                      uint8_t* __restrict__ act,
                                                      float* __restrict__ logp,
                                                      float* __restrict__ value,
-                                                     float* __restrict__ logits) {
+                                                     float* __restrict__ logits,
+                                                     float* __restrict__ hid) {
   typedef Shape<M, FP, H1, H2, AP> Sh;
   typedef typename M::elem E;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -132,9 +148,11 @@ __global__ __launch_bounds__(kThreads) void policy_k(MlpParams m, const float* _
     xs[r * Sh::SX + f] = M::from_f32(v);
   }
   __syncthreads();
-  layer<M, FP, H1, false>(xs, static_cast<const E*>(m.w1), m.b1, h1s, nullptr, 0);
+  layer<M, FP, H1, false, DBG>(xs, static_cast<const E*>(m.w1), m.b1, h1s, nullptr, 0,
+                               HidOut{hid, m.E, e0});
   __syncthreads();
-  layer<M, H1, H2, false>(h1s, static_cast<const E*>(m.w2), m.b2, h2s, nullptr, 0);
+  layer<M, H1, H2, false, DBG>(h1s, static_cast<const E*>(m.w2), m.b2, h2s, nullptr, 0,
+                               HidOut{DBG ? hid + (size_t)H1 * m.E : nullptr, m.E, e0});
   __syncthreads();
   layer<M, H2, AP, true>(h2s, static_cast<const E*>(m.w3), m.b3, nullptr, lg, Sh::SL);
   __syncthreads();
@@ -265,6 +283,21 @@ __device__ __forceinline__ u32x2 gelu_pack4(const f32x4 v) {
   return pk;
 }
 
+// diagnostic store of four packed bf16 activations (units unit0 .. unit0 + 3 of tile row `row`)
+template <bool DBG>
+__device__ __forceinline__ void hid_store4(const HidOut& ho, int unit0, int row, u32x2 v) {
+  if constexpr (DBG) {
+    const int e = ho.e0 + row;
+    if (e < ho.E) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t w = (i < 2 ? v.x : v.y) >> (16 * (i & 1));
+        ho.h[(size_t)(unit0 + i) * ho.E + e] = __uint_as_float(w << 16);
+      }
+    }
+  }
+}
+
 // One output tile (16 units) of a layer for RTN consecutive environment tiles starting at rt0:
 // acc[rt] = act[rows] W[:, tile] + bias, with a ring of D k-steps of weight fragments in flight.
 // hook(ks) runs after each k-step's MFMAs: the caller puts independent VALU work there, which
@@ -301,11 +334,11 @@ __device__ __forceinline__ void mma_tile(const uint16_t* __restrict__ act, int s
 // budget). A lane's four accumulator values are four consecutive units of one environment,
 // written as one 8-byte store. In place (out aliases act) the packed results wait in
 // registers until every wave has finished reading act.
-template <int K, int N, int RT, int NW, bool kInPlace>
+template <int K, int N, int RT, int NW, bool kInPlace, bool DBG>
 __device__ __forceinline__ void hidden_layer(const uint16_t* __restrict__ act, int sa,
                                              const uint16_t* __restrict__ W,
                                              const float* __restrict__ bias, uint16_t* out,
-                                             int so) {
+                                             int so, HidOut ho) {
   constexpr int NT = N / 16, CTW = NT / NW, KS = K / 32;
   static_assert(NT % NW == 0, "hidden tiles divide evenly over the waves");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -314,6 +347,7 @@ __device__ __forceinline__ void hidden_layer(const uint16_t* __restrict__ act, i
   u32x2 pk[kInPlace ? CTW : 1][RT];
   auto finish = [&](int c, int rt) {
     const u32x2 v = gelu_pack4(acc[c & 1][rt]);
+    hid_store4<DBG>(ho, (wave + NW * c) * 16 + kq * 4, rt * 16 + r16, v);
     if (kInPlace) pk[kInPlace ? c : 0][rt] = v;
     else *reinterpret_cast<u32x2*>(out + (rt * 16 + r16) * so + (wave + NW * c) * 16 + kq * 4) = v;
   };
@@ -399,11 +433,11 @@ __device__ __forceinline__ void mma_group(const uint16_t* __restrict__ act, int 
 // Hidden layer with TPW tiles per pass (see mma_group): the wave's CTW tiles wave, wave + NW,
 // ... in CTW / TPW passes, each followed by its GELU epilogue; in place, the packed results
 // wait in registers until every wave has finished reading act.
-template <int K, int N, int RT, int NW, int TPW, bool kInPlace>
+template <int K, int N, int RT, int NW, int TPW, bool kInPlace, bool DBG>
 __device__ __forceinline__ void hidden_layer_g(const uint16_t* __restrict__ act, int sa,
                                                const uint16_t* __restrict__ W,
                                                const float* __restrict__ bias, uint16_t* out,
-                                               int so) {
+                                               int so, HidOut ho) {
   constexpr int NT = N / 16, CTW = NT / NW, NG = CTW / TPW;
   static_assert(NT % NW == 0 && CTW % TPW == 0, "tiles divide evenly over waves and passes");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -419,6 +453,7 @@ __device__ __forceinline__ void hidden_layer_g(const uint16_t* __restrict__ act,
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
         const u32x2 v = gelu_pack4(acc[i][rt]);
+        hid_store4<DBG>(ho, (wave + NW * c) * 16 + kq * 4, rt * 16 + r16, v);
         if (kInPlace) pk[kInPlace ? c : 0][rt] = v;
         else *reinterpret_cast<u32x2*>(out + (rt * 16 + r16) * so + (wave + NW * c) * 16 + kq * 4) = v;
       }
@@ -480,13 +515,14 @@ struct BigShape {
   static constexpr size_t LDS = X_BYTES + HREG;
 };
 
-template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW>
+template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW, bool DBG>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MINB / 4 > 0 ? NW * MINB / 4 : 1))) void policy_bf16_k(MlpParams m, const float* __restrict__ obs,
                                                                uint64_t seed, uint32_t step,
                                                                uint8_t* __restrict__ act,
                                                                float* __restrict__ logp,
                                                                float* __restrict__ value,
-                                                               float* __restrict__ logits) {
+                                                               float* __restrict__ logits,
+                                                               float* __restrict__ hid) {
   typedef BigShape<FP, H1, H2, AP, RT, NW> Sh;
   constexpr int ROWS = Sh::ROWS, NTHR = NW * 64;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -507,18 +543,19 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
     *reinterpret_cast<uint32_t*>(xs + r * Sh::SX + f) = pack_bf16(v0, v1);
   }
   __syncthreads();
+  const HidOut h1o{hid, m.E, e0}, h2o{DBG ? hid + (size_t)H1 * m.E : nullptr, m.E, e0};
   if constexpr (TPW == 1) {
-    hidden_layer<FP, H1, RT, NW, false>(xs, Sh::SX, static_cast<const uint16_t*>(m.w1), m.b1, hs,
-                                        Sh::SH);
+    hidden_layer<FP, H1, RT, NW, false, DBG>(xs, Sh::SX, static_cast<const uint16_t*>(m.w1), m.b1,
+                                             hs, Sh::SH, h1o);
     __syncthreads();
-    hidden_layer<H1, H2, RT, NW, true>(hs, Sh::SH, static_cast<const uint16_t*>(m.w2), m.b2, hs,
-                                       Sh::SH);
+    hidden_layer<H1, H2, RT, NW, true, DBG>(hs, Sh::SH, static_cast<const uint16_t*>(m.w2), m.b2,
+                                            hs, Sh::SH, h2o);
   } else {
-    hidden_layer_g<FP, H1, RT, NW, TPW, false>(xs, Sh::SX, static_cast<const uint16_t*>(m.w1),
-                                               m.b1, hs, Sh::SH);
+    hidden_layer_g<FP, H1, RT, NW, TPW, false, DBG>(xs, Sh::SX, static_cast<const uint16_t*>(m.w1),
+                                                    m.b1, hs, Sh::SH, h1o);
     __syncthreads();
-    hidden_layer_g<H1, H2, RT, NW, TPW, true>(hs, Sh::SH, static_cast<const uint16_t*>(m.w2),
-                                              m.b2, hs, Sh::SH);
+    hidden_layer_g<H1, H2, RT, NW, TPW, true, DBG>(hs, Sh::SH, static_cast<const uint16_t*>(m.w2),
+                                                   m.b2, hs, Sh::SH, h2o);
   }
   __syncthreads();
   output_layer<H2, AP, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w3), m.b3, lg, Sh::SL);
@@ -579,12 +616,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
   }
 }
 
-template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW = 1>
+template <bool DBG, int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW = 1>
 hipError_t run_policy_bf16(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
-                           uint8_t* act, float* logp, float* value, float* logits, hipStream_t st) {
+                           uint8_t* act, float* logp, float* value, float* logits, float* hid,
+                           hipStream_t st) {
   typedef BigShape<FP, H1, H2, AP, RT, NW> Sh;
   static_assert(Sh::LDS <= 160 * 1024, "LDS budget");
-  auto kern = policy_bf16_k<FP, H1, H2, AP, RT, NW, MINB, TPW>;
+  auto kern = policy_bf16_k<FP, H1, H2, AP, RT, NW, MINB, TPW, DBG>;
   static bool attr = false;
   if (!attr) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -593,15 +631,17 @@ hipError_t run_policy_bf16(const MlpParams& m, const float* obs, uint64_t seed, 
     attr = true;
   }
   const dim3 grid((m.E + Sh::ROWS - 1) / Sh::ROWS), block(NW * 64);
-  hipLaunchKernelGGL(kern, grid, block, Sh::LDS, st, m, obs, seed, step, act, logp, value, logits);
+  hipLaunchKernelGGL(kern, grid, block, Sh::LDS, st, m, obs, seed, step, act, logp, value, logits,
+                     hid);
   return hipGetLastError();
 }
 
-template <class M, int FP, int H1, int H2, int AP>
+template <bool DBG, class M, int FP, int H1, int H2, int AP>
 hipError_t run_policy(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
-                      uint8_t* act, float* logp, float* value, float* logits, hipStream_t st) {
+                      uint8_t* act, float* logp, float* value, float* logits, float* hid,
+                      hipStream_t st) {
   typedef Shape<M, FP, H1, H2, AP> Sh;
-  auto kern = policy_k<M, FP, H1, H2, AP>;
+  auto kern = policy_k<M, FP, H1, H2, AP, DBG>;
   static bool attr = false;
   if (!attr) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -610,7 +650,8 @@ hipError_t run_policy(const MlpParams& m, const float* obs, uint64_t seed, uint3
     attr = true;
   }
   const dim3 grid((m.E + kRows - 1) / kRows), block(kThreads);
-  hipLaunchKernelGGL(kern, grid, block, Sh::LDS, st, m, obs, seed, step, act, logp, value, logits);
+  hipLaunchKernelGGL(kern, grid, block, Sh::LDS, st, m, obs, seed, step, act, logp, value, logits,
+                     hid);
   return hipGetLastError();
 }
 
@@ -634,26 +675,36 @@ bool policy_shape_supported(const MlpParams& m) {
   return false;
 }
 
-hipError_t launch_policy(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
-                         uint8_t* act, float* logp, float* value, float* logits, hipStream_t st) {
+template <bool DBG>
+static hipError_t launch_policy_t(const MlpParams& m, const float* obs, uint64_t seed,
+                                  uint32_t step, uint8_t* act, float* logp, float* value,
+                                  float* logits, float* hid, hipStream_t st) {
   if (!m.bf16 && m.FP == 8 && m.H1 == 64 && m.H2 == 64 && m.AP == 16)
-    return run_policy<F32Mode, 8, 64, 64, 16>(m, obs, seed, step, act, logp, value, logits, st);
+    return run_policy<DBG, F32Mode, 8, 64, 64, 16>(m, obs, seed, step, act, logp, value, logits, hid, st);
   // bf16 shapes: 64-row tiles with 4 waves, two workgroups per CU, when there are enough
   // rows to fill the chip; 32-row tiles otherwise
   const bool big = m.E >= 64 * 512;
   if (m.bf16 && m.FP == 32 && m.H1 == 128 && m.H2 == 128 && m.AP == 16)
-    return big ? run_policy_bf16<32, 128, 128, 16, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, st)
-               : run_policy_bf16<32, 128, 128, 16, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, st);
+    return big ? run_policy_bf16<DBG, 32, 128, 128, 16, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, hid, st)
+               : run_policy_bf16<DBG, 32, 128, 128, 16, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, hid, st);
   if (m.bf16 && m.FP == 32 && m.H1 == 256 && m.H2 == 256 && m.AP == 32)
-    return big ? run_policy_bf16<32, 256, 256, 32, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, st)
-               : run_policy_bf16<32, 256, 256, 32, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, st);
+    return big ? run_policy_bf16<DBG, 32, 256, 256, 32, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, hid, st)
+               : run_policy_bf16<DBG, 32, 256, 256, 32, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, hid, st);
   if (m.bf16 && m.FP == 64 && m.H1 == 256 && m.H2 == 256 && m.AP == 64)
-    return big ? run_policy_bf16<64, 256, 256, 64, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, st)
-               : run_policy_bf16<64, 256, 256, 64, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, st);
+    return big ? run_policy_bf16<DBG, 64, 256, 256, 64, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, hid, st)
+               : run_policy_bf16<DBG, 64, 256, 256, 64, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, hid, st);
   if (m.bf16 && m.FP == 96 && m.H1 == 512 && m.H2 == 512 && m.AP == 112)
-    return big ? run_policy_bf16<96, 512, 512, 112, 4, 8, 2, 2>(m, obs, seed, step, act, logp, value, logits, st)
-               : run_policy_bf16<96, 512, 512, 112, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, st);
+    return big ? run_policy_bf16<DBG, 96, 512, 512, 112, 4, 8, 2, 2>(m, obs, seed, step, act, logp, value, logits, hid, st)
+               : run_policy_bf16<DBG, 96, 512, 512, 112, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, hid, st);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_policy(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
+                         uint8_t* act, float* logp, float* value, float* logits, float* hidden,
+                         hipStream_t st) {
+  if (hidden)
+    return launch_policy_t<true>(m, obs, seed, step, act, logp, value, logits, hidden, st);
+  return launch_policy_t<false>(m, obs, seed, step, act, logp, value, logits, nullptr, st);
 }
 
 hipError_t launch_repack(const MlpParams& m, const void* d_weights, const size_t off[6],

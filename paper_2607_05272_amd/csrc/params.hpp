@@ -88,8 +88,10 @@ struct MlpParams {
 hipError_t launch_repack(const MlpParams& m, const void* d_weights, const size_t off[6],
                          void* w1, float* b1, void* w2, float* b2, void* w3, float* b3,
                          hipStream_t st);
+// hidden != NULL runs the diagnostic instantiation that also writes the hidden activations
+// passed between layers: [H1][E] then [H2][E] fp32
 hipError_t launch_policy(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
-                         uint8_t* act, float* logp, float* value, float* logits,
+                         uint8_t* act, float* logp, float* value, float* logits, float* hidden,
                          hipStream_t st);
 hipError_t launch_init_weights(int F, int H1, int H2, int Ap, int bf16, uint64_t seed,
                                void* d_weights, const size_t off[6], hipStream_t st);

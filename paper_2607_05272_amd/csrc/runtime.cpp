@@ -176,6 +176,11 @@ static int validate(const sim_cfg* c) {
       return fail(SIM_EINVAL, "deterministic service of class %d must be > 0", i);
   }
   if (std::fabs(mix - 1.0) > 1e-9) return fail(SIM_EINVAL, "class_mix must sum to 1");
+  // lognormal service median * exp(sigma Z): the normal draw is below 8.6 in magnitude and the
+  // deterministic exponential holds for arguments below 700, so sigma is kept to [0, 64]
+  for (int i = 0; i < c->n_classes; ++i)
+    if (c->service_kind[i] == SIM_SVC_LOGN && !(c->svc_sigma >= 0.0 && c->svc_sigma <= 64.0))
+      return fail(SIM_EINVAL, "svc_sigma must lie in [0, 64] for lognormal service");
   if (!(c->obs_tw > 0.0) || !(c->lambda_ref > 0.0))
     return fail(SIM_EINVAL, "obs_tw and lambda_ref must be > 0");
   if (c->static_route < SIM_ROUTE_LOWEST || c->static_route > SIM_ROUTE_ROUND_ROBIN)
@@ -548,10 +553,11 @@ static int prepare_policy(sim_ctx* x, const void* d_weights) {
 
 // the policy kernel of the configured network (after prepare_policy)
 static hipError_t policy_launch(sim_ctx* x, const float* obs, uint32_t step, uint8_t* act,
-                                float* logp, float* value, float* logits) {
+                                float* logp, float* value, float* logits,
+                                float* hidden = nullptr) {
   if (x->cfg.policy_kind == SIM_POLICY_ATTN)
     return launch_attn_policy(x->a, obs, x->seed, step, act, logp, value, logits, x->stream);
-  return launch_policy(x->m, obs, x->seed, step, act, logp, value, logits, x->stream);
+  return launch_policy(x->m, obs, x->seed, step, act, logp, value, logits, hidden, x->stream);
 }
 
 int sim_policy(sim_ctx* x, const void* d_weights, const float* d_obs, uint32_t step,
@@ -562,6 +568,21 @@ int sim_policy(sim_ctx* x, const void* d_weights, const float* d_obs, uint32_t s
   if (rc) return rc;
   HIPCHK(x->timed(SIM_KC_POLICY, [&] {
            return policy_launch(x, d_obs, step, d_act, d_logp, d_value, d_logits);
+         }), "policy kernel launch");
+  return SIM_OK;
+}
+
+int sim_policy_hidden(sim_ctx* x, const void* d_weights, const float* d_obs, uint32_t step,
+                      uint8_t* d_act, float* d_logp, float* d_value, float* d_logits,
+                      float* d_hidden) {
+  if (!x || !d_weights || !d_obs || !d_hidden) return fail(SIM_EINVAL, "NULL argument");
+  if (x->cfg.policy_kind != SIM_POLICY_MLP)
+    return fail(SIM_EUNSUPPORTED, "sim_policy_hidden is for the MLP policy");
+  if (d_value && !x->cfg.value_head) return fail(SIM_EINVAL, "d_value needs value_head = 1");
+  int rc = prepare_policy(x, d_weights);
+  if (rc) return rc;
+  HIPCHK(x->timed(SIM_KC_POLICY, [&] {
+           return policy_launch(x, d_obs, step, d_act, d_logp, d_value, d_logits, d_hidden);
          }), "policy kernel launch");
   return SIM_OK;
 }

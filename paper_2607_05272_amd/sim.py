@@ -224,6 +224,22 @@ class Sim:
                                     _p(logp), _p(val), _p(lg)), "sim_policy")
         return dict(actions=act, logp=logp, value=val, logits=lg)
 
+    def policy_hidden(self, weights, obs, step):
+        """sim_policy_hidden: the policy's outputs plus the hidden activations h1 [H1][E] and
+        h2 [H2][E] that the kernel passes between layers."""
+        E = obs.shape[1]
+        assert E == self.E and obs.shape[0] == self.F
+        H1, H2 = self.w["mlp_h1"], self.w["mlp_h2"]
+        act = torch.empty(E, dtype=torch.uint8, device=self.device)
+        logp = torch.empty(E, dtype=torch.float32, device=self.device)
+        val = torch.empty(E, dtype=torch.float32, device=self.device) if self.w["value_head"] else None
+        lg = torch.empty((self.Ap, E), dtype=torch.float32, device=self.device)
+        hid = torch.empty((H1 + H2, E), dtype=torch.float32, device=self.device)
+        L.check(self.lib.sim_policy_hidden(self._ctx, _p(weights), _p(obs), C.c_uint32(step),
+                                           _p(act), _p(logp), _p(val), _p(lg), _p(hid)),
+                "sim_policy_hidden")
+        return dict(actions=act, logp=logp, value=val, logits=lg, h1=hid[:H1], h2=hid[H1:])
+
     def rollout(self, weights, T, store_obs=False, rchk=False, traj=None):
         if traj is None:
             traj = Trajectory(T, self.E, self.F, self.device, value=bool(self.w["value_head"]),

@@ -56,6 +56,12 @@ def test_invalid_config_is_rejected_without_device_work():
     bad.obs_dim = 4
     assert L.sim_create(C.byref(bad), None, C.byref(ctx)) == -1
     assert b"obs_dim" in L.sim_last_error()
+    for sigma in (float("nan"), -0.5, 100.0):
+        bad = _lib.make_cfg(preset("C4"))
+        bad.svc_sigma = sigma
+        assert L.sim_create(C.byref(bad), None, C.byref(ctx)) == -1
+        assert b"svc_sigma" in L.sim_last_error()
+        assert not ctx.value
     bad = _lib.make_cfg(preset("C2"))
     bad.abi_version = 99
     assert L.sim_create(C.byref(bad), None, C.byref(ctx)) == -1

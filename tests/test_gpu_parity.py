@@ -9,7 +9,8 @@ import numpy as np
 import pytest
 
 from workloads import preset, trace_preset, burst_preset, baseline_preset, attn_preset
-from workloads.gen import seeded_actions, seeded_obs, seeded_rewards_values
+from workloads.gen import seeded_actions, seeded_obs, seeded_rewards_values, seeded_weights_f32
+from policy_check import attn_tol, check_attn_logits, check_layers, end_to_end_bound
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -376,97 +377,36 @@ def test_init_weights_bit_identical(bs, orc, name):
     sim.close()
 
 
-def mlp_tol(w, wts, obs):
-    """Per-output tolerance |gpu - oracle| <= tol_a = c * sum_i |W3_ia| |h2_i| + |b3_a| eps
-    (+ the GELU term below in bf16 mode).
-
-    fp32 mode: only accumulation order differs (fp32 sums of <= 64 terms): c = 2^-18.
-    bf16 mode: each layer input is rounded to bf16; a value whose fp32 (GPU) and fp64
-    (oracle) pre-rounding images straddle a rounding boundary can round one bf16 ulp
-    (2^-8 relative) apart, and the two hidden layers propagate such flips, so c = 2^-6
-    (one ulp at each of the two hidden rounding points, with a factor-of-two margin).
-    The bf16 kernels evaluate GELU to within eps_G = 2^-15 absolute (a fitted logistic
-    form); that error enters h1 directly and h2 directly and through W2 (GELU' <= 1.13):
-    + eps_G * sum_i |W3_ia| (1 + 1.13 sum_j |W2_ji|)."""
-    import torch.nn.functional as Fn
-    bf = bool(w["mlp_bf16"])
-
-    def rnd(t):
-        return t.to(torch.float32).to(torch.bfloat16).to(torch.float64) if bf else t
-    x = rnd(torch.tensor(obs, dtype=torch.float64))
-    W = {k: torch.tensor(v, dtype=torch.float64) for k, v in wts.items()}
-    h1 = rnd(Fn.gelu(x @ W["w1"] + W["b1"]))
-    h2 = rnd(Fn.gelu(h1 @ W["w2"] + W["b2"]))
-    scale = (h2.abs() @ W["w3"].abs()).numpy() + np.abs(wts["b3"])[None, :]
-    if not bf:
-        return scale * 2.0 ** -18
-    gelu_term = 2.0 ** -15 * ((1.0 + 1.13 * np.abs(wts["w2"]).sum(axis=0)) @ np.abs(wts["w3"]))
-    return scale * 2.0 ** -6 + gelu_term[None, :]
+def mlp_weights(w, seed):
+    """Random MLP weights with nonzero biases (the Xavier initialisation has zero biases, which
+    would leave the kernels' bias paths untested); bf16-representable matrices in bf16
+    configurations."""
+    dims = [w["obs_dim"], w["mlp_h1"], w["mlp_h2"], 6 * w["n_servers"] + w["value_head"]]
+    W = seeded_weights_f32(seed, dims, bf16=bool(w["mlp_bf16"]))
+    return {k: v.astype(np.float64) for k, v in W.items()}
 
 
-def attn_tol(w, W, obs):
-    """Per-output tolerance of the fp32 attention kernel against the fp64 oracle, from a
-    forward error analysis in fp64 over the exact intermediates (u = 2^-24):
-    * a fp32 dot product with fma over n terms plus a bias is off by at most (n + 1) u times
-      the sum of its terms' magnitudes (local rounding), and an input error e propagates
-      as |W|^T e;
-    * a score error ds changes the softmax weights by at most 2 max|ds| in L1 (exp, sum and
-      the division add (L + 2) u), so the weighted values move by that times max|v| plus the
-      weights' average of the values' errors;
-    * the mean pool adds L u of the mean magnitude; GELU has slope at most 1.13 and erff is
-      good to a few ulps (8 u |z|).
-    The tolerance is four times the bound (margin for the first-order treatment)."""
-    u = 2.0 ** -24
-    x = np.asarray(obs, np.float64)
-    n, F = x.shape
-    L, D, NH = w["attn_tokens"], w["attn_embed"], w["attn_heads"]
-    G, dh = F // L, D // NH
-    Wa = {k: np.abs(v) for k, v in W.items()}
+def policy_weights(orc, w, seed):
+    return attn_weights(orc, w, seed) if w.get("policy_kind", 0) == 1 else mlp_weights(w, seed)
 
-    def lin(inp, err, k_w, k_b):
-        """value, error of inp @ W + b given inp's error."""
-        val = inp @ W[k_w] + W[k_b]
-        nt = W[k_w].shape[0]
-        e = err @ Wa[k_w] + (nt + 1) * u * (np.abs(inp) @ Wa[k_w] + Wa[k_b])
-        return val, e
 
-    xt = x.reshape(n, L, G)
-    win = W["w_in"].reshape(L, G, D)
-    tok = np.einsum("nlg,lgd->nld", xt, win) + W["b_in"]
-    e_tok = (G + 1) * u * (np.einsum("nlg,lgd->nld", np.abs(xt), np.abs(win)) + Wa["b_in"])
-    qkv, e_qkv = lin(tok, e_tok, "w_qkv", "b_qkv")
-    q, k, v = qkv[..., :D], qkv[..., D:2 * D], qkv[..., 2 * D:]
-    eq, ek, ev = e_qkv[..., :D], e_qkv[..., D:2 * D], e_qkv[..., 2 * D:]
-    o = np.zeros((n, L, D))
-    eo = np.zeros((n, L, D))
-    for h in range(NH):
-        c = slice(h * dh, (h + 1) * dh)
-        sc = np.einsum("ngt,njt->ngj", q[..., c], k[..., c]) / np.sqrt(dh)
-        esc = (np.einsum("ngt,njt->ngj", eq[..., c], np.abs(k[..., c])) +
-               np.einsum("ngt,njt->ngj", np.abs(q[..., c]), ek[..., c]) +
-               (dh + 1) * u * np.einsum("ngt,njt->ngj", np.abs(q[..., c]), np.abs(k[..., c])))
-        esc = esc / np.sqrt(dh)
-        a = np.exp(sc - sc.max(axis=2, keepdims=True))
-        a = a / a.sum(axis=2, keepdims=True)
-        ea = 2.0 * esc.max(axis=2) + (L + 2) * u                        # [n][g], L1 over j
-        vmax = np.abs(v[..., c]).max(axis=1)                            # [n][t]
-        o[..., c] = np.einsum("ngj,njt->ngt", a, v[..., c])
-        eo[..., c] = (ea[..., None] * vmax[:, None, :] + np.einsum("ngj,njt->ngt", a, ev[..., c])
-                      + L * u * np.einsum("ngj,njt->ngt", a, np.abs(v[..., c])))
-    y, ey = lin(o, eo, "w_o", "b_o")
-    p = y.mean(axis=1)
-    ep = ey.mean(axis=1) + L * u * np.abs(y).mean(axis=1)
+def policy_tol(w, wts, obs):
+    return (attn_tol if w.get("policy_kind", 0) == 1 else end_to_end_bound)(w, wts, obs)
 
-    def head(k1, b1, k2, b2):
-        z, ez = lin(p, ep, k1, b1)
-        hz = 0.5 * z * (1.0 + np.vectorize(__import__("math").erf)(z / np.sqrt(2.0)))
-        eh = 1.13 * ez + 8 * u * np.abs(z)
-        return lin(hz, eh, k2, b2)[1]
 
-    cols = [head("wp1", "bp1", "wp2", "bp2")]
-    if w["value_head"]:
-        cols.append(head("wv1", "bv1", "wv2", "bv2"))
-    return 4.0 * np.concatenate(cols, axis=1)
+def check_mlp_layers(sim, wb, w, wts, obs_dev, obs_rows, step, rows, out=None):
+    """The diagnostic instantiation of the policy kernel on the same inputs: its outputs equal
+    the production kernel's bit for bit, and its hidden activations and outputs pass the
+    layer-by-layer check against fp64 arithmetic on its own layer inputs (rows `rows`)."""
+    hid = sim.policy_hidden(wb, obs_dev, step)
+    if out is not None:
+        for k in ("logits", "actions", "logp", "value"):
+            if out[k] is not None:
+                assert torch.equal(out[k], hid[k]), f"{k}: diagnostic and production kernels differ"
+    h1 = hid["h1"].cpu().numpy().T.astype(np.float64)[rows]
+    h2 = hid["h2"].cpu().numpy().T.astype(np.float64)[rows]
+    lg = hid["logits"].cpu().numpy().T.astype(np.float64)[rows]
+    return check_layers(w, wts, obs_rows, h1, h2, lg)
 
 
 def attn_weights(orc, w, seed):
@@ -481,30 +421,52 @@ def attn_weights(orc, w, seed):
 
 
 def check_policy(bs, orc, w, E, ids, step=17, seed=0x5EED):
-    """Policy on E seeded observations through the C ABI; the oracle evaluates rows `ids`.
-    MLP logits/value within the derived tolerance; sampled actions identical wherever the
-    oracle's uniform is farther than 2*max|dlogit| from a CDF boundary; logp close."""
+    """Policy on E seeded observations through the C ABI, random weights with nonzero biases;
+    the oracle evaluates rows `ids`.
+    * MLP: the hidden activations and outputs pass the layer-by-layer check (each layer
+      against fp64 arithmetic on the kernel's own inputs), and the logits lie within the
+      bound that check's windows give end to end; attention: the forward error bound.
+    * The sampler: the oracle's inverse CDF applied to the GPU's own logits with the same
+      uniform gives the GPU's action and log-probability wherever the uniform is farther
+      than 1e-5 from a CDF boundary (fp32 against fp64 sums).
+    * The decisions against the oracle's own logits agree outside the band 2 max|dlogit|
+      + 1e-5, dlogit being the logit differences already certified above (a perturbation e
+      of the logits moves each CDF value by at most about 2e)."""
     attn = w.get("policy_kind", 0) == 1
-    wts = attn_weights(orc, w, 99) if attn else orc.init_weights(w, 99)
+    wts = policy_weights(orc, w, 99)
     obs = seeded_obs(21, E, w["obs_dim"])
     sim = bs.Sim(w, n_envs=E)
     sim.reset(seed)
     wb = sim.upload_weights(wts)
-    out = sim.policy(wb, torch.from_numpy(np.ascontiguousarray(obs.T)).cuda(), step, want_logits=True)
+    obs_d = torch.from_numpy(np.ascontiguousarray(obs.T)).cuda()
+    out = sim.policy(wb, obs_d, step, want_logits=True)
     torch.cuda.synchronize()
     lg = out["logits"].cpu().numpy().T.astype(np.float64)[ids]
     act = out["actions"].cpu().numpy()[ids]
     logp = out["logp"].cpu().numpy().astype(np.float64)[ids]
     ref = orc.policy(w, wts, seed, step, obs[ids], ids)
-    tol = (attn_tol if attn else mlp_tol)(w, wts, obs[ids])
+    if not attn:
+        amb = check_mlp_layers(sim, wb, w, wts, obs_d, obs[ids], step, ids, out)
+        say(f"  hidden units with two admissible values: {amb}")
+    tol = policy_tol(w, wts, obs[ids])
     err = np.abs(lg - ref["logits"])
     assert np.all(err <= tol), f"max err/tol {np.max(err / tol):.3g}"
+    if attn:
+        check_attn_logits(err, tol)
     A = 6 * w["n_servers"]
+    near = 0
+    for i, e in enumerate(ids):
+        a_ref, lp_ref, mg = orc.sample_logits(lg[i, :A], orc.action_u(seed, int(e), step))
+        if mg > 1e-5:
+            assert act[i] == a_ref, f"env {e}: sampler"
+            assert abs(logp[i] - lp_ref) <= 1e-5 * (1.0 + abs(lp_ref)), f"env {e}: logp"
+        else:
+            near += 1
     eps = 2 * err[:, :A].max(axis=1) + 1e-5
     sure = ref["margin"] > eps
     assert np.array_equal(act[sure], ref["actions"][sure]), "actions differ away from ties"
-    say(f"  near-ties {np.sum(~sure)} of {len(ids)}; max logit err {err.max():.3g}")
-    assert np.all(np.abs(logp[sure] - ref["logp"][sure]) <= eps[sure] + 1e-5)
+    say(f"  sampler near-ties {near}, decision band excludes {np.sum(~sure)} of {len(ids)}; "
+        f"max logit err {err.max():.3g} (max err/bound {np.max(err / tol):.3g})")
     if w["value_head"]:
         v = out["value"].cpu().numpy()[ids]
         assert np.array_equal(v, lg[:, A].astype(np.float32))
@@ -582,15 +544,20 @@ def test_rollout_parity_and_validity(bs, orc, name):
     """sim_rollout (policy + sampler + simulator, T ticks) checked three ways:
     (1) the oracle's own policy rollout with the same weights agrees exactly, per env, on
         every tick before the first decision whose uniform lies within the tie band of a
-        CDF boundary (the band is 2*max|dlogit| + 1e-5, measured below);
+        CDF boundary (the band is 2*max|dlogit| + 1e-5 over logit differences certified in
+        (3));
     (2) validity of the simulator part: replaying the rollout's actions in the oracle gives
         the same running checksums, rewards and observations at every tick;
-    (3) validity of every decision: on the rollout's observations the oracle policy picks
-        the same action wherever its uniform is outside the tie band."""
+    (3) validity of every decision: on the rollout's observations the policy kernel gives the
+        rollout's own action, its logits pass the layer-by-layer check (MLP) or the forward
+        error bound (attention), and the oracle policy picks the same action wherever its
+        uniform is outside the tie band.
+    Random weights with nonzero biases."""
     w = workload(name)
     E, T, seed = 300, 100, 0xC0FFEE + 10 + (NAMES + ["attn", "attn_K4"]).index(name)
     A = 6 * w["n_servers"]
-    wts = orc.init_weights(w, 7)
+    attn = w.get("policy_kind", 0) == 1
+    wts = policy_weights(orc, w, 7)
     say(f"[rollout] {name}")
     sim = bs.Sim(w, n_envs=E)
     sim.reset(seed)
@@ -612,10 +579,19 @@ def test_rollout_parity_and_validity(bs, orc, name):
     ties = 0
     band_te = np.zeros((T, E))
     for t in range(T):
-        out = sim.policy(wb, tr.obs[t].contiguous(), t, want_logits=True)
+        ob_t = tr.obs[t].contiguous()
+        out = sim.policy(wb, ob_t, t, want_logits=True)
+        assert np.array_equal(out["actions"].cpu().numpy(), ga[t]), f"tick {t}: not the rollout's action"
         glg = out["logits"].cpu().numpy().T.astype(np.float64)
+        if not attn and t % 10 == 0:
+            check_mlp_layers(sim, wb, w, wts, ob_t, go[t], t, np.arange(E), out)
         ref = orc.policy(w, wts, seed, t, go[t], np.arange(E))
-        err = np.abs(glg - ref["logits"])[:, :A].max(axis=1)
+        full_err = np.abs(glg - ref["logits"])
+        tol_t = policy_tol(w, wts, go[t])
+        assert np.all(full_err <= tol_t), f"tick {t}: logits"
+        if attn:
+            check_attn_logits(full_err, tol_t)
+        err = full_err[:, :A].max(axis=1)
         lg_err = max(lg_err, float(err.max()))
         band_te[t] = 2 * err + 1e-5
         sure = ref["margin"] > band_te[t]
@@ -704,7 +680,7 @@ def test_rollout_full_size_sampled(bs, orc, name):
     say(f"[rollout-full] {name} E={E} T={T} sampled={len(cols)}")
     sim = bs.Sim(w)
     sim.reset(seed)
-    wb = sim.init_weights(seed + 1)
+    wb = sim.upload_weights(policy_weights(orc, w, seed + 1))
     tr = sim.rollout(wb, T, rchk=True)
     sim.sync()
     c = torch.from_numpy(cols).cuda()
@@ -743,9 +719,13 @@ def test_rollout_full_size_sampled(bs, orc, name):
         ob[:, :n] = torch.from_numpy(np.ascontiguousarray(rep["obs"][t].T)).cuda()
         out = small.policy(wsm, ob, t, want_logits=True)
         glg = out["logits"][:, :n].cpu().numpy().T.astype(np.float64)
+        if w.get("policy_kind", 0) == 0 and t % 25 == 0:
+            check_mlp_layers(small, wsm, w, wts, ob, rep["obs"][t], t, np.arange(n), out)
         ref = orc.policy(w, wts, seed, t, rep["obs"][t], cols)
-        tol = (attn_tol if w.get("policy_kind", 0) == 1 else mlp_tol)(w, wts, rep["obs"][t])
+        tol = policy_tol(w, wts, rep["obs"][t])
         assert np.all(np.abs(glg - ref["logits"]) <= tol), f"tick {t}: logits"
+        if w.get("policy_kind", 0) == 1:
+            check_attn_logits(np.abs(glg - ref["logits"]), tol)
         err = np.abs(glg - ref["logits"])[:, :A].max(axis=1)
         sure = ref["margin"] > 2 * err + 1e-5
         ties += int(np.sum(~sure))
