@@ -261,12 +261,15 @@ int returns_gae(sim_ctx* ctx, int32_t T, const double* d_r, const float* d_v, do
  * W1 [F][H1], b1 [H1], W2 [H1][H2], b2 [H2], W3 [H2][A'], b3 [A'] packed back to back
  * (A' = 6K + 1; sim_ppo_grad_count gives the total); d_loss [4] fp64 = total, policy,
  * value and entropy terms; d_index [M] int64 (t E + env) or NULL. Requires value_head = 1,
- * M > 0 and a multiple of 16. The dense products run in rocBLAS (bf16 x bf16 -> fp32 forward
- * for a bf16 policy, fp32 otherwise; fp32 backward) with its atomics disabled, so repeated
- * calls return identical results. Scratch of about 4 M (F + 3 H1 + 3 H2 + 2 A') bytes, plus
- * 2 M (F + H1 + H2) and fp32 copies of W2 and W3 for a bf16 policy, and the library handle
- * are held by the context after the first call. A stored action out of range latches SIM_ESTATE
- * (reported by sim_sync); that sample then contributes nothing.
+ * M > 0 and a multiple of 16, hidden widths that are multiples of 64, obs_dim <= 128 and
+ * A' <= 128 (SIM_EUNSUPPORTED otherwise). The dense products run on the matrix cores: bf16 x bf16 -> fp32
+ * for a bf16 policy (the fp32 gradient operand carried as two bf16 terms, 2^-17 relative),
+ * fp32 x fp32 otherwise; the reductions over the samples are summed in a fixed order, so
+ * repeated calls return identical results. Scratch of at most Mp (e (2 F + 4 H1 + 6 H2 + 4 A')
+ * + 4 (H1 + H2 + A')) bytes (Mp = M rounded up to 64, e = 2 bytes for bf16 or 4 for fp32,
+ * F and A' rounded up to 64) plus about 8 MiB of split-k partial sums is held by the context
+ * after the first call (grown if a later call needs more). A stored action out of range latches SIM_ESTATE (reported by sim_sync);
+ * that sample then contributes nothing.
  * For the attention policy (policy_kind = SIM_POLICY_ATTN) the forward is fp32 with exact
  * GELU and d_grads holds the fourteen arrays of sim_attn_layout in its order (w_in, b_in,
  * w_qkv, b_qkv, w_o, b_o, wp1, bp1, wp2, bp2, wv1, bv1, wv2, bv2), each [in][out] as in the

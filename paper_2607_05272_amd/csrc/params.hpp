@@ -135,18 +135,14 @@ hipError_t launch_pg_loss(const double* terms, int M, float c_v, float c_h, doub
 // off[14] are the byte offsets of w_in, b_in, ..., wv2, bv2; fin/fout the matrix shapes
 hipError_t launch_init_attn(uint64_t seed, void* d_weights, const size_t off[14], const int fin[7],
                             const int fout[7], hipStream_t st);
-// MLP policy-gradient minibatch (ppo_kernels.hip), value head required. The products run in
-// rocBLAS on the handle made by mb_blas_create (atomics disabled); scratch holds
-// ppo_scratch_bytes(m, M) bytes. A library failure returns hipErrorLaunchFailure and points
-// *why at a message naming the product.
+// MLP policy-gradient minibatch (ppo_kernels.hip), value head required: the library's own MFMA
+// products with fused epilogues; scratch holds ppo_scratch_bytes(m, M) bytes.
 hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t off[6], int T,
                       const float* obs, const uint8_t* act, const float* logp_old,
                       const double* adv, const double* ret, int M, uint64_t seed, float clip,
                       float c_v, float c_h, int reinforce, void* scratch, double* loss_out,
-                      float* grads, int64_t* idx_out, uint32_t* err, void* blas,
-                      const char** why, hipStream_t st);
-void* mb_blas_create(const char** why);   // nullptr on failure, *why says why
-void mb_blas_destroy(void* blas);
+                      float* grads, int64_t* idx_out, uint32_t* err, hipStream_t st);
+bool ppo_shape_supported(const MlpParams& m);
 size_t ppo_scratch_bytes(const MlpParams& m, int M);
 // Adam on fp32 parameters (train_kernels.hip): one step, bias corrections bc1 = 1 - b1^t and
 // bc2 = 1 - b2^t computed by the caller; then the policy's weights from the parameters

@@ -63,7 +63,6 @@ struct sim_ctx {
   size_t arena_bytes = 0;
   void* wpack = nullptr;   // repacked policy weights
   void* ppo_scratch = nullptr;  // minibatch activations, grown on demand
-  void* blas = nullptr;         // rocBLAS handle of the MLP minibatch, made on first use
   size_t ppo_bytes = 0;
   void* grads = nullptr;        // gradient + loss buffer of sim_update
   int64_t* d_tot_cnt = nullptr;
@@ -347,7 +346,6 @@ int sim_destroy(sim_ctx* x) {
   (void)hipFree(x->wpack);
   (void)hipFree(x->ppo_scratch);
   (void)hipFree(x->grads);
-  mb_blas_destroy(x->blas);
   delete x;
   return SIM_OK;
 }
@@ -692,11 +690,9 @@ static int pg_grad(sim_ctx* x, int reinforce, const void* d_weights, int32_t T, 
   if ((int64_t)M * (std::max(std::max(x->m.F, x->m.H1), std::max(x->m.H2, x->m.Ap)) + 1) >
       0x7FFFFFFFll)
     return fail(SIM_EINVAL, "M = %d times the widest layer must stay below 2^31", M);
-  if (!x->blas) {
-    const char* why = "rocBLAS handle set-up failed";
-    x->blas = mb_blas_create(&why);
-    if (!x->blas) return fail(SIM_EDEVICE, "%s", why);
-  }
+  if (!ppo_shape_supported(x->m))
+    return fail(SIM_EUNSUPPORTED, "%s: hidden widths must be multiples of 64, obs_dim <= 128 and A' <= 128",
+                who);
   const size_t need = ppo_scratch_bytes(x->m, M);
   if (need > x->ppo_bytes) {
     (void)hipStreamSynchronize(x->stream);
@@ -711,14 +707,11 @@ static int pg_grad(sim_ctx* x, int reinforce, const void* d_weights, int32_t T, 
   }
   size_t off[6];
   offsets(x->cfg, off);
-  const char* why = nullptr;
-  hipError_t e = x->timed(SIM_KC_PPO, [&] {
-    return launch_ppo(x->m, d_weights, off, T, d_obs, d_actions, d_logp_old, d_adv, d_ret, M, seed,
-                      clip, c_value, c_entropy, reinforce, x->ppo_scratch, d_loss, d_grads,
-                      d_index, x->s.err, x->blas, &why, x->stream);
-  });
-  if (e != hipSuccess && why) return fail(SIM_EDEVICE, "%s", why);
-  HIPCHK(e, "minibatch gradient kernel launch");
+  HIPCHK(x->timed(SIM_KC_PPO, [&] {
+           return launch_ppo(x->m, d_weights, off, T, d_obs, d_actions, d_logp_old, d_adv, d_ret,
+                             M, seed, clip, c_value, c_entropy, reinforce, x->ppo_scratch, d_loss,
+                             d_grads, d_index, x->s.err, x->stream);
+         }), "minibatch gradient kernel launch");
   return SIM_OK;
 }
 
