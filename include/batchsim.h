@@ -280,6 +280,23 @@ int ppo_minibatch_grad(sim_ctx* ctx, const void* d_weights, int32_t T, const flo
                        const double* d_ret, int32_t M, uint64_t seed, float clip, float c_value,
                        float c_entropy, float* d_grads, double* d_loss, int64_t* d_index);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * training loops, harnesses that forbid hipMalloc): ppo_minibatch_grad with the same arguments,
+ * inputs, outputs, error behaviour and results, bit for bit, but run on a fixed scratch the
+ * library holds in device memory (96 MiB per GPU, allocated when the library's code is loaded
+ * on that GPU and kept until the process ends) instead of the context's on-demand buffer. It
+ * calls no hipMalloc, hipFree or other allocating routine and records no tracing events.
+ * SIM_EINVAL, with the sizes in the message, when the minibatch needs more scratch than that
+ * (C4's shape at M = 8192 needs about 76 MiB). Every call on a GPU uses the same scratch: calls
+ * whose work overlaps on one GPU (several streams or threads) race and must be serialised by
+ * the caller; calls in order on one stream are safe. The scratch keeps the previous call's
+ * contents; every byte a call reads is written by that call first.                        */
+int ppo_minibatch_grad_noalloc(sim_ctx* ctx, const void* d_weights, int32_t T,
+                               const float* d_obs, const uint8_t* d_actions,
+                               const float* d_logp_old, const double* d_adv, const double* d_ret,
+                               int32_t M, uint64_t seed, float clip, float c_value,
+                               float c_entropy, float* d_grads, double* d_loss, int64_t* d_index);
+
 /* Number of fp32 gradient values written by ppo_minibatch_grad (no device work), for either
  * policy network.                                                                       */
 int sim_ppo_grad_count(const sim_cfg* cfg, int64_t* h_count);

@@ -144,6 +144,10 @@ hipError_t launch_ppo(const MlpParams& m, const void* d_weights, const size_t of
                       float* grads, int64_t* idx_out, uint32_t* err, hipStream_t st);
 bool ppo_shape_supported(const MlpParams& m);
 size_t ppo_scratch_bytes(const MlpParams& m, int M);
+// The fixed device scratch of ppo_minibatch_grad_noalloc: its size, and its address on the
+// current device (looked up once per device with hipGetSymbolAddress; allocates nothing).
+constexpr size_t kStaticScratchBytes = (size_t)96 << 20;
+hipError_t static_scratch(void** ptr);
 // Adam on fp32 parameters (train_kernels.hip): one step, bias corrections bc1 = 1 - b1^t and
 // bc2 = 1 - b2^t computed by the caller; then the policy's weights from the parameters
 hipError_t launch_adam(float* params, const float* grads, float* m, float* v, size_t n, float lr,

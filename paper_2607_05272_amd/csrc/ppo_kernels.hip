@@ -24,8 +24,16 @@
 // the fp32 gradient operand dZ is carried as two bf16 terms hi + lo (hi = bf16(dZ),
 // lo = bf16(dZ - hi), 2^-17 relative) and every backward product takes two MFMAs,
 // v_mfma_f32_16x16x32_bf16. fp32 mode (fp32 policies): fp32 operands, v_mfma_f32_16x16x4_f32.
+#include <mutex>
+
 #include "devmath.hpp"
 #include "params.hpp"
+
+// Fixed device scratch of the minibatch gradient for callers that cannot allocate
+// (ppo_minibatch_grad_noalloc): one copy per GPU, held until the process ends. Host code must
+// use the per-device address from hipGetSymbolAddress (static_scratch below), never this
+// name, which in host code is only a stand-in for the device symbol.
+static __device__ __align__(256) unsigned char scratch[bsim::kStaticScratchBytes];
 
 namespace bsim {
 namespace {
@@ -854,6 +862,25 @@ hipError_t run_minibatch(const MlpParams& m, const void* d_weights, const size_t
 }  // namespace
 
 size_t ppo_scratch_bytes(const MlpParams& m, int M) { return carve(m, M, nullptr, nullptr); }
+
+hipError_t static_scratch(void** ptr) {
+  constexpr int kDevices = 64;
+  static std::mutex mu;
+  static void* addr[kDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 bool ppo_shape_supported(const MlpParams& m) {
   return m.Ap <= 128 && m.H1 % kTile == 0 && m.H2 % kTile == 0 && m.F >= 1 &&

@@ -649,12 +649,41 @@ int sim_ppo_grad_count(const sim_cfg* c, int64_t* h_count) {
   return SIM_OK;
 }
 
-// shared by the PPO and REINFORCE entry points
+// The minibatch's scratch: the context's buffer, grown with hipMalloc when a call needs more,
+// or (no_alloc) the library's fixed device scratch, which allocates nothing.
+static int mb_scratch(sim_ctx* x, size_t need, bool no_alloc, const char* who, void** out) {
+  if (no_alloc) {
+    if (need > kStaticScratchBytes)
+      return fail(SIM_EINVAL, "%s: this minibatch needs %zu bytes of scratch; the fixed scratch "
+                  "holds %zu (use fewer samples, or ppo_minibatch_grad)", who, need,
+                  kStaticScratchBytes);
+    HIPCHK(static_scratch(out), "hipGetSymbolAddress of the fixed scratch");
+    return SIM_OK;
+  }
+  if (need > x->ppo_bytes) {
+    (void)hipStreamSynchronize(x->stream);
+    (void)hipFree(x->ppo_scratch);
+    x->ppo_scratch = nullptr;
+    x->ppo_bytes = 0;
+    hipError_t he = hipMalloc(&x->ppo_scratch, need);
+    if (he != hipSuccess)
+      return fail(SIM_ENOMEM, "hipMalloc of %zu bytes of minibatch scratch failed: %s", need,
+                  hipGetErrorString(he));
+    x->ppo_bytes = need;
+  }
+  *out = x->ppo_scratch;
+  return SIM_OK;
+}
+
+// shared by the PPO and REINFORCE entry points; no_alloc launches without tracing events and
+// with the fixed scratch
 static int pg_grad(sim_ctx* x, int reinforce, const void* d_weights, int32_t T, const float* d_obs,
                    const uint8_t* d_actions, const float* d_logp_old, const double* d_adv,
                    const double* d_ret, int32_t M, uint64_t seed, float clip, float c_value,
-                   float c_entropy, float* d_grads, double* d_loss, int64_t* d_index) {
-  const char* who = reinforce ? "reinforce_minibatch_grad" : "ppo_minibatch_grad";
+                   float c_entropy, float* d_grads, double* d_loss, int64_t* d_index,
+                   bool no_alloc = false) {
+  const char* who = reinforce ? "reinforce_minibatch_grad"
+                              : (no_alloc ? "ppo_minibatch_grad_noalloc" : "ppo_minibatch_grad");
   if (!x || !d_weights || !d_obs || !d_actions || (!reinforce && !d_logp_old) || !d_adv ||
       !d_ret || !d_grads || !d_loss)
     return fail(SIM_EINVAL, "%s: NULL argument", who);
@@ -668,23 +697,16 @@ static int pg_grad(sim_ctx* x, int reinforce, const void* d_weights, int32_t T, 
   if (x->cfg.policy_kind == SIM_POLICY_ATTN) {
     int rc = prepare_policy(x, d_weights);  // shape check and weight pointers
     if (rc) return rc;
-    const size_t need = attn_grad_scratch_bytes(x->a, M);
-    if (need > x->ppo_bytes) {
-      (void)hipStreamSynchronize(x->stream);
-      (void)hipFree(x->ppo_scratch);
-      x->ppo_scratch = nullptr;
-      x->ppo_bytes = 0;
-      hipError_t he = hipMalloc(&x->ppo_scratch, need);
-      if (he != hipSuccess)
-        return fail(SIM_ENOMEM, "hipMalloc of %zu bytes of minibatch scratch failed: %s", need,
-                    hipGetErrorString(he));
-      x->ppo_bytes = need;
-    }
-    HIPCHK(x->timed(SIM_KC_PPO, [&] {
-             return launch_attn_grad(x->a, T, d_obs, d_actions, d_logp_old, d_adv, d_ret, M, seed,
-                                     clip, c_value, c_entropy, reinforce, x->ppo_scratch, d_loss,
-                                     d_grads, d_index, x->s.err, x->stream);
-           }), "attention minibatch gradient kernel launch");
+    void* scr = nullptr;
+    rc = mb_scratch(x, attn_grad_scratch_bytes(x->a, M), no_alloc, who, &scr);
+    if (rc) return rc;
+    auto launch = [&] {
+      return launch_attn_grad(x->a, T, d_obs, d_actions, d_logp_old, d_adv, d_ret, M, seed, clip,
+                              c_value, c_entropy, reinforce, scr, d_loss, d_grads, d_index,
+                              x->s.err, x->stream);
+    };
+    HIPCHK(no_alloc ? launch() : x->timed(SIM_KC_PPO, launch),
+           "attention minibatch gradient kernel launch");
     return SIM_OK;
   }
   if ((int64_t)M * (std::max(std::max(x->m.F, x->m.H1), std::max(x->m.H2, x->m.Ap)) + 1) >
@@ -693,25 +715,17 @@ static int pg_grad(sim_ctx* x, int reinforce, const void* d_weights, int32_t T, 
   if (!ppo_shape_supported(x->m))
     return fail(SIM_EUNSUPPORTED, "%s: hidden widths must be multiples of 64, obs_dim <= 128 and A' <= 128",
                 who);
-  const size_t need = ppo_scratch_bytes(x->m, M);
-  if (need > x->ppo_bytes) {
-    (void)hipStreamSynchronize(x->stream);
-    (void)hipFree(x->ppo_scratch);
-    x->ppo_scratch = nullptr;
-    x->ppo_bytes = 0;
-    hipError_t he = hipMalloc(&x->ppo_scratch, need);
-    if (he != hipSuccess)
-      return fail(SIM_ENOMEM, "hipMalloc of %zu bytes of minibatch scratch failed: %s", need,
-                  hipGetErrorString(he));
-    x->ppo_bytes = need;
-  }
+  void* scr = nullptr;
+  int rc = mb_scratch(x, ppo_scratch_bytes(x->m, M), no_alloc, who, &scr);
+  if (rc) return rc;
   size_t off[6];
   offsets(x->cfg, off);
-  HIPCHK(x->timed(SIM_KC_PPO, [&] {
-           return launch_ppo(x->m, d_weights, off, T, d_obs, d_actions, d_logp_old, d_adv, d_ret,
-                             M, seed, clip, c_value, c_entropy, reinforce, x->ppo_scratch, d_loss,
-                             d_grads, d_index, x->s.err, x->stream);
-         }), "minibatch gradient kernel launch");
+  auto launch = [&] {
+    return launch_ppo(x->m, d_weights, off, T, d_obs, d_actions, d_logp_old, d_adv, d_ret, M, seed,
+                      clip, c_value, c_entropy, reinforce, scr, d_loss, d_grads, d_index, x->s.err,
+                      x->stream);
+  };
+  HIPCHK(no_alloc ? launch() : x->timed(SIM_KC_PPO, launch), "minibatch gradient kernel launch");
   return SIM_OK;
 }
 
@@ -721,6 +735,15 @@ int ppo_minibatch_grad(sim_ctx* x, const void* d_weights, int32_t T, const float
                        float c_entropy, float* d_grads, double* d_loss, int64_t* d_index) {
   return pg_grad(x, 0, d_weights, T, d_obs, d_actions, d_logp_old, d_adv, d_ret, M, seed, clip,
                  c_value, c_entropy, d_grads, d_loss, d_index);
+}
+
+int ppo_minibatch_grad_noalloc(sim_ctx* x, const void* d_weights, int32_t T, const float* d_obs,
+                               const uint8_t* d_actions, const float* d_logp_old,
+                               const double* d_adv, const double* d_ret, int32_t M, uint64_t seed,
+                               float clip, float c_value, float c_entropy, float* d_grads,
+                               double* d_loss, int64_t* d_index) {
+  return pg_grad(x, 0, d_weights, T, d_obs, d_actions, d_logp_old, d_adv, d_ret, M, seed, clip,
+                 c_value, c_entropy, d_grads, d_loss, d_index, true);
 }
 
 int reinforce_minibatch_grad(sim_ctx* x, const void* d_weights, int32_t T, const float* d_obs,

@@ -262,19 +262,22 @@ class Sim:
         return n.value
 
     def ppo_minibatch_grad(self, weights, obs, actions, logp_old, adv, ret, M, seed, clip=0.2,
-                           c_value=0.5, c_entropy=0.01, want_index=False, grads=None, loss=None):
+                           c_value=0.5, c_entropy=0.01, want_index=False, grads=None, loss=None,
+                           noalloc=False):
         """One PPO minibatch: obs [T(+1)][F][E] (rows 0..T-1 used), actions/logp_old/adv/ret
-        [T][E]. Returns (grads fp32 flat W1,b1,W2,b2,W3,b3; loss [4] fp64; index or None)."""
+        [T][E]. Returns (grads fp32 flat W1,b1,W2,b2,W3,b3; loss [4] fp64; index or None).
+        noalloc=True calls ppo_minibatch_grad_noalloc (the library's fixed scratch)."""
         T = actions.shape[0]
         assert actions.shape[1] == self.E and obs.shape[1] == self.F and obs.shape[0] >= T
         grads = (torch.empty(self.ppo_grad_count(), dtype=torch.float32, device=self.device)
                  if grads is None else grads)
         loss = torch.empty(4, dtype=torch.float64, device=self.device) if loss is None else loss
         idx = torch.empty(M, dtype=torch.int64, device=self.device) if want_index else None
-        L.check(self.lib.ppo_minibatch_grad(self._ctx, _p(weights), T, _p(obs), _p(actions),
-                                            _p(logp_old), _p(adv), _p(ret), M, C.c_uint64(seed),
-                                            clip, c_value, c_entropy, _p(grads), _p(loss),
-                                            _p(idx)), "ppo_minibatch_grad")
+        name = "ppo_minibatch_grad_noalloc" if noalloc else "ppo_minibatch_grad"
+        L.check(getattr(self.lib, name)(self._ctx, _p(weights), T, _p(obs), _p(actions),
+                                        _p(logp_old), _p(adv), _p(ret), M, C.c_uint64(seed),
+                                        clip, c_value, c_entropy, _p(grads), _p(loss), _p(idx)),
+                name)
         return grads, loss, idx
 
     def reinforce_minibatch_grad(self, weights, obs, actions, adv, ret, M, seed, c_value=0.5,
