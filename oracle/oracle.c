@@ -239,6 +239,11 @@ typedef struct sys_t {
   int rr;                        /* round-robin pointer of the static system (R23) */
   double busy[ORC_MAX_K];
   int inflight[ORC_MAX_K], last_b[ORC_MAX_K], last_cls[ORC_MAX_K];
+  /* Shortest-Queue routing (R27): each server's FIFO of assigned batches, at most two (the one
+   * it runs and one queued behind it), completion times and sizes in order */
+  int sq_cnt[ORC_MAX_K];
+  double sq_c[ORC_MAX_K][2];
+  int sq_n[ORC_MAX_K][2];
   double ewma[4];
   /* counters */
   int64_t arrivals, accepted, dropped, dispatched, batches, completed;
@@ -312,14 +317,29 @@ static double service(tick_ctx* t, sys_t* S, int h, int n) {
   return c->svc_median[h] * det_exp(c->svc_sigma * z) + c->svc_beta[h] * (double)n;
 }
 
+static void take_batch(tick_ctx* t, sys_t* S, int j, int h, int n, double now, double start,
+                       double cdone);
+
 /* Dispatch n requests of class h to server j at time now (Sec. 3.1 execution model). The
  * batch's latency L_r = c - a_r of each request is known at dispatch (R8). */
 static void batch(tick_ctx* t, sys_t* S, int j, int h, int n, double now) {
-  const orc_cfg* c = t->c;
-  int N = c->queue_cap;
   if (S->inflight[j] > 0) S->completed += S->inflight[j];  /* finished at busy[j] <= now */
   double sv = service(t, S, h, n);
   double cdone = now + sv;
+  take_batch(t, S, j, h, n, now, now, cdone);
+  S->busy[j] = cdone;
+  S->last_b[j] = n;
+  S->last_cls[j] = h;
+  S->inflight[j] = n;
+}
+
+/* The n oldest requests of class h leave the queue at `now` as one batch on server j that
+ * starts at `start` and completes at cdone: their latencies c - a_r (Sec. 4.1 reward), waits
+ * start - a_r, the counters, the dispatch record. */
+static void take_batch(tick_ctx* t, sys_t* S, int j, int h, int n, double now, double start,
+                       double cdone) {
+  const orc_cfg* c = t->c;
+  int N = c->queue_cap;
   for (int i = 0; i < n; i++) {
     double a = S->ring[h][S->head[h]];
     S->head[h] = S->head[h] + 1 == N ? 0 : S->head[h] + 1;
@@ -328,16 +348,12 @@ static void batch(tick_ctx* t, sys_t* S, int j, int h, int n, double now) {
     t->Lw = t->Lw + wl;
     S->lat_sum = S->lat_sum + lat;
     S->wlat_sum = S->wlat_sum + wl;
-    S->wait_sum = S->wait_sum + (now - a);
+    S->wait_sum = S->wait_sum + (start - a);
     S->soj_sum = S->soj_sum + ((cdone < S->horizon ? cdone : S->horizon) - a);
   }
   S->q[h] -= n;
   S->dispatched += n;
   S->batches += 1;
-  S->busy[j] = cdone;
-  S->last_b[j] = n;
-  S->last_cls[j] = h;
-  S->inflight[j] = n;
   S->chk = mix(S->chk, ((uint64_t)(t->k + 1) << 32) | ((uint64_t)j << 16) | ((uint64_t)h << 8) |
                            (uint64_t)n);
   t->n_k += n;
@@ -414,8 +430,62 @@ static void dispatch_static(tick_ctx* t, sys_t* S, double now) {
   }
 }
 
+/* Shortest-Queue routing of the static rule's batches (Sec. 5.1 baselines, R27). Each server
+ * holds the batch it runs and at most one more queued behind it, served in order. A batch
+ * whose completion time has come (c <= now) has left the server; its requests count as
+ * completed. */
+static void sq_retire(sys_t* S, int K, double now) {
+  for (int j = 0; j < K; j++) {
+    while (S->sq_cnt[j] > 0 && S->sq_c[j][0] <= now) {
+      S->completed += S->sq_n[j][0];
+      S->sq_c[j][0] = S->sq_c[j][1];
+      S->sq_n[j][0] = S->sq_n[j][1];
+      S->sq_cnt[j]--;
+    }
+    S->busy[j] = S->sq_cnt[j] > 0 ? S->sq_c[j][0] : S->busy[j];
+  }
+}
+
+static int sq_any_slot(const sys_t* S, int K) {
+  for (int j = 0; j < K; j++)
+    if (S->sq_cnt[j] < 2) return 1;
+  return 0;
+}
+
+/* While requests wait and the static rule's condition holds (Q_h >= B, or the head of the
+ * head-of-line class has waited T), the batch min(B, Q_h) goes to the server with the fewest
+ * requests assigned and not completed among those with a free slot (ties to the lower index);
+ * it starts when that server has finished what it holds. No free slot: the batch waits. */
+static void dispatch_sq(tick_ctx* t, sys_t* S, double now) {
+  const orc_cfg* c = t->c;
+  sq_retire(S, c->n_servers, now);
+  for (;;) {
+    if (sumq(S, c->n_classes) == 0) return;
+    int h = hol(S, c->n_classes);
+    double head_ts = S->ring[h][S->head[h]];
+    if (!(S->q[h] >= c->static_bmax || now >= head_ts + c->static_timeout)) return;
+    int j = -1, best = 0;
+    for (int i = 0; i < c->n_servers; i++) {
+      if (S->sq_cnt[i] >= 2) continue;
+      int load = 0;
+      for (int b = 0; b < S->sq_cnt[i]; b++) load += S->sq_n[i][b];
+      if (j < 0 || load < best) { j = i; best = load; }
+    }
+    if (j < 0) return;
+    int n = S->q[h] < c->static_bmax ? S->q[h] : c->static_bmax;
+    double start = S->sq_cnt[j] > 0 ? S->sq_c[j][S->sq_cnt[j] - 1] : now;
+    double cdone = start + service(t, S, h, n);
+    take_batch(t, S, j, h, n, now, start, cdone);
+    S->sq_c[j][S->sq_cnt[j]] = cdone;
+    S->sq_n[j][S->sq_cnt[j]] = n;
+    S->sq_cnt[j]++;
+    S->busy[j] = S->sq_c[j][0];
+  }
+}
+
 static void do_dispatch(tick_ctx* t, sys_t* S, int action, double now) {
   if (S->sys == 0) dispatch_learned(t, S, action, now);
+  else if (t->c->static_route == ORC_ROUTE_SHORTEST) dispatch_sq(t, S, now);
   else dispatch_static(t, S, now);
 }
 
@@ -424,8 +494,13 @@ static void integrate(tick_ctx* t, sys_t* S, double te) {
   const orc_cfg* c = t->c;
   int nq = sumq(S, c->n_classes);
   int ns = 0;
-  for (int j = 0; j < c->n_servers; j++)
-    if (S->busy[j] > S->t_area) ns += S->last_b[j];
+  if (S->sys == 1 && c->static_route == ORC_ROUTE_SHORTEST) {
+    for (int j = 0; j < c->n_servers; j++)
+      for (int b = 0; b < S->sq_cnt[j]; b++) ns += S->sq_n[j][b];
+  } else {
+    for (int j = 0; j < c->n_servers; j++)
+      if (S->busy[j] > S->t_area) ns += S->last_b[j];
+  }
   double dt = te - S->t_area;
   S->area_n = S->area_n + (double)(nq + ns) * dt;
   S->area_q = S->area_q + (double)nq * dt;
@@ -498,7 +573,9 @@ static double tick(tick_ctx* t, sys_t* S, int action) {
     if (S->next_arr < te) te = S->next_arr;
     for (int j = 0; j < c->n_servers; j++)
       if (S->busy[j] > now && S->busy[j] < te) te = S->busy[j];
-    if (S->sys == 1 && sumq(S, c->n_classes) > 0 && any_idle(S, c->n_servers, now)) {
+    const int sq = S->sys == 1 && c->static_route == ORC_ROUTE_SHORTEST;
+    if (S->sys == 1 && sumq(S, c->n_classes) > 0 &&
+        (sq ? sq_any_slot(S, c->n_servers) : any_idle(S, c->n_servers, now))) {
       int h = hol(S, c->n_classes);
       double tout = S->ring[h][S->head[h]] + c->static_timeout;
       if (tout > now && tout < te) te = tout;
@@ -512,6 +589,17 @@ static double tick(tick_ctx* t, sys_t* S, int action) {
   }
   integrate(t, S, t1);
   /* completions of the tick: every batch finishing before t_{k+1} (R9) */
+  if (S->sys == 1 && c->static_route == ORC_ROUTE_SHORTEST) {
+    for (int j = 0; j < c->n_servers; j++) {
+      while (S->sq_cnt[j] > 0 && S->sq_c[j][0] < t1) {
+        S->completed += S->sq_n[j][0];
+        S->sq_c[j][0] = S->sq_c[j][1];
+        S->sq_n[j][0] = S->sq_n[j][1];
+        S->sq_cnt[j]--;
+      }
+      S->busy[j] = S->sq_cnt[j] > 0 ? S->sq_c[j][0] : S->busy[j];
+    }
+  }
   for (int j = 0; j < c->n_servers; j++) {
     if (S->inflight[j] > 0 && S->busy[j] < t1) {
       S->completed += S->inflight[j];
@@ -994,7 +1082,10 @@ int orc_rollout(const orc_cfg* c, uint64_t seed, int32_t T, int32_t n, const uin
       if (out && out->counters) {
         int64_t* ct = out->counters + ((int64_t)i * 2 + s) * ORC_NCNT;
         int64_t infl = 0;
-        for (int j = 0; j < c->n_servers; j++) infl += S[s].inflight[j];
+        for (int j = 0; j < c->n_servers; j++) {
+          infl += S[s].inflight[j];
+          for (int b = 0; b < S[s].sq_cnt[j]; b++) infl += S[s].sq_n[j][b];
+        }
         ct[0] = S[s].arrivals; ct[1] = S[s].accepted; ct[2] = S[s].dropped;
         ct[3] = S[s].dispatched; ct[4] = S[s].batches; ct[5] = S[s].completed; ct[6] = infl;
       }

@@ -39,7 +39,7 @@
 
 enum { ORC_ARR_MODULATED = 0, ORC_ARR_TRACE = 1 };
 enum { ORC_DWELL_INF = 0, ORC_DWELL_EXP = 1, ORC_DWELL_PARETO = 2, ORC_DWELL_DET = 3 };
-enum { ORC_ROUTE_LOWEST = 0, ORC_ROUTE_RANDOM = 1, ORC_ROUTE_ROUND_ROBIN = 2 };
+enum { ORC_ROUTE_LOWEST = 0, ORC_ROUTE_RANDOM = 1, ORC_ROUTE_ROUND_ROBIN = 2, ORC_ROUTE_SHORTEST = 3 };
 enum { ORC_SVC_DET = 0, ORC_SVC_LOGN = 1, ORC_SVC_EXP = 2 };
 enum { ORC_POLICY_MLP = 0, ORC_POLICY_ATTN = 1 };
 #define ORC_ATTN_MAX_L 16   /* tokens */
@@ -66,7 +66,7 @@ typedef struct orc_cfg {
   double static_timeout;
   int32_t static_bmax;
   int32_t mlp_h1, mlp_h2, mlp_bf16, value_head;
-  int32_t static_route;          /* ORC_ROUTE_*: server choice of the static system (R23) */
+  int32_t static_route;          /* ORC_ROUTE_*: server choice of the static system (R23, R27) */
   /* policy network (R16, R26): the MLP, or the attention policy of Sec. 4.2 with
    * attn_tokens tokens of width attn_embed and attn_heads heads; its policy head has
    * mlp_h1 hidden units and its value head mlp_h2 */

@@ -21,6 +21,7 @@ DWELL_DET = 3       # fixed dwell (square wave), R24
 ROUTE_LOWEST = 0
 ROUTE_RANDOM = 1
 ROUTE_ROUND_ROBIN = 2
+ROUTE_SHORTEST = 3  # Shortest-Queue over per-server FIFOs of at most two batches, R27
 # policy network (R16, R26)
 POLICY_MLP = 0
 POLICY_ATTN = 1
@@ -130,10 +131,12 @@ def burst_preset(**kw):
 def baseline_preset(rule, base="C3", **kw):
     """A workload whose shadow system runs one of the paper's baselines (Sec. 5.1):
     'static8' (fixed batch 8 with the timeout of R18), 'random' or 'round_robin' routing of
-    the static rule's batches (R23)."""
+    the static rule's batches to idle servers (R23), or 'shortest' (Shortest-Queue: each batch
+    to the server with the fewest requests assigned and not completed, R27)."""
     extra = dict(static8=dict(static_bmax=8),
                  random=dict(static_route=ROUTE_RANDOM),
-                 round_robin=dict(static_route=ROUTE_ROUND_ROBIN))[rule]
+                 round_robin=dict(static_route=ROUTE_ROUND_ROBIN),
+                 shortest=dict(static_route=ROUTE_SHORTEST))[rule]
     d = preset(base, shadow=1, **extra)
     d.update(kw)
     return d
