@@ -39,6 +39,7 @@ DESCR = {
     "C3-random": "C3 with a static shadow routing each batch to a uniformly random idle server",
     "C3-round_robin": "C3 with a static shadow routing batches round-robin over the idle servers",
     "C5-random": "C5 with the static shadow routing each batch to a uniformly random idle server",
+    "C3-shortest": "C3 with a Shortest-Queue shadow: each static-rule batch to the server with the fewest requests assigned (one batch running and at most one queued per server)",
     "attn": "attention policy (Sec. 4.2): 262144 envs x 1000 ticks, C1's system (1 server, Poisson 500/s, DET 5ms+0.5ms*b), 8 features as 8 tokens, 8->4 projection, 2-head self-attention, mean pool, GELU heads of 64 (policy) and 64 (value), fp32, REINFORCE with baseline returns",
 }
 

@@ -48,7 +48,8 @@ enum sim_status {
 
 enum { SIM_ARR_MODULATED = 0, SIM_ARR_TRACE = 1 };
 enum { SIM_DWELL_INF = 0, SIM_DWELL_EXP = 1, SIM_DWELL_PARETO = 2, SIM_DWELL_DET = 3 };
-enum { SIM_ROUTE_LOWEST = 0, SIM_ROUTE_RANDOM = 1, SIM_ROUTE_ROUND_ROBIN = 2 };
+enum { SIM_ROUTE_LOWEST = 0, SIM_ROUTE_RANDOM = 1, SIM_ROUTE_ROUND_ROBIN = 2,
+       SIM_ROUTE_SHORTEST = 3 };
 /* policy network (Sec. 4.2) */
 enum { SIM_POLICY_MLP = 0, SIM_POLICY_ATTN = 1 };
 enum { SIM_SVC_DET = 0, SIM_SVC_LOGN = 1, SIM_SVC_EXP = 2 };
@@ -89,7 +90,14 @@ enum { SIM_SVC_DET = 0, SIM_SVC_LOGN = 1, SIM_SVC_EXP = 2 };
  *  static_route    server that takes a batch of the static rule: SIM_ROUTE_LOWEST idle
  *                  index, SIM_ROUTE_RANDOM (uniform over the idle servers) or
  *                  SIM_ROUTE_ROUND_ROBIN (first idle server from a per-environment
- *                  pointer); the Random and Round-Robin baselines of Sec. 5.1
+ *                  pointer); the Random and Round-Robin baselines of Sec. 5.1. Or
+ *                  SIM_ROUTE_SHORTEST, the Shortest-Queue baseline of Sec. 5.1: every
+ *                  server holds the batch it runs and at most one queued behind it; the
+ *                  rule forms a batch whenever its condition holds, whether or not a
+ *                  server is idle, and sends it to the server with the fewest requests
+ *                  assigned and not completed among those with room (lower index on
+ *                  ties), where it starts when that server is free; with no room it waits.
+ *                  At most 8 servers (SIM_EUNSUPPORTED otherwise)
  *  policy_kind     SIM_POLICY_MLP (the MLP above) or SIM_POLICY_ATTN, the attention
  *                  policy of Sec. 4.2: the obs_dim features split into attn_tokens
  *                  contiguous groups, each group's terms of the input projection summed

@@ -16,7 +16,8 @@ enum : uint32_t { ERR_ACTION = 1u, ERR_EVENTS = 2u, ERR_TRACE = 4u };
 struct SimParams {
   int E, K, C, N, F, S;
   int arrival_kind, shadow, bmax, reward_sum;
-  int route;                             // server choice of the static rule (SIM_ROUTE_*)
+  int route;                             // server choice of the static rule (SIM_ROUTE_*;
+                                         // 3 = Shortest-Queue)
   double dt;
   double rate[kMaxS], mean_gap[kMaxS], dwell_mean[kMaxS], inv_alpha[kMaxS], xm[kMaxS];
   int dwell_kind[kMaxS];
@@ -39,8 +40,10 @@ struct SysState {
   uint32_t* qpack;   // [E]     Q_c in byte c
   uint32_t* hpack;   // [E]     ring head of class c in byte c
   double* hts;       // [C][E]  arrival time of the head request of class c
-  double* busy;      // [K][E]  busy-until time of server j
-  uint32_t* meta;    // [K][E]  inflight | last_b << 8 | last_class << 16 (0xFF = none)
+  double* busy;      // [K][E]  busy-until time of server j (Shortest-Queue: its running batch)
+  double* busy2;     // [K][E]  Shortest-Queue only: completion of the batch queued on server j
+  uint32_t* meta;    // [K][E]  inflight | last_b << 8 | last_class << 16 (0xFF = none);
+                     //         Shortest-Queue: running size | queued size << 24
   uint32_t* cnt;     // [6][E]  arrivals, accepted, dropped, dispatched, batches, completed
   double* sums;      // [2][E]  latency sum, weighted latency sum
   uint64_t* chk;     // [E]     checksum of the integer-state sequence

@@ -182,8 +182,10 @@ static int validate(const sim_cfg* c) {
       return fail(SIM_EINVAL, "svc_sigma must lie in [0, 64] for lognormal service");
   if (!(c->obs_tw > 0.0) || !(c->lambda_ref > 0.0))
     return fail(SIM_EINVAL, "obs_tw and lambda_ref must be > 0");
-  if (c->static_route < SIM_ROUTE_LOWEST || c->static_route > SIM_ROUTE_ROUND_ROBIN)
+  if (c->static_route < SIM_ROUTE_LOWEST || c->static_route > SIM_ROUTE_SHORTEST)
     return fail(SIM_EINVAL, "static_route");
+  if (c->static_route == SIM_ROUTE_SHORTEST && c->n_servers > 8)
+    return fail(SIM_EUNSUPPORTED, "Shortest-Queue routing is built for at most 8 servers");
   if (c->shadow && (c->static_bmax < 1 || c->static_bmax > 255 || !(c->static_timeout >= 0.0)))
     return fail(SIM_EINVAL, "static rule needs 1 <= static_bmax <= 255, static_timeout >= 0");
   return SIM_OK;
@@ -276,6 +278,8 @@ int sim_create(const sim_cfg* cfg, void* hip_stream, sim_ctx** out) {
     parts.push_back({(void**)&g.hpack, 4 * E});
     parts.push_back({(void**)&g.hts, 8 * C * E});
     parts.push_back({(void**)&g.busy, 8 * K * E});
+    if (s == 1 && cfg->static_route == SIM_ROUTE_SHORTEST)
+      parts.push_back({(void**)&g.busy2, 8 * K * E});
     parts.push_back({(void**)&g.meta, 4 * K * E});
     parts.push_back({(void**)&g.cnt, 4 * kNcnt * E});
     parts.push_back({(void**)&g.sums, 8 * 2 * E});

@@ -709,20 +709,63 @@ __device__ __forceinline__ int route_pick(uint32_t idle, int route, uint32_t rr,
   return __builtin_ctz(idle);
 }
 
+// Shortest-Queue routing (Sec. 5.1 baselines): each server holds the batch it runs (completion
+// busy_j, size infl_j) and at most one batch queued behind it (completion c2_j, size n2_j),
+// served in order. At a scan instant `now` the batches that have completed (c <= now) leave
+// their server and count as completed; the slot mask marks servers with room for a batch
+// (nothing queued) and next_done is the next completion.
+template <int KM>
+struct SqState {
+  double c2[KM];
+  ServerBytes n2;
+};
+
+template <int KM>
+__device__ __forceinline__ void sq_scan(BusyTimes<KM>& busy, ServerBytes& infl, SqState<KM>& sq,
+                                        int K, double now, uint32_t& done, uint32_t& slots,
+                                        double& next_done) {
+  slots = 0u;
+  next_done = kInf;
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    if (j < K) {
+      double b = busy.get(j);
+      uint32_t n1 = infl.get(j);
+      if (n1 > 0 && b <= now) {
+        done += n1;
+        n1 = sq.n2.get(j);
+        if (n1 > 0) b = sq.c2[j];
+        sq.n2.set(j, 0u);
+        if (n1 > 0 && b <= now) {
+          done += n1;
+          n1 = 0;
+        }
+        busy.set(j, b);
+        infl.set(j, n1);
+      }
+      if (sq.n2.get(j) == 0u) slots |= 1u << j;
+      if (n1 > 0 && b > now && b < next_done) next_done = b;
+    }
+  }
+}
+
 // One tick [t_k, t_{k+1}) of the static system of one environment whose state is held in
 // registers: arrivals, the static rule's dispatches to the routed server, completions, and
 // the tick's reward (into rew_row[e] when given). A dispatch stores its server's meta word at
 // once; a completion clears the in-flight byte only in registers and marks the server in
 // `clear`, and `dirty` marks servers whose busy-until time changed; the caller writes both
 // back. Lanes without an environment (live = false) take part in the wave's ballots only.
-template <int KM, int CM>
+// With SQ (Shortest-Queue routing) the idle mask holds the servers with a free slot instead,
+// and completions are retired at every scan (sq_scan).
+template <int KM, int CM, bool SQ>
 __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& G, uint32_t* err,
                                             uint64_t seed, uint32_t k, bool live, int e, int ee,
                                             int e_lane0, int lane, Stage<kStageStatic>& st,
                                             Queue<CM>& Q,
                                             Count& C, Arrivals& A, BusyTimes<KM>& busy,
-                                            ServerBytes& infl, uint32_t& dirty, uint32_t& clear,
-                                            uint32_t& rr, double* __restrict__ rew_row) {
+                                            ServerBytes& infl, SqState<KM>& sq, uint32_t& dirty,
+                                            uint32_t& clear, uint32_t& rr,
+                                            double* __restrict__ rew_row) {
   const size_t E = (size_t)p.E;
   C.n_k = 0;
   C.Lw = 0.0;
@@ -735,7 +778,8 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
   double now = t0;
   uint32_t idle;
   double next_done;
-  server_scan(busy, p.K, now, idle, next_done);
+  if constexpr (SQ) sq_scan(busy, infl, sq, p.K, now, C.c[C_DONE], idle, next_done);
+  else server_scan(busy, p.K, now, idle, next_done);
   uint32_t staged_hi = 0;
   bool done = !live;
   uint32_t it = 0;
@@ -767,7 +811,10 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
     if (go) {
       ++it;
       now = te;
-      if (next_done == now) server_scan(busy, p.K, now, idle, next_done);
+      if (next_done == now) {
+        if constexpr (SQ) sq_scan(busy, infl, sq, p.K, now, C.c[C_DONE], idle, next_done);
+        else server_scan(busy, p.K, now, idle, next_done);
+      }
       const int cls = advance_staged<CM>(A, p, st, lane, seed, ee, k, now);
       if (cls >= 0) {
         ++A_k;
@@ -781,6 +828,35 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
         const int qh = Q.q(h);
         if (!(qh >= p.bmax || now >= Q.hts_h + p.static_timeout)) break;
         const int n = qh < p.bmax ? qh : p.bmax;
+        if constexpr (SQ) {
+          // the server with the fewest requests assigned among those with a free slot (nothing
+          // queued: the load is its running batch), ties to the lower index; the batch starts
+          // when that server has finished its running batch
+          int j = -1;
+          uint32_t best = 0u;
+#pragma unroll
+          for (int jj = 0; jj < KM; ++jj) {
+            const uint32_t L = infl.get(jj);
+            if (jj < p.K && ((idle >> jj) & 1u) && (j < 0 || L < best)) {
+              j = jj;
+              best = L;
+            }
+          }
+          const uint32_t n1 = infl.get(j);
+          const double start = n1 > 0u ? busy.get(j) : now;
+          const double sv = service<CM>(C, p, seed, ee, k, 1, h, n);
+          const double cdone = pop_batch(Q, C, p, k, j, h, n, start, sv);
+          if (n1 == 0u) {
+            busy.set(j, cdone);
+            infl.set(j, (uint32_t)n);
+            if (cdone > now && cdone < next_done) next_done = cdone;
+          } else {
+            put<KM>(sq.c2, j, cdone);
+            sq.n2.set(j, (uint32_t)n);
+            idle &= ~(1u << j);
+          }
+          continue;
+        }
         const int j = route_pick(idle, p.route, rr, seed, ee, k, jroute);
         if (p.route == 2) rr = (uint32_t)((j + 1) % p.K);
         C.c[C_DONE] += infl.get(j);  // the previous batch on j finished at busy_j <= now
@@ -801,13 +877,33 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
   }
   if (!live) return;
   // completions before t1
+  if constexpr (SQ) {
 #pragma unroll
-  for (int j = 0; j < KM; ++j) {
-    const uint32_t n = infl.get(j);
-    if (j < p.K && n > 0 && busy.get(j) < t1) {
-      C.c[C_DONE] += n;
-      clear |= 1u << j;
-      infl.set(j, 0u);
+    for (int j = 0; j < KM; ++j) {
+      if (j < p.K) {
+        uint32_t n1 = infl.get(j);
+        if (n1 > 0 && busy.get(j) < t1) {
+          C.c[C_DONE] += n1;
+          n1 = sq.n2.get(j);
+          if (n1 > 0) busy.set(j, sq.c2[j]);
+          sq.n2.set(j, 0u);
+          if (n1 > 0 && busy.get(j) < t1) {
+            C.c[C_DONE] += n1;
+            n1 = 0;
+          }
+          infl.set(j, n1);
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+      const uint32_t n = infl.get(j);
+      if (j < p.K && n > 0 && busy.get(j) < t1) {
+        C.c[C_DONE] += n;
+        clear |= 1u << j;
+        infl.set(j, 0u);
+      }
     }
   }
   const double r = close_tick(Q, C, p, A.proc, A_k);
@@ -819,7 +915,7 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
 // registers from tick to tick, and stored once; each wave advances at its own pace instead of
 // waiting at every tick for the slowest wave of the grid. rew [nt][E] (optional) receives the
 // rewards; nt = 1 is the per-tick kernel of the step interface.
-template <int KM, int CM>
+template <int KM, int CM, bool SQ>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void static_k(
     SimParams p, EnvState g, uint64_t seed, uint32_t k0, int nt, double* __restrict__ rew) {
   __shared__ Stage<kStageStatic> stage[4];
@@ -845,17 +941,42 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   busy.slab = &busy_lds[threadIdx.x >> 6][0][0];
   busy.lane = lane;
   ServerBytes infl;
+  SqState<KM> sq;
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
     busy.set(j, j < p.K ? G.busy[(size_t)j * E + ee] : kInf);
-    if (j < p.K) infl.set(j, G.meta[(size_t)j * E + ee] & 0xffu);
+    if (j < p.K) {
+      const uint32_t m = G.meta[(size_t)j * E + ee];
+      infl.set(j, m & 0xffu);
+      if constexpr (SQ) {
+        sq.n2.set(j, m >> 24);
+        sq.c2[j] = G.busy2[(size_t)j * E + ee];
+      }
+    }
   }
   uint32_t dirty = 0, clear = 0;
   uint32_t rr = p.route == 2 ? G.rr[ee] : 0u;
   for (int i = 0; i < nt; ++i)
-    static_tick<KM, CM>(p, G, g.err, seed, k0 + (uint32_t)i, live, e, ee, e_lane0, lane, st, Q,
-                        C, A, busy, infl, dirty, clear, rr, rew ? rew + (size_t)i * E : nullptr);
+    static_tick<KM, CM, SQ>(p, G, g.err, seed, k0 + (uint32_t)i, live, e, ee, e_lane0, lane, st,
+                            Q, C, A, busy, infl, sq, dirty, clear, rr,
+                            rew ? rew + (size_t)i * E : nullptr);
   if (!live) return;
+  if constexpr (SQ) {
+    // every server's running and queued batch: completion times and the meta word (running
+    // size in the low byte, queued size in the high byte)
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+      if (j < p.K) {
+        G.busy[(size_t)j * E + e] = busy.get(j);
+        G.busy2[(size_t)j * E + e] = sq.c2[j];
+        G.meta[(size_t)j * E + e] = infl.get(j) | (sq.n2.get(j) << 24);
+      }
+    }
+    store_queue(Q, G, p, e);
+    store_count(C, G, p, e);
+    store_arrivals(A, G, p, e);
+    return;
+  }
   // servers whose last batch completed: clear the in-flight byte of the stored meta word
   uint32_t m[KM];
 #pragma unroll
@@ -918,6 +1039,7 @@ __global__ __launch_bounds__(256) void reset_k(SimParams p, EnvState g, uint64_t
     for (int j = 0; j < p.K; ++j) {
       s.busy[(size_t)j * E + e] = 0.0;
       s.meta[(size_t)j * E + e] = 0xffu << 16;
+      if (s.busy2) s.busy2[(size_t)j * E + e] = kInf;
     }
     for (int i = 0; i < kNcnt; ++i) s.cnt[(size_t)i * E + e] = 0u;
     s.sums[e] = 0.0;
@@ -949,7 +1071,10 @@ __global__ void counters_k(SimParams p, EnvState g, int64_t* cnt, double* sums) 
       for (int i = 0; i < kNcnt; ++i)
         o[(size_t)i * E + e] = on ? (int64_t)s.cnt[(size_t)i * E + e] : 0;
       if (on)
-        for (int j = 0; j < p.K; ++j) infl += s.meta[(size_t)j * E + e] & 0xffu;
+        for (int j = 0; j < p.K; ++j) {
+          const uint32_t m = s.meta[(size_t)j * E + e];
+          infl += (m & 0xffu) + (m >> 24);   // running batch, batch queued (Shortest-Queue)
+        }
       o[(size_t)6 * E + e] = infl;
     }
     if (sums) {
@@ -974,7 +1099,10 @@ __global__ __launch_bounds__(256) void totals_k(SimParams p, EnvState g, int64_t
         if (i < kNcnt) {
           v = s.cnt[(size_t)i * E + e];
         } else {
-          for (int j = 0; j < p.K; ++j) v += s.meta[(size_t)j * E + e] & 0xffu;
+          for (int j = 0; j < p.K; ++j) {
+            const uint32_t m = s.meta[(size_t)j * E + e];
+            v += (m & 0xffu) + (m >> 24);
+          }
         }
       }
       for (int off = 32; off > 0; off >>= 1) v += __shfl_down(v, off, 64);
@@ -992,10 +1120,16 @@ template <int CM>
 void launch_static_c(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k, int nt,
                      double* rew_sh, hipStream_t st) {
   const dim3 grid((p.E + 255) / 256), block(256);
-  if (p.K <= 1) hipLaunchKernelGGL((static_k<1, CM>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
-  else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
-  else if (p.K <= 8) hipLaunchKernelGGL((static_k<8, CM>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
-  else hipLaunchKernelGGL((static_k<16, CM>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
+  if (p.route == 3) {   // Shortest-Queue (at most 8 servers)
+    if (p.K <= 2) hipLaunchKernelGGL((static_k<2, CM, true>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
+    else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM, true>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
+    else hipLaunchKernelGGL((static_k<8, CM, true>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
+    return;
+  }
+  if (p.K <= 1) hipLaunchKernelGGL((static_k<1, CM, false>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
+  else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM, false>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
+  else if (p.K <= 8) hipLaunchKernelGGL((static_k<8, CM, false>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
+  else hipLaunchKernelGGL((static_k<16, CM, false>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
 }
 
 }  // namespace

@@ -233,14 +233,18 @@ RULES = {
     "round_robin_C3": lambda: baseline_preset("round_robin", "C3"),
     "random_C5": lambda: baseline_preset("random", "C5"),
     "round_robin_C4": lambda: baseline_preset("round_robin", "C4"),
+    "shortest_C3": lambda: baseline_preset("shortest", "C3"),
+    "shortest_C3_K2": lambda: baseline_preset("shortest", "C3", n_servers=2),
+    "shortest_C2_K1": lambda: baseline_preset("shortest", "C2"),
+    "shortest_C4": lambda: baseline_preset("shortest", "C4"),
 }
 
 
 @pytest.mark.parametrize("name", sorted(RULES))
 def test_baselines_and_burst_parity(bs, orc, name):
     """The paper's baselines on the shadow system (Static-8, random and round-robin routing,
-    R23) and the Extreme Burst square wave (R24): 300 envs x 600 ticks, bit-exact integer
-    state and rewards against the oracle."""
+    R23, Shortest-Queue over per-server queues, R27) and the Extreme Burst square wave (R24):
+    300 envs x 600 ticks, bit-exact integer state and rewards against the oracle."""
     w = RULES[name]()
     E, T, seed = 300, 600, 0xBA5E + len(name)
     acts = seeded_actions(seed, T, E, 6 * w["n_servers"], small_bias=0.5)
@@ -309,7 +313,7 @@ def _trace_tensors(g, dev):
     return times, cls, cnt, L
 
 
-@pytest.mark.parametrize("tr", ["T1", "T2", "T3", "T4"])
+@pytest.mark.parametrize("tr", ["T1", "T2", "T3", "T4", "T5"])
 def test_hand_traces_on_gpu(bs, orc, tr):
     g = GOLD[tr]
     w = trace_preset(**g["cfg"])
@@ -352,6 +356,12 @@ def test_hand_traces_on_gpu(bs, orc, tr):
             np.testing.assert_allclose(obs[int(k)].cpu().numpy()[:, 0], np.array(v, np.float32),
                                        rtol=1e-6, atol=1e-9)
         assert cnt_[0, 5, 0] == g["completed_cum"][-1]
+    if tr == "T5":
+        for k, v in g["shadow_rewards"].items():
+            assert abs(rshs[int(k)].cpu().numpy()[0] - v) <= 1e-9 * max(1.0, abs(v))
+        assert abs(sums[1, 0, 0] - g["shadow_latency_sum"]) < 1e-12
+        assert cnt_[1, 4, 0] == len(g["shadow_dispatches"])
+        assert cnt_[1, 5, 0] == g["shadow_completed_cum"][-1]
     if tr == "T3":
         assert abs(sums[1, 0, 0] - g["shadow_latency_sum"]) < 1e-12
         assert cnt_[1, 4, 0] == len(g["shadow_dispatches"])
@@ -622,6 +632,7 @@ SHADOWED = {
     "static8_C3": lambda: baseline_preset("static8", "C3"),
     "random_C5": lambda: baseline_preset("random", "C5"),
     "round_robin_C4": lambda: baseline_preset("round_robin", "C4"),
+    "shortest_C3": lambda: baseline_preset("shortest", "C3"),
 }
 
 
