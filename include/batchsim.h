@@ -184,9 +184,9 @@ const char* sim_last_error(void);
 /* Library ABI version (BATCHSIM_ABI_VERSION). */
 uint32_t sim_abi_version(void);
 
-/* Creates a context on the current HIP device: validates cfg (SIM_EINVAL with a message
- * naming the field), allocates the structure-of-arrays environment state and queues in
- * HBM (SIM_ENOMEM). `hip_stream` is a hipStream_t (NULL = default stream). The context is
+/* Creates a context on the current HIP device: n_envs copies of the simulator of Sec. 3.1
+ * (and of the MDP of Sec. 4.1 around it). Validates cfg (SIM_EINVAL with a message naming the
+ * field), allocates the structure-of-arrays environment state and queues in HBM (SIM_ENOMEM). `hip_stream` is a hipStream_t (NULL = default stream). The context is
  * not usable until sim_reset. On failure *out is NULL and nothing stays allocated.     */
 int sim_create(const sim_cfg* cfg, void* hip_stream, sim_ctx** out);
 
@@ -200,14 +200,16 @@ int sim_set_trace(sim_ctx* ctx, const double* d_times, const uint8_t* d_classes,
                   const int32_t* d_counts);
 
 /* Resets every environment at t = 0 (empty queues, idle servers, zero counters, the
- * modulating state drawn from its stationary law) and sets the tick counter to 0.      */
+ * modulating state of the Sec. 3.2 arrival process drawn from its stationary law) and sets the
+ * tick counter to 0: the start of an episode (Sec. 4.3).                                */
 int sim_reset(sim_ctx* ctx, uint64_t seed);
 
 /* Copies the current observation [F][E] fp32 (the state of Sec. 4.1) to d_obs.         */
 int sim_obs(sim_ctx* ctx, float* d_obs);
 
-/* Advances every environment by one tick under the given actions (d_actions [E], values
- * in [0, 6K): server a/6, batch size 2^(a%6)). Optional outputs: the next observation
+/* One step of the MDP (Sec. 4.1): advances every environment by one tick of the simulator
+ * (Sec. 3.1) under the given actions (d_actions [E], values in [0, 6K): server a/6, batch size
+ * 2^(a%6)). Optional outputs: the next observation
  * [F][E], the learned and shadow rewards [E]. An action out of range latches SIM_ESTATE.*/
 int sim_step(sim_ctx* ctx, const uint8_t* d_actions, float* d_obs_next, double* d_reward,
              double* d_reward_shadow);
@@ -222,7 +224,8 @@ int sim_weights_layout(const sim_cfg* cfg, sim_wlayout* out);
  * cfg->policy_kind = SIM_POLICY_ATTN with a valid attention shape.                      */
 int sim_attn_weights_layout(const sim_cfg* cfg, sim_attn_layout* out);
 
-/* Writes Xavier-uniform weights drawn from `seed` and zero biases into d_weights
+/* Initialises the policy network of Sec. 4.2: writes Xavier-uniform weights drawn from
+ * `seed` and zero biases into d_weights
  * (layout of sim_weights_layout, or of sim_attn_weights_layout for the attention policy,
  * whose seven matrices take weight-stream layers 0..6 in layout order).                 */
 int sim_init_weights(sim_ctx* ctx, uint64_t seed, void* d_weights);
@@ -243,9 +246,25 @@ int sim_policy_hidden(sim_ctx* ctx, const void* d_weights, const float* d_obs, u
                       uint8_t* d_act, float* d_logp, float* d_value, float* d_logits,
                       float* d_hidden);
 
-/* T ticks of policy + simulator from the current state (obs_k -> a_k -> obs_{k+1}),
- * writing the trajectory; with a value head, row T of traj->value holds V(obs_T).       */
+/* A rollout of the MDP (Sec. 4.1) under the policy of Sec. 4.2, the trajectory that the
+ * updates of Sec. 4.3 consume: T ticks of policy + simulator from the current state
+ * (obs_k -> a_k -> obs_{k+1}), writing the trajectory; with a value head, row T of
+ * traj->value holds V(obs_T).                                                           */
 int sim_rollout(sim_ctx* ctx, const void* d_weights, int32_t T, const sim_traj* traj);
+
+/* Rollout graphs, on by default: when sim_rollout is called again with the same weights
+ * buffer, T, trajectory pointers and starting tick as the call before (a training loop that
+ * resets and rolls out into the same buffers), its launch sequence is captured into a HIP
+ * graph on a private stream of the context, and that graph is replayed by every further
+ * repeat (ordered after earlier work on the context's stream, and before later work, by
+ * events). Kernels read the seed from device memory written by sim_reset, so a new seed needs
+ * no new graph. Tracing (sim_set_timing) launches eagerly. sim_set_trace discards the graph.
+ * on = 0 launches every rollout eagerly.                                                    */
+int sim_set_graphs(sim_ctx* ctx, int32_t on);
+
+/* Diagnostics of the rollout graphs: graphs captured and rollouts replayed from a graph so far
+ * (either pointer may be NULL).                                                          */
+int sim_graph_stats(sim_ctx* ctx, int64_t* h_captures, int64_t* h_replays);
 
 /* Discounted returns and GAE (Sec. 4.3), per environment backwards in t:
  *   delta_t = (r_t + gamma V_{t+1}) - V_t,  A_t = delta_t + (gamma*lambda) A_{t+1},

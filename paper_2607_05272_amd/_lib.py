@@ -23,7 +23,7 @@ SYMBOLS = ("sim_last_error", "sim_abi_version", "sim_create", "sim_destroy", "si
            "sim_checksums", "sim_stats", "sim_sync", "sim_set_timing", "sim_get_timing",
            "ppo_minibatch_grad", "sim_ppo_grad_count", "reinforce_minibatch_grad",
            "sim_params_from_weights", "adam_update", "sim_update", "sim_attn_weights_layout",
-           "sim_get_state", "sim_set_state", "sim_device_primitive", "sim_policy_hidden",
+           "sim_get_state", "sim_set_state", "sim_device_primitive", "sim_policy_hidden", "sim_set_graphs", "sim_graph_stats",
            "ppo_minibatch_grad_noalloc")
 ALGO_PPO, ALGO_REINFORCE = 0, 1
 KERNEL_CLASSES = ("policy", "step", "static", "gae", "reset", "other", "ppo")
@@ -113,6 +113,7 @@ def load():
         "returns_gae": [vp, i32, vp, vp, dbl, dbl, vp, vp], "sim_counters": [vp, vp, vp],
         "sim_checksums": [vp, vp], "sim_stats": [vp, vp], "sim_sync": [vp],
         "sim_set_timing": [vp, i32], "sim_get_timing": [vp, vp, vp, i32],
+        "sim_set_graphs": [vp, i32], "sim_graph_stats": [vp, vp, vp],
         "ppo_minibatch_grad": [vp, vp, i32, vp, vp, vp, vp, vp, i32, u64, C.c_float, C.c_float,
                                C.c_float, vp, vp, vp],
         "ppo_minibatch_grad_noalloc": [vp, vp, i32, vp, vp, vp, vp, vp, i32, u64, C.c_float,

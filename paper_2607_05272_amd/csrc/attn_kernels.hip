@@ -32,11 +32,12 @@ __device__ __forceinline__ float gelu_exact(float x) {
 // softmax weight is one exp2 of (score - max).
 template <int L, int NH, int A>
 __global__ __launch_bounds__(kBlock) void attn_policy_k(AttnParams p, const float* __restrict__ obs,
-                                                        uint64_t seed, uint32_t step,
+                                                        const uint64_t* __restrict__ seedp, uint32_t step,
                                                         uint8_t* __restrict__ act,
                                                         float* __restrict__ logp,
                                                         float* __restrict__ value,
                                                         float* __restrict__ logits) {
+  const uint64_t seed = *seedp;   // the episode seed
   constexpr int DH = kD / NH;
   constexpr float kLog2e = 1.4426950408889634f;
   const float qscale = (DH == 1 ? 1.0f : DH == 2 ? 0.70710678118654752f : 0.5f) * kLog2e;
@@ -183,7 +184,7 @@ __global__ __launch_bounds__(kBlock) void attn_policy_k(AttnParams p, const floa
 }
 
 template <int L, int NH, int A>
-hipError_t run_attn(const AttnParams& p, const float* obs, uint64_t seed, uint32_t step,
+hipError_t run_attn(const AttnParams& p, const float* obs, const uint64_t* seed, uint32_t step,
                     uint8_t* act, float* logp, float* value, float* logits, hipStream_t st) {
   const dim3 grid((unsigned)((p.E + kBlock - 1) / kBlock)), block(kBlock);
   hipLaunchKernelGGL((attn_policy_k<L, NH, A>), grid, block, 0, st, p, obs, seed, step, act, logp,
@@ -192,7 +193,7 @@ hipError_t run_attn(const AttnParams& p, const float* obs, uint64_t seed, uint32
 }
 
 template <int L, int NH>
-hipError_t run_attn_a(const AttnParams& p, const float* obs, uint64_t seed, uint32_t step,
+hipError_t run_attn_a(const AttnParams& p, const float* obs, const uint64_t* seed, uint32_t step,
                       uint8_t* act, float* logp, float* value, float* logits, hipStream_t st) {
   switch (p.A) {
     case 6: return run_attn<L, NH, 6>(p, obs, seed, step, act, logp, value, logits, st);
@@ -203,7 +204,7 @@ hipError_t run_attn_a(const AttnParams& p, const float* obs, uint64_t seed, uint
 }
 
 template <int L>
-hipError_t run_attn_h(const AttnParams& p, const float* obs, uint64_t seed, uint32_t step,
+hipError_t run_attn_h(const AttnParams& p, const float* obs, const uint64_t* seed, uint32_t step,
                       uint8_t* act, float* logp, float* value, float* logits, hipStream_t st) {
   switch (p.NH) {
     case 1: return run_attn_a<L, 1>(p, obs, seed, step, act, logp, value, logits, st);
@@ -634,7 +635,7 @@ bool attn_shape_supported(const AttnParams& p) {
   return L_ok && H_ok && A_ok && p.D == kD && p.F % p.L == 0 && p.Hp >= 1 && p.Hv >= 1;
 }
 
-hipError_t launch_attn_policy(const AttnParams& p, const float* obs, uint64_t seed, uint32_t step,
+hipError_t launch_attn_policy(const AttnParams& p, const float* obs, const uint64_t* seed, uint32_t step,
                               uint8_t* act, float* logp, float* value, float* logits,
                               hipStream_t st) {
   if (!attn_shape_supported(p)) return hipErrorInvalidValue;

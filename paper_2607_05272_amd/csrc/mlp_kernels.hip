@@ -124,12 +124,13 @@ struct Shape {
 
 template <class M, int FP, int H1, int H2, int AP, bool DBG>
 __global__ __launch_bounds__(kThreads) void policy_k(MlpParams m, const float* __restrict__ obs,
-                                                     uint64_t seed, uint32_t step,
+                                                     const uint64_t* __restrict__ seedp, uint32_t step,
                                                      uint8_t* __restrict__ act,
                                                      float* __restrict__ logp,
                                                      float* __restrict__ value,
                                                      float* __restrict__ logits,
                                                      float* __restrict__ hid) {
+  const uint64_t seed = *seedp;   // the episode seed
   typedef Shape<M, FP, H1, H2, AP> Sh;
   typedef typename M::elem E;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -517,12 +518,13 @@ struct BigShape {
 
 template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW, bool DBG>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MINB / 4 > 0 ? NW * MINB / 4 : 1))) void policy_bf16_k(MlpParams m, const float* __restrict__ obs,
-                                                               uint64_t seed, uint32_t step,
+                                                               const uint64_t* __restrict__ seedp, uint32_t step,
                                                                uint8_t* __restrict__ act,
                                                                float* __restrict__ logp,
                                                                float* __restrict__ value,
                                                                float* __restrict__ logits,
                                                                float* __restrict__ hid) {
+  const uint64_t seed = *seedp;   // the episode seed
   typedef BigShape<FP, H1, H2, AP, RT, NW> Sh;
   constexpr int ROWS = Sh::ROWS, NTHR = NW * 64;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -617,7 +619,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
 }
 
 template <bool DBG, int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW = 1>
-hipError_t run_policy_bf16(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
+hipError_t run_policy_bf16(const MlpParams& m, const float* obs, const uint64_t* seed, uint32_t step,
                            uint8_t* act, float* logp, float* value, float* logits, float* hid,
                            hipStream_t st) {
   typedef BigShape<FP, H1, H2, AP, RT, NW> Sh;
@@ -637,7 +639,7 @@ hipError_t run_policy_bf16(const MlpParams& m, const float* obs, uint64_t seed, 
 }
 
 template <bool DBG, class M, int FP, int H1, int H2, int AP>
-hipError_t run_policy(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
+hipError_t run_policy(const MlpParams& m, const float* obs, const uint64_t* seed, uint32_t step,
                       uint8_t* act, float* logp, float* value, float* logits, float* hid,
                       hipStream_t st) {
   typedef Shape<M, FP, H1, H2, AP> Sh;
@@ -676,7 +678,7 @@ bool policy_shape_supported(const MlpParams& m) {
 }
 
 template <bool DBG>
-static hipError_t launch_policy_t(const MlpParams& m, const float* obs, uint64_t seed,
+static hipError_t launch_policy_t(const MlpParams& m, const float* obs, const uint64_t* seed,
                                   uint32_t step, uint8_t* act, float* logp, float* value,
                                   float* logits, float* hid, hipStream_t st) {
   if (!m.bf16 && m.FP == 8 && m.H1 == 64 && m.H2 == 64 && m.AP == 16)
@@ -699,7 +701,7 @@ static hipError_t launch_policy_t(const MlpParams& m, const float* obs, uint64_t
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_policy(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
+hipError_t launch_policy(const MlpParams& m, const float* obs, const uint64_t* seed, uint32_t step,
                          uint8_t* act, float* logp, float* value, float* logits, float* hidden,
                          hipStream_t st) {
   if (hidden)

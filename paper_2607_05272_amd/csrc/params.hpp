@@ -60,15 +60,16 @@ struct EnvState {
   double* ewma;      // [4][E] exponentially weighted arrival counts (learned system)
   float* obs;        // [F][E] current observation
   uint32_t* err;     // [1] latched error flags
+  uint64_t* seed;    // [1] the episode seed (written by reset_k, read by every kernel that draws)
 };
 
 // Kernel launchers (asynchronous on `st`); each returns the launch's hipError_t.
 hipError_t launch_reset(const SimParams& p, const EnvState& s, uint64_t seed, hipStream_t st);
-hipError_t launch_step(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
+hipError_t launch_step(const SimParams& p, const EnvState& s, uint32_t k,
                        const uint8_t* act, float* obs_out, double* rew, uint64_t* rchk,
                        hipStream_t st);
 // ticks k .. k + nt - 1 of the static shadow system; rew_sh [nt][E] or NULL
-hipError_t launch_static(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
+hipError_t launch_static(const SimParams& p, const EnvState& s, uint32_t k,
                          int nt, double* rew_sh, hipStream_t st);
 hipError_t launch_counters(const SimParams& p, const EnvState& s, int64_t* cnt, double* sums,
                            hipStream_t st);
@@ -93,7 +94,7 @@ hipError_t launch_repack(const MlpParams& m, const void* d_weights, const size_t
                          hipStream_t st);
 // hidden != NULL runs the diagnostic instantiation that also writes the hidden activations
 // passed between layers: [H1][E] then [H2][E] fp32
-hipError_t launch_policy(const MlpParams& m, const float* obs, uint64_t seed, uint32_t step,
+hipError_t launch_policy(const MlpParams& m, const float* obs, const uint64_t* seed, uint32_t step,
                          uint8_t* act, float* logp, float* value, float* logits, float* hidden,
                          hipStream_t st);
 hipError_t launch_init_weights(int F, int H1, int H2, int Ap, int bf16, uint64_t seed,
@@ -108,7 +109,8 @@ struct AttnParams {
   const float *wp1, *bp1, *wp2, *bp2, *wv1, *bv1, *wv2, *bv2;
 };
 bool attn_shape_supported(const AttnParams& p);
-hipError_t launch_attn_policy(const AttnParams& p, const float* obs, uint64_t seed, uint32_t step,
+hipError_t launch_attn_policy(const AttnParams& p, const float* obs, const uint64_t* seed,
+                              uint32_t step,
                               uint8_t* act, float* logp, float* value, float* logits,
                               hipStream_t st);
 // Minibatch gradient of the attention policy (REINFORCE with baseline or PPO): indices drawn

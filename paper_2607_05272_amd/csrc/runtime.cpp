@@ -51,6 +51,14 @@ int pad_to(int x, int m) { return (x + m - 1) / m * m; }
 
 }  // namespace
 
+// What a rollout's launch sequence depends on besides the context itself.
+struct RolloutKey {
+  const void* w;
+  int32_t T;
+  sim_traj tr;
+  uint32_t k0;
+};
+
 struct sim_ctx {
   sim_cfg cfg;
   hipStream_t stream = nullptr;
@@ -71,6 +79,14 @@ struct sim_ctx {
   uint64_t seed = 0;
   bool reset_done = false;
   bool trace_set = false;
+  // rollout graph (sim_rollout): captured on a private stream the second time a call repeats
+  bool graphs = true;
+  hipStream_t gstream = nullptr;
+  hipEvent_t gev_in = nullptr, gev_out = nullptr;
+  hipGraphExec_t rgraph = nullptr;
+  RolloutKey rkey{}, seen{};
+  bool rkey_valid = false, seen_valid = false;
+  int64_t graph_captures = 0, graph_replays = 0;
   // tracing: event pairs around kernel launches, per kernel class
   struct Pending { int cls; hipEvent_t a, b; };
   bool timing = false;
@@ -294,6 +310,7 @@ int sim_create(const sim_cfg* cfg, void* hip_stream, sim_ctx** out) {
   parts.push_back({(void**)&x->s.ewma, 8 * 4 * E});
   parts.push_back({(void**)&x->s.obs, 4 * (size_t)cfg->obs_dim * E});
   parts.push_back({(void**)&x->s.err, 256});
+  parts.push_back({(void**)&x->s.seed, 256});
   parts.push_back({(void**)&x->d_tot_cnt, 8 * 2 * 7});
   parts.push_back({(void**)&x->d_tot_sum, 8 * 2 * 2});
   size_t total = 0;
@@ -310,7 +327,7 @@ int sim_create(const sim_cfg* cfg, void* hip_stream, sim_ctx** out) {
     *pr.first = static_cast<unsigned char*>(x->arena) + off;
     off += align256(pr.second);
   }
-  he = hipMemsetAsync(x->s.err, 0, 256, x->stream);
+  he = hipMemsetAsync(x->s.err, 0, 512, x->stream);   // error flags and the seed word
   if (he != hipSuccess) {
     (void)hipFree(x->arena);
     delete x;
@@ -350,6 +367,13 @@ int sim_destroy(sim_ctx* x) {
   (void)hipFree(x->wpack);
   (void)hipFree(x->ppo_scratch);
   (void)hipFree(x->grads);
+  if (x->rgraph) (void)hipGraphExecDestroy(x->rgraph);
+  if (x->gev_in) (void)hipEventDestroy(x->gev_in);
+  if (x->gev_out) (void)hipEventDestroy(x->gev_out);
+  if (x->gstream) {
+    (void)hipStreamSynchronize(x->gstream);
+    (void)hipStreamDestroy(x->gstream);
+  }
   delete x;
   return SIM_OK;
 }
@@ -364,6 +388,7 @@ int sim_set_trace(sim_ctx* x, const double* d_times, const uint8_t* d_classes,
   x->p.tr_cls = d_classes;
   x->p.tr_cnt = d_counts;
   x->trace_set = true;
+  x->rkey_valid = x->seen_valid = false;   // the rollout graph holds the previous arrays
   return SIM_OK;
 }
 
@@ -388,14 +413,14 @@ int sim_obs(sim_ctx* x, float* d_obs) {
 }
 
 // the learned system's tick and, if `shadow`, the static system's
-static int enqueue_tick(sim_ctx* x, const uint8_t* act, float* obs_out, double* rew,
+static int enqueue_tick(sim_ctx* x, uint32_t k, const uint8_t* act, float* obs_out, double* rew,
                         double* rew_sh, uint64_t* rchk, bool shadow) {
   HIPCHK(x->timed(SIM_KC_STEP, [&] {
-           return launch_step(x->p, x->s, x->seed, x->tick, act, obs_out, rew, rchk, x->stream);
+           return launch_step(x->p, x->s, k, act, obs_out, rew, rchk, x->stream);
          }), "step kernel launch");
   if (shadow && x->cfg.shadow)
     HIPCHK(x->timed(SIM_KC_STATIC, [&] {
-             return launch_static(x->p, x->s, x->seed, x->tick, 1, rew_sh, x->stream);
+             return launch_static(x->p, x->s, k, 1, rew_sh, x->stream);
            }), "static kernel launch");
   return SIM_OK;
 }
@@ -408,7 +433,7 @@ static int run_static(sim_ctx* x, uint32_t k0, int32_t T, double* rew_sh) {
   for (int32_t c = 0; c < T; c += kStaticChunk) {
     const int nt = T - c < kStaticChunk ? T - c : kStaticChunk;
     HIPCHK(x->timed(SIM_KC_STATIC, [&] {
-             return launch_static(x->p, x->s, x->seed, k0 + (uint32_t)c, nt,
+             return launch_static(x->p, x->s, k0 + (uint32_t)c, nt,
                                   rew_sh ? rew_sh + (size_t)c * E : nullptr, x->stream);
            }), "static kernel launch");
   }
@@ -420,7 +445,7 @@ int sim_step(sim_ctx* x, const uint8_t* d_actions, float* d_obs_next, double* d_
   if (!x || !d_actions) return fail(SIM_EINVAL, "NULL argument");
   if (!x->reset_done) return fail(SIM_ESTATE, "sim_step before sim_reset");
   if (x->tick == 0xFFFFFFFEu) return fail(SIM_ESTATE, "tick counter exhausted");
-  int rc = enqueue_tick(x, d_actions, d_obs_next, d_reward, d_reward_shadow, nullptr, true);
+  int rc = enqueue_tick(x, x->tick, d_actions, d_obs_next, d_reward, d_reward_shadow, nullptr, true);
   if (rc) return rc;
   x->tick++;
   return SIM_OK;
@@ -558,8 +583,8 @@ static hipError_t policy_launch(sim_ctx* x, const float* obs, uint32_t step, uin
                                 float* logp, float* value, float* logits,
                                 float* hidden = nullptr) {
   if (x->cfg.policy_kind == SIM_POLICY_ATTN)
-    return launch_attn_policy(x->a, obs, x->seed, step, act, logp, value, logits, x->stream);
-  return launch_policy(x->m, obs, x->seed, step, act, logp, value, logits, hidden, x->stream);
+    return launch_attn_policy(x->a, obs, x->s.seed, step, act, logp, value, logits, x->stream);
+  return launch_policy(x->m, obs, x->s.seed, step, act, logp, value, logits, hidden, x->stream);
 }
 
 int sim_policy(sim_ctx* x, const void* d_weights, const float* d_obs, uint32_t step,
@@ -589,6 +614,91 @@ int sim_policy_hidden(sim_ctx* x, const void* d_weights, const float* d_obs, uin
   return SIM_OK;
 }
 
+// Every launch of a rollout of T ticks from tick k0 on x->stream: the policy's weight repack,
+// the static shadow system in multi-tick launches, then per tick the policy and the learned
+// system's tick, and the final value. Its arguments depend only on the weights pointer, T, the
+// trajectory pointers and k0 (the seed is read from device memory), so the sequence can be
+// captured once as a graph and replayed.
+static int enqueue_rollout(sim_ctx* x, const void* d_weights, int32_t T, const sim_traj* tr,
+                           uint32_t k0) {
+  int rc = prepare_policy(x, d_weights);
+  if (rc) return rc;
+  const size_t E = (size_t)x->cfg.n_envs, F = (size_t)x->cfg.obs_dim;
+  if (x->cfg.shadow) {
+    rc = run_static(x, k0, T, tr->reward_shadow);
+    if (rc) return rc;
+  }
+  for (int32_t i = 0; i < T; ++i) {
+    const size_t row = (size_t)i * E;
+    const uint32_t k = k0 + (uint32_t)i;
+    HIPCHK(x->timed(SIM_KC_POLICY, [&] {
+             return policy_launch(x, x->s.obs, k, tr->actions + row,
+                                  tr->logp ? tr->logp + row : nullptr,
+                                  tr->value ? tr->value + row : nullptr, nullptr);
+           }), "policy kernel launch");
+    rc = enqueue_tick(x, k, tr->actions + row, tr->obs ? tr->obs + (size_t)(i + 1) * F * E : nullptr,
+                      tr->reward ? tr->reward + row : nullptr, nullptr,
+                      tr->rchk ? tr->rchk + row : nullptr, false);
+    if (rc) return rc;
+  }
+  if (tr->value)
+    HIPCHK(x->timed(SIM_KC_POLICY, [&] {
+             return policy_launch(x, x->s.obs, k0 + (uint32_t)T, nullptr, nullptr,
+                                  tr->value + (size_t)T * E, nullptr);
+           }), "policy kernel launch (final value)");
+  return SIM_OK;
+}
+
+static bool same_key(const RolloutKey& a, const RolloutKey& b) {
+  return a.w == b.w && a.T == b.T && a.k0 == b.k0 && std::memcmp(&a.tr, &b.tr, sizeof a.tr) == 0;
+}
+
+// Captures the rollout's launch sequence on the context's private stream into a graph.
+static int capture_rollout(sim_ctx* x, const RolloutKey& key, const sim_traj* tr) {
+  if (!x->gstream) {
+    HIPCHK(hipStreamCreateWithFlags(&x->gstream, hipStreamNonBlocking), "hipStreamCreateWithFlags");
+    HIPCHK(hipEventCreateWithFlags(&x->gev_in, hipEventDisableTiming), "hipEventCreateWithFlags");
+    HIPCHK(hipEventCreateWithFlags(&x->gev_out, hipEventDisableTiming), "hipEventCreateWithFlags");
+  }
+  hipStream_t caller = x->stream;
+  x->stream = x->gstream;
+  hipError_t e = hipStreamBeginCapture(x->gstream, hipStreamCaptureModeThreadLocal);
+  int rc = e == hipSuccess ? enqueue_rollout(x, key.w, key.T, tr, key.k0) : SIM_EDEVICE;
+  hipGraph_t g = nullptr;
+  if (e == hipSuccess) {
+    const hipError_t e2 = hipStreamEndCapture(x->gstream, &g);
+    if (e2 != hipSuccess && rc == SIM_OK) rc = hip_fail(e2, "hipStreamEndCapture");
+  } else {
+    rc = hip_fail(e, "hipStreamBeginCapture");
+  }
+  x->stream = caller;
+  hipGraphExec_t ex = nullptr;
+  if (rc == SIM_OK && g) {
+    e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    if (e != hipSuccess) rc = hip_fail(e, "hipGraphInstantiate");
+  }
+  if (g) (void)hipGraphDestroy(g);
+  if (rc) return rc;
+  if (x->rgraph) (void)hipGraphExecDestroy(x->rgraph);
+  x->rgraph = ex;
+  x->rkey = key;
+  x->rkey_valid = true;
+  x->graph_captures++;
+  return SIM_OK;
+}
+
+// Replays the captured rollout on the private stream, ordered after the work already on the
+// caller's stream and before any work enqueued there later.
+static int replay_rollout(sim_ctx* x) {
+  HIPCHK(hipEventRecord(x->gev_in, x->stream), "hipEventRecord");
+  HIPCHK(hipStreamWaitEvent(x->gstream, x->gev_in, 0), "hipStreamWaitEvent");
+  HIPCHK(hipGraphLaunch(x->rgraph, x->gstream), "hipGraphLaunch");
+  HIPCHK(hipEventRecord(x->gev_out, x->gstream), "hipEventRecord");
+  HIPCHK(hipStreamWaitEvent(x->stream, x->gev_out, 0), "hipStreamWaitEvent");
+  x->graph_replays++;
+  return SIM_OK;
+}
+
 int sim_rollout(sim_ctx* x, const void* d_weights, int32_t T, const sim_traj* tr) {
   if (!x || !d_weights || !tr || !tr->actions) return fail(SIM_EINVAL, "NULL argument");
   if (T < 1) return fail(SIM_EINVAL, "T must be >= 1");
@@ -597,34 +707,42 @@ int sim_rollout(sim_ctx* x, const void* d_weights, int32_t T, const sim_traj* tr
   if (tr->reward_shadow && !x->cfg.shadow)
     return fail(SIM_EINVAL, "traj.reward_shadow needs shadow = 1");
   if ((uint64_t)x->tick + (uint64_t)T >= 0xFFFFFFFFull) return fail(SIM_ESTATE, "tick counter exhausted");
-  int rc = prepare_policy(x, d_weights);
-  if (rc) return rc;
   const size_t E = (size_t)x->cfg.n_envs, F = (size_t)x->cfg.obs_dim;
   if (tr->obs)
     HIPCHK(hipMemcpyAsync(tr->obs, x->s.obs, 4 * F * E, hipMemcpyDeviceToDevice, x->stream),
            "hipMemcpyAsync obs_0");
-  if (x->cfg.shadow) {
-    rc = run_static(x, x->tick, T, tr->reward_shadow);
-    if (rc) return rc;
+  const RolloutKey key{d_weights, T, *tr, x->tick};
+  int rc;
+  if (x->graphs && !x->timing) {
+    // a call that repeats the previous one (same weights, length, outputs, starting tick) is
+    // captured as a graph; later repeats replay it
+    bool have = x->rkey_valid && same_key(key, x->rkey);
+    if (!have && x->seen_valid && same_key(key, x->seen)) have = capture_rollout(x, key, tr) == SIM_OK;
+    if (have) {
+      rc = replay_rollout(x);
+      if (rc) return rc;
+      x->tick += (uint32_t)T;
+      return SIM_OK;
+    }
+    x->seen = key;
+    x->seen_valid = true;
   }
-  for (int32_t k = 0; k < T; ++k) {
-    const size_t row = (size_t)k * E;
-    HIPCHK(x->timed(SIM_KC_POLICY, [&] {
-             return policy_launch(x, x->s.obs, x->tick, tr->actions + row,
-                                  tr->logp ? tr->logp + row : nullptr,
-                                  tr->value ? tr->value + row : nullptr, nullptr);
-           }), "policy kernel launch");
-    rc = enqueue_tick(x, tr->actions + row, tr->obs ? tr->obs + (size_t)(k + 1) * F * E : nullptr,
-                      tr->reward ? tr->reward + row : nullptr, nullptr,
-                      tr->rchk ? tr->rchk + row : nullptr, false);
-    if (rc) return rc;
-    x->tick++;
-  }
-  if (tr->value)
-    HIPCHK(x->timed(SIM_KC_POLICY, [&] {
-             return policy_launch(x, x->s.obs, x->tick, nullptr, nullptr,
-                                  tr->value + (size_t)T * E, nullptr);
-           }), "policy kernel launch (final value)");
+  rc = enqueue_rollout(x, d_weights, T, tr, x->tick);
+  if (rc) return rc;
+  x->tick += (uint32_t)T;
+  return SIM_OK;
+}
+
+int sim_set_graphs(sim_ctx* x, int32_t on) {
+  if (!x) return fail(SIM_EINVAL, "ctx is NULL");
+  x->graphs = on != 0;
+  return SIM_OK;
+}
+
+int sim_graph_stats(sim_ctx* x, int64_t* h_captures, int64_t* h_replays) {
+  if (!x) return fail(SIM_EINVAL, "ctx is NULL");
+  if (h_captures) *h_captures = x->graph_captures;
+  if (h_replays) *h_replays = x->graph_replays;
   return SIM_OK;
 }
 

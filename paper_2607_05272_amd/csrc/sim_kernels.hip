@@ -427,11 +427,11 @@ __device__ __forceinline__ void put_obs(float* obs, size_t E, int i, int e, doub
 
 // ---- learned system: one tick ---------------------------------------------------------------
 template <int CM>
-__global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint64_t seed,
-                                                 uint32_t k, const uint8_t* __restrict__ act,
+__global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32_t k, const uint8_t* __restrict__ act,
                                                  float* __restrict__ obs_out,
                                                  double* __restrict__ rew,
                                                  uint64_t* __restrict__ rchk) {
+  const uint64_t seed = *g.seed;   // the episode seed, written by reset_k
   __shared__ Stage<kStageLearned> stage[4];
   const int lane = threadIdx.x & 63;
   Stage<kStageLearned>& st = stage[threadIdx.x >> 6];
@@ -917,7 +917,8 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
 // rewards; nt = 1 is the per-tick kernel of the step interface.
 template <int KM, int CM, bool SQ>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void static_k(
-    SimParams p, EnvState g, uint64_t seed, uint32_t k0, int nt, double* __restrict__ rew) {
+    SimParams p, EnvState g, uint32_t k0, int nt, double* __restrict__ rew) {
+  const uint64_t seed = *g.seed;   // the episode seed, written by reset_k
   __shared__ Stage<kStageStatic> stage[4];
   __shared__ double busy_lds[4][KM > 8 ? KM - kBusyRegs : 1][64];
   const int lane = threadIdx.x & 63;
@@ -997,6 +998,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 // ---- reset ------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void reset_k(SimParams p, EnvState g, uint64_t seed) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e == 0) *g.seed = seed;   // read by every later kernel of the episode
   if (e >= p.E) return;
   const size_t E = (size_t)p.E;
   // modulating state from its stationary law, its dwell, then the first arrival
@@ -1117,19 +1119,19 @@ __global__ __launch_bounds__(256) void totals_k(SimParams p, EnvState g, int64_t
 }
 
 template <int CM>
-void launch_static_c(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k, int nt,
+void launch_static_c(const SimParams& p, const EnvState& s, uint32_t k, int nt,
                      double* rew_sh, hipStream_t st) {
   const dim3 grid((p.E + 255) / 256), block(256);
   if (p.route == 3) {   // Shortest-Queue (at most 8 servers)
-    if (p.K <= 2) hipLaunchKernelGGL((static_k<2, CM, true>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
-    else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM, true>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
-    else hipLaunchKernelGGL((static_k<8, CM, true>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
+    if (p.K <= 2) hipLaunchKernelGGL((static_k<2, CM, true>), grid, block, 0, st, p, s, k, nt, rew_sh);
+    else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM, true>), grid, block, 0, st, p, s, k, nt, rew_sh);
+    else hipLaunchKernelGGL((static_k<8, CM, true>), grid, block, 0, st, p, s, k, nt, rew_sh);
     return;
   }
-  if (p.K <= 1) hipLaunchKernelGGL((static_k<1, CM, false>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
-  else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM, false>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
-  else if (p.K <= 8) hipLaunchKernelGGL((static_k<8, CM, false>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
-  else hipLaunchKernelGGL((static_k<16, CM, false>), grid, block, 0, st, p, s, seed, k, nt, rew_sh);
+  if (p.K <= 1) hipLaunchKernelGGL((static_k<1, CM, false>), grid, block, 0, st, p, s, k, nt, rew_sh);
+  else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM, false>), grid, block, 0, st, p, s, k, nt, rew_sh);
+  else if (p.K <= 8) hipLaunchKernelGGL((static_k<8, CM, false>), grid, block, 0, st, p, s, k, nt, rew_sh);
+  else hipLaunchKernelGGL((static_k<16, CM, false>), grid, block, 0, st, p, s, k, nt, rew_sh);
 }
 
 }  // namespace
@@ -1139,25 +1141,25 @@ hipError_t launch_reset(const SimParams& p, const EnvState& s, uint64_t seed, hi
   return hipGetLastError();
 }
 
-hipError_t launch_step(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
+hipError_t launch_step(const SimParams& p, const EnvState& s, uint32_t k,
                        const uint8_t* act, float* obs_out, double* rew, uint64_t* rchk,
                        hipStream_t st) {
   const dim3 grid((p.E + 255) / 256), block(256);
   if (p.C <= 1)
-    hipLaunchKernelGGL(learned_k<1>, grid, block, 0, st, p, s, seed, k, act, obs_out, rew, rchk);
+    hipLaunchKernelGGL(learned_k<1>, grid, block, 0, st, p, s, k, act, obs_out, rew, rchk);
   else if (p.C <= 2)
-    hipLaunchKernelGGL(learned_k<2>, grid, block, 0, st, p, s, seed, k, act, obs_out, rew, rchk);
+    hipLaunchKernelGGL(learned_k<2>, grid, block, 0, st, p, s, k, act, obs_out, rew, rchk);
   else
-    hipLaunchKernelGGL(learned_k<4>, grid, block, 0, st, p, s, seed, k, act, obs_out, rew, rchk);
+    hipLaunchKernelGGL(learned_k<4>, grid, block, 0, st, p, s, k, act, obs_out, rew, rchk);
   return hipGetLastError();
 }
 
-hipError_t launch_static(const SimParams& p, const EnvState& s, uint64_t seed, uint32_t k,
+hipError_t launch_static(const SimParams& p, const EnvState& s, uint32_t k,
                          int nt, double* rew_sh, hipStream_t st) {
   if (nt < 1) return hipErrorInvalidValue;
-  if (p.C <= 1) launch_static_c<1>(p, s, seed, k, nt, rew_sh, st);
-  else if (p.C <= 2) launch_static_c<2>(p, s, seed, k, nt, rew_sh, st);
-  else launch_static_c<4>(p, s, seed, k, nt, rew_sh, st);
+  if (p.C <= 1) launch_static_c<1>(p, s, k, nt, rew_sh, st);
+  else if (p.C <= 2) launch_static_c<2>(p, s, k, nt, rew_sh, st);
+  else launch_static_c<4>(p, s, k, nt, rew_sh, st);
   return hipGetLastError();
 }
 

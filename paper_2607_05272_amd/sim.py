@@ -376,6 +376,16 @@ class Sim:
     def set_timing(self, on):
         L.check(self.lib.sim_set_timing(self._ctx, 1 if on else 0), "sim_set_timing")
 
+    def set_graphs(self, on):
+        """Rollout graphs on (default) or off (every rollout launched eagerly)."""
+        L.check(self.lib.sim_set_graphs(self._ctx, 1 if on else 0), "sim_set_graphs")
+
+    def graph_stats(self):
+        """(graphs captured, rollouts replayed from a graph)."""
+        c, r = C.c_int64(0), C.c_int64(0)
+        L.check(self.lib.sim_graph_stats(self._ctx, C.byref(c), C.byref(r)), "sim_graph_stats")
+        return c.value, r.value
+
     def get_timing(self, clear=True):
         """Per kernel class: (total ms, launches) from HIP events on the context's stream."""
         ms = (C.c_double * len(L.KERNEL_CLASSES))()
