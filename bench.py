@@ -215,74 +215,258 @@ def copy_ceiling(mib=1024, reps=5):
     return best
 
 
-def cpu_baseline_sim_only(w, name, budget_s, seed):
-    """The oracle's simulator alone (replayed uniform actions, no MLP) on the host cores."""
+def host_info():
+    """The host the CPU baseline runs on."""
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        aff = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        aff = os.cpu_count() or 1
+    return {"host_cpus": os.cpu_count(), "affinity_cpus": aff, "cpu_model": model}
+
+
+# worker threads of the CPU baseline: the host's CPUs available to this process, at most 16
+# (the host-CPU share of one GPU on the machines this runs on)
+MAX_CPU_THREADS = 16
+
+
+def sample_ids(n_envs, n, seed):
+    """Environment ids of a CPU-baseline sample: the first n/2 ids, then ids drawn without
+    replacement from the rest by numpy's Philox generator."""
+    import numpy as np
+    a = min(n // 2, n_envs)
+    rest = np.arange(a, n_envs)
+    k = min(n - a, rest.size)
+    pick = np.random.Generator(np.random.Philox(seed)).choice(rest, size=k, replace=False)
+    return np.sort(np.concatenate([np.arange(a), pick])).astype(np.uint32)
+
+
+def _threaded(fn, chunks):
+    th = [threading.Thread(target=fn, args=(c,)) for c in chunks]
+    t0 = time.perf_counter()
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(w, name, budget_s, seed, sim_only=False):
+    """The oracle on the host cores over a bounded sample of the same workload, env-steps per
+    second: the sequential fp64 simulator + fp64 policy + sampler, or (sim_only) the simulator
+    alone replaying uniform random actions. Run once on the worker threads and once, on a
+    proportionally smaller sample, on one thread."""
     import numpy as np
     import oracle
-    threads = max(1, min(16, os.cpu_count() or 1))
+    info = host_info()
+    threads = max(1, min(MAX_CPU_THREADS, info["affinity_cpus"]))
     T = min(w["T"], 256)
     A = 6 * w["n_servers"]
-    cal_ids = np.linspace(0, w["n_envs"] - 1, 16).astype(np.uint32)
-    cal_act = np.random.default_rng(seed).integers(0, A, (64, 16)).astype(np.uint8)
-    oracle.rollout(w, seed, 8, cal_ids, actions=cal_act[:8], want_obs=False, want_rec=False)
+    wts = None if sim_only else oracle.init_weights(w, seed)
+
+    def run(ids, n_ticks):
+        if sim_only:
+            acts = np.random.default_rng(seed).integers(0, A, (n_ticks, ids.size)).astype(np.uint8)
+            oracle.rollout(w, seed, n_ticks, ids, actions=acts, want_obs=False, want_rec=False)
+        else:
+            oracle.rollout(w, seed, n_ticks, ids, weights=wts, want_obs=False, want_rec=False)
+
+    cal = sample_ids(w["n_envs"], 8, seed)
+    run(cal[:2], 8)
     t0 = time.perf_counter()
-    oracle.rollout(w, seed, 64, cal_ids, actions=cal_act, want_obs=False, want_rec=False)
-    per_step = (time.perf_counter() - t0) / (64 * 16)
-    n_env = max(threads, int(budget_s * threads / (per_step * T)))
-    n_env = min(n_env, w["n_envs"])
-    ids = np.linspace(0, w["n_envs"] - 1, n_env).astype(np.uint32)
-    acts = np.random.default_rng(seed).integers(0, A, (T, n_env)).astype(np.uint8)
-    chunks = np.array_split(np.arange(n_env), threads)
+    run(cal, 32)
+    per_step = (time.perf_counter() - t0) / (32 * cal.size)
+    n_env = min(w["n_envs"], max(threads, int(budget_s * threads / (per_step * T))))
+    ids = sample_ids(w["n_envs"], n_env, seed)
+    dt = _threaded(lambda c: run(ids[c], T) if len(c) else None,
+                   np.array_split(np.arange(n_env), threads))
+    n1 = max(1, n_env // threads)
+    dt1 = _threaded(lambda c: run(ids[c], T), [np.arange(n1)])
+    what = ("simulator only (uniform random actions replayed)" if sim_only else
+            f"fp64 {'attention policy' if w.get('policy_kind', 0) == 1 else 'policy MLP'} + "
+            "sampler + simulator")
+    return dict({"value": n_env * T / dt, "unit": "env-steps/s", "cores": threads,
+                 "threads": threads, "kind": "oracle",
+                 "single_thread": {"value": n1 * T / dt1, "envs": int(n1), "wall_s": dt1},
+                 "sample": f"{n_env} envs (ids 0..{n_env // 2 - 1} and the rest drawn by a "
+                           f"Philox generator) x {T} ticks of {name}, {what}; {dt:.1f} s wall "
+                           f"on {threads} worker threads (the host's {info['affinity_cpus']} "
+                           f"available CPUs, at most {MAX_CPU_THREADS}); single thread: "
+                           f"{n1} envs"}, **info)
 
-    def work(c):
-        if len(c):
-            oracle.rollout(w, seed, T, ids[c], actions=np.ascontiguousarray(acts[:, c]),
-                           want_obs=False, want_rec=False)
 
+def kernel_table(timing, steps):
+    return {k: {"total_ms_per_step": ms / steps, "launches_per_step": n // steps,
+                "avg_us": 1000.0 * ms / n} for k, (ms, n) in timing.items() if n}
+
+
+def rooflines(w, kern, tot, E, T, train, args, cfg_name):
+    """Achieved work rate of each hot kernel class against its MI355X peak."""
+    rl = {}
+    if "policy" in kern and w.get("policy_kind", 0) == 1:
+        fl = attn_flops(w) * E
+        ach = fl / (kern["policy"]["avg_us"] * 1e-6) / 1e12
+        rl["policy"] = {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS,
+                        "unit": "TFLOP/s", "frac": ach / PEAK_FP32_VALU_TFLOPS,
+                        "traffic": traffic_for("policy", cfg_name), "work_per_launch": fl}
+    elif "policy" in kern:
+        fl = mlp_flops(w) * E
+        ach = fl / (kern["policy"]["avg_us"] * 1e-6) / 1e12
+        peak = PEAK_BF16_TFLOPS if w["mlp_bf16"] else PEAK_FP32_TFLOPS
+        rl["policy"] = {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+                        "frac": ach / peak, "traffic": traffic_for("policy", cfg_name),
+                        "work_per_launch": fl}
+    if "step" in kern:
+        by = step_bytes(w, tot, E, T) * E
+        ach = by / (kern["step"]["avg_us"] * 1e-6) / 1e9
+        rl["step"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                      "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("step", cfg_name),
+                      "work_per_launch": by}
+    if "static" in kern:
+        by = static_bytes(w, tot, E, T, T / kern["static"]["launches_per_step"]) * E
+        ach = by / (kern["static"]["avg_us"] * 1e-6) / 1e9
+        rl["static"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("static", cfg_name),
+                        "work_per_launch": by}
+    if "gae" in kern:
+        by = 28.0 * E * T
+        ach = by / (kern["gae"]["avg_us"] * 1e-6) / 1e9
+        rl["gae"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("gae", cfg_name),
+                     "work_per_launch": by}
+    if "ppo" in kern:
+        # minibatch gradients per step (one, or epochs x minibatches when training), each with
+        # its share of Adam; the MLP's products run on the matrix cores (bf16, or fp32 for an
+        # fp32 policy), the attention network's on the vector units
+        n_grad = args.epochs * args.minibatches if train else 1
+        if w.get("policy_kind", 0) == 1:
+            fl = 3 * attn_flops(w) * (w.get("ppo_minibatch", 0) or 8192) * n_grad
+            bound, peak = "alu", PEAK_FP32_VALU_TFLOPS
+        else:
+            fl = ppo_flops(dict(w, ppo_minibatch=w.get("ppo_minibatch", 0) or 8192)) * n_grad
+            bound, peak = "mfma", (PEAK_BF16_TFLOPS if w["mlp_bf16"] else PEAK_FP32_TFLOPS)
+        ach = fl / (kern["ppo"]["total_ms_per_step"] * 1e-3) / 1e12
+        rl["ppo"] = {"bound": bound, "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+                     "frac": ach / peak, "traffic": None, "work_per_launch": fl}
+    return rl
+
+
+def measure(name, args, steps, warmup, timing_steps, ticks=0):
+    """One configuration: `warmup` untimed steps, a graph-priming step, `steps` timed steps
+    (rollouts replayed from the captured graph, no per-launch events), then `timing_steps`
+    steps launched eagerly with HIP events around every launch for the kernels' durations."""
+    import torch
+    import paper_2607_05272_amd as bs
+    w = workload_of(name)
+    if ticks:
+        w["T"] = ticks
+    E, T, F = w["n_envs"], w["T"], w["obs_dim"]
+    dev = torch.device("cuda")
+    seed = 0x5EED0000 + (int(name[1]) if name[0] == "C" and name[1].isdigit() else 9)
+    sim = bs.Sim(w)
+    weights = sim.init_weights(seed)
+    ppo = w.get("ppo_minibatch", 0) > 0 and args.train == "none"
+    train = args.train != "none"
+    traj = bs.Trajectory(T, E, F, dev, value=bool(w["value_head"]), shadow=bool(w["shadow"]),
+                         obs=ppo or train)
+    st = {}
+    if train:
+        st["params"] = sim.params_from_weights(weights)
+        st["m"] = torch.zeros_like(st["params"])
+        st["v"] = torch.zeros_like(st["params"])
+        st["t"] = 0
+        st["mb"] = w.get("ppo_minibatch", 0) or 8192
+        st["algo"] = bs.ALGO_PPO if args.train == "ppo" else bs.ALGO_REINFORCE
+    grads = torch.empty(sim.ppo_grad_count(), dtype=torch.float32, device=dev) if ppo else None
+    ploss = torch.empty(4, dtype=torch.float64, device=dev) if ppo else None
+    adv = torch.empty((T, E), dtype=torch.float64, device=dev)
+    ret = torch.empty((T, E), dtype=torch.float64, device=dev)
+    gae = bool(w["value_head"])
+    lam = 1.0 if args.train == "reinforce" or not gae else w["lam"]
+
+    def one_step(i, ev=None):
+        if ev:
+            ev[0].record(sim.stream)
+        sim.reset(seed + i)
+        if ev:
+            ev[1].record(sim.stream)
+        sim.rollout(weights, T, traj=traj)
+        if ev:
+            ev[2].record(sim.stream)
+        sim.returns_gae(traj.reward, traj.value if gae else None, w["gamma"], lam, adv, ret)
+        if ppo:
+            sim.ppo_minibatch_grad(weights, traj.obs, traj.actions, traj.logp, adv, ret,
+                                   w["ppo_minibatch"], seed + i, grads=grads, loss=ploss)
+        if train:
+            st["t"], _ = sim.update(weights, st["params"], st["m"], st["v"], st["t"], traj.obs,
+                                    traj.actions, traj.logp, adv, ret, st["algo"], args.epochs,
+                                    args.minibatches, st["mb"], seed + i, 3e-4, want_losses=False)
+        if ev:
+            ev[3].record(sim.stream)
+        return sim.stats()
+
+    for i in range(warmup):
+        one_step(i)
+    one_step(warmup)           # captures the rollout's graph (it repeats the previous call)
+    sim.sync()
+    torch.cuda.synchronize()
+    marks = []
     t0 = time.perf_counter()
-    th = [threading.Thread(target=work, args=(c,)) for c in chunks]
-    for t in th:
-        t.start()
-    for t in th:
-        t.join()
-    dt = time.perf_counter() - t0
-    return {"value": n_env * T / dt, "unit": "env-steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n_env} envs x {T} ticks of {name}, simulator only (uniform random "
-                      f"actions replayed), {dt:.1f} s wall on {threads} threads"}
-
-
-def cpu_baseline(w, name, budget_s, seed):
-    """The oracle (sequential fp64 simulator + fp64 policy MLP + sampler) on the host
-    cores, over a bounded sample of the same workload, env-steps per second."""
-    import numpy as np
-    import oracle
-    wts = oracle.init_weights(w, seed)
-    threads = max(1, min(16, os.cpu_count() or 1))
-    T = min(w["T"], 256)
-    # calibrate on one env
-    t0 = time.perf_counter()
-    oracle.rollout(w, seed, 32, [0], weights=wts, want_obs=False, want_rec=False)
-    per_step = (time.perf_counter() - t0) / 32
-    n_env = max(threads, int(budget_s * threads / (per_step * T)))
-    n_env = min(n_env, w["n_envs"])
-    ids = np.linspace(0, w["n_envs"] - 1, n_env).astype(np.uint32)
-    chunks = np.array_split(ids, threads)
-
-    def work(c):
-        if len(c):
-            oracle.rollout(w, seed, T, c, weights=wts, want_obs=False, want_rec=False)
-
-    t0 = time.perf_counter()
-    th = [threading.Thread(target=work, args=(c,)) for c in chunks]
-    for t in th:
-        t.start()
-    for t in th:
-        t.join()
-    dt = time.perf_counter() - t0
-    return {"value": n_env * T / dt, "unit": "env-steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n_env} envs (evenly spaced ids) x {T} ticks of {name}, fp64 "
-                      f"{'attention policy' if w.get('policy_kind', 0) == 1 else 'policy MLP'} + "
-                      f"sampler + simulator, {dt:.1f} s wall on {threads} threads"}
+    tot = None
+    for i in range(steps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        marks.append(ev)
+        tot = one_step(1000 + i, ev)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    sim.sync()
+    captures, replays = sim.graph_stats()
+    ms_per_step = (t1 - t0) * 1000.0 / steps
+    step_ms = [ev[0].elapsed_time(ev[3]) for ev in marks]
+    rollout_ms = [ev[1].elapsed_time(ev[2]) for ev in marks]
+    # kernel durations: eager launches bracketed by HIP events on the library's stream
+    sim.get_timing(clear=True)
+    sim.set_timing(True)
+    t2 = time.perf_counter()
+    for i in range(timing_steps):
+        one_step(2000 + i)
+    sim.sync()
+    t3 = time.perf_counter()
+    timing = sim.get_timing(clear=True)
+    sim.set_timing(False)
+    kern = kernel_table(timing, timing_steps)
+    rl = rooflines(w, kern, tot, E, T, train, args, name)
+    kernel_ms = sum(v["total_ms_per_step"] for v in kern.values())
+    res = {
+        "workload": (DESCR[name] if not ticks else DESCR[name] + f" [T={T}]")
+        + ("" if not train else f"; + {args.train} update, {args.epochs} epochs x "
+           f"{args.minibatches} minibatches of {st['mb']} samples, Adam"),
+        "envs": E, "ticks": T, "env_steps_per_step": E * T,
+        "value": E * T / (ms_per_step / 1000.0), "ms_per_step": ms_per_step,
+        "step_ms": {"median": statistics.median(step_ms), "min": min(step_ms),
+                    "max": max(step_ms)},
+        "rollout_only": {"median_ms": statistics.median(rollout_ms),
+                         "env_steps_per_s": E * T / (statistics.median(rollout_ms) / 1000.0)},
+        "graph": {"captures": captures, "replays": replays},
+        "eager_timed_ms_per_step": (t3 - t2) * 1000.0 / max(timing_steps, 1),
+        "kernel_ms_per_step": kernel_ms,
+        "launch_gap_frac": max(0.0, 1.0 - kernel_ms / ms_per_step),
+        "kernels": {k: dict(v, **{kk: vv for kk, vv in rl.get(k, {}).items()
+                                  if kk in ("achieved", "unit", "frac")}) for k, v in kern.items()},
+        "totals": {"arrivals": int(tot["cnt"][0][0]), "dropped": int(tot["cnt"][0][2]),
+                   "dispatched": int(tot["cnt"][0][3]), "batches": int(tot["cnt"][0][4])},
+    }
+    sim.close()
+    del traj, adv, ret, grads
+    torch.cuda.empty_cache()
+    return w, res, rl, kern
 
 
 def main():
@@ -293,12 +477,16 @@ def main():
     ap.add_argument("--config", default="C5", choices=sorted(DESCR))
     ap.add_argument("--ticks", type=int, default=0, help="override T (diagnostics only)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--timing-steps", type=int, default=2,
+                    help="eager steps with per-launch HIP events for the kernels' durations")
     ap.add_argument("--train", default="none", choices=("none", "ppo", "reinforce"),
                     help="add the policy update (epochs x minibatches of gradient + Adam over "
                          "the stored trajectory) to every step")
     ap.add_argument("--epochs", type=int, default=4)
     ap.add_argument("--minibatches", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the sub-measurements of C1-C4 that follow the headline line's")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="only copy this many MiB device-to-device (HBM counter calibration)")
     ap.add_argument("--write-traffic", default="",
@@ -325,168 +513,50 @@ def main():
               "path would shard by environment, but only the one-GPU path is built). Use --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
-    import torch
-    import paper_2607_05272_amd as bs
-    w = workload_of(args.config)
-    if args.ticks:
-        w["T"] = args.ticks
-    E, T, F = w["n_envs"], w["T"], w["obs_dim"]
-    dev = torch.device("cuda")
-    seed = 0x5EED0000 + (int(args.config[1]) if args.config[0] == "C" else 9)
-    sim = bs.Sim(w)
-    weights = sim.init_weights(seed)
-    ppo = w.get("ppo_minibatch", 0) > 0 and args.train == "none"
-    train = args.train != "none"
-    traj = bs.Trajectory(T, E, F, dev, value=bool(w["value_head"]), shadow=bool(w["shadow"]),
-                         obs=ppo or train)
-    if train:
-        params = sim.params_from_weights(weights)
-        adam_m = torch.zeros_like(params)
-        adam_v = torch.zeros_like(params)
-        adam_t = [0]
-        mb = w.get("ppo_minibatch", 0) or 8192
-        algo = bs.ALGO_PPO if args.train == "ppo" else bs.ALGO_REINFORCE
-    grads = torch.empty(sim.ppo_grad_count(), dtype=torch.float32, device=dev) if ppo else None
-    ploss = torch.empty(4, dtype=torch.float64, device=dev) if ppo else None
-    adv = torch.empty((T, E), dtype=torch.float64, device=dev)
-    ret = torch.empty((T, E), dtype=torch.float64, device=dev)
-    gae = bool(w["value_head"])
-    lam = w["lam"] if gae else 1.0
-    if args.train == "reinforce":
-        lam = 1.0  # A = G - V, R = G
-
-    marks = []   # per timed step: events before reset, around the rollout, at the end
-
-    def one_step(i, ev=None):
-        if ev:
-            ev[0].record(sim.stream)
-        sim.reset(seed + i)
-        if ev:
-            ev[1].record(sim.stream)
-        sim.rollout(weights, T, traj=traj)
-        if ev:
-            ev[2].record(sim.stream)
-        sim.returns_gae(traj.reward, traj.value if gae else None, w["gamma"], lam, adv, ret)
-        if ppo:
-            sim.ppo_minibatch_grad(weights, traj.obs, traj.actions, traj.logp, adv, ret,
-                                   w["ppo_minibatch"], seed + i, grads=grads, loss=ploss)
-        if train:
-            adam_t[0], _ = sim.update(weights, params, adam_m, adam_v, adam_t[0], traj.obs,
-                                      traj.actions, traj.logp, adv, ret, algo, args.epochs,
-                                      args.minibatches, mb, seed + i, 3e-4, want_losses=False)
-        if ev:
-            ev[3].record(sim.stream)
-        return sim.stats()
-
-    for i in range(args.warmup):
-        one_step(i)
-    sim.sync()
-    torch.cuda.synchronize()
-    sim.get_timing(clear=True)
-    sim.set_timing(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    tot = None
-    for i in range(args.steps):
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-        marks.append(ev)
-        tot = one_step(1000 + i, ev)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    step_ms = [ev[0].elapsed_time(ev[3]) for ev in marks]
-    rollout_ms = [ev[1].elapsed_time(ev[2]) for ev in marks]
-    sim.sync()
-    timing = sim.get_timing(clear=True)
-    sim.set_timing(False)
-    ms_per_step = (t1 - t0) * 1000.0 / args.steps
-    value = E * T / (ms_per_step / 1000.0)
-
-    kern = {}
-    for k, (ms, n) in timing.items():
-        if n:
-            kern[k] = {"total_ms_per_step": ms / args.steps, "launches_per_step": n // args.steps,
-                       "avg_us": 1000.0 * ms / n}
-    # roofline of each hot kernel class
-    rl = {}
-    if "policy" in kern and w.get("policy_kind", 0) == 1:
-        fl = attn_flops(w) * E
-        ach = fl / (kern["policy"]["avg_us"] * 1e-6) / 1e12
-        rl["policy"] = {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS,
-                        "unit": "TFLOP/s", "frac": ach / PEAK_FP32_VALU_TFLOPS,
-                        "traffic": traffic_for("policy", args.config), "work_per_launch": fl}
-    elif "policy" in kern:
-        fl = mlp_flops(w) * E
-        ach = fl / (kern["policy"]["avg_us"] * 1e-6) / 1e12
-        peak = PEAK_BF16_TFLOPS if w["mlp_bf16"] else PEAK_FP32_TFLOPS
-        rl["policy"] = {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
-                        "frac": ach / peak, "traffic": traffic_for("policy", args.config),
-                        "work_per_launch": fl}
-    if "step" in kern:
-        by = step_bytes(w, tot, E, T) * E
-        ach = by / (kern["step"]["avg_us"] * 1e-6) / 1e9
-        rl["step"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                      "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("step", args.config),
-                      "work_per_launch": by}
-    if "static" in kern:
-        by = static_bytes(w, tot, E, T, T / kern["static"]["launches_per_step"]) * E
-        ach = by / (kern["static"]["avg_us"] * 1e-6) / 1e9
-        rl["static"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                        "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("static", args.config),
-                        "work_per_launch": by}
-    if "gae" in kern:
-        by = 28.0 * E * T
-        ach = by / (kern["gae"]["avg_us"] * 1e-6) / 1e9
-        rl["gae"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("gae", args.config),
-                     "work_per_launch": by}
-    if "ppo" in kern:
-        # minibatch gradients per step (one, or epochs x minibatches when training), each
-        # with its share of Adam
-        n_grad = args.epochs * args.minibatches if train else 1
-        if w.get("policy_kind", 0) == 1:
-            # forward and backward of the attention network: about three forwards per sample
-            fl = 3 * attn_flops(w) * (w.get("ppo_minibatch", 0) or 8192) * n_grad
-        else:
-            fl = ppo_flops(dict(w, ppo_minibatch=w.get("ppo_minibatch", 0) or 8192)) * n_grad
-        ach = fl / (kern["ppo"]["total_ms_per_step"] * 1e-3) / 1e12
-        rl["ppo"] = {"bound": "alu", "achieved": ach, "peak": PEAK_FP32_VALU_TFLOPS,
-                     "unit": "TFLOP/s", "frac": ach / PEAK_FP32_VALU_TFLOPS,
-                     "traffic": traffic_for("ppo", args.config), "work_per_launch": fl}
+    w, res, rl, kern = measure(args.config, args, args.steps, args.warmup, args.timing_steps,
+                               args.ticks)
     dom = max(kern, key=lambda k: kern[k]["total_ms_per_step"])
     roof = dict(rl.get(dom, {}))
     roof["kernel"] = dom
     work = roof.pop("work_per_launch", None)
-
+    # the simulator kernels together against HBM (algorithmic bytes over their time)
+    sim_by = sum(rl[k]["work_per_launch"] * kern[k]["launches_per_step"] for k in ("step", "static")
+                 if k in rl)
+    sim_ms = sum(kern[k]["total_ms_per_step"] for k in ("step", "static") if k in kern)
     line = {
         "metric": "simulated env-steps/sec on 1 MI355X + % of HBM roofline (MLP: % MFMA peak)",
-        "value": value, "unit": "env-steps/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "value": res["value"], "unit": "env-steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": res["ms_per_step"], "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None,
         "dtype": "f64 simulator + bf16 MLP (fp32 accumulate)" if w["mlp_bf16"] else "f64 simulator + f32 MLP",
         "data": "synthetic (seeded workload generator; untrained Xavier policy)",
-        "config": {"workload": (DESCR[args.config] if not args.ticks else DESCR[args.config] + f" [T={T}]")
-                   + ("" if not train else f"; + {args.train} update, {args.epochs} epochs x "
-                      f"{args.minibatches} minibatches of {mb} samples, Adam"),
-                   "envs": E, "ticks": T, "env_steps_per_step": E * T},
+        "config": {"workload": res["workload"], "envs": res["envs"], "ticks": res["ticks"],
+                   "env_steps_per_step": res["env_steps_per_step"]},
         "roofline": roof,
-        "kernels": {k: dict(v, **{kk: vv for kk, vv in rl.get(k, {}).items()
-                                  if kk in ("achieved", "unit", "frac")}) for k, v in kern.items()},
+        "simulator_hbm": ({"achieved": sim_by / (sim_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS,
+                           "unit": "GB/s", "frac": sim_by / (sim_ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                           "kernels": [k for k in ("step", "static") if k in kern]}
+                          if sim_ms > 0 else None),
         "work_per_launch": work,
-        "totals": {"arrivals": int(tot["cnt"][0][0]), "dropped": int(tot["cnt"][0][2]),
-                   "dispatched": int(tot["cnt"][0][3]), "batches": int(tot["cnt"][0][4])},
-        # per-step event times on the library's stream: the median step, and the rollout
-        # alone (policy + sampling + simulator; reset and returns reported apart)
-        "step_ms": {"median": statistics.median(step_ms), "min": min(step_ms),
-                    "max": max(step_ms)},
-        "rollout_only": {"median_ms": statistics.median(rollout_ms),
-                         "env_steps_per_s": E * T / (statistics.median(rollout_ms) / 1000.0)},
-        "hbm_copy_ceiling_GBs": copy_ceiling(),
+        "graph_priming_steps": 1,
     }
+    for k in ("step_ms", "rollout_only", "graph", "eager_timed_ms_per_step", "kernel_ms_per_step",
+              "launch_gap_frac", "kernels", "totals"):
+        line[k] = res[k]
+    line["hbm_copy_ceiling_GBs"] = copy_ceiling()
+    if not args.no_other_configs and args.config == "C5" and not args.ticks and args.train == "none":
+        # every other configuration, measured the same way (fewer steps)
+        line["configs"] = {}
+        for name in ("C1", "C2", "C3", "C4"):
+            _, r2, rl2, _ = measure(name, args, 3, 1, 2)
+            r2["roofline"] = {k: {kk: v[kk] for kk in ("bound", "achieved", "peak", "unit", "frac")}
+                              for k, v in rl2.items()}
+            line["configs"][name] = r2
     if not args.no_cpu_baseline:
+        seed = 0x5EED0000 + (int(args.config[1]) if args.config[0] == "C" and args.config[1].isdigit() else 9)
         line["cpu_baseline"] = cpu_baseline(w, args.config, args.cpu_seconds, seed)
-        line["cpu_baseline_sim_only"] = cpu_baseline_sim_only(w, args.config,
-                                                              args.cpu_seconds / 3, seed)
-    sim.close()
+        line["cpu_baseline_sim_only"] = cpu_baseline(w, args.config, args.cpu_seconds / 3, seed,
+                                                     sim_only=True)
     print(json.dumps(line), flush=True)
 
 
