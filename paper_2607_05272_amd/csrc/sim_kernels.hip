@@ -199,8 +199,8 @@ template <int KS>
 struct Stage {
   double E[KS][64];
   uint8_t cls[KS][64];
-  uint32_t owner[64];
-  uint32_t j0[64];
+  uint32_t owner_j0[64];  // needing lane | first block << 6 (blocks per tick < 2^18)
+  uint32_t tick[64];
 };
 
 __device__ __forceinline__ void wave_sync_lds() {
@@ -209,15 +209,16 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Called by all 64 lanes of the wave. Lanes with `need` get blocks [jneed, jneed + n) with
-// n = KS when the arrival process can burst (`burst`: some state's rate exceeds KS / 4
-// arrivals per tick) or one of the lanes was already refilled in this tick, else KS / 2: at
-// low arrival rates most lanes need one or two blocks per tick, and the work of a pass is n
-// times the number of lanes served.
-// fill(owner lane, j) computes one block into the stage.
+// Called by all 64 lanes of the wave. Lanes with `need` get blocks [jneed, jneed + n) of
+// their tick k with n = KS when the arrival process can burst (`burst`: some state's rate
+// exceeds KS / 4 arrivals per tick) or one of the lanes was already refilled in its tick,
+// else KS / 2: at low arrival rates most lanes need one or two blocks per tick, and the work
+// of a pass is n times the number of lanes served. The lanes may be at different ticks.
+// fill(owner lane, tick, j) computes one block into the stage.
 template <int KS, class Fill>
 __device__ __forceinline__ void wave_refill(Stage<KS>& st, bool need, bool burst, uint32_t jneed,
-                                            uint32_t& staged_hi, int lane, Fill&& fill) {
+                                            uint32_t k, uint32_t& staged_hi, int lane,
+                                            Fill&& fill) {
   const uint64_t mask = __ballot(need);
   const int nneed = __popcll(mask);
   static_assert(KS >= 4 && (KS & (KS - 1)) == 0, "stage size is a power of two");
@@ -226,13 +227,14 @@ __device__ __forceinline__ void wave_refill(Stage<KS>& st, bool need, bool burst
   const int n = 1 << lg;
   if (need) {
     const int rank = __popcll(mask & ((1ull << lane) - 1ull));
-    st.owner[rank] = (uint32_t)lane;
-    st.j0[rank] = jneed;
+    st.owner_j0[rank] = (uint32_t)lane | (jneed << 6);
+    st.tick[rank] = k;
   }
   wave_sync_lds();
   for (int w = lane; w < n * nneed; w += 64) {
     const int r = w >> lg;
-    fill(st.owner[r], st.j0[r] + (uint32_t)(w & (n - 1)));
+    const uint32_t oj = st.owner_j0[r];
+    fill(oj & 63u, st.tick[r], (oj >> 6) + (uint32_t)(w & (n - 1)));
   }
   wave_sync_lds();
   if (need) staged_hi = jneed + (uint32_t)n;
@@ -246,8 +248,9 @@ __device__ __forceinline__ void refill_arrivals(Stage<KS>& st, const SimParams& 
 #pragma unroll
   for (int s = 0; s < kMaxS; ++s)
     if (s < p.S && p.rate[s] * p.dt * 4.0 > (double)KS) burst = true;
-  wave_refill<KS>(st, need, burst, jneed, staged_hi, lane, [&](uint32_t own, uint32_t j) {
-    const u32x4 d = draw(seed, (uint32_t)(e_lane0 + (int)own), k, P_ARRIVAL, j, 0);
+  wave_refill<KS>(st, need, burst, jneed, k, staged_hi, lane, [&](uint32_t own, uint32_t kk,
+                                                                   uint32_t j) {
+    const u32x4 d = draw(seed, (uint32_t)(e_lane0 + (int)own), kk, P_ARRIVAL, j, 0);
     st.E[j % KS][own] = -dlog(unit(d.x, d.y));
     const double uc = unit(d.z, d.w);
     int cls = CM - 1;
@@ -749,46 +752,81 @@ __device__ __forceinline__ void sq_scan(BusyTimes<KM>& busy, ServerBytes& infl, 
   }
 }
 
-// One tick [t_k, t_{k+1}) of the static system of one environment whose state is held in
-// registers: arrivals, the static rule's dispatches to the routed server, completions, and
-// the tick's reward (into rew_row[e] when given). A dispatch stores its server's meta word at
-// once; a completion clears the in-flight byte only in registers and marks the server in
-// `clear`, and `dirty` marks servers whose busy-until time changed; the caller writes both
-// back. Lanes without an environment (live = false) take part in the wave's ballots only.
-// With SQ (Shortest-Queue routing) the idle mask holds the servers with a free slot instead,
-// and completions are retired at every scan (sq_scan).
+// Ticks k0 .. k0 + nt - 1 of the static system of one environment whose state is held in
+// registers: per tick, arrivals, the static rule's dispatches to the routed server,
+// completions, and the tick's reward (into rew [nt][E] when given).
+//
+// Each lane runs through its own ticks, in one of four modes:
+//   EVT    it takes its next event (switch, arrival, completion or timeout instant) in the
+//          tick, or finds that none is left (-> READY);
+//   PEND   the static rule has a batch to dispatch at the lane's current instant;
+//   READY  its tick has no event left and waits to be closed;
+//   OFF    all nt ticks are done (or the lane has no environment).
+// The wave takes every lane's events one at a time, but serves dispatches and tick closes in
+// passes shared by many lanes: a dispatch (service draw, batch pop over the request ring,
+// checksum) and a close (a walk over every server) cost the wave the same whether one lane or
+// forty take them; so does a refill of the arrival stage (wave_refill). A pending lane waits
+// until a quarter of the wave's active lanes are pending too, or no lane has an event to take;
+// a lane that needs arrival draws staged waits until a quarter of the active lanes do, or no
+// lane takes an event; lanes whose tick is over wait until half of the active lanes are.
+// Waiting changes no result: a lane's state is frozen while it waits, and each lane still
+// processes its own events, dispatches and closes in the order of its timeline.
+// The event counts of bursty environments differ widely from tick to tick; stepping the lanes
+// tick by tick would take, at every tick, as many passes as the busiest lane.
+//
+// A dispatch stores its server's meta word at once; a completion clears the in-flight byte
+// only in registers and marks the server in `clear`, and `dirty` marks servers whose
+// busy-until time changed; the caller writes both back. With SQ (Shortest-Queue routing) the
+// idle mask holds the servers with a free slot instead, and completions are retired at every
+// scan (sq_scan).
+// shares of the wave's active lanes that trigger a dispatch pass, a close pass and a refill
+// pass (1 / share of the lanes; measured at C5 and on the baseline workloads)
+constexpr int kDispatchShare = 4, kCloseShare = 2, kRefillShare = 4;
 template <int KM, int CM, bool SQ>
-__device__ __forceinline__ void static_tick(const SimParams& p, const SysState& G, uint32_t* err,
-                                            uint64_t seed, uint32_t k, bool live, int e, int ee,
-                                            int e_lane0, int lane, Stage<kStageStatic>& st,
-                                            Queue<CM>& Q,
-                                            Count& C, Arrivals& A, BusyTimes<KM>& busy,
-                                            ServerBytes& infl, SqState<KM>& sq, uint32_t& dirty,
-                                            uint32_t& clear, uint32_t& rr,
-                                            double* __restrict__ rew_row) {
+__device__ __forceinline__ void static_run(const SimParams& p, const SysState& G, uint32_t* err,
+                                           uint64_t seed, uint32_t k0, int nt, bool live, int e,
+                                           int ee, int e_lane0, int lane, Stage<kStageStatic>& st,
+                                           Queue<CM>& Q, Count& C, Arrivals& A,
+                                           BusyTimes<KM>& busy, ServerBytes& infl,
+                                           SqState<KM>& sq, uint32_t& dirty, uint32_t& clear,
+                                           uint32_t& rr, double* __restrict__ rew) {
+  enum { OFF = 0, EVT = 1, PEND = 2, READY = 3 };
   const size_t E = (size_t)p.E;
-  C.n_k = 0;
-  C.Lw = 0.0;
-  C.jsvc = 0;
-  A.jarr = 0;
-  A.jproc = 0;
-  uint32_t jroute = 0;
-  const double t0 = (double)k * p.dt, t1 = (double)(k + 1) * p.dt;
+  // the lane's current tick: index i in the launch, k = k0 + i, interval [t0, t1)
+  int i = 0;
+  uint32_t k = k0;
+  double t0 = 0.0, t1 = 0.0, now = 0.0, next_done = kInf;
+  uint32_t idle = 0u, jroute = 0u, staged_hi = 0u, it = 0u;
   int A_k = 0;
-  double now = t0;
-  uint32_t idle;
-  double next_done;
-  if constexpr (SQ) sq_scan(busy, infl, sq, p.K, now, C.c[C_DONE], idle, next_done);
-  else server_scan(busy, p.K, now, idle, next_done);
-  uint32_t staged_hi = 0;
-  bool done = !live;
-  uint32_t it = 0;
-  bool first = true;
+  int mode = OFF;
+  // the static rule's condition at `now`: a server (slot) free, and B requests of the head-of-
+  // line class waiting or its head waiting for T
+  auto due = [&]() -> bool {
+    if (idle == 0u || Q.qsum <= 0) return false;
+    return Q.q(Q.hh) >= p.bmax || now >= Q.hts_h + p.static_timeout;
+  };
+  auto begin_tick = [&]() {
+    C.n_k = 0;
+    C.Lw = 0.0;
+    C.jsvc = 0;
+    A.jarr = 0;
+    A.jproc = 0;
+    jroute = 0;
+    A_k = 0;
+    staged_hi = 0;
+    it = 0;
+    t0 = (double)k * p.dt;
+    t1 = (double)(k + 1) * p.dt;
+    now = t0;
+    if constexpr (SQ) sq_scan(busy, infl, sq, p.K, now, C.c[C_DONE], idle, next_done);
+    else server_scan(busy, p.K, now, idle, next_done);
+    mode = due() ? PEND : EVT;
+  };
+  if (live && nt > 0) begin_tick();
   for (;;) {
-    bool go = false;
-    bool need = false;
+    bool go = false, need = false;
     double te = now;
-    if (!done && !first) {
+    if (mode == EVT) {
       te = A.next_sw < A.next_arr ? A.next_sw : A.next_arr;
       if (next_done < te) te = next_done;
       if (Q.qsum > 0 && idle != 0u) {
@@ -796,17 +834,19 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
         if (tout > now && tout < te) te = tout;
       }
       if (!(te < t1)) {
-        done = true;
+        mode = READY;
       } else if (it > kMaxEventsPerTick) {
         atomicOr(err, ERR_EVENTS);
-        done = true;
+        mode = READY;
       } else {
         need = p.arrival_kind != 1 && (A.next_sw == te || A.next_arr == te) &&
                A.jarr + 2u > staged_hi;
         go = !need;
       }
     }
-    if (__ballot(need) != 0ull)
+    const uint64_t need_m = __ballot(need);
+    if (need_m != 0ull && (kRefillShare * __popcll(need_m) >= __popcll(__ballot(mode != OFF)) ||
+                           __ballot(go) == 0ull))
       refill_arrivals<CM>(st, p, need, A.jarr, staged_hi, seed, e_lane0, k, lane);
     if (go) {
       ++it;
@@ -820,43 +860,44 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
         ++A_k;
         enqueue(Q, C, p, cls, now);
       }
+      if (due()) mode = PEND;
     }
-    if (go || (first && !done)) {
-      // min(B, Q_h) of the HoL class if Q_h >= B or its head waited T, to the routed server
-      while (idle != 0u && Q.qsum > 0) {
-        const int h = Q.hh;
-        const int qh = Q.q(h);
-        if (!(qh >= p.bmax || now >= Q.hts_h + p.static_timeout)) break;
-        const int n = qh < p.bmax ? qh : p.bmax;
-        if constexpr (SQ) {
-          // the server with the fewest requests assigned among those with a free slot (nothing
-          // queued: the load is its running batch), ties to the lower index; the batch starts
-          // when that server has finished its running batch
-          int j = -1;
-          uint32_t best = 0u;
+    const int n_act = __popcll(__ballot(mode != OFF));
+    const int n_pend = __popcll(__ballot(mode == PEND));
+    const int n_work = __popcll(__ballot(mode == EVT));
+    if (n_pend > 0 && (kDispatchShare * n_pend >= n_act || n_work == 0) && mode == PEND) {
+      // one batch: min(B, Q_h) requests of the head-of-line class to the routed server
+      const int h = Q.hh;
+      const int qh = Q.q(h);
+      const int n = qh < p.bmax ? qh : p.bmax;
+      if constexpr (SQ) {
+        // the server with the fewest requests assigned among those with a free slot (nothing
+        // queued: the load is its running batch), ties to the lower index; the batch starts
+        // when that server has finished its running batch
+        int j = -1;
+        uint32_t best = 0u;
 #pragma unroll
-          for (int jj = 0; jj < KM; ++jj) {
-            const uint32_t L = infl.get(jj);
-            if (jj < p.K && ((idle >> jj) & 1u) && (j < 0 || L < best)) {
-              j = jj;
-              best = L;
-            }
+        for (int jj = 0; jj < KM; ++jj) {
+          const uint32_t L = infl.get(jj);
+          if (jj < p.K && ((idle >> jj) & 1u) && (j < 0 || L < best)) {
+            j = jj;
+            best = L;
           }
-          const uint32_t n1 = infl.get(j);
-          const double start = n1 > 0u ? busy.get(j) : now;
-          const double sv = service<CM>(C, p, seed, ee, k, 1, h, n);
-          const double cdone = pop_batch(Q, C, p, k, j, h, n, start, sv);
-          if (n1 == 0u) {
-            busy.set(j, cdone);
-            infl.set(j, (uint32_t)n);
-            if (cdone > now && cdone < next_done) next_done = cdone;
-          } else {
-            put<KM>(sq.c2, j, cdone);
-            sq.n2.set(j, (uint32_t)n);
-            idle &= ~(1u << j);
-          }
-          continue;
         }
+        const uint32_t n1 = infl.get(j);
+        const double start = n1 > 0u ? busy.get(j) : now;
+        const double sv = service<CM>(C, p, seed, ee, k, 1, h, n);
+        const double cdone = pop_batch(Q, C, p, k, j, h, n, start, sv);
+        if (n1 == 0u) {
+          busy.set(j, cdone);
+          infl.set(j, (uint32_t)n);
+          if (cdone > now && cdone < next_done) next_done = cdone;
+        } else {
+          put<KM>(sq.c2, j, cdone);
+          sq.n2.set(j, (uint32_t)n);
+          idle &= ~(1u << j);
+        }
+      } else {
         const int j = route_pick(idle, p.route, rr, seed, ee, k, jroute);
         if (p.route == 2) rr = (uint32_t)((j + 1) % p.K);
         C.c[C_DONE] += infl.get(j);  // the previous batch on j finished at busy_j <= now
@@ -871,49 +912,55 @@ __device__ __forceinline__ void static_tick(const SimParams& p, const SysState& 
           if (cdone < next_done) next_done = cdone;
         }
       }
+      if (!due()) mode = EVT;
     }
-    first = false;
-    if (__ballot(!done) == 0ull) break;
-  }
-  if (!live) return;
-  // completions before t1
-  if constexpr (SQ) {
+    const int n_ready = __popcll(__ballot(mode == READY));
+    if (kCloseShare * n_ready >= n_act && mode == READY) {
+      // completions before t1, the tick's reward, then the lane's next tick
+      if constexpr (SQ) {
 #pragma unroll
-    for (int j = 0; j < KM; ++j) {
-      if (j < p.K) {
-        uint32_t n1 = infl.get(j);
-        if (n1 > 0 && busy.get(j) < t1) {
-          C.c[C_DONE] += n1;
-          n1 = sq.n2.get(j);
-          if (n1 > 0) busy.set(j, sq.c2[j]);
-          sq.n2.set(j, 0u);
-          if (n1 > 0 && busy.get(j) < t1) {
-            C.c[C_DONE] += n1;
-            n1 = 0;
+        for (int j = 0; j < KM; ++j) {
+          if (j < p.K) {
+            uint32_t n1 = infl.get(j);
+            if (n1 > 0 && busy.get(j) < t1) {
+              C.c[C_DONE] += n1;
+              n1 = sq.n2.get(j);
+              if (n1 > 0) busy.set(j, sq.c2[j]);
+              sq.n2.set(j, 0u);
+              if (n1 > 0 && busy.get(j) < t1) {
+                C.c[C_DONE] += n1;
+                n1 = 0;
+              }
+              infl.set(j, n1);
+            }
           }
-          infl.set(j, n1);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+          const uint32_t n = infl.get(j);
+          if (j < p.K && n > 0 && busy.get(j) < t1) {
+            C.c[C_DONE] += n;
+            clear |= 1u << j;
+            infl.set(j, 0u);
+          }
         }
       }
+      const double r = close_tick(Q, C, p, A.proc, A_k);
+      if (rew) rew[(size_t)i * E + e] = r;
+      ++i;
+      ++k;
+      if (i < nt) begin_tick();
+      else mode = OFF;
     }
-  } else {
-#pragma unroll
-    for (int j = 0; j < KM; ++j) {
-      const uint32_t n = infl.get(j);
-      if (j < p.K && n > 0 && busy.get(j) < t1) {
-        C.c[C_DONE] += n;
-        clear |= 1u << j;
-        infl.set(j, 0u);
-      }
-    }
+    if (__ballot(mode != OFF) == 0ull) break;
   }
-  const double r = close_tick(Q, C, p, A.proc, A_k);
-  if (rew_row) rew_row[e] = r;
 }
 
 // Ticks k0 .. k0 + nt - 1 of the static shadow system. The static rule never looks at the
 // learned system, so one launch may cover many ticks: the state is loaded once, kept in
-// registers from tick to tick, and stored once; each wave advances at its own pace instead of
-// waiting at every tick for the slowest wave of the grid. rew [nt][E] (optional) receives the
+// registers from tick to tick, and stored once; each lane advances at its own pace instead of
+// waiting at every tick for the slowest lane of its wave. rew [nt][E] (optional) receives the
 // rewards; nt = 1 is the per-tick kernel of the step interface.
 template <int KM, int CM, bool SQ>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void static_k(
@@ -957,10 +1004,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   }
   uint32_t dirty = 0, clear = 0;
   uint32_t rr = p.route == 2 ? G.rr[ee] : 0u;
-  for (int i = 0; i < nt; ++i)
-    static_tick<KM, CM, SQ>(p, G, g.err, seed, k0 + (uint32_t)i, live, e, ee, e_lane0, lane, st,
-                            Q, C, A, busy, infl, sq, dirty, clear, rr,
-                            rew ? rew + (size_t)i * E : nullptr);
+  static_run<KM, CM, SQ>(p, G, g.err, seed, k0, nt, live, e, ee, e_lane0, lane, st, Q, C, A,
+                         busy, infl, sq, dirty, clear, rr, rew);
   if (!live) return;
   if constexpr (SQ) {
     // every server's running and queued batch: completion times and the meta word (running
