@@ -429,6 +429,8 @@ __device__ __forceinline__ void put_obs(float* obs, size_t E, int i, int e, doub
 }
 
 // ---- learned system: one tick ---------------------------------------------------------------
+// share of the wave's lanes still in the tick that triggers a dispatch pass (1 / share)
+constexpr int kLearnedDispatchShare = 4;
 template <int CM>
 __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32_t k, const uint8_t* __restrict__ act,
                                                  float* __restrict__ obs_out,
@@ -468,14 +470,22 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32
   int A_k = 0;
   double now = t0;
   uint32_t staged_hi = 0;
-  bool done = !live;
   uint32_t it = 0;
-  bool first = true;
+  // the action's rule at `now`: exactly b requests of the head-of-line class whenever
+  // server s is idle
+  auto due = [&]() -> bool { return busy_s <= now && Q.qsum > 0 && Q.q(Q.hh) >= b; };
+  // done: no event left in the tick; pend: a batch to dispatch at `now`. As in the static
+  // system's kernel, dispatches are served in passes shared by many lanes: a lane with a batch
+  // due waits (its state frozen) until a quarter of the wave's lanes still in the tick have one
+  // too, or no lane can take an event. (Arrival refills are not held back here: within one
+  // tick a waiting lane lengthens the tick of the whole wave.)
+  bool done = !live;
+  bool pend = !done && due();
   for (;;) {
     bool go = false;
     bool need = false;
     double te = now;
-    if (!done && !first) {
+    if (!done && !pend) {
       te = A.next_sw < A.next_arr ? A.next_sw : A.next_arr;
       if (busy_s > now && busy_s < te) te = busy_s;
       if (!(te < t1)) {
@@ -499,20 +509,20 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32
         ++A_k;
         enqueue(Q, C, p, cls, now);
       }
+      pend = due();
     }
-    if (go || (first && !done)) {
-      // exactly b requests of the head-of-line class whenever server s is idle
-      while (busy_s <= now && Q.qsum > 0) {
-        const int h = Q.hh;
-        if (Q.q(h) < b) break;
-        C.c[C_DONE] += meta_s & 0xffu;  // the previous batch on s finished at busy_s <= now
-        const double sv = service<CM>(C, p, seed, ee, k, 0, h, b);
-        busy_s = pop_batch(Q, C, p, k, s, h, b, now, sv);
-        meta_s = (uint32_t)b | ((uint32_t)b << 8) | ((uint32_t)h << 16);
-        dirty_s = true;
-      }
+    const int n_act = __popcll(__ballot(!done)), n_pend = __popcll(__ballot(pend));
+    const bool working = !done && !pend;
+    if (n_pend > 0 && (kLearnedDispatchShare * n_pend >= n_act || __ballot(working) == 0ull) &&
+        pend) {
+      const int h = Q.hh;
+      C.c[C_DONE] += meta_s & 0xffu;  // the previous batch on s finished at busy_s <= now
+      const double sv = service<CM>(C, p, seed, ee, k, 0, h, b);
+      busy_s = pop_batch(Q, C, p, k, s, h, b, now, sv);
+      meta_s = (uint32_t)b | ((uint32_t)b << 8) | ((uint32_t)h << 16);
+      dirty_s = true;
+      pend = due();
     }
-    first = false;
     if (__ballot(!done) == 0ull) break;
   }
   if (!live) return;
