@@ -371,6 +371,8 @@ def measure(name, args, steps, warmup, timing_steps, ticks=0):
     dev = torch.device("cuda")
     seed = 0x5EED0000 + (int(name[1]) if name[0] == "C" and name[1].isdigit() else 9)
     sim = bs.Sim(w)
+    if args.no_graphs:
+        sim.set_graphs(False)
     weights = sim.init_weights(seed)
     ppo = w.get("ppo_minibatch", 0) > 0 and args.train == "none"
     train = args.train != "none"
@@ -412,11 +414,16 @@ def measure(name, args, steps, warmup, timing_steps, ticks=0):
             ev[3].record(sim.stream)
         return sim.stats()
 
+    def progress(what):
+        print(f"[bench] {name}: {what}", file=sys.stderr, flush=True)
+
     for i in range(warmup):
         one_step(i)
+        progress(f"warmup step {i + 1} of {warmup}")
     one_step(warmup)           # captures the rollout's graph (it repeats the previous call)
     sim.sync()
     torch.cuda.synchronize()
+    progress("graph-priming step")
     marks = []
     t0 = time.perf_counter()
     tot = None
@@ -426,6 +433,7 @@ def measure(name, args, steps, warmup, timing_steps, ticks=0):
         tot = one_step(1000 + i, ev)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    progress(f"{steps} timed steps")
     sim.sync()
     captures, replays = sim.graph_stats()
     ms_per_step = (t1 - t0) * 1000.0 / steps
@@ -437,6 +445,7 @@ def measure(name, args, steps, warmup, timing_steps, ticks=0):
     t2 = time.perf_counter()
     for i in range(timing_steps):
         one_step(2000 + i)
+        progress(f"event-timed step {i + 1} of {timing_steps}")
     sim.sync()
     t3 = time.perf_counter()
     timing = sim.get_timing(clear=True)
@@ -485,6 +494,9 @@ def main():
     ap.add_argument("--epochs", type=int, default=4)
     ap.add_argument("--minibatches", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graphs", action="store_true",
+                    help="launch every rollout eagerly (for counter collection, which serializes "
+                         "each dispatch)")
     ap.add_argument("--no-other-configs", action="store_true",
                     help="skip the sub-measurements of C1-C4 that follow the headline line's")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
