@@ -199,9 +199,12 @@ template <int KS>
 struct Stage {
   double E[KS][64];
   uint8_t cls[KS][64];
-  uint32_t owner_j0[64];  // needing lane | first block << 6 (blocks per tick < 2^18)
+  uint32_t owner_j0[64];  // needing lane | first block << 6
   uint32_t tick[64];
 };
+// A tick takes at most kMaxEventsPerTick events and each consumes at most two ARRIVAL blocks,
+// so a first block index fits the 26 bits above the lane.
+static_assert(2ull * kMaxEventsPerTick + 2 * kStageLearned < (1ull << 26), "owner_j0 packing");
 
 __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
