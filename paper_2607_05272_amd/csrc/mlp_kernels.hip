@@ -7,8 +7,10 @@
 // log-probability and value.
 //
 // Two kernels. policy_k (fp32 policies, v_mfma_f32_16x16x4_f32): one workgroup of 4 waves owns
-// 64 environments whose activations live in LDS; each wave produces a quarter of the output
-// columns of every layer, reading weight fragments straight from the repacked weights in L2.
+// 16 RT environments whose activations live in LDS (RT = 1 for small batches, whose launch
+// lasts as long as one workgroup's chain of layers; 4 otherwise); each wave produces a quarter
+// of the output columns of every layer, loading all of its weight fragments of a layer from
+// the repacked weights in L2 before the layer's first MFMA.
 // policy_bf16_k (bf16 policies): every layer's input rounded to bf16 (RNE), bf16 weights,
 // fp32 accumulation (v_mfma_f32_16x16x32_bf16), bias and GELU in fp32; its layout and
 // scheduling are described above the kernel.
@@ -21,7 +23,6 @@ namespace {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 
-constexpr int kRows = 64;      // environments per workgroup
 constexpr int kThreads = 256;  // 4 waves
 
 struct F32Mode {
@@ -48,49 +49,56 @@ struct HidOut {
   int E, e0;
 };
 
-// out[64][N] = act_in[64][K] * W^T  (W packed out-major [N][K]); epilogue: +bias, then
+// out[16 RT][N] = act_in[16 RT][K] * W^T  (W packed out-major [N][K]); epilogue: +bias, then
 // GELU + rounding into act_out (hidden layers) or fp32 into lg (last layer).
-template <class M, int K, int N, bool LAST, bool DBG = false>
+template <class M, int K, int N, int RT, bool LAST, bool DBG = false>
 __device__ __forceinline__ void layer(const typename M::elem* __restrict__ in,
                                       const typename M::elem* __restrict__ W,
                                       const float* __restrict__ bias,
                                       typename M::elem* __restrict__ out, float* __restrict__ lg,
                                       int lg_stride, HidOut ho = {}) {
   constexpr int NT = N / 16;             // column tiles
-  constexpr int NTW = (NT + 3) / 4;      // column tiles per wave
+  // wave w owns tiles w, w + 4, ...: all NT / 4 of them, or (NT < 4) one tile or none, so
+  // that no MFMA or load below sits behind a per-tile branch (which would make every MFMA wait
+  // for its own operand loads)
+  static_assert(NT % 4 == 0 || NT < 4, "a wave owns all of its column tiles or none");
+  constexpr int NTW = NT < 4 ? 1 : NT / 4;
   constexpr int SIN = K + M::PAD;        // LDS row stride of the input
   constexpr int SOUT = N + M::PAD;
+  constexpr int KSTEPS = K / M::KS;
+  static_assert(K % M::KS == 0, "whole k-steps");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, kq = lane >> 4;
-  f32x4 acc[4][NTW];
+  if (wave >= NT) return;  // only when NT < 4; uniform over the wave
+  // every weight fragment of the wave's tiles is loaded before the first MFMA: the loads are
+  // independent, so the layer waits out one L2 round trip instead of one per k-step (at most
+  // 64 x 64 weights per layer here: NTW * K / KS registers per lane)
+  typename M::frag wfr[KSTEPS][NTW];
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt)
+  for (int ks = 0; ks < KSTEPS; ++ks)
+#pragma unroll
+    for (int c = 0; c < NTW; ++c)
+      wfr[ks][c] = M::load(W + (size_t)((wave + 4 * c) * 16 + r16) * K + ks * M::KS + kq * M::KL);
+  f32x4 acc[RT][NTW];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int c = 0; c < NTW; ++c) acc[rt][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 2
-  for (int kb = 0; kb < K; kb += M::KS) {
-    typename M::frag bfr[NTW];
 #pragma unroll
-    for (int c = 0; c < NTW; ++c) {
-      const int ct = wave + 4 * c;
-      if (ct < NT) bfr[c] = M::load(W + (size_t)(ct * 16 + r16) * K + kb + kq * M::KL);
-    }
+  for (int ks = 0; ks < KSTEPS; ++ks) {
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
-      const typename M::frag a = M::load(in + (rt * 16 + r16) * SIN + kb + kq * M::KL);
+    for (int rt = 0; rt < RT; ++rt) {
+      const typename M::frag a = M::load(in + (rt * 16 + r16) * SIN + ks * M::KS + kq * M::KL);
 #pragma unroll
-      for (int c = 0; c < NTW; ++c)
-        if (wave + 4 * c < NT) acc[rt][c] = M::mfma(a, bfr[c], acc[rt][c]);
+      for (int c = 0; c < NTW; ++c) acc[rt][c] = M::mfma(a, wfr[ks][c], acc[rt][c]);
     }
   }
 #pragma unroll
   for (int c = 0; c < NTW; ++c) {
-    const int ct = wave + 4 * c;
-    if (ct >= NT) continue;
-    const int col = ct * 16 + r16;
+    const int col = (wave + 4 * c) * 16 + r16;
     const float bv = bias[col];
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = rt * 16 + kq * 4 + i;
@@ -108,21 +116,86 @@ __device__ __forceinline__ void layer(const typename M::elem* __restrict__ in,
   }
 }
 
-template <class M, int FP, int H1, int H2, int AP>
+template <class M, int FP, int H1, int H2, int AP, int RT>
 struct Shape {
   typedef typename M::elem E;
+  static constexpr int ROWS = 16 * RT;
   static constexpr int SX = FP + M::PAD, S1 = H1 + M::PAD, S2 = H2 + M::PAD, SL = AP + 1;
-  static constexpr size_t X_BYTES = (size_t)kRows * SX * sizeof(E);
-  static constexpr size_t H1_BYTES = (size_t)kRows * S1 * sizeof(E);
-  static constexpr size_t H2_BYTES = (size_t)kRows * S2 * sizeof(E);
-  static constexpr size_t L_BYTES = (size_t)kRows * SL * sizeof(float);
+  static constexpr size_t X_BYTES = (size_t)ROWS * SX * sizeof(E);
+  static constexpr size_t H1_BYTES = (size_t)ROWS * S1 * sizeof(E);
+  static constexpr size_t H2_BYTES = (size_t)ROWS * S2 * sizeof(E);
+  static constexpr size_t L_BYTES = (size_t)ROWS * SL * sizeof(float);
   // x shares the h2 region (dead before h2 is written), logits share the h1 region
   static constexpr size_t REGION_A = H2_BYTES > X_BYTES ? H2_BYTES : X_BYTES;
   static constexpr size_t REGION_B = H1_BYTES > L_BYTES ? H1_BYTES : L_BYTES;
   static constexpr size_t LDS = REGION_A + REGION_B;
 };
 
-template <class M, int FP, int H1, int H2, int AP, bool DBG>
+// Sampling epilogue of both policy kernels: for each of the workgroup's ROWS environment rows
+// of logits lg [row][sl], the action by inverse CDF of the fp32 softmax with the ACTION
+// uniform of (env, step), its log-probability and the value output. G lanes per row (an
+// aligned group of G lanes), each over a contiguous slice of the actions whose exponentials
+// it keeps in registers; max, prefix sums and the first slice holding the target u*S by
+// shuffles within the group.
+template <int AP, int ROWS, int NTHR>
+__device__ __forceinline__ void sample_rows(const float* lg, int sl, const MlpParams& m, int e0,
+                                            uint64_t seed, uint32_t step, uint8_t* act,
+                                            float* logp, float* value, float* logits) {
+  constexpr int G = 8, KMAX = (AP + G - 1) / G;
+  static_assert(NTHR % G == 0, "sampler groups");
+  const int tid = threadIdx.x;
+  for (int row0 = 0; row0 < ROWS; row0 += NTHR / G) {
+    const int row = row0 + tid / G, part = tid % G;
+    const int e = e0 + row;
+    const bool live = row < ROWS && e < m.E;
+    const float* l = lg + (row < ROWS ? row : 0) * sl;
+    const int A = m.A;
+    const int chunk = (A + G - 1) / G;
+    const int lo = part * chunk;
+    float mx = -3.0e38f;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i)
+      if (i < chunk && lo + i < A) mx = fmaxf(mx, l[lo + i]);
+#pragma unroll
+    for (int off = 1; off < G; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, G));
+    float pe[KMAX];
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) {
+      pe[i] = (i < chunk && lo + i < A) ? __expf(l[lo + i] - mx) : 0.f;
+      ps += pe[i];
+    }
+    float incl = ps;
+#pragma unroll
+    for (int off = 1; off < G; off <<= 1) {
+      const float t = __shfl_up(incl, off, G);
+      if (part >= off) incl += t;
+    }
+    const float S = __shfl(incl, G - 1, G);
+    const u32x4 w = draw(seed, (uint32_t)(live ? e : 0), step, P_ACTION, 0, 0);
+    const float u = ((float)(w.x >> 9) + 0.5f) * 0x1p-23f;
+    const float target = u * S;
+    int found = 0x7fffffff;
+    float cum = incl - ps;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) {
+      cum += pe[i];
+      if (found == 0x7fffffff && i < chunk && lo + i < A && target < cum) found = lo + i;
+    }
+#pragma unroll
+    for (int off = 1; off < G; off <<= 1) found = min(found, __shfl_xor(found, off, G));
+    if (live && part == 0) {
+      const int a = found < A ? found : A - 1;
+      if (act) act[e] = (uint8_t)a;
+      if (logp) logp[e] = (l[a] - mx) - __logf(S);
+      if (value && m.value_head) value[e] = l[A];
+    }
+    if (live && logits)
+      for (int i = part; i < m.Ap; i += G) logits[(size_t)i * m.E + e] = l[i];
+  }
+}
+
+template <class M, int FP, int H1, int H2, int AP, int RT, bool DBG>
 __global__ __launch_bounds__(kThreads) void policy_k(MlpParams m, const float* __restrict__ obs,
                                                      const uint64_t* __restrict__ seedp, uint32_t step,
                                                      uint8_t* __restrict__ act,
@@ -131,60 +204,34 @@ __global__ __launch_bounds__(kThreads) void policy_k(MlpParams m, const float* _
                                                      float* __restrict__ logits,
                                                      float* __restrict__ hid) {
   const uint64_t seed = *seedp;   // the episode seed
-  typedef Shape<M, FP, H1, H2, AP> Sh;
+  typedef Shape<M, FP, H1, H2, AP, RT> Sh;
   typedef typename M::elem E;
+  constexpr int ROWS = Sh::ROWS;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   E* xs = reinterpret_cast<E*>(smem);
   E* h2s = reinterpret_cast<E*>(smem);
   E* h1s = reinterpret_cast<E*>(smem + Sh::REGION_A);
   float* lg = reinterpret_cast<float*>(smem + Sh::REGION_A);
-  const int e0 = blockIdx.x * kRows;
+  const int e0 = blockIdx.x * ROWS;
   const int tid = threadIdx.x;
   // stage x: obs [F][E] fp32 -> rows of the tile, rounded to the layer's input type
-  for (int idx = tid; idx < kRows * FP; idx += kThreads) {
-    const int r = idx % kRows, f = idx / kRows;
+  for (int idx = tid; idx < ROWS * FP; idx += kThreads) {
+    const int r = idx % ROWS, f = idx / ROWS;
     const int e = e0 + r;
     float v = 0.f;
     if (f < m.F && e < m.E) v = obs[(size_t)f * m.E + e];
     xs[r * Sh::SX + f] = M::from_f32(v);
   }
   __syncthreads();
-  layer<M, FP, H1, false, DBG>(xs, static_cast<const E*>(m.w1), m.b1, h1s, nullptr, 0,
+  layer<M, FP, H1, RT, false, DBG>(xs, static_cast<const E*>(m.w1), m.b1, h1s, nullptr, 0,
                                HidOut{hid, m.E, e0});
   __syncthreads();
-  layer<M, H1, H2, false, DBG>(h1s, static_cast<const E*>(m.w2), m.b2, h2s, nullptr, 0,
+  layer<M, H1, H2, RT, false, DBG>(h1s, static_cast<const E*>(m.w2), m.b2, h2s, nullptr, 0,
                                HidOut{DBG ? hid + (size_t)H1 * m.E : nullptr, m.E, e0});
   __syncthreads();
-  layer<M, H2, AP, true>(h2s, static_cast<const E*>(m.w3), m.b3, nullptr, lg, Sh::SL);
+  layer<M, H2, AP, RT, true>(h2s, static_cast<const E*>(m.w3), m.b3, nullptr, lg, Sh::SL);
   __syncthreads();
-  // sampling epilogue: one lane per environment row
-  if (tid < kRows) {
-    const int e = e0 + tid;
-    if (e < m.E) {
-      const float* l = lg + tid * Sh::SL;
-      const int A = m.A;
-      if (act || logp) {
-        float mx = l[0];
-        for (int i = 1; i < A; ++i) mx = l[i] > mx ? l[i] : mx;
-        float S = 0.f;
-        for (int i = 0; i < A; ++i) S += expf(l[i] - mx);
-        const u32x4 w = draw(seed, (uint32_t)e, step, P_ACTION, 0, 0);
-        const float u = ((float)(w.x >> 9) + 0.5f) * 0x1p-23f;
-        const float target = u * S;
-        float cum = 0.f;
-        int a = A - 1;
-        for (int i = 0; i < A; ++i) {
-          cum += expf(l[i] - mx);
-          if (target < cum) { a = i; break; }
-        }
-        if (act) act[e] = (uint8_t)a;
-        if (logp) logp[e] = (l[a] - mx) - logf(S);
-      }
-      if (value && m.value_head) value[e] = l[A];
-      if (logits)
-        for (int i = 0; i < m.Ap; ++i) logits[(size_t)i * m.E + e] = l[i];
-    }
-  }
+  sample_rows<AP, ROWS, kThreads>(lg, Sh::SL, m, e0, seed, step, act, logp, value, logits);
 }
 
 // packed bf16 weights in MFMA fragment order: for output tile t (16 units) and k-step ks (32
@@ -562,60 +609,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
   __syncthreads();
   output_layer<H2, AP, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w3), m.b3, lg, Sh::SL);
   __syncthreads();
-  // sampling: G lanes per environment row (an aligned group of G lanes), each over a
-  // contiguous slice of the actions whose exponentials it keeps in registers; max, prefix
-  // sums and the first slice holding the target u*S by shuffles within the group
-  constexpr int G = 8, KMAX = (AP + G - 1) / G;
-  static_assert(NTHR % G == 0, "sampler groups");
-  for (int row0 = 0; row0 < ROWS; row0 += NTHR / G) {
-    const int row = row0 + tid / G, part = tid % G;
-    const int e = e0 + row;
-    const bool live = row < ROWS && e < m.E;
-    const float* l = lg + (row < ROWS ? row : 0) * Sh::SL;
-    const int A = m.A;
-    const int chunk = (A + G - 1) / G;
-    const int lo = part * chunk;
-    float mx = -3.0e38f;
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i)
-      if (i < chunk && lo + i < A) mx = fmaxf(mx, l[lo + i]);
-#pragma unroll
-    for (int off = 1; off < G; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, G));
-    float pe[KMAX];
-    float ps = 0.f;
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) {
-      pe[i] = (i < chunk && lo + i < A) ? __expf(l[lo + i] - mx) : 0.f;
-      ps += pe[i];
-    }
-    float incl = ps;
-#pragma unroll
-    for (int off = 1; off < G; off <<= 1) {
-      const float t = __shfl_up(incl, off, G);
-      if (part >= off) incl += t;
-    }
-    const float S = __shfl(incl, G - 1, G);
-    const u32x4 w = draw(seed, (uint32_t)(live ? e : 0), step, P_ACTION, 0, 0);
-    const float u = ((float)(w.x >> 9) + 0.5f) * 0x1p-23f;
-    const float target = u * S;
-    int found = 0x7fffffff;
-    float cum = incl - ps;
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) {
-      cum += pe[i];
-      if (found == 0x7fffffff && i < chunk && lo + i < A && target < cum) found = lo + i;
-    }
-#pragma unroll
-    for (int off = 1; off < G; off <<= 1) found = min(found, __shfl_xor(found, off, G));
-    if (live && part == 0) {
-      const int a = found < A ? found : A - 1;
-      if (act) act[e] = (uint8_t)a;
-      if (logp) logp[e] = (l[a] - mx) - __logf(S);
-      if (value && m.value_head) value[e] = l[A];
-    }
-    if (live && logits)
-      for (int i = part; i < m.Ap; i += G) logits[(size_t)i * m.E + e] = l[i];
-  }
+  sample_rows<AP, ROWS, NTHR>(lg, Sh::SL, m, e0, seed, step, act, logp, value, logits);
 }
 
 template <bool DBG, int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW = 1>
@@ -638,12 +632,12 @@ hipError_t run_policy_bf16(const MlpParams& m, const float* obs, const uint64_t*
   return hipGetLastError();
 }
 
-template <bool DBG, class M, int FP, int H1, int H2, int AP>
+template <bool DBG, class M, int FP, int H1, int H2, int AP, int RT>
 hipError_t run_policy(const MlpParams& m, const float* obs, const uint64_t* seed, uint32_t step,
                       uint8_t* act, float* logp, float* value, float* logits, float* hid,
                       hipStream_t st) {
-  typedef Shape<M, FP, H1, H2, AP> Sh;
-  auto kern = policy_k<M, FP, H1, H2, AP, DBG>;
+  typedef Shape<M, FP, H1, H2, AP, RT> Sh;
+  auto kern = policy_k<M, FP, H1, H2, AP, RT, DBG>;
   static bool attr = false;
   if (!attr) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -651,11 +645,15 @@ hipError_t run_policy(const MlpParams& m, const float* obs, const uint64_t* seed
     if (e != hipSuccess) return e;
     attr = true;
   }
-  const dim3 grid((m.E + kRows - 1) / kRows), block(kThreads);
+  const dim3 grid((m.E + Sh::ROWS - 1) / Sh::ROWS), block(kThreads);
   hipLaunchKernelGGL(kern, grid, block, Sh::LDS, st, m, obs, seed, step, act, logp, value, logits,
                      hid);
   return hipGetLastError();
 }
+
+// fp32 policy row tiles per workgroup (16 environments each): small batches take small tiles,
+// so that a workgroup's serial chain of layers is short
+constexpr int kF32SmallE = 4096, kF32SmallRT = 1, kF32RT = 4;
 
 struct ShapeKey { int bf16, FP, H1, H2, AP; };
 constexpr ShapeKey kShapes[] = {
@@ -682,7 +680,9 @@ static hipError_t launch_policy_t(const MlpParams& m, const float* obs, const ui
                                   uint32_t step, uint8_t* act, float* logp, float* value,
                                   float* logits, float* hid, hipStream_t st) {
   if (!m.bf16 && m.FP == 8 && m.H1 == 64 && m.H2 == 64 && m.AP == 16)
-    return run_policy<DBG, F32Mode, 8, 64, 64, 16>(m, obs, seed, step, act, logp, value, logits, hid, st);
+    return m.E <= kF32SmallE
+               ? run_policy<DBG, F32Mode, 8, 64, 64, 16, kF32SmallRT>(m, obs, seed, step, act, logp, value, logits, hid, st)
+               : run_policy<DBG, F32Mode, 8, 64, 64, 16, kF32RT>(m, obs, seed, step, act, logp, value, logits, hid, st);
   // bf16 shapes: 64-row tiles with 4 waves, two workgroups per CU, when there are enough
   // rows to fill the chip; 32-row tiles otherwise
   const bool big = m.E >= 64 * 512;
