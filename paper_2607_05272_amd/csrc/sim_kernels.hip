@@ -435,7 +435,8 @@ __device__ __forceinline__ void put_obs(float* obs, size_t E, int i, int e, doub
 // share of the wave's lanes still in the tick that triggers a dispatch pass (1 / share)
 constexpr int kLearnedDispatchShare = 4;
 template <int CM>
-__global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32_t k, const uint8_t* __restrict__ act,
+__global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32_t k, int lpw,
+                                                 const uint8_t* __restrict__ act,
                                                  float* __restrict__ obs_out,
                                                  double* __restrict__ rew,
                                                  uint64_t* __restrict__ rchk) {
@@ -443,10 +444,11 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32
   __shared__ Stage<kStageLearned> stage[4];
   const int lane = threadIdx.x & 63;
   Stage<kStageLearned>& st = stage[threadIdx.x >> 6];
-  const int e_lane0 = blockIdx.x * blockDim.x + (threadIdx.x & ~63);
+  // wave w owns environments w * lpw .. + lpw - 1 in its first lpw lanes (lanes_per_wave)
+  const int e_lane0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * lpw;
   const int e = e_lane0 + lane;
-  // lanes past the last environment stay in the loop (the wave refills together) but idle
-  const bool live = e < p.E;
+  // lanes without an environment stay in the loop (the wave refills together) but idle
+  const bool live = lane < lpw && e < p.E;
   if (__ballot(live) == 0ull) return;
   const int ee = live ? e : 0;
   const size_t E = (size_t)p.E;
@@ -977,15 +979,16 @@ __device__ __forceinline__ void static_run(const SimParams& p, const SysState& G
 // rewards; nt = 1 is the per-tick kernel of the step interface.
 template <int KM, int CM, bool SQ>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void static_k(
-    SimParams p, EnvState g, uint32_t k0, int nt, double* __restrict__ rew) {
+    SimParams p, EnvState g, uint32_t k0, int nt, int lpw, double* __restrict__ rew) {
   const uint64_t seed = *g.seed;   // the episode seed, written by reset_k
   __shared__ Stage<kStageStatic> stage[4];
   __shared__ double busy_lds[4][KM > 8 ? KM - kBusyRegs : 1][64];
   const int lane = threadIdx.x & 63;
   Stage<kStageStatic>& st = stage[threadIdx.x >> 6];
-  const int e_lane0 = blockIdx.x * blockDim.x + (threadIdx.x & ~63);
+  // wave w owns environments w * lpw .. + lpw - 1 in its first lpw lanes (lanes_per_wave)
+  const int e_lane0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * lpw;
   const int e = e_lane0 + lane;
-  const bool live = e < p.E;
+  const bool live = lane < lpw && e < p.E;
   if (__ballot(live) == 0ull) return;
   const int ee = live ? e : 0;
   const size_t E = (size_t)p.E;
@@ -1176,20 +1179,33 @@ __global__ __launch_bounds__(256) void totals_k(SimParams p, EnvState g, int64_t
   }
 }
 
+// Lanes per wave of the tick kernels (one environment per lane). A wave's tick lasts as long
+// as its busiest lane, and a batch of fewer than kFillWaves * 64 environments leaves SIMDs
+// without a wave: such batches are spread over more waves with fewer environments each (down
+// to 4), which shortens every wave's tick at no cost in issue slots.
+constexpr int kFillWaves = 1024;
+int lanes_per_wave(int E) {
+  int lpw = 64;
+  while (lpw > 4 && (E + lpw - 1) / lpw < kFillWaves) lpw >>= 1;
+  return lpw;
+}
+
 template <int CM>
 void launch_static_c(const SimParams& p, const EnvState& s, uint32_t k, int nt,
                      double* rew_sh, hipStream_t st) {
-  const dim3 grid((p.E + 255) / 256), block(256);
+  const int lpw = lanes_per_wave(p.E);
+  const int waves = (p.E + lpw - 1) / lpw;
+  const dim3 grid((waves + 3) / 4), block(256);
   if (p.route == 3) {   // Shortest-Queue (at most 8 servers)
-    if (p.K <= 2) hipLaunchKernelGGL((static_k<2, CM, true>), grid, block, 0, st, p, s, k, nt, rew_sh);
-    else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM, true>), grid, block, 0, st, p, s, k, nt, rew_sh);
-    else hipLaunchKernelGGL((static_k<8, CM, true>), grid, block, 0, st, p, s, k, nt, rew_sh);
+    if (p.K <= 2) hipLaunchKernelGGL((static_k<2, CM, true>), grid, block, 0, st, p, s, k, nt, lpw, rew_sh);
+    else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM, true>), grid, block, 0, st, p, s, k, nt, lpw, rew_sh);
+    else hipLaunchKernelGGL((static_k<8, CM, true>), grid, block, 0, st, p, s, k, nt, lpw, rew_sh);
     return;
   }
-  if (p.K <= 1) hipLaunchKernelGGL((static_k<1, CM, false>), grid, block, 0, st, p, s, k, nt, rew_sh);
-  else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM, false>), grid, block, 0, st, p, s, k, nt, rew_sh);
-  else if (p.K <= 8) hipLaunchKernelGGL((static_k<8, CM, false>), grid, block, 0, st, p, s, k, nt, rew_sh);
-  else hipLaunchKernelGGL((static_k<16, CM, false>), grid, block, 0, st, p, s, k, nt, rew_sh);
+  if (p.K <= 1) hipLaunchKernelGGL((static_k<1, CM, false>), grid, block, 0, st, p, s, k, nt, lpw, rew_sh);
+  else if (p.K <= 4) hipLaunchKernelGGL((static_k<4, CM, false>), grid, block, 0, st, p, s, k, nt, lpw, rew_sh);
+  else if (p.K <= 8) hipLaunchKernelGGL((static_k<8, CM, false>), grid, block, 0, st, p, s, k, nt, lpw, rew_sh);
+  else hipLaunchKernelGGL((static_k<16, CM, false>), grid, block, 0, st, p, s, k, nt, lpw, rew_sh);
 }
 
 }  // namespace
@@ -1202,13 +1218,15 @@ hipError_t launch_reset(const SimParams& p, const EnvState& s, uint64_t seed, hi
 hipError_t launch_step(const SimParams& p, const EnvState& s, uint32_t k,
                        const uint8_t* act, float* obs_out, double* rew, uint64_t* rchk,
                        hipStream_t st) {
-  const dim3 grid((p.E + 255) / 256), block(256);
+  const int lpw = lanes_per_wave(p.E);
+  const int waves = (p.E + lpw - 1) / lpw;
+  const dim3 grid((waves + 3) / 4), block(256);
   if (p.C <= 1)
-    hipLaunchKernelGGL(learned_k<1>, grid, block, 0, st, p, s, k, act, obs_out, rew, rchk);
+    hipLaunchKernelGGL(learned_k<1>, grid, block, 0, st, p, s, k, lpw, act, obs_out, rew, rchk);
   else if (p.C <= 2)
-    hipLaunchKernelGGL(learned_k<2>, grid, block, 0, st, p, s, k, act, obs_out, rew, rchk);
+    hipLaunchKernelGGL(learned_k<2>, grid, block, 0, st, p, s, k, lpw, act, obs_out, rew, rchk);
   else
-    hipLaunchKernelGGL(learned_k<4>, grid, block, 0, st, p, s, k, act, obs_out, rew, rchk);
+    hipLaunchKernelGGL(learned_k<4>, grid, block, 0, st, p, s, k, lpw, act, obs_out, rew, rchk);
   return hipGetLastError();
 }
 
