@@ -13,20 +13,26 @@
  *   - the policy networks of Sec. 4.2: the MLP (GELU hidden layers, categorical head,
  *     value column) and the attention policy (input projection to tokens, multi-head
  *     self-attention, mean pooling, GELU policy head and a separate GELU value head);
+ *   - the static timeout rule run as a shadow system (Sec. 1) and the baseline routing rules
+ *     of Sec. 5.1 (lowest idle, random and round-robin idle server, Shortest-Queue over
+ *     per-server FIFOs of two batches);
  *   - discounted returns (REINFORCE) and GAE (PPO) of Sec. 4.3.
- * Every reading of a point the paper leaves open is numbered R1..R26 (the design notes list
- * them); the comments in oracle.c name them.
+ * Every reading of a point the paper leaves open is numbered R1..R27; the comments in
+ * oracle.c name the reading each step follows.
  *
  * Every function runs one environment at a time, event by event, in fp64 with no
  * implicit contraction (built with -ffp-contract=off). Parity functions:
- *   pinned:   Philox structure (vs numpy's Philox4x64), det_log/det_exp/det_cos (vs libm),
- *             samplers (KS / chi-square vs scipy), queue dynamics (M/D/1, M/M/1, M/M/1/K,
- *             M/M/c closed forms), Little's law (exact sample-path identity), conservation,
- *             hand-enumerated traces, MLP (vs torch fp64), attention policy (vs
- *             torch.nn.MultiheadAttention in fp64, one-token and uniform-attention closed
- *             forms, feature-permutation invariance), GAE (closed forms).
- *   unpinned: the Philox4x32 multipliers (no known-answer vectors available here; pinned
- *             only statistically and by GPU/CPU bit identity).
+ *   pinned:   the Philox4x32-10 block (bit for bit vs PyTorch's independent engine; its
+ *             structure also vs numpy's Philox4x64), det_log/det_exp/det_cos (vs libm),
+ *             samplers (KS / chi-square vs scipy), the class draw and the arrival stream's
+ *             counter layout, the lognormal service law with its linear term, the
+ *             stationary start, queue dynamics (M/D/1, M/M/1, M/M/1/K, M/M/c closed forms;
+ *             the M/M/2 bracket of Shortest-Queue), Little's law (exact sample-path
+ *             identity), conservation, hand-enumerated traces (incl. the multi-server,
+ *             multi-class observation and Shortest-Queue routing), MLP (vs torch fp64),
+ *             attention policy (vs torch.nn.MultiheadAttention in fp64, one-token and
+ *             uniform-attention closed forms, feature-permutation invariance), GAE (closed
+ *             forms).
  */
 #ifndef ORACLE_H
 #define ORACLE_H

@@ -29,7 +29,8 @@ def test_philox_weyl_constants_from_closed_forms(orc):
     m0, m1, w0, w1 = (int(x) for x in orc.philox_constants())
     assert w0 == int(phi1 * 2**32)
     assert w1 == int(s31 * 2**32)
-    # multipliers are odd 32-bit constants (parity with the published table unpinned)
+    # multipliers are odd 32-bit constants (their values are pinned by the bit-for-bit
+    # comparison with PyTorch's engine in test_oracle_pins.py)
     assert m0 % 2 == 1 and m1 % 2 == 1
 
 
