@@ -304,6 +304,47 @@ def test_sim_step_parity_full_size_sampled(bs, orc, name):
         assert_close_rel(rsh, res["reward_shadow"], "reward_shadow")
 
 
+@pytest.mark.parametrize("E,lpw", [(9001, 8), (40001, 32)])
+def test_lanes_per_wave_mappings(bs, orc, E, lpw):
+    """Batch sizes for which the tick kernels spread the environments over waves of 8 and of
+    32 lanes (the other spreads, 4, 16 and 64, are covered by the small, C3 and full-size
+    cases): C5's workload (16 servers, bursts, static shadow) for 40 ticks, sampled
+    environments at wave boundaries and a ragged last wave, against the oracle."""
+    w = dict(preset("C5"), n_envs=E, T=40)
+    T = w["T"]
+    seed = 0xC0FFEE + lpw
+    A = 6 * w["n_servers"]
+    rng = np.random.default_rng(seed)
+    cols = np.unique(np.concatenate([[0, lpw - 1, lpw, 2 * lpw - 1, E - 2, E - 1],
+                                     rng.choice(E, 20, replace=False)]))
+    say(f"[lanes per wave] E={E} lpw={lpw} sampled={len(cols)}")
+    sim = bs.Sim(w)
+    sim.reset(seed)
+    dev = torch.device("cuda")
+    rew = np.zeros((T, len(cols)))
+    rsh = np.zeros((T, len(cols)))
+    acts_cols = np.zeros((T, len(cols)), np.uint8)
+    cols_dev = torch.from_numpy(cols).to(dev)
+    for k in range(T):
+        a = _step_actions(seed, k, E, A)
+        acts_cols[k] = a[cols]
+        _, r, rs = sim.step(torch.from_numpy(a).to(dev), want_obs=False)
+        rew[k] = r[cols_dev].cpu().numpy()
+        rsh[k] = rs[cols_dev].cpu().numpy()
+    sim.sync()
+    cnt, sums = sim.counters()
+    chk = sim.checksums().cpu().numpy().view(np.uint64)
+    cnt = cnt.cpu().numpy(); sums = sums.cpu().numpy()
+    sim.close()
+    res = orc.rollout(w, seed, T, cols, actions=acts_cols, want_obs=False, want_rec=False)
+    for s_ in range(2):
+        assert np.array_equal(chk[s_, cols], res["chk"][:, s_]), f"checksum sys {s_}"
+        assert np.array_equal(cnt[s_][:, cols].T, res["counters"][:, s_])
+        assert_close_rel(sums[s_][:, cols].T, res["sums"][:, s_, :2], "sums")
+    assert_close_rel(rew, res["reward"], "reward")
+    assert_close_rel(rsh, res["reward_shadow"], "reward_shadow")
+
+
 def _trace_tensors(g, dev):
     arr = g["arrivals"]
     L = len(arr)
