@@ -434,7 +434,13 @@ __device__ __forceinline__ void put_obs(float* obs, size_t E, int i, int e, doub
 // ---- learned system: one tick ---------------------------------------------------------------
 // share of the wave's lanes still in the tick that triggers a dispatch pass (1 / share)
 constexpr int kLearnedDispatchShare = 4;
-template <int CM>
+constexpr int kEndChunk = 8;   // server rows read per round trip at the end of the tick
+// PF: the end-of-tick reads of the server rows (K <= kEndChunk) and of the arrival-rate
+// averages are issued at the start of the tick instead, so that their latency passes under
+// the event loop; they cost registers, which waves that have a SIMD to themselves can spare.
+// Only this kernel writes those arrays, at the end of a tick, so the early reads see the same
+// values.
+template <int CM, bool PF>
 __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32_t k, int lpw,
                                                  const uint8_t* __restrict__ act,
                                                  float* __restrict__ obs_out,
@@ -470,6 +476,17 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32
   uint32_t meta_s = G.meta[(size_t)s * E + ee];
   if (bad_action) atomicOr(g.err, ERR_ACTION);
   bool dirty_s = false;
+  double brow_pf[PF ? kEndChunk : 1], ew_pf[PF ? 4 : 1];
+  uint32_t mrow_pf[PF ? kEndChunk : 1];
+  if constexpr (PF) {
+#pragma unroll
+    for (int i = 0; i < kEndChunk; ++i) {
+      brow_pf[i] = i < p.K ? G.busy[(size_t)i * E + ee] : 0.0;
+      mrow_pf[i] = i < p.K ? G.meta[(size_t)i * E + ee] : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ew_pf[i] = g.ewma[(size_t)i * E + ee];
+  }
 
   const double t0 = (double)k * p.dt, t1 = (double)(k + 1) * p.dt;
   int A_k = 0;
@@ -538,17 +555,21 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32
   // chunk costs one memory round trip instead of two per server.
   float* obs = g.obs;
   const int per = p.K > 1 ? 4 : 2;
-  constexpr int kEndChunk = 8;
   for (int j0 = 0; j0 < p.K; j0 += kEndChunk) {
     double brow[kEndChunk];
     uint32_t mrow[kEndChunk];
 #pragma unroll
     for (int i = 0; i < kEndChunk; ++i) {
-      brow[i] = 0.0;
-      mrow[i] = 0u;
-      if (j0 + i < p.K) {
-        brow[i] = G.busy[(size_t)(j0 + i) * E + e];
-        mrow[i] = G.meta[(size_t)(j0 + i) * E + e];
+      if constexpr (PF) {
+        brow[i] = brow_pf[i];
+        mrow[i] = mrow_pf[i];
+      } else {
+        brow[i] = 0.0;
+        mrow[i] = 0u;
+        if (j0 + i < p.K) {
+          brow[i] = G.busy[(size_t)(j0 + i) * E + e];
+          mrow[i] = G.meta[(size_t)(j0 + i) * E + e];
+        }
       }
     }
 #pragma unroll
@@ -600,7 +621,7 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32
   double ew[4];
   const double ewc[4] = {1.0, 0.25, 0.0625, 0.015625};
 #pragma unroll
-  for (int i = 0; i < 4; ++i) ew[i] = g.ewma[(size_t)i * E + e];
+  for (int i = 0; i < 4; ++i) ew[i] = PF ? ew_pf[PF ? i : 0] : g.ewma[(size_t)i * E + e];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     ew[i] = ew[i] + ewc[i] * ((double)A_k - ew[i]);
@@ -1215,18 +1236,30 @@ hipError_t launch_reset(const SimParams& p, const EnvState& s, uint64_t seed, hi
   return hipGetLastError();
 }
 
+template <bool PF>
+void launch_learned(const SimParams& p, const EnvState& s, uint32_t k, int lpw, dim3 grid,
+                    const uint8_t* act, float* obs_out, double* rew, uint64_t* rchk,
+                    hipStream_t st) {
+  const dim3 block(256);
+  if (p.C <= 1)
+    hipLaunchKernelGGL((learned_k<1, PF>), grid, block, 0, st, p, s, k, lpw, act, obs_out, rew, rchk);
+  else if (p.C <= 2)
+    hipLaunchKernelGGL((learned_k<2, PF>), grid, block, 0, st, p, s, k, lpw, act, obs_out, rew, rchk);
+  else
+    hipLaunchKernelGGL((learned_k<4, PF>), grid, block, 0, st, p, s, k, lpw, act, obs_out, rew, rchk);
+}
+
 hipError_t launch_step(const SimParams& p, const EnvState& s, uint32_t k,
                        const uint8_t* act, float* obs_out, double* rew, uint64_t* rchk,
                        hipStream_t st) {
   const int lpw = lanes_per_wave(p.E);
   const int waves = (p.E + lpw - 1) / lpw;
-  const dim3 grid((waves + 3) / 4), block(256);
-  if (p.C <= 1)
-    hipLaunchKernelGGL(learned_k<1>, grid, block, 0, st, p, s, k, lpw, act, obs_out, rew, rchk);
-  else if (p.C <= 2)
-    hipLaunchKernelGGL(learned_k<2>, grid, block, 0, st, p, s, k, lpw, act, obs_out, rew, rchk);
+  const dim3 grid((waves + 3) / 4);
+  // early end-of-tick reads when every wave has a SIMD to itself
+  if (waves <= kFillWaves && p.K <= kEndChunk)
+    launch_learned<true>(p, s, k, lpw, grid, act, obs_out, rew, rchk, st);
   else
-    hipLaunchKernelGGL(learned_k<4>, grid, block, 0, st, p, s, k, lpw, act, obs_out, rew, rchk);
+    launch_learned<false>(p, s, k, lpw, grid, act, obs_out, rew, rchk, st);
   return hipGetLastError();
 }
 
