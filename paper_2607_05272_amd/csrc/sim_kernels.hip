@@ -334,6 +334,30 @@ __device__ __forceinline__ void enqueue(Queue<CM>& Q, Count& C, const SimParams&
   C.c[C_ACC] += 1u;
 }
 
+// The same arrival as enqueue, written as selects (the ring store aside) for the arrival runs
+// of the learned tick: a loop over branchy code keeps copies of the whole queue state in
+// flight, while this straight-line form updates it in place.
+template <int CM>
+__device__ __forceinline__ void enqueue_sel(Queue<CM>& Q, Count& C, const SimParams& p, int cls,
+                                            double now) {
+  const bool acc = Q.qsum != p.N;
+  const int qc = Q.q(cls);
+  int pos = Q.hd(cls) + qc;
+  pos = pos >= p.N ? pos - p.N : pos;
+  if (acc) Q.ring[(size_t)cls * p.N + pos] = now;
+  const bool first = acc && qc == 0;
+  const bool lead = first && (Q.qsum == 0 || (now == Q.hts_h && cls < Q.hh));
+#pragma unroll
+  for (int c = 0; c < CM; ++c) Q.hts[c] = first && cls == c ? now : Q.hts[c];
+  Q.hh = lead ? cls : Q.hh;
+  Q.hts_h = lead ? now : Q.hts_h;
+  Q.qp += acc ? 1u << (8 * cls) : 0u;
+  Q.qsum += acc ? 1 : 0;
+  C.c[C_ARR] += 1u;
+  C.c[C_DROP] += acc ? 0u : 1u;
+  C.c[C_ACC] += acc ? 1u : 0u;
+}
+
 // Service time of a batch of n requests of class h. kind 0: alpha + beta n; kind 1:
 // median * exp(sigma Z) + beta n with Z = sqrt(-2 log u1) cos(2 pi u2) (Box-Muller); kind 2:
 // -log(u1) (alpha + beta n), with u1, u2 from SERVICE block j of (env, tick, system). Inline in
@@ -439,13 +463,12 @@ constexpr int kEndChunk = 8;   // server rows read per round trip at the end of 
 // averages are issued at the start of the tick instead, so that their latency passes under
 // the event loop; they cost registers, which waves that have a SIMD to themselves can spare.
 // Only this kernel writes those arrays, at the end of a tick, so the early reads see the same
-// values.
+// values. Without PF the kernel is held to four waves per SIMD (128 VGPRs): the largest grid
+// fills the chip exactly at that occupancy.
 template <int CM, bool PF>
-__global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32_t k, int lpw,
-                                                 const uint8_t* __restrict__ act,
-                                                 float* __restrict__ obs_out,
-                                                 double* __restrict__ rew,
-                                                 uint64_t* __restrict__ rchk) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF ? 1 : 4))) void learned_k(
+    SimParams p, EnvState g, uint32_t k, int lpw, const uint8_t* __restrict__ act,
+    float* __restrict__ obs_out, double* __restrict__ rew, uint64_t* __restrict__ rchk) {
   const uint64_t seed = *g.seed;   // the episode seed, written by reset_k
   __shared__ Stage<kStageLearned> stage[4];
   const int lane = threadIdx.x & 63;
@@ -532,6 +555,26 @@ __global__ __launch_bounds__(256) void learned_k(SimParams p, EnvState g, uint32
         enqueue(Q, C, p, cls, now);
       }
       pend = due();
+      // a run of arrivals: arrivals strictly before the next switch, the tick's end and (while
+      // server s is busy) its completion are the lane's only events, so they are taken here,
+      // each exactly as a pass would take it (the same staged blocks, the same event bound),
+      // until one makes a batch due, without the pass's wave-wide bookkeeping
+      if (!pend && p.arrival_kind != 1) {
+        const double wend = fmin(fmin(A.next_sw, busy_s > now ? busy_s : kInf), t1);
+        bool more = A.next_arr < wend && A.jarr + 2u <= staged_hi && it <= kMaxEventsPerTick;
+        while (more) {
+          ++it;
+          now = A.next_arr;
+          const uint32_t j = A.jarr++;
+          const int c = st.cls[j % kStageLearned][lane];
+          A.next_arr = now + st.E[j % kStageLearned][lane] * A.gap;
+          ++A_k;
+          enqueue_sel(Q, C, p, c, now);
+          pend = due();
+          more = !pend && A.next_arr < wend && A.jarr + 2u <= staged_hi &&
+                 it <= kMaxEventsPerTick;
+        }
+      }
     }
     const int n_act = __popcll(__ballot(!done)), n_pend = __popcll(__ballot(pend));
     const bool working = !done && !pend;
