@@ -87,10 +87,14 @@ def step_bytes(w, tot, E, T):
     """Algorithmic HBM bytes per env-tick of the learned-system kernel: the structure-of-
     arrays state it must read and write, the action, reward and observation, the ring
     entries touched by accepted arrivals and dispatched requests, and the server entries
-    rewritten by dispatches (busy + meta) and completions (meta)."""
+    rewritten by dispatches (busy + meta) and completions (meta). Inside a rollout with a
+    bf16 MLP policy the tick writes the observation as bf16 feature pairs (2 bytes per
+    feature; the fp32 observation only on the rollout's last tick), otherwise as fp32."""
     K, C, F = w["n_servers"], w["n_classes"], w["obs_dim"]
+    from workloads.presets import POLICY_MLP
+    obs_b = 4 * ((F + 1) // 2) if (w["mlp_bf16"] and w["policy_kind"] == POLICY_MLP) else 4 * F
     state_rw = 4 + 4 + 8 * C + 4 * 6 + 16 + 8 + 4 + 8 + 8 + 32   # queues, counters, arrivals, ewma
-    fixed = 1 + 2 * state_rw + 12 * K + 4 * F + 8                 # + action, servers read, obs, reward
+    fixed = 1 + 2 * state_rw + 12 * K + obs_b + 8                 # + action, servers read, obs, reward
     n = E * T
     c = tot["cnt"][0]
     var = 8.0 * (c[1] + c[3]) / n + 12.0 * c[4] / n + 4.0 * c[4] / n

@@ -152,6 +152,14 @@ __device__ __forceinline__ uint16_t bf16_bits(float f) {
 }
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
+// two fp32 values -> their bf16 roundings (nearest even, the hardware's packed conversion),
+// lo in the low half of the word and hi in the high half
+__device__ __forceinline__ uint32_t pack_bf16_pair(float lo, float hi) {
+  typedef __attribute__((ext_vector_type(2))) float f32x2_t;
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
+}
+
 // FNV-1a over 64-bit words: checksum of the integer state sequence.
 constexpr uint64_t kFnvInit = 0xcbf29ce484222325ull;
 __device__ __forceinline__ uint64_t fnv(uint64_t h, uint64_t v) { return (h ^ v) * 0x100000001b3ull; }

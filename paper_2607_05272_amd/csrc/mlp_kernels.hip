@@ -308,9 +308,7 @@ typedef __attribute__((ext_vector_type(2))) float f32x2;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
-}
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) { return pack_bf16_pair(lo, hi); }
 
 // GELU(x) = x Phi(x) = max(x, 0) - |x| Phi(-|x|) (Phi(-t) = 1 - Phi(t) folds the positive half
 // onto the negative one), with Phi(-t) = 2^q(t) and q a degree-5 polynomial fitted to
@@ -572,6 +570,7 @@ struct BigShape {
 
 template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW, bool DBG>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MINB / 4 > 0 ? NW * MINB / 4 : 1))) void policy_bf16_k(MlpParams m, const float* __restrict__ obs,
+                                                               const uint32_t* __restrict__ obs_bf,
                                                                const uint64_t* __restrict__ seedp, uint32_t step,
                                                                uint8_t* __restrict__ act,
                                                                float* __restrict__ logp,
@@ -593,6 +592,25 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
   // (issuing them together cost it 1%, and saved 2-5% in the others).
   constexpr int NIT = (ROWS * (FP / 2) + NTHR - 1) / NTHR;
   constexpr int NPRE = TPW == 1 ? NIT : 1;
+  if (obs_bf) {
+    // the observation's bf16 pairs [F/2][E] (written by the simulator's tick): one 4-byte load
+    // per feature pair and environment, stored as is
+    uint32_t v[NIT];
+#pragma unroll
+    for (int i = 0; i < NIT; ++i) {
+      const int idx = tid + i * NTHR;
+      const int r = idx % ROWS, f = 2 * (idx / ROWS);
+      const int e = e0 + r;
+      v[i] = 0u;
+      if (idx < ROWS * (FP / 2) && e < m.E && f < m.F) v[i] = obs_bf[(size_t)(f / 2) * m.E + e];
+    }
+#pragma unroll
+    for (int i = 0; i < NIT; ++i) {
+      const int idx = tid + i * NTHR;
+      const int r = idx % ROWS, f = 2 * (idx / ROWS);
+      if (idx < ROWS * (FP / 2)) *reinterpret_cast<uint32_t*>(xs + r * Sh::SX + f) = v[i];
+    }
+  } else
   for (int it0 = 0; it0 < NIT; it0 += NPRE) {
     float v0[NPRE], v1[NPRE];
 #pragma unroll
@@ -637,7 +655,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
 }
 
 template <bool DBG, int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW = 1>
-hipError_t run_policy_bf16(const MlpParams& m, const float* obs, const uint64_t* seed, uint32_t step,
+hipError_t run_policy_bf16(const MlpParams& m, const float* obs, const uint32_t* obs_bf,
+                           const uint64_t* seed, uint32_t step,
                            uint8_t* act, float* logp, float* value, float* logits, float* hid,
                            hipStream_t st) {
   typedef BigShape<FP, H1, H2, AP, RT, NW> Sh;
@@ -651,8 +670,8 @@ hipError_t run_policy_bf16(const MlpParams& m, const float* obs, const uint64_t*
     attr = true;
   }
   const dim3 grid((m.E + Sh::ROWS - 1) / Sh::ROWS), block(NW * 64);
-  hipLaunchKernelGGL(kern, grid, block, Sh::LDS, st, m, obs, seed, step, act, logp, value, logits,
-                     hid);
+  hipLaunchKernelGGL(kern, grid, block, Sh::LDS, st, m, obs, obs_bf, seed, step, act, logp, value,
+                     logits, hid);
   return hipGetLastError();
 }
 
@@ -700,7 +719,8 @@ bool policy_shape_supported(const MlpParams& m) {
 }
 
 template <bool DBG>
-static hipError_t launch_policy_t(const MlpParams& m, const float* obs, const uint64_t* seed,
+static hipError_t launch_policy_t(const MlpParams& m, const float* obs, const uint32_t* obs_bf,
+                                  const uint64_t* seed,
                                   uint32_t step, uint8_t* act, float* logp, float* value,
                                   float* logits, float* hid, hipStream_t st) {
   if (!m.bf16 && m.FP == 8 && m.H1 == 64 && m.H2 == 64 && m.AP == 16)
@@ -711,26 +731,27 @@ static hipError_t launch_policy_t(const MlpParams& m, const float* obs, const ui
   // rows to fill the chip; 32-row tiles otherwise
   const bool big = m.E >= 64 * 512;
   if (m.bf16 && m.FP == 32 && m.H1 == 128 && m.H2 == 128 && m.AP == 16)
-    return big ? run_policy_bf16<DBG, 32, 128, 128, 16, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, hid, st)
-               : run_policy_bf16<DBG, 32, 128, 128, 16, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, hid, st);
+    return big ? run_policy_bf16<DBG, 32, 128, 128, 16, 4, 8, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st)
+               : run_policy_bf16<DBG, 32, 128, 128, 16, 2, 4, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st);
   if (m.bf16 && m.FP == 32 && m.H1 == 256 && m.H2 == 256 && m.AP == 32)
-    return big ? run_policy_bf16<DBG, 32, 256, 256, 32, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, hid, st)
-               : run_policy_bf16<DBG, 32, 256, 256, 32, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, hid, st);
+    return big ? run_policy_bf16<DBG, 32, 256, 256, 32, 4, 8, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st)
+               : run_policy_bf16<DBG, 32, 256, 256, 32, 2, 4, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st);
   if (m.bf16 && m.FP == 64 && m.H1 == 256 && m.H2 == 256 && m.AP == 64)
-    return big ? run_policy_bf16<DBG, 64, 256, 256, 64, 4, 8, 2>(m, obs, seed, step, act, logp, value, logits, hid, st)
-               : run_policy_bf16<DBG, 64, 256, 256, 64, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, hid, st);
+    return big ? run_policy_bf16<DBG, 64, 256, 256, 64, 4, 8, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st)
+               : run_policy_bf16<DBG, 64, 256, 256, 64, 2, 4, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st);
   if (m.bf16 && m.FP == 96 && m.H1 == 512 && m.H2 == 512 && m.AP == 112)
-    return big ? run_policy_bf16<DBG, 96, 512, 512, 112, 4, 8, 2, 2>(m, obs, seed, step, act, logp, value, logits, hid, st)
-               : run_policy_bf16<DBG, 96, 512, 512, 112, 2, 4, 2>(m, obs, seed, step, act, logp, value, logits, hid, st);
+    return big ? run_policy_bf16<DBG, 96, 512, 512, 112, 4, 8, 2, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st)
+               : run_policy_bf16<DBG, 96, 512, 512, 112, 2, 4, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st);
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_policy(const MlpParams& m, const float* obs, const uint64_t* seed, uint32_t step,
-                         uint8_t* act, float* logp, float* value, float* logits, float* hidden,
-                         hipStream_t st) {
+hipError_t launch_policy(const MlpParams& m, const float* obs, const uint32_t* obs_bf,
+                         const uint64_t* seed, uint32_t step, uint8_t* act, float* logp,
+                         float* value, float* logits, float* hidden, hipStream_t st) {
+  if (obs_bf && !m.bf16) return hipErrorInvalidValue;
   if (hidden)
-    return launch_policy_t<true>(m, obs, seed, step, act, logp, value, logits, hidden, st);
-  return launch_policy_t<false>(m, obs, seed, step, act, logp, value, logits, nullptr, st);
+    return launch_policy_t<true>(m, obs, obs_bf, seed, step, act, logp, value, logits, hidden, st);
+  return launch_policy_t<false>(m, obs, obs_bf, seed, step, act, logp, value, logits, nullptr, st);
 }
 
 hipError_t launch_repack(const MlpParams& m, const void* d_weights, const size_t off[6],

@@ -59,15 +59,22 @@ struct EnvState {
   SysState sys[2];   // 0 learned, 1 static shadow
   double* ewma;      // [4][E] exponentially weighted arrival counts (learned system)
   float* obs;        // [F][E] current observation
+  uint32_t* obs_bf;  // [ceil(F/2)][E] its bf16 pairs, for a bf16 policy (NULL otherwise); the
+                     // pairs are packed from obs at the start of a rollout, then written by
+                     // its ticks (which skip obs except on the rollout's last tick)
   uint32_t* err;     // [1] latched error flags
   uint64_t* seed;    // [1] the episode seed (written by reset_k, read by every kernel that draws)
 };
 
 // Kernel launchers (asynchronous on `st`); each returns the launch's hipError_t.
 hipError_t launch_reset(const SimParams& p, const EnvState& s, uint64_t seed, hipStream_t st);
+// obs_mode: kObsF32 writes the current observation s.obs, kObsBf16 its bf16 pairs s.obs_bf
+constexpr int kObsF32 = 1, kObsBf16 = 2;
 hipError_t launch_step(const SimParams& p, const EnvState& s, uint32_t k,
-                       const uint8_t* act, float* obs_out, double* rew, uint64_t* rchk,
-                       hipStream_t st);
+                       const uint8_t* act, float* obs_out, int obs_mode, double* rew,
+                       uint64_t* rchk, hipStream_t st);
+// s.obs_bf from s.obs (feature pairs (2m, 2m + 1), a missing last feature as zero)
+hipError_t launch_obs_pack(const SimParams& p, const EnvState& s, hipStream_t st);
 // ticks k .. k + nt - 1 of the static shadow system; rew_sh [nt][E] or NULL
 hipError_t launch_static(const SimParams& p, const EnvState& s, uint32_t k,
                          int nt, double* rew_sh, hipStream_t st);
@@ -94,9 +101,11 @@ hipError_t launch_repack(const MlpParams& m, const void* d_weights, const size_t
                          hipStream_t st);
 // hidden != NULL runs the diagnostic instantiation that also writes the hidden activations
 // passed between layers: [H1][E] then [H2][E] fp32
-hipError_t launch_policy(const MlpParams& m, const float* obs, const uint64_t* seed, uint32_t step,
-                         uint8_t* act, float* logp, float* value, float* logits, float* hidden,
-                         hipStream_t st);
+// obs_bf != NULL (bf16 policies only) reads the observation as its bf16 pairs [F/2][E] instead
+// of obs
+hipError_t launch_policy(const MlpParams& m, const float* obs, const uint32_t* obs_bf,
+                         const uint64_t* seed, uint32_t step, uint8_t* act, float* logp,
+                         float* value, float* logits, float* hidden, hipStream_t st);
 hipError_t launch_init_weights(int F, int H1, int H2, int Ap, int bf16, uint64_t seed,
                                void* d_weights, const size_t off[6], hipStream_t st);
 bool policy_shape_supported(const MlpParams& m);

@@ -309,6 +309,8 @@ int sim_create(const sim_cfg* cfg, void* hip_stream, sim_ctx** out) {
   }
   parts.push_back({(void**)&x->s.ewma, 8 * 4 * E});
   parts.push_back({(void**)&x->s.obs, 4 * (size_t)cfg->obs_dim * E});
+  if (cfg->policy_kind == SIM_POLICY_MLP && cfg->mlp_bf16)
+    parts.push_back({(void**)&x->s.obs_bf, 4 * (size_t)((cfg->obs_dim + 1) / 2) * E});
   parts.push_back({(void**)&x->s.err, 256});
   parts.push_back({(void**)&x->s.seed, 256});
   parts.push_back({(void**)&x->d_tot_cnt, 8 * 2 * 7});
@@ -414,9 +416,9 @@ int sim_obs(sim_ctx* x, float* d_obs) {
 
 // the learned system's tick and, if `shadow`, the static system's
 static int enqueue_tick(sim_ctx* x, uint32_t k, const uint8_t* act, float* obs_out, double* rew,
-                        double* rew_sh, uint64_t* rchk, bool shadow) {
+                        double* rew_sh, uint64_t* rchk, bool shadow, int obs_mode = kObsF32) {
   HIPCHK(x->timed(SIM_KC_STEP, [&] {
-           return launch_step(x->p, x->s, k, act, obs_out, rew, rchk, x->stream);
+           return launch_step(x->p, x->s, k, act, obs_out, obs_mode, rew, rchk, x->stream);
          }), "step kernel launch");
   if (shadow && x->cfg.shadow)
     HIPCHK(x->timed(SIM_KC_STATIC, [&] {
@@ -581,10 +583,11 @@ static int prepare_policy(sim_ctx* x, const void* d_weights) {
 // the policy kernel of the configured network (after prepare_policy)
 static hipError_t policy_launch(sim_ctx* x, const float* obs, uint32_t step, uint8_t* act,
                                 float* logp, float* value, float* logits,
-                                float* hidden = nullptr) {
+                                float* hidden = nullptr, const uint32_t* obs_bf = nullptr) {
   if (x->cfg.policy_kind == SIM_POLICY_ATTN)
     return launch_attn_policy(x->a, obs, x->s.seed, step, act, logp, value, logits, x->stream);
-  return launch_policy(x->m, obs, x->s.seed, step, act, logp, value, logits, hidden, x->stream);
+  return launch_policy(x->m, obs, obs_bf, x->s.seed, step, act, logp, value, logits, hidden,
+                       x->stream);
 }
 
 int sim_policy(sim_ctx* x, const void* d_weights, const float* d_obs, uint32_t step,
@@ -628,23 +631,32 @@ static int enqueue_rollout(sim_ctx* x, const void* d_weights, int32_t T, const s
     rc = run_static(x, k0, T, tr->reward_shadow);
     if (rc) return rc;
   }
+  // a bf16 policy reads the observation as bf16 pairs, which the ticks write instead of the
+  // fp32 observation (half its bytes, both for the tick that writes it and the policy that
+  // reads it); the fp32 observation is written again by the last tick
+  const uint32_t* obs_bf = x->s.obs_bf;
+  if (obs_bf)
+    HIPCHK(x->timed(SIM_KC_OTHER, [&] { return launch_obs_pack(x->p, x->s, x->stream); }),
+           "observation packing launch");
   for (int32_t i = 0; i < T; ++i) {
     const size_t row = (size_t)i * E;
     const uint32_t k = k0 + (uint32_t)i;
     HIPCHK(x->timed(SIM_KC_POLICY, [&] {
              return policy_launch(x, x->s.obs, k, tr->actions + row,
                                   tr->logp ? tr->logp + row : nullptr,
-                                  tr->value ? tr->value + row : nullptr, nullptr);
+                                  tr->value ? tr->value + row : nullptr, nullptr, nullptr,
+                                  obs_bf);
            }), "policy kernel launch");
+    const int mode = !obs_bf ? kObsF32 : i + 1 < T ? kObsBf16 : kObsF32 | kObsBf16;
     rc = enqueue_tick(x, k, tr->actions + row, tr->obs ? tr->obs + (size_t)(i + 1) * F * E : nullptr,
                       tr->reward ? tr->reward + row : nullptr, nullptr,
-                      tr->rchk ? tr->rchk + row : nullptr, false);
+                      tr->rchk ? tr->rchk + row : nullptr, false, mode);
     if (rc) return rc;
   }
   if (tr->value)
     HIPCHK(x->timed(SIM_KC_POLICY, [&] {
              return policy_launch(x, x->s.obs, k0 + (uint32_t)T, nullptr, nullptr,
-                                  tr->value + (size_t)T * E, nullptr);
+                                  tr->value + (size_t)T * E, nullptr, nullptr, obs_bf);
            }), "policy kernel launch (final value)");
   return SIM_OK;
 }

@@ -451,9 +451,29 @@ __device__ __forceinline__ double close_tick(const Queue<CM>& Q, Count& C, const
   return p.w_thr * thr - (C.n_k > 0 ? C.Lw / (double)C.n_k : 0.0);
 }
 
-__device__ __forceinline__ void put_obs(float* obs, size_t E, int i, int e, double v) {
-  obs[(size_t)i * E + e] = (float)v;
-}
+// Writes the observation of one environment a pair of features (2m, 2m + 1) at a time, each
+// feature rounded once to fp32: into the current observation [F][E] (cur, may be NULL), a
+// trajectory row [F][E] (traj, may be NULL), and as the pair's two bf16 roundings packed in
+// one word [F/2][E] (bf, may be NULL): what a bf16 policy reads, half the bytes of the fp32 pair.
+struct ObsPairs {
+  float* cur;
+  float* traj;
+  uint32_t* bf;
+  size_t E;
+  int e;
+  __device__ __forceinline__ void put(int i, double v0, double v1) const {
+    const float a = (float)v0, b = (float)v1;
+    if (cur) {
+      cur[(size_t)i * E + e] = a;
+      cur[(size_t)(i + 1) * E + e] = b;
+    }
+    if (traj) {
+      traj[(size_t)i * E + e] = a;
+      traj[(size_t)(i + 1) * E + e] = b;
+    }
+    if (bf) bf[(size_t)(i >> 1) * E + e] = pack_bf16_pair(a, b);
+  }
+};
 
 // ---- learned system: one tick ---------------------------------------------------------------
 // share of the wave's lanes still in the tick that triggers a dispatch pass (1 / share)
@@ -468,7 +488,8 @@ constexpr int kEndChunk = 8;   // server rows read per round trip at the end of 
 template <int CM, bool PF>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF ? 1 : 4))) void learned_k(
     SimParams p, EnvState g, uint32_t k, int lpw, const uint8_t* __restrict__ act,
-    float* __restrict__ obs_out, double* __restrict__ rew, uint64_t* __restrict__ rchk) {
+    float* __restrict__ obs_out, int obs_mode, double* __restrict__ rew,
+    uint64_t* __restrict__ rchk) {
   const uint64_t seed = *g.seed;   // the episode seed, written by reset_k
   __shared__ Stage<kStageLearned> stage[4];
   const int lane = threadIdx.x & 63;
@@ -596,7 +617,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF ? 1 : 4)
   // are read kEndChunk at a time, all loads of a chunk issued before any of its stores (the
   // compiler cannot reorder them across the stores, which it must assume may alias), so a
   // chunk costs one memory round trip instead of two per server.
-  float* obs = g.obs;
+  const ObsPairs ob{(obs_mode & kObsF32) ? g.obs : nullptr, obs_out,
+                    (obs_mode & kObsBf16) ? g.obs_bf : nullptr, E, e};
   const int per = p.K > 1 ? 4 : 2;
   for (int j0 = 0; j0 < p.K; j0 += kEndChunk) {
     double brow[kEndChunk];
@@ -636,22 +658,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF ? 1 : 4)
       const int base = 2 + per * j;
       const double bflag = bu > t1 ? 1.0 : 0.0;
       const double lb = (double)((m >> 8) & 0xffu) * 0.03125;
-      put_obs(obs, E, base, e, bflag);
-      put_obs(obs, E, base + 1, e, lb);
-      if (obs_out) {
-        put_obs(obs_out, E, base, e, bflag);
-        put_obs(obs_out, E, base + 1, e, lb);
-      }
+      ob.put(base, bflag, lb);
       if (p.K > 1) {
         const double rem = (bu > t1 ? bu - t1 : 0.0) * p.inv_tw;
         const uint32_t lc = (m >> 16) & 0xffu;
         const double lcv = (double)((lc == 0xffu ? -1 : (int)lc) + 1) * p.inv_c;
-        put_obs(obs, E, base + 2, e, rem);
-        put_obs(obs, E, base + 3, e, lcv);
-        if (obs_out) {
-          put_obs(obs_out, E, base + 2, e, rem);
-          put_obs(obs_out, E, base + 3, e, lcv);
-        }
+        ob.put(base + 2, rem, lcv);
       }
     }
   }
@@ -673,12 +685,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF ? 1 : 4)
   // queue part of obs_{k+1}
   const int h = Q.hh;
   const double f0 = (double)Q.qsum * p.inv_n, f1 = (h >= 0 ? t1 - Q.hts_h : 0.0) * p.inv_tw;
-  put_obs(obs, E, 0, e, f0);
-  put_obs(obs, E, 1, e, f1);
-  if (obs_out) {
-    put_obs(obs_out, E, 0, e, f0);
-    put_obs(obs_out, E, 1, e, f1);
-  }
+  ob.put(0, f0, f1);
   int i = 2 + per * p.K;
   if (p.C > 1) {
 #pragma unroll
@@ -687,25 +694,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF ? 1 : 4)
         const int qc = Q.q(c);
         const double fq = (double)qc * p.inv_n;
         const double fa = (qc > 0 ? t1 - Q.hts[c] : 0.0) * p.inv_tw;
-        put_obs(obs, E, i, e, fq);
-        put_obs(obs, E, i + 1, e, fa);
-        if (obs_out) {
-          put_obs(obs_out, E, i, e, fq);
-          put_obs(obs_out, E, i + 1, e, fa);
-        }
+        ob.put(i, fq, fa);
         i += 2;
       }
     }
   }
-#pragma unroll
-  for (int r4 = 0; r4 < 4; ++r4) {
-    const double fr = ew[r4] * p.inv_rs;
-    put_obs(obs, E, i, e, fr);
-    if (obs_out) put_obs(obs_out, E, i, e, fr);
-    ++i;
-  }
-  // the padding rows past the observation's width: zero in the current observation since the
-  // reset (nothing else writes them), so only a trajectory row needs them
+  ob.put(i, ew[0] * p.inv_rs, ew[1] * p.inv_rs);
+  ob.put(i + 2, ew[2] * p.inv_rs, ew[3] * p.inv_rs);
+  i += 4;
+  // the padding rows past the observation's width: zero in the current observation (and its
+  // bf16 pairs) since the reset or the pairs' packing (nothing else writes them), so only a
+  // trajectory row needs them
   if (obs_out)
     for (; i < p.F; ++i) obs_out[(size_t)i * E + e] = 0.0f;
 
@@ -1185,6 +1184,17 @@ __global__ __launch_bounds__(256) void reset_k(SimParams p, EnvState g, uint64_t
 }
 
 // per-env counters out: [2][7][E] int64 (7th = inflight), sums [2][2][E]
+// bf16 pairs of the current observation: pair m of environment e packs features 2m and 2m + 1
+// (zero past the last feature), rounded as a bf16 policy rounds its input
+__global__ __launch_bounds__(256) void obs_pack_k(SimParams p, EnvState g) {
+  const int e = blockIdx.x * 256 + threadIdx.x, m = blockIdx.y;
+  if (e >= p.E) return;
+  const size_t E = (size_t)p.E;
+  const float a = g.obs[(size_t)(2 * m) * E + e];
+  const float b = 2 * m + 1 < p.F ? g.obs[(size_t)(2 * m + 1) * E + e] : 0.0f;
+  g.obs_bf[(size_t)m * E + e] = pack_bf16_pair(a, b);
+}
+
 __global__ void counters_k(SimParams p, EnvState g, int64_t* cnt, double* sums) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= p.E) return;
@@ -1281,28 +1291,36 @@ hipError_t launch_reset(const SimParams& p, const EnvState& s, uint64_t seed, hi
 
 template <bool PF>
 void launch_learned(const SimParams& p, const EnvState& s, uint32_t k, int lpw, dim3 grid,
-                    const uint8_t* act, float* obs_out, double* rew, uint64_t* rchk,
-                    hipStream_t st) {
+                    const uint8_t* act, float* obs_out, int obs_mode, double* rew,
+                    uint64_t* rchk, hipStream_t st) {
   const dim3 block(256);
   if (p.C <= 1)
-    hipLaunchKernelGGL((learned_k<1, PF>), grid, block, 0, st, p, s, k, lpw, act, obs_out, rew, rchk);
+    hipLaunchKernelGGL((learned_k<1, PF>), grid, block, 0, st, p, s, k, lpw, act, obs_out, obs_mode, rew, rchk);
   else if (p.C <= 2)
-    hipLaunchKernelGGL((learned_k<2, PF>), grid, block, 0, st, p, s, k, lpw, act, obs_out, rew, rchk);
+    hipLaunchKernelGGL((learned_k<2, PF>), grid, block, 0, st, p, s, k, lpw, act, obs_out, obs_mode, rew, rchk);
   else
-    hipLaunchKernelGGL((learned_k<4, PF>), grid, block, 0, st, p, s, k, lpw, act, obs_out, rew, rchk);
+    hipLaunchKernelGGL((learned_k<4, PF>), grid, block, 0, st, p, s, k, lpw, act, obs_out, obs_mode, rew, rchk);
 }
 
 hipError_t launch_step(const SimParams& p, const EnvState& s, uint32_t k,
-                       const uint8_t* act, float* obs_out, double* rew, uint64_t* rchk,
-                       hipStream_t st) {
+                       const uint8_t* act, float* obs_out, int obs_mode, double* rew,
+                       uint64_t* rchk, hipStream_t st) {
+  if ((obs_mode & kObsBf16) && !s.obs_bf) return hipErrorInvalidValue;
   const int lpw = lanes_per_wave(p.E);
   const int waves = (p.E + lpw - 1) / lpw;
   const dim3 grid((waves + 3) / 4);
   // early end-of-tick reads when every wave has a SIMD to itself
   if (waves <= kFillWaves && p.K <= kEndChunk)
-    launch_learned<true>(p, s, k, lpw, grid, act, obs_out, rew, rchk, st);
+    launch_learned<true>(p, s, k, lpw, grid, act, obs_out, obs_mode, rew, rchk, st);
   else
-    launch_learned<false>(p, s, k, lpw, grid, act, obs_out, rew, rchk, st);
+    launch_learned<false>(p, s, k, lpw, grid, act, obs_out, obs_mode, rew, rchk, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_obs_pack(const SimParams& p, const EnvState& s, hipStream_t st) {
+  if (!s.obs_bf) return hipErrorInvalidValue;
+  const int pairs = (p.F + 1) / 2;
+  hipLaunchKernelGGL(obs_pack_k, dim3((p.E + 255) / 256, pairs), dim3(256), 0, st, p, s);
   return hipGetLastError();
 }
 

@@ -626,6 +626,9 @@ def test_rollout_parity_and_validity(bs, orc, name):
     assert np.array_equal(rep["rchk"], grchk), "running checksums differ"
     assert_close_rel(gr, rep["reward"], "reward")
     assert np.array_equal(rep["obs"], go), "observations differ"
+    # the current observation after the rollout (its last tick writes it in fp32; the ticks
+    # before it may write only the bf16 pairs a bf16 policy reads)
+    assert np.array_equal(sim.obs().cpu().numpy(), gobs[T]), "current observation after the rollout"
     # (3) every decision against the oracle policy on the same observation
     lg_err = 0.0
     ties = 0
