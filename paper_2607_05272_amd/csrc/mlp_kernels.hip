@@ -137,10 +137,19 @@ struct Shape {
 // aligned group of G lanes), each over a contiguous slice of the actions whose exponentials
 // it keeps in registers; max, prefix sums and the first slice holding the target u*S by
 // shuffles within the group.
+// The ACTION uniform of a row's environment: ((w.x >> 9) + 1/2) 2^-23 from its block.
+__device__ __forceinline__ float action_uniform(uint64_t seed, uint32_t env, uint32_t step) {
+  const u32x4 w = draw(seed, env, step, P_ACTION, 0, 0);
+  return ((float)(w.x >> 9) + 0.5f) * 0x1p-23f;
+}
+
+// us: the rows' uniforms, drawn beforehand (one lane per row), or NULL to draw them here (every
+// lane of a row's group then computes the same block).
 template <int AP, int ROWS, int NTHR>
 __device__ __forceinline__ void sample_rows(const float* lg, int sl, const MlpParams& m, int e0,
                                             uint64_t seed, uint32_t step, uint8_t* act,
-                                            float* logp, float* value, float* logits) {
+                                            float* logp, float* value, float* logits,
+                                            const float* us = nullptr) {
   constexpr int G = 8, KMAX = (AP + G - 1) / G;
   static_assert(NTHR % G == 0, "sampler groups");
   const int tid = threadIdx.x;
@@ -172,8 +181,8 @@ __device__ __forceinline__ void sample_rows(const float* lg, int sl, const MlpPa
       if (part >= off) incl += t;
     }
     const float S = __shfl(incl, G - 1, G);
-    const u32x4 w = draw(seed, (uint32_t)(live ? e : 0), step, P_ACTION, 0, 0);
-    const float u = ((float)(w.x >> 9) + 0.5f) * 0x1p-23f;
+    const float u = us ? us[row < ROWS ? row : 0]
+                       : action_uniform(seed, (uint32_t)(live ? e : 0), step);
     const float target = u * S;
     int found = 0x7fffffff;
     float cum = incl - ps;
@@ -565,7 +574,8 @@ struct BigShape {
   static constexpr size_t H_BYTES = (size_t)ROWS * SH * 2;
   static constexpr size_t L_BYTES = (size_t)ROWS * SL * 4;
   static constexpr size_t HREG = H_BYTES > L_BYTES ? H_BYTES : L_BYTES;
-  static constexpr size_t LDS = X_BYTES + HREG;
+  static constexpr size_t U_BYTES = (size_t)ROWS * 4;   // the rows' ACTION uniforms
+  static constexpr size_t LDS = X_BYTES + HREG + U_BYTES;
 };
 
 template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW, bool DBG>
@@ -584,8 +594,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
   uint16_t* xs = reinterpret_cast<uint16_t*>(smem);
   uint16_t* hs = reinterpret_cast<uint16_t*>(smem + Sh::X_BYTES);
   float* lg = reinterpret_cast<float*>(smem + Sh::X_BYTES);
+  float* us = reinterpret_cast<float*>(smem + Sh::X_BYTES + Sh::HREG);
   const int e0 = blockIdx.x * ROWS;
   const int tid = threadIdx.x;
+  // the sampler's uniforms, one lane per row (the first ROWS lanes), read after the layers
+  if (tid < ROWS) us[tid] = action_uniform(seed, (uint32_t)(e0 + tid < m.E ? e0 + tid : 0), step);
   // stage x: obs [F][E] fp32 -> [env][feature] bf16, two features per 4-byte store. Every
   // load of a thread's share is issued before its first store (one round trip instead of
   // one per share), except in the two-tile variant, which is at its register limit there
@@ -651,7 +664,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
   __syncthreads();
   output_layer<H2, AP, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w3), m.b3, lg, Sh::SL);
   __syncthreads();
-  sample_rows<AP, ROWS, NTHR>(lg, Sh::SL, m, e0, seed, step, act, logp, value, logits);
+  sample_rows<AP, ROWS, NTHR>(lg, Sh::SL, m, e0, seed, step, act, logp, value, logits, us);
 }
 
 template <bool DBG, int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW = 1>
