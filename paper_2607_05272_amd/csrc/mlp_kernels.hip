@@ -597,8 +597,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
   float* us = reinterpret_cast<float*>(smem + Sh::X_BYTES + Sh::HREG);
   const int e0 = blockIdx.x * ROWS;
   const int tid = threadIdx.x;
-  // the sampler's uniforms, one lane per row (the first ROWS lanes), read after the layers
-  if (tid < ROWS) us[tid] = action_uniform(seed, (uint32_t)(e0 + tid < m.E ? e0 + tid : 0), step);
+  // the sampler's uniforms, one lane per row (the first ROWS lanes), read after the layers;
+  // drawn while the observation loads are in flight
+  auto draw_uniforms = [&]() {
+    if (tid < ROWS) us[tid] = action_uniform(seed, (uint32_t)(e0 + tid < m.E ? e0 + tid : 0), step);
+  };
   // stage x: obs [F][E] fp32 -> [env][feature] bf16, two features per 4-byte store. Every
   // load of a thread's share is issued before its first store (one round trip instead of
   // one per share), except in the two-tile variant, which is at its register limit there
@@ -617,6 +620,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
       v[i] = 0u;
       if (idx < ROWS * (FP / 2) && e < m.E && f < m.F) v[i] = obs_bf[(size_t)(f / 2) * m.E + e];
     }
+    draw_uniforms();
 #pragma unroll
     for (int i = 0; i < NIT; ++i) {
       const int idx = tid + i * NTHR;
@@ -646,6 +650,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
         *reinterpret_cast<uint32_t*>(xs + r * Sh::SX + f) = pack_bf16(v0[i], v1[i]);
     }
   }
+  if (!obs_bf) draw_uniforms();
   __syncthreads();
   const HidOut h1o{hid, m.E, e0}, h2o{DBG ? hid + (size_t)H1 * m.E : nullptr, m.E, e0};
   if constexpr (TPW == 1) {
