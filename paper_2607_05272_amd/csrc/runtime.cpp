@@ -84,6 +84,10 @@ struct sim_ctx {
   hipStream_t gstream = nullptr;
   hipEvent_t gev_in = nullptr, gev_out = nullptr;
   hipGraphExec_t rgraph = nullptr;
+  // a rollout's static shadow launches run on a second stream (default priority), forked
+  // from and joined back to the rollout's stream by events
+  hipStream_t sstream = nullptr;
+  hipEvent_t sev_fork = nullptr, sev_join = nullptr;
   RolloutKey rkey{}, seen{};
   bool rkey_valid = false, seen_valid = false;
   int64_t graph_captures = 0, graph_replays = 0;
@@ -376,6 +380,12 @@ int sim_destroy(sim_ctx* x) {
     (void)hipStreamSynchronize(x->gstream);
     (void)hipStreamDestroy(x->gstream);
   }
+  if (x->sstream) {
+    (void)hipStreamSynchronize(x->sstream);
+    (void)hipStreamDestroy(x->sstream);
+  }
+  if (x->sev_fork) (void)hipEventDestroy(x->sev_fork);
+  if (x->sev_join) (void)hipEventDestroy(x->sev_join);
   delete x;
   return SIM_OK;
 }
@@ -627,7 +637,26 @@ static int enqueue_rollout(sim_ctx* x, const void* d_weights, int32_t T, const s
   int rc = prepare_policy(x, d_weights);
   if (rc) return rc;
   const size_t E = (size_t)x->cfg.n_envs, F = (size_t)x->cfg.obs_dim;
-  if (x->cfg.shadow) {
+  // The static shadow system never reads the learned system, so its launches run beside the
+  // learned chain on a second stream (forked from and joined back to the rollout's stream,
+  // which a graph capture follows); with per-launch timing on, everything stays on one stream
+  // so that each kernel's duration is its own.
+  const bool side = x->cfg.shadow && !x->timing;
+  if (side) {
+    if (!x->sstream) {
+      HIPCHK(hipStreamCreateWithFlags(&x->sstream, hipStreamNonBlocking), "hipStreamCreateWithFlags");
+      HIPCHK(hipEventCreateWithFlags(&x->sev_fork, hipEventDisableTiming), "hipEventCreateWithFlags");
+      HIPCHK(hipEventCreateWithFlags(&x->sev_join, hipEventDisableTiming), "hipEventCreateWithFlags");
+    }
+    HIPCHK(hipEventRecord(x->sev_fork, x->stream), "hipEventRecord");
+    HIPCHK(hipStreamWaitEvent(x->sstream, x->sev_fork, 0), "hipStreamWaitEvent");
+    hipStream_t main = x->stream;
+    x->stream = x->sstream;
+    rc = run_static(x, k0, T, tr->reward_shadow);
+    x->stream = main;
+    if (rc) return rc;
+    HIPCHK(hipEventRecord(x->sev_join, x->sstream), "hipEventRecord");
+  } else if (x->cfg.shadow) {
     rc = run_static(x, k0, T, tr->reward_shadow);
     if (rc) return rc;
   }
@@ -658,6 +687,7 @@ static int enqueue_rollout(sim_ctx* x, const void* d_weights, int32_t T, const s
              return policy_launch(x, x->s.obs, k0 + (uint32_t)T, nullptr, nullptr,
                                   tr->value + (size_t)T * E, nullptr, nullptr, obs_bf);
            }), "policy kernel launch (final value)");
+  if (side) HIPCHK(hipStreamWaitEvent(x->stream, x->sev_join, 0), "hipStreamWaitEvent");
   return SIM_OK;
 }
 
