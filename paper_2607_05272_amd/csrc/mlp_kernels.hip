@@ -14,6 +14,8 @@
 // policy_bf16_k (bf16 policies): every layer's input rounded to bf16 (RNE), bf16 weights,
 // fp32 accumulation (v_mfma_f32_16x16x32_bf16), bias and GELU in fp32; its layout and
 // scheduling are described above the kernel.
+#include <type_traits>
+
 #include "devmath.hpp"
 #include "params.hpp"
 
@@ -145,12 +147,14 @@ __device__ __forceinline__ float action_uniform(uint64_t seed, uint32_t env, uin
 
 // us: the rows' uniforms, drawn beforehand (one lane per row), or NULL to draw them here (every
 // lane of a row's group then computes the same block).
-template <int AP, int ROWS, int NTHR>
+// AC: the action count when the padded width fixes it (0: m.A at run time); with it the
+// slices' bounds are compile-time and the per-logit guards vanish.
+template <int AP, int ROWS, int NTHR, int AC = 0>
 __device__ __forceinline__ void sample_rows(const float* lg, int sl, const MlpParams& m, int e0,
                                             uint64_t seed, uint32_t step, uint8_t* act,
                                             float* logp, float* value, float* logits,
                                             const float* us = nullptr) {
-  constexpr int G = 8, KMAX = (AP + G - 1) / G;
+  constexpr int G = 8, KMAX = AC > 0 ? (AC + G - 1) / G : (AP + G - 1) / G;
   static_assert(NTHR % G == 0, "sampler groups");
   const int tid = threadIdx.x;
   for (int row0 = 0; row0 < ROWS; row0 += NTHR / G) {
@@ -158,7 +162,7 @@ __device__ __forceinline__ void sample_rows(const float* lg, int sl, const MlpPa
     const int e = e0 + row;
     const bool live = row < ROWS && e < m.E;
     const float* l = lg + (row < ROWS ? row : 0) * sl;
-    const int A = m.A;
+    const int A = AC > 0 ? AC : m.A;
     const int chunk = (A + G - 1) / G;
     const int lo = part * chunk;
     float mx = -3.0e38f;
@@ -578,7 +582,8 @@ struct BigShape {
   static constexpr size_t LDS = X_BYTES + HREG + U_BYTES;
 };
 
-template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW, bool DBG>
+// AC: the action count compiled into the sampler (0: m.A at run time)
+template <int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW, bool DBG, int AC>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MINB / 4 > 0 ? NW * MINB / 4 : 1))) void policy_bf16_k(MlpParams m, const float* __restrict__ obs,
                                                                const uint32_t* __restrict__ obs_bf,
                                                                const uint64_t* __restrict__ seedp, uint32_t step,
@@ -669,17 +674,18 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW * MI
   __syncthreads();
   output_layer<H2, AP, RT, NW>(hs, Sh::SH, static_cast<const uint16_t*>(m.w3), m.b3, lg, Sh::SL);
   __syncthreads();
-  sample_rows<AP, ROWS, NTHR>(lg, Sh::SL, m, e0, seed, step, act, logp, value, logits, us);
+  sample_rows<AP, ROWS, NTHR, AC>(lg, Sh::SL, m, e0, seed, step, act, logp, value, logits, us);
 }
 
-template <bool DBG, int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW = 1>
+template <bool DBG, int FP, int H1, int H2, int AP, int RT, int NW, int MINB, int TPW, int AC>
 hipError_t run_policy_bf16(const MlpParams& m, const float* obs, const uint32_t* obs_bf,
                            const uint64_t* seed, uint32_t step,
                            uint8_t* act, float* logp, float* value, float* logits, float* hid,
                            hipStream_t st) {
   typedef BigShape<FP, H1, H2, AP, RT, NW> Sh;
   static_assert(Sh::LDS <= 160 * 1024, "LDS budget");
-  auto kern = policy_bf16_k<FP, H1, H2, AP, RT, NW, MINB, TPW, DBG>;
+  if (AC > 0 && m.A != AC) return hipErrorInvalidValue;
+  auto kern = policy_bf16_k<FP, H1, H2, AP, RT, NW, MINB, TPW, DBG, AC>;
   static bool attr = false;
   if (!attr) {
     hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -736,6 +742,19 @@ bool policy_shape_supported(const MlpParams& m) {
   return false;
 }
 
+// One bf16 shape: the configurations' own action count AC0 for that width (6K of their K)
+// compiled into the sampler, any other with run-time bounds (the diagnostic instantiation
+// always takes the run-time bounds; AC0 = 0 compiles none). run(big, ac) launches the variant.
+template <bool DBG, int AC0, class Run>
+static hipError_t run_shape_bf16(const MlpParams& m, bool big, Run&& run) {
+  typedef std::integral_constant<bool, true> T;
+  typedef std::integral_constant<bool, false> F;
+  typedef std::integral_constant<int, 0> A0;
+  typedef std::integral_constant<int, DBG ? 0 : AC0> AC;
+  if (!DBG && AC0 > 0 && m.A == AC0) return big ? run(T{}, AC{}) : run(F{}, AC{});
+  return big ? run(T{}, A0{}) : run(F{}, A0{});
+}
+
 template <bool DBG>
 static hipError_t launch_policy_t(const MlpParams& m, const float* obs, const uint32_t* obs_bf,
                                   const uint64_t* seed,
@@ -748,18 +767,36 @@ static hipError_t launch_policy_t(const MlpParams& m, const float* obs, const ui
   // bf16 shapes: 64-row tiles with 4 waves, two workgroups per CU, when there are enough
   // rows to fill the chip; 32-row tiles otherwise
   const bool big = m.E >= 64 * 512;
+#define BSIM_BF16_ARGS (m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st)
   if (m.bf16 && m.FP == 32 && m.H1 == 128 && m.H2 == 128 && m.AP == 16)
-    return big ? run_policy_bf16<DBG, 32, 128, 128, 16, 4, 8, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st)
-               : run_policy_bf16<DBG, 32, 128, 128, 16, 2, 4, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st);
+    return run_shape_bf16<DBG, 0>(m, big, [&](auto big_v, auto ac_v) {   // 6 measured slower
+      constexpr bool B = decltype(big_v)::value;
+      constexpr int C = decltype(ac_v)::value;
+      return B ? run_policy_bf16<DBG, 32, 128, 128, 16, 4, 8, 2, 1, C> BSIM_BF16_ARGS
+               : run_policy_bf16<DBG, 32, 128, 128, 16, 2, 4, 2, 1, C> BSIM_BF16_ARGS;
+    });
   if (m.bf16 && m.FP == 32 && m.H1 == 256 && m.H2 == 256 && m.AP == 32)
-    return big ? run_policy_bf16<DBG, 32, 256, 256, 32, 4, 8, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st)
-               : run_policy_bf16<DBG, 32, 256, 256, 32, 2, 4, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st);
+    return run_shape_bf16<DBG, 24>(m, big, [&](auto big_v, auto ac_v) {
+      constexpr bool B = decltype(big_v)::value;
+      constexpr int C = decltype(ac_v)::value;
+      return B ? run_policy_bf16<DBG, 32, 256, 256, 32, 4, 8, 2, 1, C> BSIM_BF16_ARGS
+               : run_policy_bf16<DBG, 32, 256, 256, 32, 2, 4, 2, 1, C> BSIM_BF16_ARGS;
+    });
   if (m.bf16 && m.FP == 64 && m.H1 == 256 && m.H2 == 256 && m.AP == 64)
-    return big ? run_policy_bf16<DBG, 64, 256, 256, 64, 4, 8, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st)
-               : run_policy_bf16<DBG, 64, 256, 256, 64, 2, 4, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st);
+    return run_shape_bf16<DBG, 48>(m, big, [&](auto big_v, auto ac_v) {
+      constexpr bool B = decltype(big_v)::value;
+      constexpr int C = decltype(ac_v)::value;
+      return B ? run_policy_bf16<DBG, 64, 256, 256, 64, 4, 8, 2, 1, C> BSIM_BF16_ARGS
+               : run_policy_bf16<DBG, 64, 256, 256, 64, 2, 4, 2, 1, C> BSIM_BF16_ARGS;
+    });
   if (m.bf16 && m.FP == 96 && m.H1 == 512 && m.H2 == 512 && m.AP == 112)
-    return big ? run_policy_bf16<DBG, 96, 512, 512, 112, 4, 8, 2, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st)
-               : run_policy_bf16<DBG, 96, 512, 512, 112, 2, 4, 2>(m, obs, obs_bf, seed, step, act, logp, value, logits, hid, st);
+    return run_shape_bf16<DBG, 96>(m, big, [&](auto big_v, auto ac_v) {
+      constexpr bool B = decltype(big_v)::value;
+      constexpr int C = decltype(ac_v)::value;
+      return B ? run_policy_bf16<DBG, 96, 512, 512, 112, 4, 8, 2, 2, C> BSIM_BF16_ARGS
+               : run_policy_bf16<DBG, 96, 512, 512, 112, 2, 4, 2, 1, C> BSIM_BF16_ARGS;
+    });
+#undef BSIM_BF16_ARGS
   return hipErrorInvalidValue;
 }
 
