@@ -62,7 +62,7 @@ constexpr double kTwoPi = 0x1.921fb54442d18p+2;
 
 // Natural log of a positive normal x. With x = 2^e m, m in (sqrt2/2, sqrt2]:
 // log m = 2 atanh s, s = (m-1)/(m+1); atanh s = s + s^3/3 + s^5/5 + ... to s^23/23.
-__device__ __noinline__ double dlog(double x) {
+__device__ __forceinline__ double dlog_inl(double x) {
   const uint64_t b = (uint64_t)__double_as_longlong(x);
   int e = (int)((b >> 52) & 0x7ff) - 1023;
   double m = __longlong_as_double((long long)((b & 0x000fffffffffffffull) | 0x3ff0000000000000ull));
@@ -86,7 +86,7 @@ __device__ __noinline__ double dlog(double x) {
 }
 
 // exp x for |x| < 700: x = k ln2 + r, |r| <= ln2/2; exp r = sum_{n<=14} r^n/n!; times 2^k.
-__device__ __noinline__ double dexp(double x) {
+__device__ __forceinline__ double dexp_inl(double x) {
   const double kd = floor(x * kInvLn2 + 0.5);
   const int k = (int)kd;
   const double r = (x - kd * kLn2Hi) - kd * kLn2Lo;
@@ -111,7 +111,7 @@ __device__ __noinline__ double dexp(double x) {
 
 // cos x for 0 <= x <= 8: x = q pi/2 + r, |r| <= pi/4; by q mod 4 the value is cos r,
 // -sin r, -cos r, sin r, with the Taylor series of cos to r^18/18! and sin to r^19/19!.
-__device__ __noinline__ double dcos(double x) {
+__device__ __forceinline__ double dcos_inl(double x) {
   const double qd = floor(x * kTwoOverPi + 0.5);
   const int q = (int)qd;
   const double r = (x - qd * kPio2Hi) - qd * kPio2Lo;
@@ -143,6 +143,13 @@ __device__ __noinline__ double dcos(double x) {
     default: return s;
   }
 }
+
+// Out-of-line copies of the three (one call site each in the code, instead of the body at every
+// use): kernels held to 128 VGPRs call these; kernels with registers to spare inline the
+// bodies above. The same operations either way, so the results are the same bits.
+__device__ __noinline__ double dlog(double x) { return dlog_inl(x); }
+__device__ __noinline__ double dexp(double x) { return dexp_inl(x); }
+__device__ __noinline__ double dcos(double x) { return dcos_inl(x); }
 
 // fp32 -> bf16 bits, round to nearest even (finite inputs).
 __device__ __forceinline__ uint16_t bf16_bits(float f) {

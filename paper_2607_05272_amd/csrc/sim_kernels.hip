@@ -175,10 +175,13 @@ __device__ __forceinline__ void store_arrivals(const Arrivals& A, const SysState
   if (p.arrival_kind == 1) g.tr_idx[e] = A.tr_idx;
 }
 
+template <bool INL = false>
 __device__ __forceinline__ double dwell(const SimParams& p, int st, double u) {
   const int kind = pick<kMaxS>(p.dwell_kind, st);
-  if (kind == 1) return -dlog(u) * pick<kMaxS>(p.dwell_mean, st);
-  if (kind == 2) return pick<kMaxS>(p.xm, st) * dexp(-dlog(u) * pick<kMaxS>(p.inv_alpha, st));
+  auto lg = [](double v) { return INL ? dlog_inl(v) : dlog(v); };
+  auto ex = [](double v) { return INL ? dexp_inl(v) : dexp(v); };
+  if (kind == 1) return -lg(u) * pick<kMaxS>(p.dwell_mean, st);
+  if (kind == 2) return pick<kMaxS>(p.xm, st) * ex(-lg(u) * pick<kMaxS>(p.inv_alpha, st));
   if (kind == 3) return pick<kMaxS>(p.dwell_mean, st);  // fixed dwell: square wave
   return kInf;
 }
@@ -243,7 +246,8 @@ __device__ __forceinline__ void wave_refill(Stage<KS>& st, bool need, bool burst
   if (need) staged_hi = jneed + (uint32_t)n;
 }
 
-template <int CM, int KS>
+// INL: the logarithm inline (kernels with registers to spare) rather than called
+template <int CM, int KS, bool INL = false>
 __device__ __forceinline__ void refill_arrivals(Stage<KS>& st, const SimParams& p, bool need,
                                                 uint32_t jneed, uint32_t& staged_hi,
                                                 uint64_t seed, int e_lane0, uint32_t k, int lane) {
@@ -254,7 +258,7 @@ __device__ __forceinline__ void refill_arrivals(Stage<KS>& st, const SimParams& 
   wave_refill<KS>(st, need, burst, jneed, k, staged_hi, lane, [&](uint32_t own, uint32_t kk,
                                                                    uint32_t j) {
     const u32x4 d = draw(seed, (uint32_t)(e_lane0 + (int)own), kk, P_ARRIVAL, j, 0);
-    st.E[j % KS][own] = -dlog(unit(d.x, d.y));
+    st.E[j % KS][own] = -(INL ? dlog_inl(unit(d.x, d.y)) : dlog(unit(d.x, d.y)));
     const double uc = unit(d.z, d.w);
     int cls = CM - 1;
 #pragma unroll
@@ -268,7 +272,7 @@ __device__ __forceinline__ void refill_arrivals(Stage<KS>& st, const SimParams& 
 // arrival from the switch instant). Returns the class of an arrival at `now`, or -1. ARRIVAL
 // blocks are read from the stage (the caller guarantees that the two blocks an instant can
 // consume, a switch redraw and an arrival, are staged).
-template <int CM, int KS>
+template <int CM, int KS, bool INL = false>
 __device__ __forceinline__ int advance_staged(Arrivals& A, const SimParams& p, const Stage<KS>& st,
                                               int lane, uint64_t seed, int e, uint32_t k,
                                               double now) {
@@ -283,7 +287,7 @@ __device__ __forceinline__ int advance_staged(Arrivals& A, const SimParams& p, c
     }
     A.proc = (uint32_t)nxt;
     A.gap = pick<kMaxS>(p.mean_gap, nxt);
-    A.next_sw = now + dwell(p, nxt, unit(w.x, w.y));
+    A.next_sw = now + dwell<INL>(p, nxt, unit(w.x, w.y));
     if (pick<kMaxS>(p.rate, nxt) > 0.0) {
       const uint32_t j = A.jarr++;
       A.next_arr = now + st.E[j % KS][lane] * A.gap;
@@ -363,24 +367,26 @@ __device__ __forceinline__ void enqueue_sel(Queue<CM>& Q, Count& C, const SimPar
 // -log(u1) (alpha + beta n), with u1, u2 from SERVICE block j of (env, tick, system). Inline in
 // both tick kernels: as a call it saved and restored registers through scratch memory at every
 // dispatch (its fp64 elementary functions stay out of line, see devmath.hpp).
+template <bool INL = false>
 __device__ __forceinline__ double service_draw(int kind, double al, double be, double med,
                                             double sigma, int n, uint64_t seed, uint32_t env,
                                             uint32_t k, uint32_t j, uint32_t sys) {
   const u32x4 w = draw(seed, env, k, P_SERVICE, j, sys);
   const double u1 = unit(w.x, w.y);
-  if (kind == 2) return -dlog(u1) * (al + be * (double)n);
+  auto lg = [](double v) { return INL ? dlog_inl(v) : dlog(v); };
+  if (kind == 2) return -lg(u1) * (al + be * (double)n);
   const double u2 = unit(w.z, w.w);
-  const double z = sqrt(-2.0 * dlog(u1)) * dcos(kTwoPi * u2);
-  return med * dexp(sigma * z) + be * (double)n;
+  const double z = sqrt(-2.0 * lg(u1)) * (INL ? dcos_inl(kTwoPi * u2) : dcos(kTwoPi * u2));
+  return med * (INL ? dexp_inl(sigma * z) : dexp(sigma * z)) + be * (double)n;
 }
 
-template <int CM>
+template <int CM, bool INL = false>
 __device__ __forceinline__ double service(Count& C, const SimParams& p, uint64_t seed, int e,
                                           uint32_t k, int sys, int h, int n) {
   const int kind = pick<CM>(p.svc_kind, h);
   const double al = pick<CM>(p.svc_alpha, h), be = pick<CM>(p.svc_beta, h);
   if (kind == 0) return al + be * (double)n;
-  return service_draw(kind, al, be, pick<CM>(p.svc_median, h), p.svc_sigma, n, seed,
+  return service_draw<INL>(kind, al, be, pick<CM>(p.svc_median, h), p.svc_sigma, n, seed,
                       (uint32_t)e, k, C.jsvc++, (uint32_t)sys);
 }
 
@@ -491,6 +497,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF ? 1 : 4)
     float* __restrict__ obs_out, int obs_mode, double* __restrict__ rew,
     uint64_t* __restrict__ rchk) {
   const uint64_t seed = *g.seed;   // the episode seed, written by reset_k
+  // the fp64 logarithm, exponential and cosine of the arrival, switch and service draws
+  // inline rather than called: a call waits for every outstanding memory access first and
+  // saves registers, which waves that have a SIMD to themselves can spare (measured with four
+  // request classes: the 8-server tick -4.9%; with fewer classes even or slower)
+  constexpr bool kInl = PF && CM >= 4;
   __shared__ Stage<kStageLearned> stage[4];
   const int lane = threadIdx.x & 63;
   Stage<kStageLearned>& st = stage[threadIdx.x >> 6];
@@ -566,11 +577,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF ? 1 : 4)
       }
     }
     if (__ballot(need) != 0ull)
-      refill_arrivals<CM>(st, p, need, A.jarr, staged_hi, seed, e_lane0, k, lane);
+      refill_arrivals<CM, kStageLearned, kInl>(st, p, need, A.jarr, staged_hi, seed, e_lane0,
+                                               k, lane);
     if (go) {
       ++it;
       now = te;
-      const int cls = advance_staged<CM>(A, p, st, lane, seed, ee, k, now);
+      const int cls = advance_staged<CM, kStageLearned, kInl>(A, p, st, lane, seed, ee, k, now);
       if (cls >= 0) {
         ++A_k;
         enqueue(Q, C, p, cls, now);
@@ -603,7 +615,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(PF ? 1 : 4)
         pend) {
       const int h = Q.hh;
       C.c[C_DONE] += meta_s & 0xffu;  // the previous batch on s finished at busy_s <= now
-      const double sv = service<CM>(C, p, seed, ee, k, 0, h, b);
+      const double sv = service<CM, kInl>(C, p, seed, ee, k, 0, h, b);
       busy_s = pop_batch(Q, C, p, k, s, h, b, now, sv);
       meta_s = (uint32_t)b | ((uint32_t)b << 8) | ((uint32_t)h << 16);
       dirty_s = true;
