@@ -671,6 +671,56 @@ def test_rollout_parity_and_validity(bs, orc, name):
     sim.close()
 
 
+@pytest.mark.parametrize("name,kw", [("C3", dict(obs_dim=31)), ("C5", {}), ("C1", {})])
+def test_rollout_observation_handoff(bs, orc, name, kw):
+    """Inside a rollout with a bf16 policy the ticks write the observation as the bf16 feature
+    pairs the policy reads, the pairs are packed from the fp32 observation when a rollout
+    starts, and the rollout's last tick writes the fp32 observation again. After a reset (which
+    writes only the fp32 observation): a rollout of one tick, a sim_step (fp32 only again), a
+    rollout of three ticks, a sim_step. The oracle's replay of the six ticks' actions gives the
+    same running checksums and, after each call, the same current observation; and the policy
+    kernel on the oracle's observation of every rollout tick (the fp32 input path) gives the
+    rollout's own action, which a stale or unpacked pair buffer would not. C3 with an odd
+    observation width (31: the last pair holds one feature and a zero) and C1's fp32 policy,
+    which keeps the fp32 observation throughout, take the same checks."""
+    w = workload(name, **kw)
+    E, seed = 300, 0x0B5E + len(name) + w["obs_dim"]
+    A = 6 * w["n_servers"]
+    wts = policy_weights(orc, w, 9)
+    say(f"[observation handoff] {name} F={w['obs_dim']}")
+    sim = bs.Sim(w, n_envs=E)
+    sim.reset(seed)
+    wb = sim.upload_weights(wts)
+    steps = seeded_actions(seed, 2, E, A, small_bias=0.5)
+    acts, cur, rollout_ticks, rchk = [], [], [], {}
+    tick = 0
+    for part, T in enumerate((1, 3)):
+        tr = sim.rollout(wb, T, rchk=True)
+        sim.sync()
+        acts.append(tr.actions.cpu().numpy())
+        for t in range(T):
+            rchk[tick + t] = tr.rchk.cpu().numpy().view(np.uint64)[t]
+            rollout_ticks.append(tick + t)
+        tick += T
+        cur.append((tick, sim.obs().cpu().numpy()))
+        sim.step(torch.from_numpy(steps[part]).cuda(), want_obs=False)
+        sim.sync()
+        acts.append(steps[part:part + 1])
+        tick += 1
+        cur.append((tick, sim.obs().cpu().numpy()))
+    ga = np.concatenate(acts)
+    rep = orc.rollout(w, seed, tick, np.arange(E), actions=ga, want_rchk=True)
+    for t, c in rchk.items():
+        assert np.array_equal(rep["rchk"][t], c), f"tick {t}: running checksums differ"
+    for t, o in cur:
+        assert np.array_equal(rep["obs"][t], o.T), f"current observation after tick {t}"
+    for t in rollout_ticks:
+        ob_t = torch.from_numpy(np.ascontiguousarray(rep["obs"][t].T)).cuda()
+        out = sim.policy(wb, ob_t, t)
+        assert np.array_equal(out["actions"].cpu().numpy(), ga[t]), f"tick {t}: not the rollout's action"
+    sim.close()
+
+
 SHADOWED = {
     "C5": lambda: preset("C5"),
     "burst": lambda: burst_preset(),
