@@ -249,7 +249,10 @@ int sim_policy_hidden(sim_ctx* ctx, const void* d_weights, const float* d_obs, u
 /* A rollout of the MDP (Sec. 4.1) under the policy of Sec. 4.2, the trajectory that the
  * updates of Sec. 4.3 consume: T ticks of policy + simulator from the current state
  * (obs_k -> a_k -> obs_{k+1}), writing the trajectory; with a value head, row T of
- * traj->value holds V(obs_T).                                                           */
+ * traj->value holds V(obs_T). Ordered on the context's stream like every other call: the
+ * static shadow system's launches run on a second stream of the context, forked from the
+ * context's stream when the rollout starts and joined back before it ends (one stream when
+ * sim_set_timing is on). Afterwards sim_obs returns obs_T.                              */
 int sim_rollout(sim_ctx* ctx, const void* d_weights, int32_t T, const sim_traj* traj);
 
 /* Rollout graphs, on by default: when sim_rollout is called again with the same weights
@@ -426,7 +429,7 @@ enum sim_kernel_class {
   SIM_KC_STATIC = 2,  /* static shadow system, one tick */
   SIM_KC_GAE = 3,     /* returns / GAE */
   SIM_KC_RESET = 4,   /* reset */
-  SIM_KC_OTHER = 5,   /* weight repack / init, counters, totals */
+  SIM_KC_OTHER = 5,   /* weight repack / init, observation packing, counters, totals */
   SIM_KC_PPO = 6,     /* policy update: minibatch gradients, Adam */
   SIM_KC_COUNT = 7
 };
