@@ -116,14 +116,17 @@ def static_bytes(w, tot, E, T, ticks_per_launch):
 
 
 # the source of each kernel class (with the shared device headers)
-KERNEL_SOURCE = {"policy": "mlp_kernels.hip", "step": "sim_kernels.hip",
-                 "static": "sim_kernels.hip", "gae": "gae_kernels.hip", "ppo": "ppo_kernels.hip"}
+KERNEL_SOURCE = {"policy": ["mlp_kernels.hip", "policy_dev.hpp"],
+                 "step": ["sim_kernels.hip", "sim_dev.hpp"],
+                 "static": ["sim_kernels.hip", "sim_dev.hpp"], "gae": ["gae_kernels.hip"],
+                 "ppo": ["ppo_kernels.hip"],
+                 "rollout": ["rollout_kernels.hip", "policy_dev.hpp", "sim_dev.hpp"]}
 
 
 def kernel_hash(cls=None):
     """Hash of the sources a kernel class is built from (all kernel sources without a class)."""
     d = os.path.join(ROOT, "paper_2607_05272_amd", "csrc")
-    files = ([KERNEL_SOURCE[cls], "devmath.hpp", "params.hpp"] if cls in KERNEL_SOURCE else
+    files = (KERNEL_SOURCE[cls] + ["devmath.hpp", "params.hpp"] if cls in KERNEL_SOURCE else
              sorted(f for f in os.listdir(d) if f.endswith((".hip", ".hpp"))))
     h = hashlib.sha256()
     for f in files:
@@ -339,6 +342,21 @@ def rooflines(w, kern, tot, E, T, train, args, cfg_name):
         rl["static"] = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": ach / PEAK_HBM_GBS, "traffic": traffic_for("static", cfg_name),
                         "work_per_launch": by}
+    if "rollout" in kern:
+        # the fused small-batch rollout: every tick's policy and learned tick in one launch,
+        # against both ceilings (a launch this small is bound by latency, far below either)
+        n_pol = T + (1 if w["value_head"] else 0)
+        fl = mlp_flops(w) * E * n_pol
+        by = step_bytes(w, tot, E, T) * E * T
+        sec = kern["rollout"]["avg_us"] * 1e-6
+        peak = PEAK_BF16_TFLOPS if w["mlp_bf16"] else PEAK_FP32_TFLOPS
+        rl["rollout"] = {"bound": "mfma", "achieved": fl / sec / 1e12, "peak": peak,
+                         "unit": "TFLOP/s", "frac": fl / sec / 1e12 / peak, "traffic": None,
+                         "work_per_launch": fl,
+                         "simulator": {"achieved": by / sec / 1e9, "peak": PEAK_HBM_GBS,
+                                       "unit": "GB/s", "frac": by / sec / 1e9 / PEAK_HBM_GBS,
+                                       "bytes_per_launch": by},
+                         "us_per_tick": kern["rollout"]["avg_us"] / T}
     if "gae" in kern:
         by = 28.0 * E * T
         ach = by / (kern["gae"]["avg_us"] * 1e-6) / 1e9
@@ -565,7 +583,8 @@ def main():
         line["configs"] = {}
         for name in ("C1", "C2", "C3", "C4"):
             _, r2, rl2, _ = measure(name, args, 3, 1, 2)
-            r2["roofline"] = {k: {kk: v[kk] for kk in ("bound", "achieved", "peak", "unit", "frac")}
+            r2["roofline"] = {k: {kk: v[kk] for kk in ("bound", "achieved", "peak", "unit", "frac",
+                                                     "simulator", "us_per_tick") if kk in v}
                               for k, v in rl2.items()}
             line["configs"][name] = r2
     if not args.no_cpu_baseline:

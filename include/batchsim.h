@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define BATCHSIM_ABI_VERSION 1u
+#define BATCHSIM_ABI_VERSION 2u
 
 enum sim_status {
   SIM_OK = 0,
@@ -265,6 +265,18 @@ int sim_rollout(sim_ctx* ctx, const void* d_weights, int32_t T, const sim_traj* 
  * on = 0 launches every rollout eagerly.                                                    */
 int sim_set_graphs(sim_ctx* ctx, int32_t on);
 
+/* Fused rollouts of small batches (Sec. 4.1-4.2: the same ticks and policy as above): with a
+ * few thousand environments a tick's two launches are bound by their start-up and memory
+ * latency rather than their work, so sim_rollout may instead run all T ticks in one launch,
+ * each workgroup alternating the policy and the tick of its own environments (outputs
+ * bit-identical to the per-tick launches). mode SIM_FUSE_AUTO (the default) fuses when the
+ * policy is an MLP of a shape that has a fused kernel (8-64-64-6 fp32, 12-128-128-6 bf16) and
+ * n_envs <= SIM_FUSE_MAX_ENVS; SIM_FUSE_ON fuses whenever the shape has a fused kernel;
+ * SIM_FUSE_OFF always launches per tick. SIM_EINVAL for another mode. A change discards the
+ * rollout graph.                                                                          */
+enum { SIM_FUSE_OFF = 0, SIM_FUSE_AUTO = 1, SIM_FUSE_ON = 2, SIM_FUSE_MAX_ENVS = 8192 };
+int sim_set_fused_rollout(sim_ctx* ctx, int32_t mode);
+
 /* Diagnostics of the rollout graphs: graphs captured and rollouts replayed from a graph so far
  * (either pointer may be NULL).                                                          */
 int sim_graph_stats(sim_ctx* ctx, int64_t* h_captures, int64_t* h_replays);
@@ -431,7 +443,8 @@ enum sim_kernel_class {
   SIM_KC_RESET = 4,   /* reset */
   SIM_KC_OTHER = 5,   /* weight repack / init, observation packing, counters, totals */
   SIM_KC_PPO = 6,     /* policy update: minibatch gradients, Adam */
-  SIM_KC_COUNT = 7
+  SIM_KC_ROLLOUT = 7, /* fused rollout: every tick's policy and learned tick in one launch */
+  SIM_KC_COUNT = 8
 };
 
 /* Tracing: with `on` != 0 every kernel launch of the context is bracketed by a pair of

@@ -6,4 +6,5 @@ in the library's HIP kernels. Torch provides device memory and the stream.
 """
 from .sim import (Sim, weights_layout, pack_weights, unpack_weights,  # noqa: F401
                   Trajectory)
-from ._lib import SimError, load, ALGO_PPO, ALGO_REINFORCE  # noqa: F401
+from ._lib import (SimError, load, ALGO_PPO, ALGO_REINFORCE, FUSE_OFF, FUSE_AUTO,  # noqa: F401
+                   FUSE_ON, FUSE_MAX_ENVS)

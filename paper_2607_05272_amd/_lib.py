@@ -11,7 +11,7 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libbatchsim.so")
 
-ABI_VERSION = 1
+ABI_VERSION = 2
 MAX_K, MAX_C, MAX_S = 16, 4, 4
 NCNT, NSUM = 7, 2
 STATUS = {0: "SIM_OK", -1: "SIM_EINVAL", -2: "SIM_ENOMEM", -3: "SIM_EDEVICE", -4: "SIM_ESTATE",
@@ -24,9 +24,10 @@ SYMBOLS = ("sim_last_error", "sim_abi_version", "sim_create", "sim_destroy", "si
            "ppo_minibatch_grad", "sim_ppo_grad_count", "reinforce_minibatch_grad",
            "sim_params_from_weights", "adam_update", "sim_update", "sim_attn_weights_layout",
            "sim_get_state", "sim_set_state", "sim_device_primitive", "sim_policy_hidden", "sim_set_graphs", "sim_graph_stats",
-           "ppo_minibatch_grad_noalloc")
+           "ppo_minibatch_grad_noalloc", "sim_set_fused_rollout")
 ALGO_PPO, ALGO_REINFORCE = 0, 1
-KERNEL_CLASSES = ("policy", "step", "static", "gae", "reset", "other", "ppo")
+KERNEL_CLASSES = ("policy", "step", "static", "gae", "reset", "other", "ppo", "rollout")
+FUSE_OFF, FUSE_AUTO, FUSE_ON, FUSE_MAX_ENVS = 0, 1, 2, 8192
 
 
 class SimCfg(C.Structure):
@@ -114,6 +115,7 @@ def load():
         "sim_checksums": [vp, vp], "sim_stats": [vp, vp], "sim_sync": [vp],
         "sim_set_timing": [vp, i32], "sim_get_timing": [vp, vp, vp, i32],
         "sim_set_graphs": [vp, i32], "sim_graph_stats": [vp, vp, vp],
+        "sim_set_fused_rollout": [vp, i32],
         "ppo_minibatch_grad": [vp, vp, i32, vp, vp, vp, vp, vp, i32, u64, C.c_float, C.c_float,
                                C.c_float, vp, vp, vp],
         "ppo_minibatch_grad_noalloc": [vp, vp, i32, vp, vp, vp, vp, vp, i32, u64, C.c_float,

@@ -15,8 +15,8 @@ LIB = os.path.join(HERE, "libbatchsim.so")
 BUILD = os.path.join(HERE, "_build")
 SOURCES = ["runtime.cpp", "sim_kernels.hip", "mlp_kernels.hip", "gae_kernels.hip",
            "ppo_kernels.hip", "train_kernels.hip", "attn_kernels.hip",
-           "prim_kernels.hip"]
-HEADERS = ["devmath.hpp", "params.hpp"]
+           "prim_kernels.hip", "rollout_kernels.hip"]
+HEADERS = ["devmath.hpp", "params.hpp", "policy_dev.hpp", "sim_dev.hpp"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",
          "-fno-fast-math", "-Wall", "-Wno-unused-function",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -108,6 +108,24 @@ hipError_t launch_policy(const MlpParams& m, const float* obs, const uint32_t* o
                          float* value, float* logits, float* hidden, hipStream_t st);
 hipError_t launch_init_weights(int F, int H1, int H2, int Ap, int bf16, uint64_t seed,
                                void* d_weights, const size_t off[6], hipStream_t st);
+
+// Trajectory rows written by a fused rollout: act, logp, value, rew, rchk [T][E] (value
+// [T + 1][E]), obs [T + 1][F][E] from row 1; NULL entries (act excepted) are not written.
+struct RolloutOut {
+  uint8_t* act;
+  float* logp;
+  float* value;
+  double* rew;
+  uint64_t* rchk;
+  float* obs;
+};
+// policy shapes that have a fused rollout kernel
+bool fused_rollout_supported(const MlpParams& m);
+// T ticks from k0 of the learned system with its MLP policy in one launch (the static shadow
+// system is not part of it); a bf16 policy needs s.obs_bf packed from s.obs beforehand.
+// hipErrorNotSupported for other policy shapes.
+hipError_t launch_rollout_fused(const SimParams& p, const EnvState& s, const MlpParams& m,
+                                uint32_t k0, int T, const RolloutOut& o, hipStream_t st);
 bool policy_shape_supported(const MlpParams& m);
 
 // The attention policy (attn_kernels.hip): fp32 weights [in][out] inside the caller's

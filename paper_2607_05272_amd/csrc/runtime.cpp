@@ -90,6 +90,7 @@ struct sim_ctx {
   hipEvent_t sev_fork = nullptr, sev_join = nullptr;
   RolloutKey rkey{}, seen{};
   bool rkey_valid = false, seen_valid = false;
+  int fuse = SIM_FUSE_AUTO;   // fused small-batch rollouts (sim_set_fused_rollout)
   int64_t graph_captures = 0, graph_replays = 0;
   // tracing: event pairs around kernel launches, per kernel class
   struct Pending { int cls; hipEvent_t a, b; };
@@ -333,7 +334,9 @@ int sim_create(const sim_cfg* cfg, void* hip_stream, sim_ctx** out) {
     *pr.first = static_cast<unsigned char*>(x->arena) + off;
     off += align256(pr.second);
   }
-  he = hipMemsetAsync(x->s.err, 0, 512, x->stream);   // error flags and the seed word
+  // every byte zero, the arrays' alignment padding included, so that snapshots of equal
+  // states are equal byte for byte (and the error flags start cleared)
+  he = hipMemsetAsync(x->arena, 0, total, x->stream);
   if (he != hipSuccess) {
     (void)hipFree(x->arena);
     delete x;
@@ -627,6 +630,14 @@ int sim_policy_hidden(sim_ctx* x, const void* d_weights, const float* d_obs, uin
   return SIM_OK;
 }
 
+// whether a rollout runs as one fused launch (sim_set_fused_rollout)
+static bool use_fused(const sim_ctx* x) {
+  if (x->fuse == SIM_FUSE_OFF || x->cfg.policy_kind != SIM_POLICY_MLP ||
+      !fused_rollout_supported(x->m))
+    return false;
+  return x->fuse == SIM_FUSE_ON || x->cfg.n_envs <= SIM_FUSE_MAX_ENVS;
+}
+
 // Every launch of a rollout of T ticks from tick k0 on x->stream: the policy's weight repack,
 // the static shadow system in multi-tick launches, then per tick the policy and the learned
 // system's tick, and the final value. Its arguments depend only on the weights pointer, T, the
@@ -667,6 +678,14 @@ static int enqueue_rollout(sim_ctx* x, const void* d_weights, int32_t T, const s
   if (obs_bf)
     HIPCHK(x->timed(SIM_KC_OTHER, [&] { return launch_obs_pack(x->p, x->s, x->stream); }),
            "observation packing launch");
+  if (use_fused(x)) {
+    const RolloutOut o{tr->actions, tr->logp, tr->value, tr->reward, tr->rchk, tr->obs};
+    HIPCHK(x->timed(SIM_KC_ROLLOUT, [&] {
+             return launch_rollout_fused(x->p, x->s, x->m, k0, T, o, x->stream);
+           }), "fused rollout launch");
+    if (side) HIPCHK(hipStreamWaitEvent(x->stream, x->sev_join, 0), "hipStreamWaitEvent");
+    return SIM_OK;
+  }
   for (int32_t i = 0; i < T; ++i) {
     const size_t row = (size_t)i * E;
     const uint32_t k = k0 + (uint32_t)i;
@@ -778,6 +797,15 @@ int sim_rollout(sim_ctx* x, const void* d_weights, int32_t T, const sim_traj* tr
 int sim_set_graphs(sim_ctx* x, int32_t on) {
   if (!x) return fail(SIM_EINVAL, "ctx is NULL");
   x->graphs = on != 0;
+  return SIM_OK;
+}
+
+int sim_set_fused_rollout(sim_ctx* x, int32_t mode) {
+  if (!x) return fail(SIM_EINVAL, "ctx is NULL");
+  if (mode != SIM_FUSE_OFF && mode != SIM_FUSE_AUTO && mode != SIM_FUSE_ON)
+    return fail(SIM_EINVAL, "fused rollout mode %d", (int)mode);
+  if (mode != x->fuse) x->rkey_valid = x->seen_valid = false;   // the graph holds the other form
+  x->fuse = mode;
   return SIM_OK;
 }
 

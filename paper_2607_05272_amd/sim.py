@@ -380,6 +380,11 @@ class Sim:
         """Rollout graphs on (default) or off (every rollout launched eagerly)."""
         L.check(self.lib.sim_set_graphs(self._ctx, 1 if on else 0), "sim_set_graphs")
 
+    def set_fused_rollout(self, mode):
+        """Fused small-batch rollouts: FUSE_AUTO (default), FUSE_ON or FUSE_OFF (per-tick
+        launches); see sim_set_fused_rollout."""
+        L.check(self.lib.sim_set_fused_rollout(self._ctx, int(mode)), "sim_set_fused_rollout")
+
     def graph_stats(self):
         """(graphs captured, rollouts replayed from a graph)."""
         c, r = C.c_int64(0), C.c_int64(0)
