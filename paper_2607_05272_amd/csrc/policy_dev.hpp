@@ -138,7 +138,48 @@ struct Shape {
 // uniform of (env, step), its log-probability and the value output. G lanes per row (an
 // aligned group of G lanes), each over a contiguous slice of the actions whose exponentials
 // it keeps in registers; max, prefix sums and the first slice holding the target u*S by
-// shuffles within the group.
+// DPP moves within the group (below), the same operands in the same order as a chain of
+// shuffles would combine, without a round trip through LDS for each of the ten steps.
+//
+// Cross-lane moves within aligned groups of 8 lanes (half a DPP row of 16): lane ^ 1 and
+// lane ^ 2 as quad permutations, 7 - lane as the half-row mirror, lane - d (d = 1, 2, 4) as
+// a row shift (lanes without a source keep 0; the callers mask them), and lane 3 of each quad.
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppQuad3 = 0xFF, kDppHalfMirror = 0x141;
+constexpr int kDppShr = 0x110;   // + d: row shift right by d
+template <int CTRL>
+__device__ __forceinline__ int dpp8(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp8(float v) {
+  return __int_as_float(dpp8<CTRL>(__float_as_int(v)));
+}
+// max / min over the lane's group of 8: within each quad, then across the two quads
+__device__ __forceinline__ float group8_max(float v) {
+  v = fmaxf(v, dpp8<kDppXor1>(v));
+  v = fmaxf(v, dpp8<kDppXor2>(v));
+  return fmaxf(v, dpp8<kDppHalfMirror>(v));
+}
+__device__ __forceinline__ int group8_min(int v) {
+  v = min(v, dpp8<kDppXor1>(v));
+  v = min(v, dpp8<kDppXor2>(v));
+  return min(v, dpp8<kDppHalfMirror>(v));
+}
+// inclusive prefix sum over the group (part = lane % 8), in the order of a shift-by-1, 2, 4
+// scan, and the group's total (lane 7's prefix) in every lane
+__device__ __forceinline__ float group8_scan(float v, int part, float& total) {
+  float t = dpp8<kDppShr + 1>(v);
+  if (part >= 1) v += t;
+  t = dpp8<kDppShr + 2>(v);
+  if (part >= 2) v += t;
+  t = dpp8<kDppShr + 4>(v);
+  if (part >= 4) v += t;
+  const float q3 = dpp8<kDppQuad3>(v);         // lanes 0-3: lane 3's prefix; 4-7: lane 7's
+  const float m3 = dpp8<kDppHalfMirror>(q3);   // lanes 0-3: lane 7's (from lanes 7..4)
+  total = part >= 4 ? q3 : m3;
+  return v;
+}
+
 // The ACTION uniform of a row's environment: ((w.x >> 9) + 1/2) 2^-23 from its block.
 __device__ __forceinline__ float action_uniform(uint64_t seed, uint32_t env, uint32_t step) {
   const u32x4 w = draw(seed, env, step, P_ACTION, 0, 0);
@@ -155,7 +196,7 @@ __device__ __forceinline__ void sample_rows(const float* lg, int sl, const MlpPa
                                             float* logp, float* value, float* logits,
                                             const float* us = nullptr) {
   constexpr int G = 8, KMAX = AC > 0 ? (AC + G - 1) / G : (AP + G - 1) / G;
-  static_assert(NTHR % G == 0, "sampler groups");
+  static_assert(NTHR % G == 0 && G == 8, "sampler groups of 8 lanes (group8_*)");
   const int tid = threadIdx.x;
   for (int row0 = 0; row0 < ROWS; row0 += NTHR / G) {
     const int row = row0 + tid / G, part = tid % G;
@@ -169,8 +210,7 @@ __device__ __forceinline__ void sample_rows(const float* lg, int sl, const MlpPa
 #pragma unroll
     for (int i = 0; i < KMAX; ++i)
       if (i < chunk && lo + i < A) mx = fmaxf(mx, l[lo + i]);
-#pragma unroll
-    for (int off = 1; off < G; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, G));
+    mx = group8_max(mx);
     float pe[KMAX];
     float ps = 0.f;
 #pragma unroll
@@ -178,13 +218,8 @@ __device__ __forceinline__ void sample_rows(const float* lg, int sl, const MlpPa
       pe[i] = (i < chunk && lo + i < A) ? __expf(l[lo + i] - mx) : 0.f;
       ps += pe[i];
     }
-    float incl = ps;
-#pragma unroll
-    for (int off = 1; off < G; off <<= 1) {
-      const float t = __shfl_up(incl, off, G);
-      if (part >= off) incl += t;
-    }
-    const float S = __shfl(incl, G - 1, G);
+    float S;
+    const float incl = group8_scan(ps, part, S);
     const float u = us ? us[row < ROWS ? row : 0]
                        : action_uniform(seed, (uint32_t)(live ? e : 0), step);
     const float target = u * S;
@@ -195,8 +230,7 @@ __device__ __forceinline__ void sample_rows(const float* lg, int sl, const MlpPa
       cum += pe[i];
       if (found == 0x7fffffff && i < chunk && lo + i < A && target < cum) found = lo + i;
     }
-#pragma unroll
-    for (int off = 1; off < G; off <<= 1) found = min(found, __shfl_xor(found, off, G));
+    found = group8_min(found);
     if (live && part == 0) {
       const int a = found < A ? found : A - 1;
       if (act) act[e] = (uint8_t)a;
