@@ -270,11 +270,12 @@ int sim_set_graphs(sim_ctx* ctx, int32_t on);
  * latency rather than their work, so sim_rollout may instead run all T ticks in one launch,
  * each workgroup alternating the policy and the tick of its own environments (outputs
  * bit-identical to the per-tick launches). mode SIM_FUSE_AUTO (the default) fuses when the
- * policy is an MLP of a shape that has a fused kernel (8-64-64-6 fp32, 12-128-128-6 bf16) and
- * n_envs <= SIM_FUSE_MAX_ENVS; SIM_FUSE_ON fuses whenever the shape has a fused kernel;
- * SIM_FUSE_OFF always launches per tick. SIM_EINVAL for another mode. A change discards the
- * rollout graph.                                                                          */
-enum { SIM_FUSE_OFF = 0, SIM_FUSE_AUTO = 1, SIM_FUSE_ON = 2, SIM_FUSE_MAX_ENVS = 8192 };
+ * policy is an MLP of a shape that has a fused kernel (the 8-64-64-6 fp32, 12-128-128-6,
+ * 32-256-256-24 and 64-256-256-48 bf16 networks, any action count up to the padded width)
+ * and all of the batch's workgroups of that kernel are resident on the GPU at once;
+ * SIM_FUSE_ON fuses whenever the shape has a fused kernel; SIM_FUSE_OFF always launches per
+ * tick. SIM_EINVAL for another mode. A change discards the rollout graph.                  */
+enum { SIM_FUSE_OFF = 0, SIM_FUSE_AUTO = 1, SIM_FUSE_ON = 2 };
 int sim_set_fused_rollout(sim_ctx* ctx, int32_t mode);
 
 /* Diagnostics of the rollout graphs: graphs captured and rollouts replayed from a graph so far

@@ -7,4 +7,4 @@ in the library's HIP kernels. Torch provides device memory and the stream.
 from .sim import (Sim, weights_layout, pack_weights, unpack_weights,  # noqa: F401
                   Trajectory)
 from ._lib import (SimError, load, ALGO_PPO, ALGO_REINFORCE, FUSE_OFF, FUSE_AUTO,  # noqa: F401
-                   FUSE_ON, FUSE_MAX_ENVS)
+                   FUSE_ON)

@@ -27,7 +27,7 @@ SYMBOLS = ("sim_last_error", "sim_abi_version", "sim_create", "sim_destroy", "si
            "ppo_minibatch_grad_noalloc", "sim_set_fused_rollout")
 ALGO_PPO, ALGO_REINFORCE = 0, 1
 KERNEL_CLASSES = ("policy", "step", "static", "gae", "reset", "other", "ppo", "rollout")
-FUSE_OFF, FUSE_AUTO, FUSE_ON, FUSE_MAX_ENVS = 0, 1, 2, 8192
+FUSE_OFF, FUSE_AUTO, FUSE_ON = 0, 1, 2
 
 
 class SimCfg(C.Structure):

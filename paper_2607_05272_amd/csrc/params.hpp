@@ -119,8 +119,9 @@ struct RolloutOut {
   uint64_t* rchk;
   float* obs;
 };
-// policy shapes that have a fused rollout kernel
-bool fused_rollout_supported(const MlpParams& m);
+// the number of environments whose workgroups of the fused rollout kernel are all resident on
+// the current device at once (0 with hipErrorNotSupported: no fused kernel for the network)
+hipError_t fused_rollout_capacity(const SimParams& p, const MlpParams& m, int* max_envs);
 // T ticks from k0 of the learned system with its MLP policy in one launch (the static shadow
 // system is not part of it); a bf16 policy needs s.obs_bf packed from s.obs beforehand.
 // hipErrorNotSupported for other policy shapes.

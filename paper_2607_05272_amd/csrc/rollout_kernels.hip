@@ -86,36 +86,85 @@ __global__ __launch_bounds__(256) void rollout_fused_k(SimParams p, EnvState g, 
              smem, e0);
 }
 
-template <int TW, class Pol>
-hipError_t run_fused(const SimParams& p, const EnvState& s, const MlpParams& m, uint32_t k0, int T,
-                     const RolloutOut& o, hipStream_t st) {
-  static_assert(Pol::LDS <= 64 * 1024, "LDS budget");
+template <int CM, int TW, class Pol>
+hipError_t launch_fused(const SimParams& p, const EnvState& s, const MlpParams& m, uint32_t k0,
+                        int T, const RolloutOut& o, hipStream_t st) {
+  static_assert(Pol::LDS + sizeof(Stage<kStageLearned>) * TW <= 160 * 1024, "LDS budget");
+  auto kern = rollout_fused_k<CM, TW, Pol>;
+  static bool attr = false;   // dynamic LDS beyond the default limit, once per kernel
+  if (!attr) {
+    const hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)Pol::LDS);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
   const dim3 grid((p.E + Pol::ROWS - 1) / Pol::ROWS), block(256);
-  if (p.C <= 1)
-    hipLaunchKernelGGL((rollout_fused_k<1, TW, Pol>), grid, block, Pol::LDS, st, p, s, m, k0, T, o);
-  else if (p.C <= 2)
-    hipLaunchKernelGGL((rollout_fused_k<2, TW, Pol>), grid, block, Pol::LDS, st, p, s, m, k0, T, o);
-  else
-    hipLaunchKernelGGL((rollout_fused_k<4, TW, Pol>), grid, block, Pol::LDS, st, p, s, m, k0, T, o);
+  hipLaunchKernelGGL(kern, grid, block, Pol::LDS, st, p, s, m, k0, T, o);
   return hipGetLastError();
+}
+
+template <int CM, int TW, class P>
+struct FusedTag {
+  static constexpr int kCM = CM, kTW = TW;
+  typedef P Pol;
+};
+template <class P>
+struct PolTag {
+  typedef P Pol;
+};
+
+// f(FusedTag<CM, TW, Pol>{}) for the configuration's fused kernel: the policy network's shape
+// (and, where it is the configurations' own, its action count compiled into the sampler), the
+// class count; hipErrorNotSupported for a network without one
+template <class F>
+hipError_t with_fused(const SimParams& p, const MlpParams& m, F&& f) {
+  auto by_classes = [&](auto pol) -> hipError_t {
+    typedef typename decltype(pol)::Pol Pol;
+    if (p.C <= 1) return f(FusedTag<1, 4, Pol>{});
+    if (p.C <= 2) return f(FusedTag<2, 4, Pol>{});
+    return f(FusedTag<4, 4, Pol>{});
+  };
+  if (!m.bf16 && m.FP == 8 && m.H1 == 64 && m.H2 == 64 && m.AP == 16)
+    return by_classes(PolTag<PolicyF32<8, 64, 64, 16>>{});
+  if (m.bf16 && m.FP == 32 && m.H1 == 128 && m.H2 == 128 && m.AP == 16)
+    return by_classes(PolTag<PolicyBf16<32, 128, 128, 16, 1, 0>>{});
+  if (m.bf16 && m.FP == 32 && m.H1 == 256 && m.H2 == 256 && m.AP == 32)
+    return m.A == 24 ? by_classes(PolTag<PolicyBf16<32, 256, 256, 32, 4, 24>>{})
+                     : by_classes(PolTag<PolicyBf16<32, 256, 256, 32, 4, 0>>{});
+  if (m.bf16 && m.FP == 64 && m.H1 == 256 && m.H2 == 256 && m.AP == 64)
+    return m.A == 48 ? by_classes(PolTag<PolicyBf16<64, 256, 256, 64, 4, 48>>{})
+                     : by_classes(PolTag<PolicyBf16<64, 256, 256, 64, 4, 0>>{});
+  return hipErrorNotSupported;
 }
 
 }  // namespace
 
-bool fused_rollout_supported(const MlpParams& m) {
-  if (!m.bf16) return m.FP == 8 && m.H1 == 64 && m.H2 == 64 && m.AP == 16;
-  return m.FP == 32 && m.H1 == 128 && m.H2 == 128 && m.AP == 16;
+hipError_t fused_rollout_capacity(const SimParams& p, const MlpParams& m, int* max_envs) {
+  *max_envs = 0;
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  return with_fused(p, m, [&](auto t) -> hipError_t {
+    typedef typename decltype(t)::Pol Pol;
+    int per_cu = 0;
+    const hipError_t e2 = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &per_cu, rollout_fused_k<decltype(t)::kCM, decltype(t)::kTW, Pol>, 256, Pol::LDS);
+    if (e2 != hipSuccess) return e2;
+    *max_envs = per_cu * cus * Pol::ROWS;
+    return hipSuccess;
+  });
 }
 
 hipError_t launch_rollout_fused(const SimParams& p, const EnvState& s, const MlpParams& m,
                                 uint32_t k0, int T, const RolloutOut& o, hipStream_t st) {
   if (T < 1 || !o.act) return hipErrorInvalidValue;
   if (m.bf16 && !s.obs_bf) return hipErrorInvalidValue;
-  if (!m.bf16 && m.FP == 8 && m.H1 == 64 && m.H2 == 64 && m.AP == 16)
-    return run_fused<4, PolicyF32<8, 64, 64, 16>>(p, s, m, k0, T, o, st);
-  if (m.bf16 && m.FP == 32 && m.H1 == 128 && m.H2 == 128 && m.AP == 16)
-    return run_fused<4, PolicyBf16<32, 128, 128, 16, 1, 0>>(p, s, m, k0, T, o, st);
-  return hipErrorNotSupported;
+  return with_fused(p, m, [&](auto t) -> hipError_t {
+    return launch_fused<decltype(t)::kCM, decltype(t)::kTW, typename decltype(t)::Pol>(
+        p, s, m, k0, T, o, st);
+  });
 }
 
 }  // namespace bsim

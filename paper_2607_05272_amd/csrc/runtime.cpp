@@ -91,6 +91,7 @@ struct sim_ctx {
   RolloutKey rkey{}, seen{};
   bool rkey_valid = false, seen_valid = false;
   int fuse = SIM_FUSE_AUTO;   // fused small-batch rollouts (sim_set_fused_rollout)
+  int fuse_cap = -1;          // environments the fused kernel holds at once (0: none; -1: not asked)
   int64_t graph_captures = 0, graph_replays = 0;
   // tracing: event pairs around kernel launches, per kernel class
   struct Pending { int cls; hipEvent_t a, b; };
@@ -630,12 +631,17 @@ int sim_policy_hidden(sim_ctx* x, const void* d_weights, const float* d_obs, uin
   return SIM_OK;
 }
 
-// whether a rollout runs as one fused launch (sim_set_fused_rollout)
-static bool use_fused(const sim_ctx* x) {
-  if (x->fuse == SIM_FUSE_OFF || x->cfg.policy_kind != SIM_POLICY_MLP ||
-      !fused_rollout_supported(x->m))
-    return false;
-  return x->fuse == SIM_FUSE_ON || x->cfg.n_envs <= SIM_FUSE_MAX_ENVS;
+// whether a rollout runs as one fused launch (sim_set_fused_rollout): forced on, whenever the
+// network has a fused kernel; automatically, when all of the batch's workgroups of that kernel
+// are resident at once (a second round would run every tick again for its workgroups alone)
+static bool use_fused(sim_ctx* x) {
+  if (x->fuse == SIM_FUSE_OFF || x->cfg.policy_kind != SIM_POLICY_MLP) return false;
+  if (x->fuse_cap < 0) {
+    int cap = 0;
+    x->fuse_cap = fused_rollout_capacity(x->p, x->m, &cap) == hipSuccess && cap > 0 ? cap : 0;
+  }
+  if (x->fuse_cap == 0) return false;
+  return x->fuse == SIM_FUSE_ON || x->cfg.n_envs <= x->fuse_cap;
 }
 
 // Every launch of a rollout of T ticks from tick k0 on x->stream: the policy's weight repack,

@@ -3,7 +3,7 @@ policy and the learned tick of its own environments) against the per-tick launch
 the C ABI. Both run the same device code, so every trajectory output, the current
 observation, the environments' state, the counters and the checksums must be bit-identical.
 The oracle parity of the rollout itself (test_gpu_parity.py) covers the fused kernel too: at
-these batch sizes sim_rollout fuses by default."""
+those batch sizes sim_rollout fuses by default."""
 import sys
 
 import numpy as np
@@ -68,6 +68,10 @@ CASES = [
     ("C2", dict(value_head=1), 333, 5),        # value rows, including row T
     ("C2", dict(obs_dim=13), 517, 6),          # odd observation width: a half-filled last pair
     ("C2", dict(queue_cap=3), 200, 9),         # drops every tick
+    ("C3", {}, 1000, 6),                       # 64-environment tiles, 16 lanes per wave, ragged
+    ("C3", dict(n_servers=3), 300, 5),         # 18 actions: the sampler's run-time bound
+    ("C3", dict(obs_dim=31), 200, 4),
+    ("C4", {}, 700, 4),                        # 8 servers, 4 classes, lognormal service
 ]
 
 
@@ -159,8 +163,10 @@ def test_fused_rollout_graph_and_tracing(bs):
 
 
 def test_fused_rollout_modes(bs):
-    """sim_set_fused_rollout takes the three modes and rejects others; a network without a
-    fused kernel (C3's) keeps the per-tick launches even when fusing is forced."""
+    """sim_set_fused_rollout takes the three modes and rejects others. Automatic fusing takes a
+    batch whose workgroups are all resident at once (C3's 16384 environments: one 64-environment
+    workgroup per CU) and leaves a larger one (C4's 65536) to the per-tick launches; a network
+    without a fused kernel (C5's) keeps the per-tick launches even when fusing is forced."""
     sim = bs.Sim(preset("C1"), n_envs=64)
     for mode in (bs.FUSE_OFF, bs.FUSE_AUTO, bs.FUSE_ON):
         sim.set_fused_rollout(mode)
@@ -168,13 +174,18 @@ def test_fused_rollout_modes(bs):
         with pytest.raises(bs.SimError):
             sim.set_fused_rollout(bad)
     sim.close()
-    w = preset("C3")
-    sim = bs.Sim(w, n_envs=64)
-    sim.set_fused_rollout(bs.FUSE_ON)
-    sim.set_timing(True)
-    sim.reset(1)
-    wb = sim.upload_weights(weights(w, 2))
-    sim.rollout(wb, 3)
-    timing = sim.get_timing(clear=True)
-    assert timing["rollout"][1] == 0 and timing["step"][1] == 3, timing
-    sim.close()
+    for name, E, mode, fused in (("C3", 16384, bs.FUSE_AUTO, True),
+                                 ("C4", 65536, bs.FUSE_AUTO, False),
+                                 ("C5", 64, bs.FUSE_ON, False)):
+        say(f"[fused mode] {name} E={E} mode={mode}")
+        w = preset(name)
+        sim = bs.Sim(w, n_envs=E)
+        sim.set_fused_rollout(mode)
+        sim.set_timing(True)
+        sim.reset(1)
+        wb = sim.upload_weights(weights(w, 2))
+        sim.rollout(wb, 3)
+        timing = sim.get_timing(clear=True)
+        want = (1, 0) if fused else (0, 3)
+        assert (timing["rollout"][1], timing["step"][1]) == want, (name, timing)
+        sim.close()
