@@ -23,6 +23,7 @@ template <int FP, int H1, int H2, int AP>
 struct PolicyF32 {
   static constexpr int ROWS = 16;
   static constexpr bool kBf16 = false;
+  static constexpr int kWavesPerEU = 1;
   typedef Shape<F32Mode, FP, H1, H2, AP, 1> Sh;
   static constexpr size_t LDS = Sh::LDS;
   __device__ static void run(const MlpParams& m, const float* obs, const uint32_t*, uint64_t seed,
@@ -34,11 +35,13 @@ struct PolicyF32 {
 };
 
 // bf16 policy on one 16 RT-environment tile (4 waves, one output tile per pass); AC as in
-// policy_tile_bf16
-template <int FP, int H1, int H2, int AP, int RT, int AC>
+// policy_tile_bf16; WPE: waves per SIMD the kernel is compiled for (2: at most 256 VGPRs, two
+// workgroups per CU)
+template <int FP, int H1, int H2, int AP, int RT, int AC, int WPE = 1>
 struct PolicyBf16 {
   static constexpr int ROWS = 16 * RT;
   static constexpr bool kBf16 = true;
+  static constexpr int kWavesPerEU = WPE;
   typedef BigShape<FP, H1, H2, AP, RT, 4> Sh;
   static constexpr size_t LDS = Sh::LDS;
   __device__ static void run(const MlpParams& m, const float* obs, const uint32_t* obs_bf,
@@ -56,7 +59,7 @@ struct PolicyBf16 {
 // the ticks write the observation's bf16 pairs (packed before the launch) and the last one
 // also the fp32 observation.
 template <int CM, int TW, class Pol>
-__global__ __launch_bounds__(256) void rollout_fused_k(SimParams p, EnvState g, MlpParams m,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(Pol::kWavesPerEU))) void rollout_fused_k(SimParams p, EnvState g, MlpParams m,
                                                        uint32_t k0, int T, RolloutOut o) {
   static_assert(Pol::ROWS % TW == 0 && TW <= 4, "tick lanes per wave");
   constexpr int LPW = Pol::ROWS / TW;
@@ -130,8 +133,8 @@ hipError_t with_fused(const SimParams& p, const MlpParams& m, F&& f) {
   if (m.bf16 && m.FP == 32 && m.H1 == 128 && m.H2 == 128 && m.AP == 16)
     return by_classes(PolTag<PolicyBf16<32, 128, 128, 16, 1, 0>>{});
   if (m.bf16 && m.FP == 32 && m.H1 == 256 && m.H2 == 256 && m.AP == 32)
-    return m.A == 24 ? by_classes(PolTag<PolicyBf16<32, 256, 256, 32, 4, 24>>{})
-                     : by_classes(PolTag<PolicyBf16<32, 256, 256, 32, 4, 0>>{});
+    return m.A == 24 ? by_classes(PolTag<PolicyBf16<32, 256, 256, 32, 2, 24, 2>>{})
+                     : by_classes(PolTag<PolicyBf16<32, 256, 256, 32, 2, 0, 2>>{});
   if (m.bf16 && m.FP == 64 && m.H1 == 256 && m.H2 == 256 && m.AP == 64)
     return m.A == 48 ? by_classes(PolTag<PolicyBf16<64, 256, 256, 64, 4, 48>>{})
                      : by_classes(PolTag<PolicyBf16<64, 256, 256, 64, 4, 0>>{});
