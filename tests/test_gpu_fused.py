@@ -189,3 +189,38 @@ def test_fused_rollout_modes(bs):
         want = (1, 0) if fused else (0, 3)
         assert (timing["rollout"][1], timing["step"][1]) == want, (name, timing)
         sim.close()
+
+
+def test_fused_rollout_trace_arrivals(bs):
+    """Trace arrivals (several per instant, classes in random order, some environments running
+    out of arrivals mid-rollout) with a Static-8 shadow system beside: fused against per tick,
+    C3's network over 4 servers and 4 classes."""
+    from workloads import trace_preset
+    from workloads.presets import SVC_DET
+    E, T, L, C = 200, 40, 120, 4
+    w = trace_preset(n_servers=4, n_classes=C, queue_cap=20, obs_dim=32, shadow=1,
+                     mlp_h1=256, mlp_h2=256, mlp_bf16=1, value_head=1,
+                     static_bmax=4, static_timeout=2e-3, class_mix=[0.25] * C,
+                     service_kind=[SVC_DET] * C, svc_alpha=[0.3e-3, 1e-3, 2e-3, 4e-3],
+                     svc_beta=[0.1e-3, 0.2e-3, 0.5e-3, 1e-3], svc_median=[0.0] * C,
+                     w_class=[200.0, 100.0, 40.0, 20.0])
+    w["trace_max_len"] = L
+    rng = np.random.default_rng(0x7ACE)
+    times = np.cumsum(0.25e-3 * rng.integers(0, 3, size=(E, L)), axis=1) + 0.25e-3
+    cls = rng.integers(0, C, size=(E, L)).astype(np.uint8)
+    counts = np.full(E, L, np.int32)
+    counts[::5] = L // 3
+    dev = torch.device("cuda")
+    say(f"[fused, trace arrivals] E={E} T={T} L={L}")
+    out = []
+    for mode in (bs.FUSE_OFF, bs.FUSE_ON):
+        sim = bs.Sim(w, n_envs=E)
+        sim.set_fused_rollout(mode)
+        sim.set_trace(torch.from_numpy(times).to(dev), torch.from_numpy(cls).to(dev),
+                      torch.from_numpy(counts).to(dev))
+        sim.reset(3)
+        wb = sim.upload_weights(weights(w, 8))
+        tr = sim.rollout(wb, T, store_obs=True, rchk=True)
+        out.append(snapshot(sim, tr))
+        sim.close()
+    assert_same(out[0], out[1], "trace arrivals")
