@@ -252,7 +252,8 @@ int sim_policy_hidden(sim_ctx* ctx, const void* d_weights, const float* d_obs, u
  * traj->value holds V(obs_T). Ordered on the context's stream like every other call: the
  * static shadow system's launches run on a second stream of the context, forked from the
  * context's stream when the rollout starts and joined back before it ends (one stream when
- * sim_set_timing is on). Afterwards sim_obs returns obs_T.                              */
+ * sim_set_timing is on). Small batches run all T ticks in one fused launch
+ * (sim_set_fused_rollout), with the same outputs. Afterwards sim_obs returns obs_T.      */
 int sim_rollout(sim_ctx* ctx, const void* d_weights, int32_t T, const sim_traj* traj);
 
 /* Rollout graphs, on by default: when sim_rollout is called again with the same weights
