@@ -731,16 +731,19 @@ SHADOWED = {
 }
 
 
-@pytest.mark.parametrize("name", sorted(SHADOWED))
-def test_rollout_static_chunks_then_steps(bs, orc, name):
-    """sim_rollout runs the static shadow system in launches of 256 ticks with its state in
-    registers; 600 ticks (chunks of 256, 256, 88) followed by 20 sim_step calls (the per-tick
-    kernel) must equal the oracle's replay of the same 620 ticks, bit for bit in the integer
-    state and checksums."""
+@pytest.mark.parametrize("name,E,T", [(n, 300, 600) for n in sorted(SHADOWED)] +
+                         [("burst", 6, 4100)])
+def test_rollout_static_chunks_then_steps(bs, orc, name, E, T):
+    """sim_rollout runs the static shadow system in launches of up to 4096 ticks with its
+    state in registers; 600 ticks in one launch followed by 20 sim_step calls (the per-tick
+    kernel, which resumes from the state the long launch stored) must equal the oracle's replay
+    of the same ticks, bit for bit in the integer state and checksums. A longer rollout over a
+    few environments (4100 ticks: launches of 4096 and 4) crosses a boundary inside the
+    rollout as well."""
     w = SHADOWED[name]()
-    E, T, T2 = 300, 600, 20
+    T2 = 20
     seed = 0x5EED5 + len(name)
-    say(f"[static chunks] {name}")
+    say(f"[static chunks] {name} E={E} T={T}")
     sim = bs.Sim(w, n_envs=E)
     sim.reset(seed)
     wb = sim.init_weights(3)
@@ -772,8 +775,8 @@ FULL_ROLLOUT = {"C5": lambda: preset("C5"), "attn": lambda: attn_preset(n_envs=2
 @pytest.mark.parametrize("name", sorted(FULL_ROLLOUT))
 def test_rollout_full_size_sampled(bs, orc, name):
     """sim_rollout at the full environment count in the launch configuration the bench times
-    (large-batch policy kernel, learned tick, static shadow system in 256-tick launches), 300
-    ticks so that the shadow system crosses a launch boundary. For sampled environments the
+    (large-batch policy kernel, learned tick, static shadow system in one launch of up to 4096
+    ticks), 300 ticks. For sampled environments the
     oracle replays the rollout's actions: running checksums, rewards (both systems), final
     checksums and counters agree exactly; and every sampled decision equals the oracle
     policy's on the replayed observation outside the tie band (logits from the same GPU

@@ -56,7 +56,7 @@ def test_resume_reproduces_the_continuation(bs, name):
     snap_dev = sim.get_state(device=True)
     snap_host = sim.get_state(device=False)
     assert torch.equal(snap_dev.cpu(), snap_host)
-    first = continuation(sim, wb, 300)          # crosses a 256-tick static launch
+    first = continuation(sim, wb, 300)          # one static launch of 300 ticks
     sim.set_state(snap_dev)
     same(first, continuation(sim, wb, 300))
     sim.set_state(snap_host)
